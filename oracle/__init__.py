@@ -1,0 +1,111 @@
+"""CPU oracle for batched Monotonic Alignment Search.
+
+TEST INFRASTRUCTURE ONLY: imported by ``tests/``, ``__graft_entry__.smoke()``
+and the CPU-baseline leg of ``bench.py``; never by the product package, which
+must fail loudly rather than fall back to this code.
+
+The arithmetic lives in ``mas_oracle.c`` (plain C99, Algorithm 1 of the
+Super-MAS paper with the readings listed in its header).  This module only
+compiles it with gcc and marshals numpy arrays through ctypes.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "mas_oracle.c")
+_LIB = os.path.join(_HERE, "libmas_oracle.so")
+
+ITEM_OK, ITEM_EMPTY, ITEM_INFEASIBLE, ITEM_OUT_OF_RANGE = 0, 1, 2, 3
+
+# Strict IEEE evaluation: no contraction into FMA, no fast-math, SSE2 scalar
+# float arithmetic (x86-64 default), no flush-to-zero.
+CFLAGS = ["-O2", "-std=c99", "-ffp-contract=off", "-fno-fast-math", "-fPIC", "-shared"]
+
+
+def build(force: bool = True) -> str:
+    """Compile the oracle into ``oracle/libmas_oracle.so`` with gcc."""
+    if force or not os.path.exists(_LIB):
+        tmp = _LIB + ".tmp"
+        subprocess.check_call(["gcc", *CFLAGS, _SRC, "-o", tmp, "-lm"])
+        os.replace(tmp, _LIB)
+    return _LIB
+
+
+_lib = None
+
+
+def _load():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_LIB):
+            build()
+        lib = ctypes.CDLL(_LIB)
+        P = ctypes.c_void_p
+        i32 = ctypes.c_int32
+        lib.oracle_mas_batch_neg.argtypes = [P, i32, i32, i32, P, P, ctypes.c_float, P, P, P, P]
+        lib.oracle_mas_batch_neg.restype = ctypes.c_int
+        lib.oracle_durations.argtypes = [P, i32, i32, i32, P]
+        lib.oracle_durations.restype = None
+        _lib = lib
+    return _lib
+
+
+def _ptr(a: np.ndarray | None):
+    return None if a is None else a.ctypes.data_as(ctypes.c_void_p)
+
+
+def mas(value: np.ndarray, t_x, t_y, *, neg: float = -np.inf, with_dec: bool = False):
+    """Run the oracle on a batch.
+
+    value: float32 [B, T, S] (C-contiguous); t_x, t_y: int [B].
+    Returns (path u8 [B,T,S], score f32 [B], status i32 [B]) and, when
+    ``with_dec``, the per-cell forward choice u8 [B,T,S] as a fourth item.
+    """
+    value = np.ascontiguousarray(value, dtype=np.float32)
+    if value.ndim != 3:
+        raise ValueError("value must be [B, T, S]")
+    B, T, S = value.shape
+    tx = np.ascontiguousarray(t_x, dtype=np.int32).reshape(B)
+    ty = np.ascontiguousarray(t_y, dtype=np.int32).reshape(B)
+    path = np.empty((B, T, S), dtype=np.uint8)
+    score = np.empty(B, dtype=np.float32)
+    status = np.empty(B, dtype=np.int32)
+    dec = np.empty((B, T, S), dtype=np.uint8) if with_dec else None
+    rc = _load().oracle_mas_batch_neg(_ptr(value), B, T, S, _ptr(tx), _ptr(ty), float(neg),
+                                      _ptr(path), _ptr(score), _ptr(status), _ptr(dec))
+    if rc != 0:
+        raise MemoryError("oracle allocation failed")
+    return (path, score, status, dec) if with_dec else (path, score, status)
+
+
+def durations(path: np.ndarray) -> np.ndarray:
+    """Row sums of each item's path slab: int32 [B, T]."""
+    path = np.ascontiguousarray(path, dtype=np.uint8)
+    B, T, S = path.shape
+    dur = np.empty((B, T), dtype=np.int32)
+    _load().oracle_durations(_ptr(path), B, T, S, _ptr(dur))
+    return dur
+
+
+def row_start(path: np.ndarray, t_x, t_y) -> np.ndarray:
+    """First speech column of every text row on each item's path, plus t_y.
+
+    int32 [B, T+1]; entries past t_x are t_y, and invalid items are all 0.
+    Derived from the path only (test helper, not part of the method).
+    """
+    B, T, S = path.shape
+    out = np.zeros((B, T + 1), dtype=np.int32)
+    for b in range(B):
+        tx, ty = int(t_x[b]), int(t_y[b])
+        if not (0 < tx <= ty and tx <= T and ty <= S):
+            continue
+        rows = path[b, :tx, :ty]
+        first = rows.argmax(axis=1)
+        out[b, :tx] = first
+        out[b, tx:] = ty
+    return out
