@@ -1,0 +1,147 @@
+/*
+ * libmas — batched Monotonic Alignment Search (MAS) on AMD Instinct MI355X
+ * (gfx950).
+ *
+ * MAS (Super-MAS paper, Sec. 2, Algorithm 1; parallel form in Algorithm 2)
+ * finds, for every item b of a batch, the monotonic alignment between t_x[b]
+ * text tokens and t_y[b] speech frames that maximises the summed
+ * log-likelihood value[b, i, j]:
+ *   - forward pass: Q[i][j] = max(Q[i-1][j-1], Q[i][j-1]) + value[i][j] over
+ *     0 <= i < t_x, 0 <= j < t_y, with Q[0][0] = value[0][0] and every cell
+ *     a path cannot reach by column j (i > j) at -inf; each speech column
+ *     depends only on the previous one and is parallel over text rows
+ *     (Algorithm 2);
+ *   - backtrack from (t_x-1, t_y-1): at column j in row i the path continues
+ *     in row i-1 at column j-1 when Q[i][j-1] < Q[i-1][j-1] strictly or
+ *     i == j, and stays in row i otherwise (ties stay);
+ *   - output: the 0/1 alignment A* of the input's [T, S] size per item, with
+ *     exactly one 1 per speech column j < t_y (Sec. 2).
+ * The max is the select (stay < diag) ? diag : stay and every add is one
+ * fp32 round-to-nearest-even operation in column order, so paths and scores
+ * are bit-for-bit reproducible and equal to a sequential CPU evaluation.
+ *
+ * Conventions for every entry point:
+ *   - value is [B, T, S] fp32, t_x / t_y are [B] int32, path_out is
+ *     [B, T, S] uint8, row_start is [B, T+1] int32, all contiguous row-major
+ *     and all DEVICE pointers (memory of the current HIP device).
+ *   - T and S are the padded extents; each item uses its own t_x <= T text
+ *     rows and t_y <= S speech columns.  Padding of value is never read and
+ *     padding of path_out is written as 0.
+ *   - Every call only enqueues work on `stream` (0 = the null stream) and
+ *     returns; results are valid once the stream reaches that point.  No call
+ *     synchronises the host or copies device data to the host.
+ *   - The caller owns every buffer; the library never frees or retains
+ *     caller memory.  value, t_x and t_y are read-only.
+ *   - Errors detectable on the host return a non-zero mas_status and enqueue
+ *     nothing.  Per-item length errors can only be seen on the device (the
+ *     lengths live there); they give the item an all-zero slab, score -inf
+ *     and a code in item_status_out.
+ *   - Alignment: when S is a multiple of 4 and value is 16-byte aligned the
+ *     forward pass uses 16-byte loads; other shapes take a general path with
+ *     the same results.  Likewise the path writer uses 16-byte stores when S
+ *     is a multiple of 16 and path_out is 16-byte aligned.
+ */
+#ifndef LIBMAS_MAS_H_
+#define LIBMAS_MAS_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define MAS_VERSION 1
+
+typedef enum mas_status {
+  MAS_OK = 0,
+  MAS_ERR_NULL_POINTER = 1, /* a required pointer is NULL */
+  MAS_ERR_BAD_SHAPE = 2,    /* B, T or S < 1, or a size that overflows */
+  MAS_ERR_WORKSPACE = 3,    /* workspace NULL, misaligned or too small */
+  MAS_ERR_HIP = 4           /* a HIP runtime call or kernel launch failed */
+} mas_status;
+
+/* Per-item status codes written to item_status_out[b]. */
+#define MAS_ITEM_OK 0
+#define MAS_ITEM_EMPTY 1        /* t_x == 0 or t_y == 0 */
+#define MAS_ITEM_INFEASIBLE 2   /* t_y < t_x: no monotonic alignment exists */
+#define MAS_ITEM_OUT_OF_RANGE 3 /* t_x or t_y negative, t_x > T or t_y > S */
+#define MAS_ITEM_SYNC_TIMEOUT 4 /* an internal device-side wait hit its bound; the item's outputs are invalid */
+
+/*
+ * Bytes of device workspace that mas_search / mas_forward_ex need for a
+ * batch of this shape (decision bits, row hand-off slots, progress flags
+ * and, for mas_forward_ex, the row_start table).  Returns 0 for invalid
+ * shapes.  The workspace must be 256-byte aligned.
+ */
+size_t mas_workspace_bytes(int32_t B, int32_t T, int32_t S);
+
+/*
+ * Prepare a workspace for first use: zero-fills it on `stream`.  Required
+ * once per workspace allocation before the first mas_search /
+ * mas_forward_ex that uses it; every later call leaves the workspace ready
+ * for the next one.  A workspace serves one call at a time: calls that share
+ * a workspace must be ordered (same stream or synchronised).
+ */
+mas_status mas_workspace_init(void* workspace, size_t workspace_bytes, hipStream_t stream);
+
+/*
+ * Forward pass and backtrack without the dense path (Sec. 2 and Algorithm 1
+ * up to A*(j); Algorithm 2 for the column-parallel forward loop).
+ *
+ * row_start_out [B, T+1] int32 (required): for a valid item, row_start[b][i]
+ * is the first speech column whose alignment is text row i (i < t_x), so row
+ * i covers columns [row_start[b][i], row_start[b][i+1]) and its duration is
+ * the difference; entries i >= t_x equal t_y.  Invalid items get all zeros.
+ * score_out [B] fp32 (nullable): Q[t_x-1][t_y-1], the log-likelihood of the
+ * chosen alignment, -inf for invalid items.
+ * item_status_out [B] int32 (nullable): MAS_ITEM_* per item.
+ * workspace: at least mas_workspace_bytes(B, T, S) bytes, initialised once by
+ * mas_workspace_init.
+ */
+mas_status mas_search(const float* value, const int32_t* t_x, const int32_t* t_y,
+                      int32_t B, int32_t T, int32_t S,
+                      int32_t* row_start_out, float* score_out, int32_t* item_status_out,
+                      void* workspace, size_t workspace_bytes, hipStream_t stream);
+
+/*
+ * Dense alignment from a row_start table (Sec. 2: the path is a zero matrix
+ * of the input's size with the alignment marked in it).  Writes every byte of
+ * path_out [B, T, S]: path[b][i][j] = 1 iff row_start[b][i] <= j <
+ * row_start[b][i+1], else 0.  row_start [B, T+1] must satisfy
+ * 0 <= row_start[b][i] <= row_start[b][i+1] <= S (as mas_search produces).
+ */
+mas_status mas_expand_path(const int32_t* row_start, int32_t B, int32_t T, int32_t S,
+                           uint8_t* path_out, hipStream_t stream);
+
+/*
+ * Full alignment: mas_search into the workspace's row_start table followed by
+ * mas_expand_path.  score_out and item_status_out are nullable as above.
+ * No allocation; workspace as for mas_search.
+ */
+mas_status mas_forward_ex(const float* value, const int32_t* t_x, const int32_t* t_y,
+                          uint8_t* path_out, int32_t B, int32_t T, int32_t S,
+                          float* score_out, int32_t* item_status_out,
+                          void* workspace, size_t workspace_bytes, hipStream_t stream);
+
+/*
+ * Full alignment with a stream-ordered workspace: allocates it with
+ * hipMallocAsync on `stream`, initialises it, runs mas_forward_ex and frees
+ * it with hipFreeAsync on the same stream.
+ */
+mas_status mas_forward(const float* value, const int32_t* t_x, const int32_t* t_y,
+                       uint8_t* path_out, int32_t B, int32_t T, int32_t S, hipStream_t stream);
+
+/* Human-readable name of a status code (static storage). */
+const char* mas_status_string(mas_status status);
+
+/* MAS_VERSION of the loaded library. */
+int mas_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* LIBMAS_MAS_H_ */

@@ -1,0 +1,120 @@
+// libmas host entry points (C ABI declared in include/mas.h).
+//
+// Every entry point validates its arguments on the host, then only enqueues
+// kernels on the caller's stream; nothing synchronises or copies to the host.
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "mas.h"
+#include "mas_internal.h"
+
+namespace mas {
+
+static bool ws_ok(const void* ws, size_t bytes, const Layout& L) {
+  return ws != nullptr && ((uintptr_t)ws % kAlign) == 0 && bytes >= L.bytes;
+}
+
+static mas_status search_into(const float* value, const int32_t* t_x, const int32_t* t_y, const Layout& L,
+                              int32_t* row_start, float* score, int32_t* status, void* ws, hipStream_t stream) {
+  char* base = static_cast<char*>(ws);
+  SearchParams p;
+  p.value = value;
+  p.t_x = t_x;
+  p.t_y = t_y;
+  p.row_start = row_start;
+  p.score = score;
+  p.status = status;
+  p.hdr = reinterpret_cast<WsHeader*>(base);
+  p.done = reinterpret_cast<uint32_t*>(base + L.off_done);
+  p.slots = reinterpret_cast<uint64_t*>(base + L.off_slots);
+  p.dec = reinterpret_cast<uint32_t*>(base + L.off_dec);
+  p.B = L.B;
+  p.T = L.T;
+  p.S = L.S;
+  p.NW = L.NW;
+  p.NC = L.NC;
+  p.TP = L.TP;
+  const bool aligned = (L.S % 4 == 0) && ((uintptr_t)value % 16 == 0);
+  return launch_search(p, aligned, stream) == hipSuccess ? MAS_OK : MAS_ERR_HIP;
+}
+}  // namespace mas
+
+using namespace mas;
+
+extern "C" {
+
+size_t mas_workspace_bytes(int32_t B, int32_t T, int32_t S) {
+  Layout L;
+  return make_layout(B, T, S, &L) ? L.bytes : 0;
+}
+
+mas_status mas_workspace_init(void* workspace, size_t workspace_bytes, hipStream_t stream) {
+  if (!workspace) return MAS_ERR_NULL_POINTER;
+  if ((uintptr_t)workspace % kAlign != 0 || workspace_bytes < sizeof(WsHeader) || workspace_bytes % 16 != 0)
+    return MAS_ERR_WORKSPACE;
+  return launch_zero(workspace, workspace_bytes, stream) == hipSuccess ? MAS_OK : MAS_ERR_HIP;
+}
+
+mas_status mas_search(const float* value, const int32_t* t_x, const int32_t* t_y, int32_t B, int32_t T, int32_t S,
+                      int32_t* row_start_out, float* score_out, int32_t* item_status_out, void* workspace,
+                      size_t workspace_bytes, hipStream_t stream) {
+  if (!value || !t_x || !t_y || !row_start_out) return MAS_ERR_NULL_POINTER;
+  Layout L;
+  if (!make_layout(B, T, S, &L)) return MAS_ERR_BAD_SHAPE;
+  if (!ws_ok(workspace, workspace_bytes, L)) return MAS_ERR_WORKSPACE;
+  return search_into(value, t_x, t_y, L, row_start_out, score_out, item_status_out, workspace, stream);
+}
+
+mas_status mas_expand_path(const int32_t* row_start, int32_t B, int32_t T, int32_t S, uint8_t* path_out,
+                           hipStream_t stream) {
+  if (!row_start || !path_out) return MAS_ERR_NULL_POINTER;
+  Layout L;
+  if (!make_layout(B, T, S, &L)) return MAS_ERR_BAD_SHAPE;
+  return launch_path(row_start, B, T, S, path_out, stream) == hipSuccess ? MAS_OK : MAS_ERR_HIP;
+}
+
+mas_status mas_forward_ex(const float* value, const int32_t* t_x, const int32_t* t_y, uint8_t* path_out, int32_t B,
+                          int32_t T, int32_t S, float* score_out, int32_t* item_status_out, void* workspace,
+                          size_t workspace_bytes, hipStream_t stream) {
+  if (!value || !t_x || !t_y || !path_out) return MAS_ERR_NULL_POINTER;
+  Layout L;
+  if (!make_layout(B, T, S, &L)) return MAS_ERR_BAD_SHAPE;
+  if (!ws_ok(workspace, workspace_bytes, L)) return MAS_ERR_WORKSPACE;
+  int32_t* rs = reinterpret_cast<int32_t*>(static_cast<char*>(workspace) + L.off_rs);
+  mas_status s = search_into(value, t_x, t_y, L, rs, score_out, item_status_out, workspace, stream);
+  if (s != MAS_OK) return s;
+  return launch_path(rs, B, T, S, path_out, stream) == hipSuccess ? MAS_OK : MAS_ERR_HIP;
+}
+
+mas_status mas_forward(const float* value, const int32_t* t_x, const int32_t* t_y, uint8_t* path_out, int32_t B,
+                       int32_t T, int32_t S, hipStream_t stream) {
+  if (!value || !t_x || !t_y || !path_out) return MAS_ERR_NULL_POINTER;
+  Layout L;
+  if (!make_layout(B, T, S, &L)) return MAS_ERR_BAD_SHAPE;
+  void* ws = nullptr;
+  if (hipMallocAsync(&ws, L.bytes, stream) != hipSuccess) return MAS_ERR_HIP;
+  mas_status s = mas_workspace_init(ws, L.bytes, stream);
+  if (s == MAS_OK) s = mas_forward_ex(value, t_x, t_y, path_out, B, T, S, nullptr, nullptr, ws, L.bytes, stream);
+  if (hipFreeAsync(ws, stream) != hipSuccess && s == MAS_OK) s = MAS_ERR_HIP;
+  return s;
+}
+
+const char* mas_status_string(mas_status status) {
+  switch (status) {
+    case MAS_OK:
+      return "MAS_OK";
+    case MAS_ERR_NULL_POINTER:
+      return "MAS_ERR_NULL_POINTER";
+    case MAS_ERR_BAD_SHAPE:
+      return "MAS_ERR_BAD_SHAPE";
+    case MAS_ERR_WORKSPACE:
+      return "MAS_ERR_WORKSPACE";
+    case MAS_ERR_HIP:
+      return "MAS_ERR_HIP";
+  }
+  return "MAS_ERR_UNKNOWN";
+}
+
+int mas_version(void) { return MAS_VERSION; }
+
+}  // extern "C"

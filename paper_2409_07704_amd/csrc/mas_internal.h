@@ -1,0 +1,34 @@
+// Kernel parameter block and launchers shared by the libmas host code and
+// kernel translation unit.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "mas_layout.h"
+
+namespace mas {
+
+struct SearchParams {
+  const float* value;
+  const int32_t* t_x;
+  const int32_t* t_y;
+  int32_t* row_start;   // [B][T+1]
+  float* score;         // nullable [B]
+  int32_t* status;      // nullable [B]
+  WsHeader* hdr;
+  uint32_t* done;       // [B][NW]
+  uint64_t* slots;      // [B][NW][NC*32]
+  uint32_t* dec;        // [B][NC][TP]
+  int32_t B, T, S, NW, NC, TP;
+};
+
+// Forward sweep + backtrack; one 256-thread workgroup per 256 text rows of
+// every item.  `aligned`: S % 4 == 0 and value 16-byte aligned.
+hipError_t launch_search(const SearchParams& p, bool aligned, hipStream_t stream);
+// Dense [B, T, S] u8 path from row_start [B, T+1].
+hipError_t launch_path(const int32_t* row_start, int32_t B, int32_t T, int32_t S, uint8_t* path, hipStream_t stream);
+// Zero-fill of `bytes` (a multiple of 16) at a 16-byte aligned pointer.
+hipError_t launch_zero(void* p, size_t bytes, hipStream_t stream);
+
+}  // namespace mas

@@ -1,0 +1,90 @@
+// Workspace and bit layout shared by the libmas kernels and host code.
+//
+// Rows of an item are processed by 64-lane waves, one text row per lane
+// (wave g of an item owns rows [64g, 64g+64)); four waves form a 256-thread
+// workgroup.  Speech columns are processed in chunks of 32, and every lane
+// packs its row's 32 forward decisions of a chunk into one 32-bit word.
+#pragma once
+
+#include <stddef.h>
+#include <stdint.h>
+
+namespace mas {
+
+constexpr int kWave = 64;                    // lanes per wavefront (CDNA)
+constexpr int kWavesPerBlock = 4;            // one wave per SIMD of a CU
+constexpr int kRowsPerBlock = kWave * kWavesPerBlock;
+constexpr int kChunk = 32;                   // speech columns per decision word
+constexpr size_t kAlign = 256;
+
+// Decision bit of text row i at speech column j (j >= 1): 1 when the forward
+// max took the diagonal predecessor Q[i-1][j-1] (the backtrack then moves to
+// row i-1), 0 when it kept Q[i][j-1].  Stored as
+//   dec[b][c][i]  (uint32, c = j / 32, bit 31 - (j % 32)),
+// i.e. the first column of a chunk is the most significant bit.
+__host__ __device__ constexpr int dec_bit(int j) { return 31 - (j % kChunk); }
+
+// Boundary hand-off between consecutive waves of an item: wave g publishes
+// Q[64g+63][j] for every column j it computes as one 64-bit word
+// {low: fp32 bits, high: tag}.  The tag identifies the call (see WsHeader),
+// so stale words from earlier calls are never mistaken for fresh ones.
+struct WsHeader {
+  uint32_t gen;         // call generation; tag of a call = 2 * gen + 1
+  uint32_t exit_count;  // waves that finished the current call
+  uint32_t error;       // sticky: non-zero once a device-side wait timed out
+  uint32_t pad[61];
+};
+static_assert(sizeof(WsHeader) == kAlign, "header is one alignment unit");
+
+__host__ __device__ inline size_t round_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
+
+struct Layout {
+  int32_t B, T, S;
+  int32_t NW;      // waves per item = ceil(T / 64)
+  int32_t NB;      // workgroups per item = ceil(T / 256)
+  int32_t NC;      // decision chunks per item = ceil(S / 32)
+  int32_t TP;      // padded rows per item = 64 * NW
+  size_t off_done;   // uint32 [B][NW]   wave-finished flags (tag values)
+  size_t off_slots;  // uint64 [B][NW][NC*32] boundary hand-off words
+  size_t off_dec;    // uint32 [B][NC][TP] decision words
+  size_t off_rs;     // int32  [B][T+1] row_start table (mas_forward_ex)
+  size_t bytes;
+};
+
+// Returns false when the shape is invalid or its byte counts overflow.
+__host__ inline bool make_layout(int32_t B, int32_t T, int32_t S, Layout* L) {
+  if (B < 1 || T < 1 || S < 1) return false;
+  L->B = B;
+  L->T = T;
+  L->S = S;
+  L->NW = (T + kWave - 1) / kWave;
+  L->NB = (T + kRowsPerBlock - 1) / kRowsPerBlock;
+  L->NC = (S + kChunk - 1) / kChunk;
+  L->TP = L->NW * kWave;
+  // Overflow guard: every product below stays far under 2^62 when these hold.
+  if ((uint64_t)B * (uint64_t)L->NB > 0x7fffffffull) return false;  // grid size
+  if ((uint64_t)B * (uint64_t)T * (uint64_t)S > (1ull << 46)) return false;
+  size_t off = sizeof(WsHeader);
+  L->off_done = off;
+  off = round_up(off + (size_t)B * L->NW * sizeof(uint32_t), kAlign);
+  L->off_slots = off;
+  off = round_up(off + (size_t)B * L->NW * (size_t)L->NC * kChunk * sizeof(uint64_t), kAlign);
+  L->off_dec = off;
+  off = round_up(off + (size_t)B * L->NC * (size_t)L->TP * sizeof(uint32_t), kAlign);
+  L->off_rs = off;
+  off = round_up(off + (size_t)B * ((size_t)T + 1) * sizeof(int32_t), kAlign);
+  L->bytes = off;
+  return true;
+}
+
+// Per-item status codes (same values as MAS_ITEM_* in the public header).
+enum ItemStatus : int32_t { kItemOk = 0, kItemEmpty = 1, kItemInfeasible = 2, kItemOutOfRange = 3, kItemSyncTimeout = 4 };
+
+__host__ __device__ inline int32_t item_status(int32_t tx, int32_t ty, int32_t T, int32_t S) {
+  if (tx < 0 || ty < 0 || tx > T || ty > S) return kItemOutOfRange;
+  if (tx == 0 || ty == 0) return kItemEmpty;
+  if (ty < tx) return kItemInfeasible;
+  return kItemOk;
+}
+
+}  // namespace mas
