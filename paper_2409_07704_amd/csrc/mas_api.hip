@@ -14,28 +14,44 @@ static bool ws_ok(const void* ws, size_t bytes, const Layout& L) {
   return ws != nullptr && ((uintptr_t)ws % kAlign) == 0 && bytes >= L.bytes;
 }
 
-static mas_status search_into(const float* value, const int32_t* t_x, const int32_t* t_y, const Layout& L,
-                              int32_t* row_start, float* score, int32_t* status, void* ws, hipStream_t stream) {
+// Zero-fill workgroups for a path of `bytes` bytes: enough to stream at full
+// bandwidth, few enough to leave room for the sweep.
+static int32_t zero_blocks(size_t bytes) {
+  const size_t per = (size_t)256 << 10;  // ~256 KiB per workgroup at least
+  size_t n = (bytes + per - 1) / per;
+  if (n < 1) n = 1;
+  if (n > (size_t)kMaxZero) n = kMaxZero;
+  return (int32_t)n;
+}
+
+static mas_status run(const float* value, const int32_t* t_x, const int32_t* t_y, const Layout& L,
+                      int32_t* row_start, float* score, int32_t* status, uint8_t* path, void* ws,
+                      hipStream_t stream) {
   char* base = static_cast<char*>(ws);
-  SearchParams p;
+  KParams p;
   p.value = value;
   p.t_x = t_x;
   p.t_y = t_y;
   p.row_start = row_start;
   p.score = score;
   p.status = status;
+  p.path = path;
   p.hdr = reinterpret_cast<WsHeader*>(base);
   p.done = reinterpret_cast<uint32_t*>(base + L.off_done);
   p.slots = reinterpret_cast<uint64_t*>(base + L.off_slots);
   p.dec = reinterpret_cast<uint32_t*>(base + L.off_dec);
+  p.zprog = reinterpret_cast<uint64_t*>(base + L.off_zprog);
   p.B = L.B;
   p.T = L.T;
   p.S = L.S;
   p.NW = L.NW;
   p.NC = L.NC;
   p.TP = L.TP;
+  p.NB = L.NB;
+  p.NZ = path ? zero_blocks((size_t)L.B * L.T * L.S) : 0;
+  p.path16 = path && (L.S % 16 == 0) && ((uintptr_t)path % 16 == 0);
   const bool aligned = (L.S % 4 == 0) && ((uintptr_t)value % 16 == 0);
-  return launch_search(p, aligned, stream) == hipSuccess ? MAS_OK : MAS_ERR_HIP;
+  return launch_mas(p, aligned, stream) == hipSuccess ? MAS_OK : MAS_ERR_HIP;
 }
 }  // namespace mas
 
@@ -62,7 +78,7 @@ mas_status mas_search(const float* value, const int32_t* t_x, const int32_t* t_y
   Layout L;
   if (!make_layout(B, T, S, &L)) return MAS_ERR_BAD_SHAPE;
   if (!ws_ok(workspace, workspace_bytes, L)) return MAS_ERR_WORKSPACE;
-  return search_into(value, t_x, t_y, L, row_start_out, score_out, item_status_out, workspace, stream);
+  return run(value, t_x, t_y, L, row_start_out, score_out, item_status_out, nullptr, workspace, stream);
 }
 
 mas_status mas_expand_path(const int32_t* row_start, int32_t B, int32_t T, int32_t S, uint8_t* path_out,
@@ -81,9 +97,7 @@ mas_status mas_forward_ex(const float* value, const int32_t* t_x, const int32_t*
   if (!make_layout(B, T, S, &L)) return MAS_ERR_BAD_SHAPE;
   if (!ws_ok(workspace, workspace_bytes, L)) return MAS_ERR_WORKSPACE;
   int32_t* rs = reinterpret_cast<int32_t*>(static_cast<char*>(workspace) + L.off_rs);
-  mas_status s = search_into(value, t_x, t_y, L, rs, score_out, item_status_out, workspace, stream);
-  if (s != MAS_OK) return s;
-  return launch_path(rs, B, T, S, path_out, stream) == hipSuccess ? MAS_OK : MAS_ERR_HIP;
+  return run(value, t_x, t_y, L, rs, score_out, item_status_out, path_out, workspace, stream);
 }
 
 mas_status mas_forward(const float* value, const int32_t* t_x, const int32_t* t_y, uint8_t* path_out, int32_t B,

@@ -16,6 +16,8 @@ constexpr int kWavesPerBlock = 4;            // one wave per SIMD of a CU
 constexpr int kRowsPerBlock = kWave * kWavesPerBlock;
 constexpr int kChunk = 32;                   // speech columns per decision word
 constexpr size_t kAlign = 256;
+constexpr int kMaxRows = 8192;               // largest T (the walker keeps row_start in LDS)
+constexpr int kMaxZero = 256;                // zero-fill workgroups of a launch
 
 // Decision bit of text row i at speech column j (j >= 1): 1 when the forward
 // max took the diagonal predecessor Q[i-1][j-1] (the backtrack then moves to
@@ -48,12 +50,13 @@ struct Layout {
   size_t off_slots;  // uint64 [B][NW][NC*32] boundary hand-off words
   size_t off_dec;    // uint32 [B][NC][TP] decision words
   size_t off_rs;     // int32  [B][T+1] row_start table (mas_forward_ex)
+  size_t off_zprog;  // uint64 [kMaxZero] zero-fill progress words
   size_t bytes;
 };
 
 // Returns false when the shape is invalid or its byte counts overflow.
 __host__ inline bool make_layout(int32_t B, int32_t T, int32_t S, Layout* L) {
-  if (B < 1 || T < 1 || S < 1) return false;
+  if (B < 1 || T < 1 || S < 1 || T > kMaxRows) return false;
   L->B = B;
   L->T = T;
   L->S = S;
@@ -73,6 +76,8 @@ __host__ inline bool make_layout(int32_t B, int32_t T, int32_t S, Layout* L) {
   off = round_up(off + (size_t)B * L->NC * (size_t)L->TP * sizeof(uint32_t), kAlign);
   L->off_rs = off;
   off = round_up(off + (size_t)B * ((size_t)T + 1) * sizeof(int32_t), kAlign);
+  L->off_zprog = off;
+  off = round_up(off + (size_t)kMaxZero * sizeof(uint64_t), kAlign);
   L->bytes = off;
   return true;
 }
