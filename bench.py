@@ -1,18 +1,30 @@
 """Benchmark of batched monotonic alignment search on one MI355X.
 
 One step = one full alignment of a synthetic TTS-shaped batch already resident
-in HBM: the forward sweep with backtrack (mas_search) and the dense path
-writer (mas_expand_path) — the two launches mas_forward_ex makes.  Timing
-follows the paper's protocol (warm-up steps, then the mean over timed steps).
+in HBM: one ``mas_forward_ex`` call, i.e. one launch of the fused kernel that
+clears the path, runs the forward sweep, walks the decisions back and writes
+the path (workspace preallocated).  Timing follows the paper's protocol
+(warm-up calls, then the mean over timed calls; Section 4).
 
 Prints ONE JSON line.  Metric: MAS cells per second (sum over items of
-t_x * t_y) for the whole batch; plus the roofline of the dominant kernel,
-measured with HIP events on the launch stream, and the CPU oracle timed on
-the host's cores as a reported baseline.
+t_x * t_y) for the whole batch; plus the roofline of the kernel, whose
+per-launch duration is measured with HIP events on the launch stream, and the
+CPU oracle timed on the host as a reported baseline.
+
+Two extra modes serve the HBM-traffic measurement:
+  --copy-probe      after the timed region, also run a few device-to-device
+                    copies of a known size, so that one rocprofv3 --pmc pass
+                    sees the copy kernel beside the MAS kernel;
+  --pmc-summary F   (no GPU) reduce rocprofv3 counter_collection.csv files
+                    (one per counter pass) into the traffic summary that
+                    later bench runs read back.
 """
 from __future__ import annotations
 
 import argparse
+import csv
+import glob
+import hashlib
 import json
 import os
 import sys
@@ -22,27 +34,40 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0  # MI355X HBM3E, public spec
+KERNEL = "mas_kernel"  # the fused kernel one mas_forward_ex call launches
+COPY_BYTES = 1 << 30  # copy-probe size (read once, written once)
+COPY_REPS = 4
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "mas_kernel_tts-b64-t1024-s4096_traffic.json")
+KERNEL_SOURCES = ("mas_kernels.hip", "mas_api.hip", "mas_layout.h", "mas_internal.h")
+
+
+def kernel_source_hash() -> str:
+    """SHA-256 over the sources of the kernel, to tell stale counters apart."""
+    h = hashlib.sha256()
+    for name in KERNEL_SOURCES:
+        with open(os.path.join(ROOT, "paper_2409_07704_amd", "csrc", name), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()
 
 
 def algorithmic_bytes(tx, ty, B, T, S):
-    """Bytes one step must move, per kernel (the HBM floor of the method).
+    """Bytes one call must move (the HBM floor of the method), per launch.
 
-    search: value read over each item's extent (4 B/cell), one decision bit
-    per cell packed into 64-row words per column (8 B per 64 rows per column),
-    the row_start table written (4 B per entry).
-    path:   every byte of the [B, T, S] u8 path written, row_start read.
+    value read over each item's extent (4 B per cell), one decision bit per
+    cell packed into 64-row words per column (8 B per 64 rows per column),
+    every byte of the [B, T, S] u8 path written.  Also the smaller band-only
+    read (cells that can lie on a path: t_x * (t_y - t_x + 1) per item).
     """
     import numpy as np
 
     tx = tx.astype(np.int64)
     ty = ty.astype(np.int64)
+    ok = (tx >= 1) & (ty >= tx)
     cells = int((tx * ty).sum())
     dec = int((((tx + 63) // 64) * 8 * ty).sum())
-    rs = 4 * B * (T + 1)
-    search = 4 * cells + dec + rs
-    path = B * T * S + rs
     metric = 4 * cells + B * T * S + dec
-    return cells, search, path, metric
+    band = int(np.where(ok, tx * (ty - tx + 1), 0).sum())
+    return cells, metric, 4 * band + B * T * S + dec
 
 
 def cpu_oracle_rate(value, tx, ty, budget_s: float):
@@ -62,6 +87,88 @@ def cpu_oracle_rate(value, tx, ty, budget_s: float):
     return cells * reps / t, reps, t, out
 
 
+def read_counter_csv(path):
+    rows = []
+    with open(path, newline="") as f:
+        for r in csv.DictReader(f):
+            rows.append((r["Kernel_Name"], r["Counter_Name"], float(r["Counter_Value"]), int(r["Dispatch_Id"])))
+    return rows
+
+
+def pmc_summary(paths, out_path):
+    """Per-launch HBM bytes of the MAS kernel from FETCH_SIZE / WRITE_SIZE.
+
+    Each counter is in KiB per dispatch.  The copy kernel of the same run
+    moved COPY_BYTES in and out per dispatch, so its counter readings give the
+    scale factor that turns a counter reading into bytes.
+    """
+    acc = {}
+    for p in paths:
+        for kname, cname, val, _ in read_counter_csv(p):
+            base = cname.replace("_sum", "")
+            if base not in ("FETCH_SIZE", "WRITE_SIZE"):
+                continue
+            if KERNEL in kname:
+                key = "mas"
+            elif "copyBuffer" in kname or "copy" in kname.lower():
+                key = "copy"
+            else:
+                continue
+            acc.setdefault((key, base), []).append(val)
+    need = [("mas", "FETCH_SIZE"), ("mas", "WRITE_SIZE"), ("copy", "FETCH_SIZE"), ("copy", "WRITE_SIZE")]
+    missing = [k for k in need if k not in acc]
+    if missing:
+        raise SystemExit(f"pmc-summary: no readings for {missing}")
+    import numpy as np
+
+    def stats(k):
+        v = np.array(acc[k])
+        return float(np.median(v)), len(v)
+
+    # Copy dispatches can include small ones (warm-up copies of other sizes):
+    # the calibration uses the largest readings, one per COPY_BYTES dispatch.
+    cf = sorted(acc[("copy", "FETCH_SIZE")])[-COPY_REPS:]
+    cw = sorted(acc[("copy", "WRITE_SIZE")])[-COPY_REPS:]
+    f_fetch = float(np.median(cf)) * 1024.0 / COPY_BYTES
+    f_write = float(np.median(cw)) * 1024.0 / COPY_BYTES
+    mf, nf = stats(("mas", "FETCH_SIZE"))
+    mw, nw = stats(("mas", "WRITE_SIZE"))
+    fetch_b = mf * 1024.0 / f_fetch
+    write_b = mw * 1024.0 / f_write
+    out = {
+        "kernel": KERNEL,
+        "workload": "tts-b64-t1024-s4096",
+        "kernel_source_sha256": kernel_source_hash(),
+        "fetch_kib_per_dispatch": mf,
+        "write_kib_per_dispatch": mw,
+        "dispatches": [nf, nw],
+        "copy_bytes_per_dispatch": COPY_BYTES,
+        "copy_fetch_kib": float(np.median(cf)),
+        "copy_write_kib": float(np.median(cw)),
+        "scale_fetch": f_fetch,
+        "scale_write": f_write,
+        "fetch_bytes": fetch_b,
+        "write_bytes": write_b,
+        "traffic_bytes_per_launch": fetch_b + write_b,
+    }
+    with open(out_path, "w") as f:
+        json.dump(out, f, indent=1)
+        f.write("\n")
+    print(json.dumps(out))
+
+
+def load_traffic(wname):
+    """Counter-derived bytes per launch, or None when absent or stale."""
+    try:
+        with open(TRAFFIC_FILE) as f:
+            t = json.load(f)
+    except (OSError, ValueError):
+        return None
+    if t.get("workload") != wname or t.get("kernel_source_sha256") != kernel_source_hash():
+        return None
+    return t
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -69,8 +176,13 @@ def main():
     ap.add_argument("--warmup", type=int, default=25)
     ap.add_argument("--workload", default=None)
     ap.add_argument("--cpu-budget", type=float, default=10.0, help="seconds of oracle timing")
-    ap.add_argument("--no-cpu", action="store_true")
+    ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle timing (parity still checked)")
+    ap.add_argument("--copy-probe", action="store_true", help="run copies of a known size after the timed region")
+    ap.add_argument("--pmc-summary", nargs="+", default=None, metavar="CSV")
     args = ap.parse_args()
+    if args.pmc_summary:
+        pmc_summary(args.pmc_summary, TRAFFIC_FILE)
+        return
     if args.gpus != 1:
         print(f"bench.py: this build measures one GPU; --gpus {args.gpus} is not supported "
               "(items are independent, so more GPUs would each run their own share of the batch)",
@@ -86,7 +198,7 @@ def main():
     wname = args.workload or synth.BENCH_WORKLOAD
     value, tx, ty = synth.generate(wname)
     B, T, S = value.shape
-    cells, bytes_search, bytes_path, bytes_metric = algorithmic_bytes(tx, ty, B, T, S)
+    cells, bytes_metric, bytes_band = algorithmic_bytes(tx, ty, B, T, S)
 
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
@@ -94,54 +206,55 @@ def main():
     x = torch.from_numpy(tx).to(dev)
     y = torch.from_numpy(ty).to(dev)
     path = torch.empty((B, T, S), dtype=torch.uint8, device=dev)
-    rs = torch.empty((B, T + 1), dtype=torch.int32, device=dev)
     score = torch.empty(B, dtype=torch.float32, device=dev)
     status = torch.empty(B, dtype=torch.int32, device=dev)
     ws = mas.Workspace(B, T, S, device=dev)
     stream = torch.cuda.current_stream(dev)
 
     def step():
-        mas.mas_search(v, x, y, rs, score, status, workspace=ws, stream=stream)
-        mas.mas_expand_path(rs, S, path, stream=stream)
+        mas.mas_forward_ex(v, x, y, path, score, status, workspace=ws, stream=stream)
 
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize(dev)
 
     K = args.steps
-    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(K)]
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(K + 1)]
     torch.cuda.synchronize(dev)
     t0 = time.perf_counter()
+    ev[0].record(stream)
     for k in range(K):
-        ev[k][0].record(stream)
-        mas.mas_search(v, x, y, rs, score, status, workspace=ws, stream=stream)
-        ev[k][1].record(stream)
-        mas.mas_expand_path(rs, S, path, stream=stream)
-        ev[k][2].record(stream)
+        step()
+        ev[k + 1].record(stream)
     torch.cuda.synchronize(dev)
     wall = time.perf_counter() - t0
+    per_launch = np.array([ev[k].elapsed_time(ev[k + 1]) for k in range(K)]) * 1e-3  # seconds
+    t_mean = float(per_launch.mean())
 
-    t_search = float(np.mean([ev[k][0].elapsed_time(ev[k][1]) for k in range(K)])) * 1e-3
-    t_path = float(np.mean([ev[k][1].elapsed_time(ev[k][2]) for k in range(K)])) * 1e-3
-    t_step_ev = float(np.mean([ev[k][0].elapsed_time(ev[k][2]) for k in range(K)])) * 1e-3
+    if args.copy_probe:
+        src = torch.empty(COPY_BYTES, dtype=torch.uint8, device=dev)
+        dst = torch.empty_like(src)
+        for _ in range(COPY_REPS):
+            dst.copy_(src)
+        torch.cuda.synchronize(dev)
+        del src, dst
 
     # Parity of the timed outputs against the oracle (and the CPU baseline).
     gpu_path = path.cpu().numpy()
     gpu_score = score.cpu().numpy()
+    gpu_status = status.cpu().numpy()
     if args.no_cpu:
         cpu = None
-        _, _, _, (op, os_, _) = cpu_oracle_rate(value, tx, ty, 0.0)
+        _, _, _, (op, os_, ost) = cpu_oracle_rate(value, tx, ty, 0.0)
     else:
-        rate, reps, tcpu, (op, os_, _) = cpu_oracle_rate(value, tx, ty, args.cpu_budget)
+        rate, reps, tcpu, (op, os_, ost) = cpu_oracle_rate(value, tx, ty, args.cpu_budget)
         cpu = {"value": rate, "unit": "cells/s", "cores": 1, "kind": "oracle",
                "sample": f"full {wname} batch ({cells} cells) x {reps} reps, {tcpu:.1f} s, single thread"}
-    parity = bool(np.array_equal(gpu_path, op) and gpu_score.tobytes() == os_.tobytes())
+    parity = bool(np.array_equal(gpu_path, op) and gpu_score.tobytes() == os_.tobytes()
+                  and np.array_equal(gpu_status, ost))
 
-    if t_search >= t_path:
-        dom, t_dom, b_dom = "mas_search_kernel", t_search, bytes_search
-    else:
-        dom, t_dom, b_dom = "mas_path_kernel16", t_path, bytes_path
-    achieved = b_dom / t_dom / 1e9
+    achieved = bytes_metric / t_mean / 1e9
+    tr = load_traffic(wname)
     out = {
         "metric": "MAS cells/s (sum t_x*t_y per second), 1 GPU",
         "value": cells * K / wall,
@@ -156,12 +269,16 @@ def main():
         "dtype": "f32",
         "data": "synthetic",
         "config": {"workload": wname, "B": B, "T": T, "S": S, "cells": cells,
-                   "metric_bytes": bytes_metric,
-                   "metric_gbs": bytes_metric / (wall / K) / 1e9,
-                   "metric_frac_of_hbm_peak": bytes_metric / (wall / K) / 1e9 / HBM_PEAK_GBS,
-                   "search_us": t_search * 1e6, "path_us": t_path * 1e6, "step_us_events": t_step_ev * 1e6},
-        "roofline": {"bound": "hbm", "kernel": dom, "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": achieved / HBM_PEAK_GBS, "traffic": None, "algorithmic_bytes": b_dom},
+                   "launch_us_mean": t_mean * 1e6,
+                   "launch_us_median": float(np.median(per_launch)) * 1e6,
+                   "launch_us_min": float(per_launch.min()) * 1e6,
+                   "band_bytes": bytes_band,
+                   "band_gbs": bytes_band / t_mean / 1e9},
+        "roofline": {"bound": "hbm", "kernel": KERNEL, "achieved": achieved, "peak": HBM_PEAK_GBS,
+                     "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS,
+                     "traffic": None if tr is None else tr["traffic_bytes_per_launch"],
+                     "traffic_unit": "bytes/launch",
+                     "algorithmic_bytes": bytes_metric},
         "cpu_baseline": cpu,
         "parity": "bit-exact" if parity else "MISMATCH",
     }

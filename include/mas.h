@@ -25,8 +25,14 @@
  *     [B, T, S] uint8, row_start is [B, T+1] int32, all contiguous row-major
  *     and all DEVICE pointers (memory of the current HIP device).
  *   - T and S are the padded extents; each item uses its own t_x <= T text
- *     rows and t_y <= S speech columns.  Padding of value is never read and
- *     padding of path_out is written as 0.
+ *     rows and t_y <= S speech columns.  Padding of value and the cells no
+ *     path can reach (i > j) never influence any result: they are either not
+ *     loaded or loaded and discarded (loads never leave the [B, T, S] tensor).
+ *     Padding of path_out is written as 0.
+ *   - Shape limits: B, T, S >= 1, T <= 8192 (the backtrack keeps an item's
+ *     row_start table in on-chip memory), T * S * 4 < 2^31 (one item's value
+ *     slab is addressed with 32-bit byte offsets) and B * T * S <= 2^46.
+ *     Other shapes return MAS_ERR_BAD_SHAPE.
  *   - Every call only enqueues work on `stream` (0 = the null stream) and
  *     returns; results are valid once the stream reaches that point.  No call
  *     synchronises the host or copies device data to the host.
@@ -58,7 +64,7 @@ extern "C" {
 typedef enum mas_status {
   MAS_OK = 0,
   MAS_ERR_NULL_POINTER = 1, /* a required pointer is NULL */
-  MAS_ERR_BAD_SHAPE = 2,    /* B, T or S < 1, or a size that overflows */
+  MAS_ERR_BAD_SHAPE = 2,    /* B, T or S < 1, or past the shape limits above */
   MAS_ERR_WORKSPACE = 3,    /* workspace NULL, misaligned or too small */
   MAS_ERR_HIP = 4           /* a HIP runtime call or kernel launch failed */
 } mas_status;

@@ -67,6 +67,8 @@ __host__ inline bool make_layout(int32_t B, int32_t T, int32_t S, Layout* L) {
   // Overflow guard: every product below stays far under 2^62 when these hold.
   if ((uint64_t)B * (uint64_t)L->NB > 0x7fffffffull) return false;  // grid size
   if ((uint64_t)B * (uint64_t)T * (uint64_t)S > (1ull << 46)) return false;
+  // One item's value slab is addressed with signed 32-bit byte offsets.
+  if ((uint64_t)T * (uint64_t)S * 4u >= (1ull << 31)) return false;
   size_t off = sizeof(WsHeader);
   L->off_done = off;
   off = round_up(off + (size_t)B * L->NW * sizeof(uint32_t), kAlign);

@@ -53,6 +53,11 @@ def test_workspace_bytes():
     assert mas.mas_workspace_bytes(64, 1024, 4097) > n
     # sizes whose product overflows are refused
     assert mas.mas_workspace_bytes(2**30, 2**20, 2**20) == 0
+    # T above the on-chip row_start table, and item slabs of 2 GiB or more
+    assert mas.mas_workspace_bytes(1, 8192, 16) > 0
+    assert mas.mas_workspace_bytes(1, 8193, 16) == 0
+    assert mas.mas_workspace_bytes(1, 8192, 65535) > 0
+    assert mas.mas_workspace_bytes(1, 8192, 65536) == 0
 
 
 FAKE = ctypes.c_void_p(0x10000)  # never dereferenced: validation fails first
