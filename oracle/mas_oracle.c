@@ -24,10 +24,13 @@
  * oracle, shared by the GPU path through the specification, not code):
  *   R1 backtrack tie: the paper's argmax over {A*(j+1)-1, A*(j+1)} does not
  *      say what happens on a tie.  We keep the row (stay) on ties and step
- *      up only when Q[i][j-1] < Q[i-1][j-1] strictly, or when i == j (the
- *      stay candidate is outside the reachable triangle).
- *   R2 the forward max is the select  (stay < diag) ? diag : stay , never
- *      fmaxf, so signed zeros and the score's bits are defined.
+ *      up only when Q[i][j-1] is strictly below Q[i-1][j-1] (in the order of
+ *      R2), or when i == j (the stay candidate is outside the reachable
+ *      triangle).
+ *   R2 max and argmax order values as IEEE 754-2019 maximum() does: the
+ *      numeric order, with -0 below +0 (the paper's max leaves signed zeros
+ *      open; this order defines the score's bits).  The forward max is
+ *      (stay below diag) ? diag : stay.  NaN is outside the method's domain.
  *   R3 masked cells are IEEE -inf (the paper names -inf in Algorithm 1 and
  *      discusses finite stand-ins -1e9 / -1e32 in Sec. 2); a finite sentinel
  *      is kept only as a test knob to reproduce the -1e9 failure the paper
@@ -47,6 +50,11 @@
 #include <stdint.h>
 #include <stdlib.h>
 #include <string.h>
+
+/* R2: a strictly below b (numeric order, -0 below +0). */
+static int below(float a, float b) {
+  return a < b || (a == 0.0f && b == 0.0f && signbit(a) && !signbit(b));
+}
 
 /* Per-item status codes (R7). */
 #define ORACLE_ITEM_OK 0
@@ -90,7 +98,7 @@ static void mas_one(const float* q, int32_t S, int32_t tx, int32_t ty, float neg
     for (int32_t i = 1; i <= imax; ++i) {
       float stay = QC(i, j - 1);     /* neg when i == j: outside the triangle */
       float diag = QC(i - 1, j - 1);
-      int take_diag = stay < diag;   /* R2 */
+      int take_diag = below(stay, diag); /* R2 */
       QC(i, j) = (take_diag ? diag : stay) + QV(i, j);
       if (dec) dec[(size_t)i * (size_t)ty + (size_t)j] = (uint8_t)take_diag;
     }
@@ -98,11 +106,11 @@ static void mas_one(const float* q, int32_t S, int32_t tx, int32_t ty, float neg
 
   /* Algorithm 1: backtrack from the last text row at the last speech column.
    * At column j the path sits in row idx; the row for column j-1 is idx-1
-   * when that candidate's Q is strictly larger, or when idx == j (R1). */
+   * when that candidate's Q is strictly above (R2 order), or when idx == j (R1). */
   int32_t idx = tx - 1;
   for (int32_t j = ty - 1; j >= 0; --j) {
     path[(size_t)idx * (size_t)S + (size_t)j] = 1;
-    if (j > 0 && idx > 0 && (idx == j || QC(idx, j - 1) < QC(idx - 1, j - 1))) idx -= 1;
+    if (j > 0 && idx > 0 && (idx == j || below(QC(idx, j - 1), QC(idx - 1, j - 1)))) idx -= 1;
   }
   *score = QC(tx - 1, ty - 1);
 #undef QC
@@ -168,4 +176,4 @@ void oracle_durations(const uint8_t* path, int32_t B, int32_t T, int32_t S, int3
     }
 }
 
-int oracle_version(void) { return 1; }
+int oracle_version(void) { return 2; }

@@ -8,7 +8,9 @@ at most one per column) and scores each one as the fp32 left-to-right sum of
 its log-likelihoods.  Maximising that sum is what Algorithm 1 computes:
 x -> fl(x + v) is monotone, so fl(max(a, b) + v) = max(fl(a + v), fl(b + v))
 and by induction the dynamic programme's Q[t_x-1][t_y-1] equals the largest
-fp32 path sum, bit for bit.
+fp32 path sum, bit for bit.  That also holds in the order IEEE 754-2019
+maximum() uses (+0 above -0): fl(-0 + v) and fl(+0 + v) differ only for
+v = -0, giving -0 and +0 in that same order.
 """
 from __future__ import annotations
 
@@ -37,14 +39,24 @@ def path_sum_f32(v: np.ndarray, a) -> np.float32:
     return s
 
 
+def above(a, b) -> bool:
+    """a > b in the order IEEE 754-2019 maximum() uses: numeric, with +0
+    above -0."""
+    a, b = np.float32(a), np.float32(b)
+    if a > b:
+        return True
+    return bool(a == 0 and b == 0 and not np.signbit(a) and np.signbit(b))
+
+
 def brute_force(v: np.ndarray, tx: int, ty: int):
-    """(best score, list of all maximising alignments)."""
+    """(best score, list of all maximising alignments), maximising in the
+    order of `above` (ties: same numeric value and same sign of zero)."""
     best, arg = None, []
     for a in enumerate_alignments(tx, ty):
         s = path_sum_f32(v, a)
-        if best is None or s > best:
+        if best is None or above(s, best):
             best, arg = s, [a]
-        elif s == best:
+        elif not above(best, s):
             arg.append(a)
     return best, arg
 

@@ -44,7 +44,7 @@ def test_hand_derived_cases(case):
     path, score, status = _one(v, case["t_x"], case["t_y"])
     assert status == oracle.ITEM_OK
     assert _pins.alignment_of(path, case["t_x"], case["t_y"]) == tuple(case["rows"])
-    assert np.float32(score) == np.float32(case["score"])
+    assert np.float32(score).tobytes() == np.float32(case["score"]).tobytes()
     assert not _pins.check_invariants(path[None], [case["t_x"]], [case["t_y"]])
     if "legacy_neg" in case:
         lp, ls, _ = _one(v, case["t_x"], case["t_y"], neg=case["legacy_neg"])
@@ -161,6 +161,19 @@ def test_negative_zero_single_cell():
     assert score.tobytes() == np.float32(-0.0).tobytes()
 
 
+def test_signed_zero_tie_takes_positive_zero():
+    # t_x = 2, t_y = 3 has two alignments: rows [0,1,1] sums -0 + -0 + -0 = -0
+    # and rows [0,0,1] sums -0 + +0 + -0 = +0.  In the order of IEEE 754-2019
+    # maximum() +0 is the larger, so the forward max takes the diagonal at
+    # (1, 2) (Q[1][1] = -0 below Q[0][1] = +0) and the backtrack steps there.
+    v = np.array([[-0.0, 0.0, 7.0], [5.0, -0.0, -0.0]], dtype=np.float32)
+    path, score, _ = _one(v, 2, 3)
+    assert _pins.alignment_of(path, 2, 3) == (0, 0, 1)
+    assert score.tobytes() == np.float32(0.0).tobytes()
+    best, arg = _pins.brute_force(v, 2, 3)
+    assert best.tobytes() == np.float32(0.0).tobytes() and arg == [(0, 0, 1)]
+
+
 # ------------------------------------------------------------- metamorphic
 def test_power_of_two_scaling():
     value, tx, ty = synth.generate("tts-b16-t128-s512")
@@ -234,12 +247,13 @@ def test_invariants_at_workload_sizes(name):
 _MUTATIONS = {
     # (a tie flip in the forward select only swaps equal values, so it is not
     # a mistake; the tie that decides the path is the backtrack's)
-    "backtrack_tie_flipped": ("QC(idx, j - 1) < QC(idx - 1, j - 1)", "QC(idx, j - 1) <= QC(idx - 1, j - 1)"),
+    "backtrack_tie_flipped": ("below(QC(idx, j - 1), QC(idx - 1, j - 1))", "!below(QC(idx - 1, j - 1), QC(idx, j - 1))"),
     "dropped_value_term": ("QC(i, j) = (take_diag ? diag : stay) + QV(i, j);", "QC(i, j) = (take_diag ? diag : stay);"),
     "wrong_value_index": ("QC(i, j) = (take_diag ? diag : stay) + QV(i, j);", "QC(i, j) = (take_diag ? diag : stay) + QV(i, j - 1);"),
     "max_became_min": ("QC(i, j) = (take_diag ? diag : stay) + QV(i, j);", "QC(i, j) = (take_diag ? stay : diag) + QV(i, j);"),
     "first_row_not_summed": ("QC(0, j) = QC(0, j - 1) + QV(0, j);", "QC(0, j) = QV(0, j);"),
-    "backtrack_compare_reversed": ("QC(idx, j - 1) < QC(idx - 1, j - 1)", "QC(idx, j - 1) > QC(idx - 1, j - 1)"),
+    "backtrack_compare_reversed": ("below(QC(idx, j - 1), QC(idx - 1, j - 1))", "below(QC(idx - 1, j - 1), QC(idx, j - 1))"),
+    "signed_zero_order_dropped": ("return a < b || (a == 0.0f && b == 0.0f && signbit(a) && !signbit(b));", "return a < b;"),
     "diag_wrong_row": ("float diag = QC(i - 1, j - 1);", "float diag = QC(i - 1, j);"),
     "loop_bound_off_by_one": ("int32_t imax = j < tx - 1 ? j : tx - 1;", "int32_t imax = j - 1 < tx - 1 ? j - 1 : tx - 1;"),
 }
@@ -280,7 +294,7 @@ def _pins_pass(mas) -> bool:
             v = _load_case(case)
             path, score, _ = _one(v, case["t_x"], case["t_y"], impl=mas)
             assert _pins.alignment_of(path, case["t_x"], case["t_y"]) == tuple(case["rows"])
-            assert np.float32(score) == np.float32(case["score"])
+            assert np.float32(score).tobytes() == np.float32(case["score"]).tobytes()
         st = synth.Stream(31)
         for tx, ty in _all_pairs():
             v = st.normal_f32(50).reshape(5, 10)
