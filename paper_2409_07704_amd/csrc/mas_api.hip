@@ -14,16 +14,6 @@ static bool ws_ok(const void* ws, size_t bytes, const Layout& L) {
   return ws != nullptr && ((uintptr_t)ws % kAlign) == 0 && bytes >= L.bytes;
 }
 
-// Zero-fill workgroups for a path of `bytes` bytes: enough to stream at full
-// bandwidth, few enough to leave room for the sweep.
-static int32_t zero_blocks(size_t bytes) {
-  const size_t per = (size_t)256 << 10;  // ~256 KiB per workgroup at least
-  size_t n = (bytes + per - 1) / per;
-  if (n < 1) n = 1;
-  if (n > (size_t)kMaxZero) n = kMaxZero;
-  return (int32_t)n;
-}
-
 static mas_status run(const float* value, const int32_t* t_x, const int32_t* t_y, const Layout& L,
                       int32_t* row_start, float* score, int32_t* status, uint8_t* path, void* ws,
                       hipStream_t stream) {
@@ -38,9 +28,9 @@ static mas_status run(const float* value, const int32_t* t_x, const int32_t* t_y
   p.path = path;
   p.hdr = reinterpret_cast<WsHeader*>(base);
   p.done = reinterpret_cast<uint32_t*>(base + L.off_done);
+  p.zdone = p.done + (size_t)L.B * L.NW;
   p.slots = reinterpret_cast<uint64_t*>(base + L.off_slots);
   p.dec = reinterpret_cast<uint32_t*>(base + L.off_dec);
-  p.zprog = reinterpret_cast<uint64_t*>(base + L.off_zprog);
   p.B = L.B;
   p.T = L.T;
   p.S = L.S;
@@ -48,7 +38,6 @@ static mas_status run(const float* value, const int32_t* t_x, const int32_t* t_y
   p.NC = L.NC;
   p.TP = L.TP;
   p.NB = L.NB;
-  p.NZ = path ? zero_blocks((size_t)L.B * L.T * L.S) : 0;
   p.path16 = path && (L.S % 16 == 0) && ((uintptr_t)path % 16 == 0);
   const bool aligned = (L.S % 4 == 0) && ((uintptr_t)value % 16 == 0);
   return launch_mas(p, aligned, stream) == hipSuccess ? MAS_OK : MAS_ERR_HIP;

@@ -18,17 +18,17 @@ struct KParams {
   int32_t* status;      // nullable [B]
   uint8_t* path;        // nullable [B][T][S]; null: no path is written
   WsHeader* hdr;
-  uint32_t* done;       // [B][NW]
+  uint32_t* done;       // [B][NW] sweep finished (decision words published)
+  uint32_t* zdone;      // [B][NW] this wave's path rows cleared
   uint64_t* slots;      // [B][NW][NC*32]
   uint32_t* dec;        // [B][NC][TP]
-  uint64_t* zprog;      // [NZ]
-  int32_t B, T, S, NW, NC, TP, NZ, NB;
+  int32_t B, T, S, NW, NC, TP, NB;
   int32_t path16;       // path 16-byte aligned and S % 16 == 0
 };
 
 // Forward sweep, backtrack and (when p.path) the dense path, in one launch:
-// p.NZ zero-fill workgroups, then one 256-thread workgroup per 256 text rows
-// of every item.  `aligned`: S % 4 == 0 and value 16-byte aligned.
+// one 256-thread workgroup per 256 text rows of every item.  `aligned`:
+// S % 4 == 0 and value 16-byte aligned.
 hipError_t launch_mas(const KParams& p, bool aligned, hipStream_t stream);
 // Dense [B, T, S] u8 path from row_start [B, T+1].
 hipError_t launch_path(const int32_t* row_start, int32_t B, int32_t T, int32_t S, uint8_t* path, hipStream_t stream);

@@ -2,43 +2,44 @@
 // (Super-MAS Sec. 2, Algorithm 1; column-parallel forward loop of
 // Algorithm 2) and the dense path writer.
 //
-// One launch computes everything (mas_kernel):
-//   * Zero workgroups (the lowest block ids) stream zeros over the whole
-//     [B, T, S] path while the sweep runs.
-//   * Sweep workgroups own 256 text rows of one item: four waves, one text
-//     row per lane, 64 rows per wave.  A wave walks the speech axis in
-//     chunks of 32 columns.  The recurrence's only cross-row dependency, the
-//     diagonal predecessor Q[i-1][j-1], crosses lanes with one DPP
-//     wave_shr:1 per column, crosses waves of a workgroup through an LDS
-//     ring, and crosses workgroups through 64-bit {value, tag} words in
-//     global memory.  Wave g starts at chunk floor(64g / 32): all earlier
-//     cells of its rows lie in the masked triangle i > j, so waves are
-//     naturally skewed by 64 columns, which covers the hand-off latency.
-//   * Each lane reads its own row's 32 values of a chunk (128 contiguous
-//     bytes, eight 16-byte buffer loads with the chunk offset in a scalar
-//     register) three chunks ahead, straight into the registers the
-//     recurrence uses.
+// One launch computes everything (mas_kernel).  A workgroup owns 256 text
+// rows of one item: four waves, one text row per lane, 64 rows per wave.  A
+// wave walks the speech axis in chunks of 32 columns.
+//   * The recurrence's only cross-row dependency, the diagonal predecessor
+//     Q[i-1][j-1], crosses lanes with one DPP wave_shr:1 per column, crosses
+//     waves of a workgroup through an LDS ring, and crosses workgroups
+//     through 64-bit {value, tag} words in global memory.  Wave g starts at
+//     chunk floor(64g / 32): all earlier cells of its rows lie in the masked
+//     triangle i > j, so waves are naturally skewed by 64 columns.
+//   * Value tiles (64 rows x 32 columns) travel HBM -> LDS by buffer loads
+//     with the lds flag, three chunks ahead, eight coalesced 16-byte pieces
+//     per lane, into an XOR-swizzled layout from which each lane reads its
+//     own row's 32 values.
 //   * Q is never materialised: each lane keeps its row's previous column in
 //     a register.  Each column's 64-row decision mask is the compare's SGPR
 //     mask; every lane shifts its bit into a 32-bit word (v_addc with the
 //     mask as carry-in), stored once per chunk.
-//   * The wave owning row t_x-1 then walks the decision words backwards
-//     from (t_x-1, t_y-1), four chunks per block.  A block's words are
-//     fetched two blocks ahead into registers (a block descends at most 128
-//     rows, so a 448-row band bounds every word it can need) and staged in
-//     LDS.  Within a chunk each row step is a find-first-set over one word
-//     and sets one bit of a scalar path mask; the chunk's rows are then
-//     scattered to row_start in LDS in one step.  Finally the wave writes
-//     row_start and the item's ones into the zero-filled path.
+//   * The dense path is cleared by the same waves: each wave zeroes its own
+//     64 rows of the path, two 1 KiB stores per chunk step.
+//   * The wave owning row t_x-1 then walks the decision words backwards from
+//     (t_x-1, t_y-1), four chunks per block (words fetched two blocks ahead,
+//     staged in LDS; one find-first-set per row change), builds row_start
+//     in LDS and writes the item's ones into the cleared path.
 //
-// Memory ordering: data handed between workgroups (decision words, boundary
-// words, progress flags, path bytes) is written with device-scope
-// write-through stores and read with device-scope loads, and a wave waits
-// for its own stores to complete (vmcnt(0)) before raising a flag, so no
-// cache write-back or invalidation is needed.  On gfx9 the vector memory
-// counter retires in issue order and counts stores too, so the loops keep a
-// fixed sequence of loads per iteration (exact compiler waits) and keep
-// loads that are waited on soon from queueing behind slow stores.
+// Vector-memory accounting: gfx9 retires a wave's vector-memory operations
+// (loads and stores alike) in issue order, so "the operation issued N
+// operations ago has completed" is s_waitcnt vmcnt(N).  Every vector-memory
+// operation of the sweep loop is issued from inline assembly in a fixed
+// sequence per step, and each step waits with a count derived from that
+// sequence; the compiler neither sees these operations nor inserts waits
+// for them.  Loads that feed the loop write LDS, never registers, so no
+// register is written behind the compiler's back.
+//
+// Memory ordering across workgroups: data handed between workgroups
+// (decision words, boundary words, flags, path bytes) is written with
+// device-scope write-through stores and read with device-scope loads, and a
+// wave waits for all its stores (vmcnt(0)) before raising a flag, so no cache
+// write-back or invalidation is needed.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -74,9 +75,6 @@ __device__ __forceinline__ float shift_rows(float src, float lane0) {
   return __int_as_float(__builtin_amdgcn_update_dpp(__float_as_int(lane0), __float_as_int(src), 0x138, 0xF, 0xF, false));
 }
 
-// acc[lane] = v for one (uniform) lane.
-__device__ __forceinline__ void write_lane(int& acc, int v, int sel, int lane) { acc = lane == sel ? v : acc; }
-
 // Keeps the compiler from moving LDS accesses across this point; LDS
 // operations of one wave execute in order, so no wait is needed.
 __device__ __forceinline__ void wave_lds_sync() {
@@ -86,12 +84,11 @@ __device__ __forceinline__ void wave_lds_sync() {
 }
 
 // Device-scope (write-through) stores and loads of data shared across
-// workgroups, and a wait for this wave's outstanding memory operations.
+// workgroups, outside the sweep loop.
 __device__ __forceinline__ void st_dev(uint32_t* p, uint32_t v) { __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT); }
 __device__ __forceinline__ void st_dev(uint64_t* p, uint64_t v) { __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT); }
+__device__ __forceinline__ void st_dev(uint8_t* p, uint8_t v) { __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT); }
 __device__ __forceinline__ uint32_t ld_dev(const uint32_t* p) { return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT); }
-__device__ __forceinline__ uint64_t ld_dev(const uint64_t* p) { return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT); }
-__device__ __forceinline__ void wait_mem() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
 
 __device__ __forceinline__ int lds_load(const int* p) { return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP); }
 __device__ __forceinline__ void lds_store(int* p, int v) { __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP); }
@@ -100,49 +97,180 @@ __device__ __forceinline__ uint32_t call_tag(uint32_t gen) { return 2u * gen + 1
 
 constexpr int kSpinLimit = 1 << 21;  // bound of every device-side wait (~seconds)
 constexpr int kRing = 16;            // LDS hand-off ring depth (chunks)
+constexpr int kDepth = 3;            // value tiles in flight ahead of the one computed
+constexpr int kStages = 4;           // LDS tile slots per wave (kDepth + 1, a power of two)
+constexpr int kPollSlots = 4;        // LDS slots of polled boundary words
+static_assert(kStages == kDepth + 1 && (kStages & (kStages - 1)) == 0, "tile ring");
 
-// Buffer resource over one item's [T, S] value slab (T*S*4 < 2^31 bytes).
-__device__ __forceinline__ __amdgpu_buffer_rsrc_t slab_rsrc(const float* vb, int T, int S) {
-  return __builtin_amdgcn_make_buffer_rsrc((void*)vb, 0, T * S * 4, 0x00020000);
+// ---------------------------------------------------------------- vector memory (inline asm)
+// Byte offset of a __shared__ object inside the workgroup's LDS allocation.
+template <typename T>
+__device__ __forceinline__ uint32_t lds_off(T* p) {
+  return (uint32_t)(uintptr_t)(__attribute__((address_space(3))) T*)p;
 }
-constexpr int kOob = 0x7fffff00;  // a byte offset past every slab: buffer loads return 0
+
+// Waits until at most N vector-memory operations of this wave are outstanding.
+template <int N>
+__device__ __forceinline__ void vm_wait() {
+  static_assert(N >= 0 && N <= 63, "vmcnt is a 6-bit counter");
+  asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
+}
+
+// One value tile, 16-byte variant: load q (q = 0..7) brings every lane's
+// 16-byte piece at byte offset voff[q] of the resource to LDS at
+// lds + 1024 q + 16 lane.  Eight operations.  (Offsets are kept in the
+// range-checked per-lane operand: the resource base moves per chunk.)
+__device__ __forceinline__ void dma_tile16(uint32_t lds, __amdgpu_buffer_rsrc_t r, const int (&vo)[8]) {
+  asm volatile(
+      "s_mov_b32 m0, %[l]\n\ts_nop 0\n\t"
+      "buffer_load_dwordx4 %[v0], %[r], 0 offen lds\n\t"
+      "s_add_u32 m0, %[l], 0x400\n\ts_nop 0\n\t"
+      "buffer_load_dwordx4 %[v1], %[r], 0 offen lds\n\t"
+      "s_add_u32 m0, %[l], 0x800\n\ts_nop 0\n\t"
+      "buffer_load_dwordx4 %[v2], %[r], 0 offen lds\n\t"
+      "s_add_u32 m0, %[l], 0xc00\n\ts_nop 0\n\t"
+      "buffer_load_dwordx4 %[v3], %[r], 0 offen lds\n\t"
+      "s_add_u32 m0, %[l], 0x1000\n\ts_nop 0\n\t"
+      "buffer_load_dwordx4 %[v4], %[r], 0 offen lds\n\t"
+      "s_add_u32 m0, %[l], 0x1400\n\ts_nop 0\n\t"
+      "buffer_load_dwordx4 %[v5], %[r], 0 offen lds\n\t"
+      "s_add_u32 m0, %[l], 0x1800\n\ts_nop 0\n\t"
+      "buffer_load_dwordx4 %[v6], %[r], 0 offen lds\n\t"
+      "s_add_u32 m0, %[l], 0x1c00\n\ts_nop 0\n\t"
+      "buffer_load_dwordx4 %[v7], %[r], 0 offen lds"
+      :
+      : [l] "s"(lds), [r] "s"(r), [v0] "v"(vo[0]), [v1] "v"(vo[1]), [v2] "v"(vo[2]), [v3] "v"(vo[3]),
+        [v4] "v"(vo[4]), [v5] "v"(vo[5]), [v6] "v"(vo[6]), [v7] "v"(vo[7])
+      : "memory", "m0", "scc");
+}
+
+// Eight 4-byte loads: load k brings every lane's word at voff[k] of the
+// resource to LDS at lds + 256 k + 4 lane.
+__device__ __forceinline__ void dma_words8(uint32_t lds, __amdgpu_buffer_rsrc_t r, const int (&vo)[8]) {
+  asm volatile(
+      "s_mov_b32 m0, %[l]\n\ts_nop 0\n\t"
+      "buffer_load_dword %[v0], %[r], 0 offen lds\n\t"
+      "s_add_u32 m0, %[l], 0x100\n\ts_nop 0\n\t"
+      "buffer_load_dword %[v1], %[r], 0 offen lds\n\t"
+      "s_add_u32 m0, %[l], 0x200\n\ts_nop 0\n\t"
+      "buffer_load_dword %[v2], %[r], 0 offen lds\n\t"
+      "s_add_u32 m0, %[l], 0x300\n\ts_nop 0\n\t"
+      "buffer_load_dword %[v3], %[r], 0 offen lds\n\t"
+      "s_add_u32 m0, %[l], 0x400\n\ts_nop 0\n\t"
+      "buffer_load_dword %[v4], %[r], 0 offen lds\n\t"
+      "s_add_u32 m0, %[l], 0x500\n\ts_nop 0\n\t"
+      "buffer_load_dword %[v5], %[r], 0 offen lds\n\t"
+      "s_add_u32 m0, %[l], 0x600\n\ts_nop 0\n\t"
+      "buffer_load_dword %[v6], %[r], 0 offen lds\n\t"
+      "s_add_u32 m0, %[l], 0x700\n\ts_nop 0\n\t"
+      "buffer_load_dword %[v7], %[r], 0 offen lds"
+      :
+      : [l] "s"(lds), [r] "s"(r), [v0] "v"(vo[0]), [v1] "v"(vo[1]), [v2] "v"(vo[2]), [v3] "v"(vo[3]),
+        [v4] "v"(vo[4]), [v5] "v"(vo[5]), [v6] "v"(vo[6]), [v7] "v"(vo[7])
+      : "memory", "m0", "scc");
+}
+
+// Five 4-byte loads, device-scope: load k brings the word at voff[k] of the
+// resource to LDS at lds + 256 k + 4 lane.
+__device__ __forceinline__ void dma_words5(uint32_t lds, __amdgpu_buffer_rsrc_t r, const int (&vo)[5]) {
+  asm volatile(
+      "s_mov_b32 m0, %[l]\n\ts_nop 0\n\t"
+      "buffer_load_dword %[v0], %[r], 0 offen sc1 lds\n\t"
+      "s_add_u32 m0, %[l], 0x100\n\ts_nop 0\n\t"
+      "buffer_load_dword %[v1], %[r], 0 offen sc1 lds\n\t"
+      "s_add_u32 m0, %[l], 0x200\n\ts_nop 0\n\t"
+      "buffer_load_dword %[v2], %[r], 0 offen sc1 lds\n\t"
+      "s_add_u32 m0, %[l], 0x300\n\ts_nop 0\n\t"
+      "buffer_load_dword %[v3], %[r], 0 offen sc1 lds\n\t"
+      "s_add_u32 m0, %[l], 0x400\n\ts_nop 0\n\t"
+      "buffer_load_dword %[v4], %[r], 0 offen sc1 lds"
+      :
+      : [l] "s"(lds), [r] "s"(r), [v0] "v"(vo[0]), [v1] "v"(vo[1]), [v2] "v"(vo[2]), [v3] "v"(vo[3]), [v4] "v"(vo[4])
+      : "memory", "m0", "scc");
+}
+
+// One 16-byte piece per lane, device-scope, to LDS at lds + 16 lane.
+__device__ __forceinline__ void dma_poll(uint32_t lds, __amdgpu_buffer_rsrc_t r, int voff) {
+  asm volatile("s_mov_b32 m0, %[l]\n\ts_nop 0\n\tbuffer_load_dwordx4 %[v], %[r], 0 offen sc1 lds"
+               :
+               : [l] "s"(lds), [r] "s"(r), [v] "v"(voff)
+               : "memory", "m0");
+}
+
+// A placeholder operation that keeps a step's operation count when it has
+// nothing to store: one 4-byte load per lane into a scratch LDS area.
+__device__ __forceinline__ void dma_dummy(uint32_t lds, __amdgpu_buffer_rsrc_t r, int voff) {
+  asm volatile("s_mov_b32 m0, %[l]\n\ts_nop 0\n\tbuffer_load_dword %[v], %[r], 0 offen lds"
+               :
+               : [l] "s"(lds), [r] "s"(r), [v] "v"(voff)
+               : "memory", "m0");
+}
+
+__device__ __forceinline__ void vm_store32(uint64_t a, uint32_t v) {
+  asm volatile("global_store_dword %0, %1, off sc1" ::"v"(a), "v"(v) : "memory");
+}
+__device__ __forceinline__ void vm_store64(uint64_t a, uint64_t v) {
+  asm volatile("global_store_dwordx2 %0, %1, off sc1" ::"v"(a), "v"(v) : "memory");
+}
+// Two 16-byte zero stores (s_nop: a VALU write of store data needs one wait state).
+__device__ __forceinline__ void vm_zero2(uint64_t a0, uint64_t a1, u32x4 z) {
+  asm volatile("global_store_dwordx4 %0, %2, off sc1\n\tglobal_store_dwordx4 %1, %2, off sc1\n\ts_nop 0" ::"v"(a0), "v"(a1),
+               "v"(z)
+               : "memory");
+}
+__device__ __forceinline__ void vm_zero1(uint64_t a, u32x4 z) {
+  asm volatile("global_store_dwordx4 %0, %1, off sc1\n\ts_nop 0" ::"v"(a), "v"(z) : "memory");
+}
+
+// Vector-memory operations of one sweep step, in issue order:
+//   [poll of chunk c+2]  (waves fed by another workgroup)
+//   tile of chunk c+kDepth (8 ops, or 32 for the 4-byte variant)
+//   decision word of chunk c (1)
+//   [boundary words of chunk c]  (waves that feed another workgroup)
+//   [2 zero stores]      (when the path is written)
+constexpr int step_ops(int nl, bool in2, bool h, bool z) { return (in2 ? 1 : 0) + nl + 1 + (h ? 1 : 0) + (z ? 2 : 0); }
+// Count for the wait at the start of step c: tile c was issued kDepth steps
+// earlier (followed by that step's stores and kDepth-1 whole steps), the
+// poll of chunk c two steps earlier (followed by that step's tile and stores
+// and one whole step).  Counts above 63 are clamped: at most 63 operations
+// are ever outstanding, so the clamped wait still covers the operation.
+constexpr int wait_count(int nl, bool in2, bool h, bool z) {
+  const int k = step_ops(nl, in2, h, z);
+  const int tail = 1 + (h ? 1 : 0) + (z ? 2 : 0);
+  const int n_tile = tail + (kDepth - 1) * k;
+  const int n_poll = nl + tail + k;
+  const int n = in2 && n_poll < n_tile ? n_poll : n_tile;
+  return n > 63 ? 63 : n;
+}
+
+template <int NL, bool IN2>
+__device__ __forceinline__ void wait_step(bool h, bool z) {
+  if (h) {
+    if (z)
+      vm_wait<wait_count(NL, IN2, true, true)>();
+    else
+      vm_wait<wait_count(NL, IN2, true, false)>();
+  } else {
+    if (z)
+      vm_wait<wait_count(NL, IN2, false, true)>();
+    else
+      vm_wait<wait_count(NL, IN2, false, false)>();
+  }
+}
+
+// Buffer resource over the bytes [off, total) of the region at p (empty
+// when off >= total; total < 2^31).  Loads outside a resource return 0.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t sub_rsrc(const void* p, uint64_t total, uint64_t off) {
+  const uint64_t o = off < total ? off : total;
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<char*>(static_cast<const char*>(p)) + o, 0, (int)(uint32_t)(total - o),
+                                           0x00020000);
+}
 
 // XOR swizzle of 16-byte slots inside a tile row: slot (r, p) holds piece
 // p ^ swz(r).  Distinct over 8 consecutive rows and over the 8 same-parity
 // rows of any 16 consecutive rows, so 8- and 16-lane LDS phases are
-// conflict-free for both the transposing writes and the per-row reads.
+// conflict-free for both the tile writes and the per-row reads.
 __device__ __forceinline__ int swz(int r) { return (r & 7) ^ ((r >> 3) & 1); }
-
-template <bool ALIGNED>
-struct TileLoader {
-  // A chunk of the wave's 64 rows x 32 columns is fetched with 8 coalesced
-  // 16-byte loads: lane L of load q reads tile row tr = 8q + L/8, piece
-  // (L%8) ^ swz(tr), so 8 consecutive lanes cover one 128-byte row segment.
-  // voff[q]: byte offset of the lane's piece in chunk 0 (or kOob for rows
-  // past t_x).  Pieces at or past column t_y are not fetched (read as 0),
-  // except inside the 16-byte piece holding column t_y-1.
-  static __device__ __forceinline__ void load(f32x4 (&v)[8], __amdgpu_buffer_rsrc_t rsrc, const int (&voff)[8],
-                                              const int (&col0)[8], int ty, int c) {
-    const int soff = c * kChunk * 4;
-    if ((c + 1) * kChunk <= ty) {  // whole chunk inside the extent
-#pragma unroll
-      for (int q = 0; q < 8; ++q) piece(v[q], rsrc, voff[q], soff);
-      return;
-    }
-#pragma unroll
-    for (int q = 0; q < 8; ++q) piece(v[q], rsrc, c * kChunk + col0[q] < ty ? voff[q] : kOob, soff);
-  }
-  static __device__ __forceinline__ void piece(f32x4& x, __amdgpu_buffer_rsrc_t rsrc, int vo, int so) {
-    if (ALIGNED) {
-      x = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(rsrc, vo, so, 0));
-    } else {
-      x.x = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rsrc, vo, so + 0, 0));
-      x.y = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rsrc, vo, so + 4, 0));
-      x.z = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rsrc, vo, so + 8, 0));
-      x.w = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rsrc, vo, so + 12, 0));
-    }
-  }
-};
 
 // One 32-column chunk of the recurrence for one row per lane.
 //   q   : this lane's Q at the column before the chunk (updated)
@@ -150,7 +278,7 @@ struct TileLoader {
 //   bd  : Q[row0-1][j0-1 .. j0+30] (the row above the wave), read by lane 0
 //   qc  : this lane's Q at every column of the chunk (out)
 //   bits: decisions of the chunk, first column in bit 31 (out)
-// MASKED handles the chunks that cross the triangle i > j (value not read
+// MASKED handles the chunks that cross the triangle i > j (value not used
 // there, Q = -inf) and the first cell Q[0][0] = value[0][0].
 // FIRST: the wave holding row 0, whose row above is the virtual -inf row:
 // `diag` keeps -inf in lane 0 (DPP leaves lane 0 untouched), so bd is unused.
@@ -198,112 +326,189 @@ __device__ __forceinline__ uint4 path_piece(int lo, int hi, int j0) {
 }
 
 // ---------------------------------------------------------------- LDS layout
-constexpr int kWalkChunks = 4;                 // chunks per walk block
-constexpr int kWalkRows = 7 * kWave;           // rows staged per chunk of a block
+// The walk fetches each chunk's decision words kWalkAhead chunks before it
+// walks that chunk, as a window of kWalkWin rows below the walker's row at
+// fetch time: the path descends at most 32 rows per chunk and a chunk reads
+// the words of at most 32 rows below its entry row, so the window
+// 32 (kWalkAhead + 1) + 1 rows deep covers every word the chunk can need.
+constexpr int kWalkAhead = 8;
+constexpr int kWalkWin = 5 * kWave;   // 320 rows: five 256-byte loads
+constexpr int kWalkSlots = 16;        // window ring (power of two > kWalkAhead)
+static_assert(kWalkWin >= 32 * (kWalkAhead + 1) + 1, "walk window");
 
 struct SweepLds {
-  f32x4 tile[kWavesPerBlock][8 * kWave];          // value tile of the chunk per wave (8 KiB)
+  union {
+    // Value tiles: [wave][slot] 64 rows x 32 columns, 16-byte unit 8 r + s
+    // holds piece s ^ swz(r) of row r.
+    f32x4 tile[kWavesPerBlock][kStages][8 * kWave];
+    // The walker's staging, once every sweep of its item (and so of its
+    // workgroup) has finished.
+    struct {
+      uint32_t win[kWalkSlots][kWalkWin];  // decision-word windows of upcoming chunks
+      int rs[kMaxRows + 2 * kWave];        // row_start under construction
+    } walk;
+  } u;
   float ring[kWavesPerBlock - 1][kRing][kChunk];  // wave w -> w+1 boundary values
+  uint64_t poll[kPollSlots][2 * kWave];           // polled boundary words (4 copies of 32)
   f32x4 bout[kWavesPerBlock][kChunk / 4];         // boundary staging (global hand-off)
+  uint32_t dummy[kWavesPerBlock][kWave];          // target of placeholder loads
   int prod[kWavesPerBlock];                       // chunks wave w has published (exclusive end)
   int cons[kWavesPerBlock];                       // next chunk wave w will consume
-  uint32_t blk[kWalkChunks][kWalkRows];           // decision words of the walk block
 };
 
-// Dynamic LDS: the walker's row_start table (T + 128 ints).
-extern __shared__ int mas_rs_lds[];
+// ---------------------------------------------------------------- path clearing
+// The bytes [p0, p1) of the path that one wave clears: its 64 rows of its
+// item.  16-byte aligned pieces [a0, a1) go through the sweep schedule; the
+// unaligned head and tail are cleared up front with byte stores.
+struct ZeroPlan {
+  uint64_t a0;    // address of the first aligned piece
+  uint64_t last;  // address of the last aligned piece (a1 - 16)
+  bool any;       // at least one aligned piece
+};
 
-// ---------------------------------------------------------------- zero fill
-// Zero workgroup z writes its share of the whole path with device-scope
-// stores, then publishes the call's tag in zprog[z].
-__device__ __forceinline__ void zero_block(const KParams& p, int z, uint32_t tag) {
-  const size_t total = (size_t)p.B * (size_t)p.T * (size_t)p.S;
-  const size_t nthr = (size_t)p.NZ * blockDim.x;
-  const size_t t0 = (size_t)z * blockDim.x + threadIdx.x;
-  if (p.path16) {
-    uint64_t* q = reinterpret_cast<uint64_t*>(p.path);
-    const size_t n = total / 8;
-    for (size_t k = t0; k < n; k += nthr) st_dev(q + k, 0ull);
-  } else {
-    for (size_t k = t0; k < total; k += nthr) __hip_atomic_store(p.path + k, (uint8_t)0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-  }
-  wait_mem();
-  __syncthreads();
-  if (threadIdx.x == 0) st_dev(p.zprog + z, (uint64_t)tag);
+__device__ __forceinline__ ZeroPlan zero_plan(const KParams& p, int b, int g, int lane) {
+  const uint64_t base = (uint64_t)b * (uint64_t)p.T * (uint64_t)p.S;  // offsets from p.path
+  const int r0 = min(g * kWave, p.T), r1 = min(g * kWave + kWave, p.T);
+  const uint64_t p0 = base + (uint64_t)r0 * (uint64_t)p.S, p1 = base + (uint64_t)r1 * (uint64_t)p.S;
+  const uint64_t pa = (uint64_t)(uintptr_t)p.path;
+  const uint64_t a0 = ((pa + p0 + 15) & ~15ull) - pa, a1 = ((pa + p1) & ~15ull) - pa;
+  ZeroPlan z;
+  z.any = a1 > a0 && a1 - a0 >= 16;
+  z.a0 = pa + a0;
+  z.last = pa + a1 - 16;
+  // Unaligned head and tail bytes (at most 15 + 15; all bytes if no piece).
+  const uint64_t h1 = z.any ? a0 : p1;
+  for (uint64_t o = p0 + lane; o < h1; o += kWave) st_dev(p.path + o, (uint8_t)0);
+  if (z.any)
+    for (uint64_t o = a1 + lane; o < p1; o += kWave) st_dev(p.path + o, (uint8_t)0);
+  return z;
+}
+
+// Clears the aligned pieces from address `from` to the last one with 1 KiB
+// stores (outside the sweep schedule).
+__device__ __forceinline__ void zero_rest(const ZeroPlan& z, uint64_t from, int lane) {
+  const u32x4 zero = {0u, 0u, 0u, 0u};
+  for (uint64_t a = from + 16u * (uint64_t)lane; a <= z.last; a += 16u * kWave) vm_zero1(a, zero);
 }
 
 // ---------------------------------------------------------------- sweep
 // Per-wave constants of the sweep.
 struct WaveCtx {
   int lane, wv, b, g, g_last, tx, ty, row, c_begin, c_end, out_mode;
-  __amdgpu_buffer_rsrc_t rsrc;
-  int voff[8];  // byte offset of this lane's piece of load q in chunk 0
-  int col0[8];  // its first column in chunk 0
-  uint32_t* decp;
-  const uint64_t* poll_base;
-  uint64_t* slots_out;
+  int prev_end;                     // chunks the previous wave computes (exclusive end)
+  bool zero;                        // this wave clears its path rows during its steps
+  const float* slab;                // the item's value slab [T][S]
+  uint64_t slab_bytes;
+  uint64_t row_off;                 // byte offset of this wave's first row in the slab
+  const uint64_t* pslots;           // the previous wave's boundary words (IN == 2)
+  uint64_t pslot_bytes;
+  int voff[8];                      // per-lane byte offsets of the tile loads
+  uint32_t tile0;                   // LDS offset of this wave's tile slot 0
+  uint32_t dummy;                   // LDS offset of this wave's placeholder area
+  uint64_t decp;                    // &dec[b][0][row]
+  uint64_t slotp;                   // &slots[b][g][lane % 32] (boundary words out)
+  ZeroPlan zp;
 };
 
-// Sweeps this wave's 64 rows over all chunks of its item and returns the
-// score candidate (Q at (row, t_y-1) of this lane; only meaningful for the
-// wave holding row t_x-1).  IN: where the row above the wave comes from —
-// 0 nowhere (the wave holds row 0), 1 the LDS ring of the previous wave of
-// the workgroup, 2 global hand-off words of the previous workgroup.
-// out_mode: 0 no consumer, 1 LDS ring, 2 global hand-off words.
+// Chunks of wave g worth computing: from the first chunk holding a cell with
+// i <= j of its rows, to the last chunk holding a cell of its rows that can
+// still reach (t_x-1, t_y-1) (a path descends at most one row per column, so
+// row r is useful up to column r + t_y - t_x).  Cells outside only feed
+// cells outside (a reachable cell's two predecessors are reachable), so
+// whatever they hold never reaches a decision the walk reads or the score.
+__device__ __forceinline__ int chunk_end(int g, int tx, int ty) {
+  const int by_len = (ty + kChunk - 1) / kChunk;
+  const int by_reach = (g * kWave + kWave - 1 + ty - tx) / kChunk + 1;
+  return by_len < by_reach ? by_len : by_reach;
+}
+
+// Sweeps this wave's 64 rows over its chunks and returns the score candidate
+// (Q at (row, t_y-1) of this lane; only meaningful for the wave holding row
+// t_x-1).  IN: where the row above the wave comes from — 0 nowhere (the wave
+// holds row 0), 1 the LDS ring of the previous wave of the workgroup, 2
+// global boundary words of the previous workgroup.  out_mode: 0 no
+// consumer, 1 LDS ring, 2 global boundary words.
 template <bool ALIGNED, int IN>
 __device__ __forceinline__ float sweep_rows(const KParams& p, SweepLds& L, const WaveCtx& x, uint32_t tag, bool& timed_out) {
+  constexpr int NL = ALIGNED ? 8 : 32;
+  constexpr bool IN2 = IN == 2;
   const int lane = x.lane, wv = x.wv;
+  const bool h = x.out_mode == 2, zero = x.zero;
   float q = neg_inf();
   float diag = neg_inf();  // lane 0 keeps -inf when IN == 0
   float score = neg_inf();
+  const u32x4 zv = {0u, 0u, 0u, 0u};
+  const int dvo = 4 * lane;  // placeholder loads read the slab's first 256 bytes
+  const __amdgpu_buffer_rsrc_t drsrc = sub_rsrc(x.slab, x.slab_bytes, 0);
 
-  // Global boundary words (IN == 2), polled two chunks ahead into a ring of
-  // three registers that follows the three value buffers; waiting for a poll
-  // then only waits for stores issued three chunks earlier.  Every lane loads
-  // (lanes 32..63 repeat lanes 0..31) so the loads stay outside divergent
-  // control flow.
-  uint64_t bwa = 0, bwb = 0, bwc = 0;
-  auto poll_issue = [&](uint64_t& bw, int c) __attribute__((always_inline)) {
-    const int cc = c < x.c_end ? c : x.c_end - 1;  // past the end: re-read valid words
-    bw = ld_dev(x.poll_base + (size_t)cc * kChunk);
+  // Tile of chunk c into its slot.
+  auto issue_tile = [&](int c) __attribute__((always_inline)) {
+    const uint32_t dst = x.tile0 + (uint32_t)((c & (kStages - 1)) * 8 * kWave * 16);
+    const uint64_t off = x.row_off + (uint64_t)c * (kChunk * 4);
+    if (ALIGNED) {
+      dma_tile16(dst, sub_rsrc(x.slab, x.slab_bytes, off), x.voff);
+    } else {
+      // Four groups of 8 loads; group hh covers tile rows 16hh .. 16hh+15.
+#pragma unroll
+      for (int hh = 0; hh < 4; ++hh)
+        dma_words8(dst + hh * 2048, sub_rsrc(x.slab, x.slab_bytes, off + (uint64_t)hh * 16u * (uint64_t)p.S * 4u), x.voff);
+    }
   };
-  auto poll_wait = [&](uint64_t& bw, int c) __attribute__((always_inline)) {
-    if (__builtin_amdgcn_ballot_w64((uint32_t)(bw >> 32) != tag) == 0) return;
-    int spins = 0;
-    do {
-      if (++spins > kSpinLimit) {
-        timed_out = true;
-        return;
-      }
-      __builtin_amdgcn_s_sleep(1);
-      poll_issue(bw, c);
-    } while (__builtin_amdgcn_ballot_w64((uint32_t)(bw >> 32) != tag) != 0);
+  // Boundary words of chunk c (32 u64 = 256 bytes, 4 copies) into poll slot c % 4.
+  const int pvo = 16 * (lane & 15);
+  auto issue_poll = [&](int c) __attribute__((always_inline)) {
+    dma_poll(lds_off(&L.poll[c & (kPollSlots - 1)][0]), sub_rsrc(x.pslots, x.pslot_bytes, (uint64_t)c * kChunk * 8u), pvo);
   };
-  if (IN == 2) {
-    poll_issue(bwa, x.c_begin);
-    poll_issue(bwb, x.c_begin + 1);
+  int zk = 0;  // zero steps issued
+  auto issue_zero = [&]() __attribute__((always_inline)) {
+    if (zero) {
+      uint64_t a0 = x.zp.a0 + (uint64_t)zk * 2048u + 16u * (uint64_t)lane;
+      uint64_t a1 = a0 + 1024u;
+      a0 = a0 < x.zp.last ? a0 : x.zp.last;
+      a1 = a1 < x.zp.last ? a1 : x.zp.last;
+      vm_zero2(a0, a1, zv);
+      ++zk;
+    }
+  };
+
+  // Pieces beyond what the steps will clear, up front.
+  if (zero) zero_rest(x.zp, x.zp.a0 + (uint64_t)(kDepth + x.c_end - x.c_begin) * 2048u, lane);
+
+  // Prologue: kDepth placeholder steps with the steady-state operation
+  // sequence, so that the loop's wait counts hold from its first step.
+  for (int c = x.c_begin - kDepth; c < x.c_begin; ++c) {
+    if (IN2) issue_poll(c + 2);  // chunks c_begin-1 .. c_begin+1
+    issue_tile(c + kDepth);
+    dma_dummy(x.dummy, drsrc, dvo);
+    if (h) dma_dummy(x.dummy, drsrc, dvo);
+    issue_zero();
   }
 
-  // bw: this chunk's polled words; bw2: the register chunk c+2 will check.
   const int rsw = swz(lane);
-  int prod_seen = 0;                    // last value read of the producer's counter
-  int cons_seen = x.c_begin + 2;        // last value read of the consumer's counter
-  uint32_t bits_prev = 0;               // decision word of the previous chunk (stored one step late)
-  auto step = [&](int c, const f32x4 (&stg)[8], uint64_t& bw, uint64_t& bw2) __attribute__((always_inline)) {
-    // Transpose the chunk's tile through LDS: this lane's row, 32 values.
-#pragma unroll
-    for (int k = 0; k < 8; ++k) L.tile[wv][64 * k + lane] = stg[k];
-    wave_lds_sync();
+  int prod_seen = 0;               // last value read of the producer's counter
+  int cons_seen = x.c_begin + 2;   // last value read of the consumer's counter
+  for (int c = x.c_begin; c < x.c_end; ++c) {
+    wait_step<NL, IN2>(h, zero);
+    if (IN2) issue_poll(c + 2);
+    issue_tile(c + kDepth);
+
+    // This lane's row of the chunk, 32 values.
     f32x4 v[8];
+    {
+      const f32x4* t = L.u.tile[wv][c & (kStages - 1)];
 #pragma unroll
-    for (int k = 0; k < 8; ++k) v[k] = L.tile[wv][8 * lane + (k ^ rsw)];
-    // Boundary column values bd[m] = Q[row0-1][j0-1+m].
+      for (int k = 0; k < 8; ++k) v[k] = t[8 * lane + (k ^ rsw)];
+    }
+    // Boundary column values bd[m] = Q[row0-1][j0-1+m].  The previous wave
+    // computes chunks below prev_end; past them its row cannot reach the end,
+    // so -inf stands in (bd[0] of chunk prev_end is its last real value).
     float bd[kChunk];
     if (IN == 1) {
+      const int need = c < x.prev_end ? c + 1 : x.prev_end;
       int spins = 0;
-      while (prod_seen <= c) {
+      while (prod_seen < need) {
         prod_seen = lds_load(&L.prod[wv - 1]);
-        if (prod_seen > c) break;
+        if (prod_seen >= need) break;
         if (++spins > kSpinLimit) {
           timed_out = true;
           break;
@@ -312,24 +517,43 @@ __device__ __forceinline__ float sweep_rows(const KParams& p, SweepLds& L, const
       }
       wave_lds_sync();
       const float* cur = L.ring[wv - 1][c % kRing];
-      bd[0] = L.ring[wv - 1][(c + kRing - 1) % kRing][kChunk - 1];
+      bd[0] = c <= x.prev_end ? L.ring[wv - 1][(c + kRing - 1) % kRing][kChunk - 1] : neg_inf();
+      if (c < x.prev_end) {
 #pragma unroll
-      for (int m = 1; m < kChunk; ++m) bd[m] = cur[m - 1];
+        for (int m = 1; m < kChunk; ++m) bd[m] = cur[m - 1];
+      } else {
+#pragma unroll
+        for (int m = 1; m < kChunk; ++m) bd[m] = neg_inf();
+      }
       wave_lds_sync();
       if (lane == 0) lds_store(&L.cons[wv], c + 1);
     } else if (IN == 2) {
-      poll_wait(bw, c);
-      reinterpret_cast<float*>(L.bout[wv])[lane & (kChunk - 1)] = __uint_as_float((uint32_t)bw);
+      // Lanes 0..31: word m of chunk c; lane 32: word 31 of chunk c-1.
+      const int wsl = lane < 32 ? (c & (kPollSlots - 1)) : ((c - 1) & (kPollSlots - 1));
+      const int wix = lane < 32 ? lane : kChunk - 1;
+      const bool check = lane < 32 ? c < x.prev_end : (lane == 32 && c <= x.prev_end);
+      uint64_t wd = L.poll[wsl][wix];
+      int spins = 0;
+      while (__builtin_amdgcn_ballot_w64(check && (uint32_t)(wd >> 32) != tag) != 0) {
+        if (++spins > kSpinLimit) {
+          timed_out = true;
+          break;
+        }
+        __builtin_amdgcn_s_sleep(1);
+        issue_poll(c - 1);
+        issue_poll(c);
+        vm_wait<0>();
+        wd = L.poll[wsl][wix];
+      }
+      // bd[0] = word 31 of chunk c-1 (lane 32), bd[m] = word m-1 of chunk c.
+      const float val = check ? __uint_as_float((uint32_t)wd) : neg_inf();
+      bd[0] = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(val), 32));
+      float* bf = reinterpret_cast<float*>(L.bout[wv]);
+      if (lane < kChunk) bf[lane] = val;
       wave_lds_sync();
 #pragma unroll
-      for (int k = 0; k < kChunk / 4; ++k) {
-        const f32x4 t = L.bout[wv][k];
-        bd[4 * k + 0] = t.x;
-        bd[4 * k + 1] = t.y;
-        bd[4 * k + 2] = t.z;
-        bd[4 * k + 3] = t.w;
-      }
-      poll_issue(bw2, c + 2);
+      for (int m = 1; m < kChunk; ++m) bd[m] = bf[m - 1];
+      wave_lds_sync();
     }
     wave_lds_sync();
     float qc[kChunk];
@@ -338,8 +562,9 @@ __device__ __forceinline__ float sweep_rows(const KParams& p, SweepLds& L, const
       sweep_chunk<true, IN == 0>(q, diag, v, bd, qc, bits, x.row, c * kChunk);
     else
       sweep_chunk<false, IN == 0>(q, diag, v, bd, qc, bits, x.row, c * kChunk);
-    if (c > x.c_begin) st_dev(x.decp + (size_t)(c - 1) * p.TP, bits_prev);
-    bits_prev = bits;
+
+    // Stores of the step: decision word, boundary words, path zeros.
+    vm_store32(x.decp + (uint64_t)c * (uint64_t)p.TP * 4u, bits);
     if (x.out_mode == 1) {
       // Wait until the consumer no longer needs the ring slot, then publish.
       int spins = 0;
@@ -359,7 +584,7 @@ __device__ __forceinline__ float sweep_rows(const KParams& p, SweepLds& L, const
       }
       wave_lds_sync();
       if (lane == 0) lds_store(&L.prod[wv], c + 1);
-    } else if (x.out_mode == 2) {
+    } else if (h) {
       if (lane == kWave - 1) {
 #pragma unroll
         for (int k = 0; k < kChunk / 4; ++k) L.bout[wv][k] = f32x4{qc[4 * k], qc[4 * k + 1], qc[4 * k + 2], qc[4 * k + 3]};
@@ -367,36 +592,35 @@ __device__ __forceinline__ float sweep_rows(const KParams& p, SweepLds& L, const
       wave_lds_sync();
       const float val = reinterpret_cast<const float*>(L.bout[wv])[lane & (kChunk - 1)];
       const uint64_t word = ((uint64_t)tag << 32) | (uint64_t)__float_as_uint(val);
-      st_dev(x.slots_out + (size_t)c * kChunk + (lane & (kChunk - 1)), word);
+      vm_store64(x.slotp + (uint64_t)c * kChunk * 8u, word);
       wave_lds_sync();
     }
+    issue_zero();
     if (x.g == x.g_last && c == x.c_end - 1) {
       const int m_last = (x.ty - 1) % kChunk;
 #pragma unroll
       for (int m = 0; m < kChunk; ++m) score = (m == m_last) ? qc[m] : score;
     }
-  };
-
-  // Three chunks of values in flight; loads past the last chunk read
-  // nothing (out of range).  Full triples first: every iteration issues the
-  // same memory operations, so wait counts stay exact.
-  f32x4 va[8], vbk[8], vc[8];
-  TileLoader<ALIGNED>::load(va, x.rsrc, x.voff, x.col0, x.ty, x.c_begin);
-  TileLoader<ALIGNED>::load(vbk, x.rsrc, x.voff, x.col0, x.ty, x.c_begin + 1);
-  TileLoader<ALIGNED>::load(vc, x.rsrc, x.voff, x.col0, x.ty, x.c_begin + 2);
-  int c = x.c_begin;
-  for (; c + 2 < x.c_end; c += 3) {
-    step(c, va, bwa, bwc);
-    TileLoader<ALIGNED>::load(va, x.rsrc, x.voff, x.col0, x.ty, c + 3);
-    step(c + 1, vbk, bwb, bwa);
-    TileLoader<ALIGNED>::load(vbk, x.rsrc, x.voff, x.col0, x.ty, c + 4);
-    step(c + 2, vc, bwc, bwb);
-    TileLoader<ALIGNED>::load(vc, x.rsrc, x.voff, x.col0, x.ty, c + 5);
   }
-  if (c < x.c_end) step(c, va, bwa, bwc);
-  if (c + 1 < x.c_end) step(c + 1, vbk, bwb, bwa);
-  st_dev(x.decp + (size_t)(x.c_end - 1) * p.TP, bits_prev);
+  vm_wait<0>();
   return score;
+}
+
+// Waits (bounded) until flag[k] == tag for every k in [0, n).
+__device__ __forceinline__ void wait_flags(const uint32_t* flag, int n, uint32_t tag, int lane, bool& timed_out) {
+  for (int k0 = 0; k0 < n; k0 += kWave) {
+    const int k = k0 + lane;
+    int spins = 0;
+    while (true) {
+      const bool ready = k >= n || ld_dev(flag + k) == tag;
+      if (__builtin_amdgcn_ballot_w64(!ready) == 0) break;
+      if (++spins > kSpinLimit) {
+        timed_out = true;
+        break;
+      }
+      __builtin_amdgcn_s_sleep(1);
+    }
+  }
 }
 
 template <bool ALIGNED>
@@ -420,7 +644,12 @@ __device__ __forceinline__ void sweep_block(const KParams& p, SweepLds& L, int s
   __syncthreads();
 
   int32_t* rs_out = p.row_start + (size_t)b * ((size_t)p.T + 1);
+  const bool has_rows = g * kWave < p.T;
+  ZeroPlan zp{};
+  if (p.path && has_rows) zp = zero_plan(p, b, g, lane);
+  const bool clear = p.path && has_rows && zp.any;
   if (st != kItemOk) {
+    if (clear) zero_rest(zp, zp.a0, lane);
     if (g == 0) {
       for (int i = lane; i <= p.T; i += kWave) rs_out[i] = 0;
       if (lane == 0) {
@@ -430,7 +659,19 @@ __device__ __forceinline__ void sweep_block(const KParams& p, SweepLds& L, int s
     }
     return;
   }
-  if (g * kWave >= tx) return;  // no rows of this item here
+  const int g_last = (tx - 1) / kWave;
+  if (g > g_last) {
+    // No rows of the alignment here: clear the path rows once the item's
+    // sweep is over (the HBM is less busy then).
+    if (clear) {
+      if (lane == 0) {
+        int spins = 0;
+        while (ld_dev(p.done + (size_t)b * p.NW + g_last) != tag && ++spins <= kSpinLimit) __builtin_amdgcn_s_sleep(8);
+      }
+      zero_rest(zp, zp.a0, lane);
+    }
+    return;
+  }
   if (g == 0 && lane == 0 && p.status) p.status[b] = kItemOk;
 
   WaveCtx x;
@@ -438,186 +679,159 @@ __device__ __forceinline__ void sweep_block(const KParams& p, SweepLds& L, int s
   x.wv = wv;
   x.b = b;
   x.g = g;
-  x.g_last = (tx - 1) / kWave;
+  x.g_last = g_last;
   x.tx = tx;
   x.ty = ty;
   x.row = g * kWave + lane;
   x.c_begin = c_begin;
-  x.c_end = (ty + kChunk - 1) / kChunk;
-  x.out_mode = g == x.g_last ? 0 : (wv < kWavesPerBlock - 1 ? 1 : 2);
-  x.rsrc = slab_rsrc(p.value + (size_t)b * (size_t)p.T * (size_t)p.S, p.T, p.S);
-#pragma unroll
-  for (int q = 0; q < 8; ++q) {
-    const int tr = 8 * q + (lane >> 3);
-    const int pc = (lane & 7) ^ swz(tr);
-    const int trow = g * kWave + tr;
-    x.col0[q] = 4 * pc;
-    x.voff[q] = trow < tx ? (trow * p.S + 4 * pc) * 4 : kOob;
-  }
-  x.decp = p.dec + (size_t)b * p.NC * (size_t)p.TP + x.row;
+  x.c_end = chunk_end(g, tx, ty);
+  x.prev_end = g > 0 ? chunk_end(g - 1, tx, ty) : 0;
+  x.out_mode = g == g_last ? 0 : (wv < kWavesPerBlock - 1 ? 1 : 2);
+  // The walker's wave clears its rows during its steps; the others after.
+  x.zero = clear && g == g_last;
+  x.zp = zp;
+  x.slab = p.value + (size_t)b * (size_t)p.T * (size_t)p.S;
+  x.slab_bytes = (uint64_t)p.T * (uint64_t)p.S * 4u;
+  x.row_off = (uint64_t)g * kWave * (uint64_t)p.S * 4u;
   const size_t slot_stride = (size_t)p.NC * kChunk;
-  x.poll_base = p.slots + ((size_t)b * p.NW + (g > 0 ? g - 1 : 0)) * slot_stride + (lane & (kChunk - 1)) - 1;
-  x.slots_out = p.slots + ((size_t)b * p.NW + g) * slot_stride;
-  const int g_last = x.g_last;
+  x.pslots = p.slots + ((size_t)b * p.NW + (g > 0 ? g - 1 : 0)) * slot_stride;
+  x.pslot_bytes = slot_stride * 8u;
+  // Offsets relative to the wave's first row at the chunk's first column;
+  // rows past the slab fall outside the resource and read 0.  Tile rows
+  // below 64 and S * 4 * 64 < 2^31 keep them in range of an int.
+  if (ALIGNED) {
+    // Load q: lane L reads tile row 8q + L/8, piece (L%8) ^ swz(row).
+#pragma unroll
+    for (int q = 0; q < 8; ++q) {
+      const int tr = 8 * q + (lane >> 3);
+      const int pc = (lane & 7) ^ swz(tr);
+      x.voff[q] = (tr * p.S + 4 * pc) * 4;
+    }
+  } else {
+    // Load k of group hh: lane L writes LDS word 64k + L of the group, i.e.
+    // tile row 16hh + 2k + L/32, slot (L%32)/4, word L%4 (swz has period 16).
+#pragma unroll
+    for (int k = 0; k < 8; ++k) {
+      const int tr = 2 * k + (lane >> 5);
+      const int pc = ((lane & 31) >> 2) ^ swz(tr);
+      x.voff[k] = (tr * p.S + 4 * pc + (lane & 3)) * 4;
+    }
+  }
+  x.tile0 = lds_off(&L.u.tile[wv][0][0]);
+  x.dummy = lds_off(&L.dummy[wv][0]);
+  x.decp = (uint64_t)(uintptr_t)(p.dec + (size_t)b * p.NC * (size_t)p.TP + x.row);
+  x.slotp = (uint64_t)(uintptr_t)(p.slots + ((size_t)b * p.NW + g) * slot_stride + (lane & (kChunk - 1)));
   const float score = g == 0 ? sweep_rows<ALIGNED, 0>(p, L, x, tag, timed_out)
                              : (wv > 0 ? sweep_rows<ALIGNED, 1>(p, L, x, tag, timed_out)
                                        : sweep_rows<ALIGNED, 2>(p, L, x, tag, timed_out));
 
   // Publish this wave's decision words to the item's walker.
-  wait_mem();
   if (lane == 0) st_dev(p.done + (size_t)b * p.NW + g, tag);
-  if (g != g_last) return;
+  if (g != g_last) {
+    // Then clear this wave's path rows, and say so.
+    if (clear) {
+      zero_rest(zp, zp.a0, lane);
+      asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+      if (lane == 0) st_dev(p.zdone + (size_t)b * p.NW + g, tag);
+    }
+    return;
+  }
 
   // ------------------------------------------------------------ backtrack
   if (lane == ((tx - 1) & (kWave - 1)) && p.score) p.score[b] = score;
-  for (int k0 = 0; k0 < g_last; k0 += kWave) {
-    const int k = k0 + lane;
-    int spins = 0;
-    while (true) {
-      const bool ready = k >= g_last || ld_dev(p.done + (size_t)b * p.NW + k) == tag;
-      if (__builtin_amdgcn_ballot_w64(!ready) == 0) break;
-      if (++spins > kSpinLimit) {
-        timed_out = true;
-        break;
-      }
-      __builtin_amdgcn_s_sleep(1);
-    }
-  }
-
-  // Walk blocks of kWalkChunks chunks from the right.  Within a block the
-  // path descends at most 32 * kWalkChunks rows, and a chunk reads rows down
-  // to 32 below its entry row, so every row block n+2 reads lies within
-  // 3 * 32 * kWalkChunks + 1 (<= kWalkRows) rows below the entry row of
-  // block n: block n+2's words (rows [e - kWalkRows + 1, e] of each of its
-  // chunks, e = entry row of block n) are fetched while block n is walked.
+  wait_flags(p.done + (size_t)b * p.NW, g_last, tag, lane, timed_out);
+  // Every sweep of this workgroup has finished (lower waves: flags above;
+  // higher waves hold no rows of the alignment), so the tile area is free.
+  int* rsl = L.u.walk.rs;
   const uint32_t* db = p.dec + (size_t)b * p.NC * (size_t)p.TP;
-  auto fetch = [&](uint32_t (&w)[kWalkChunks][kWalkRows / kWave], int cb, int e) __attribute__((always_inline)) {
+  const uint64_t chunk_bytes = (uint64_t)p.TP * 4u;
+  int wvo[5];
 #pragma unroll
-    for (int k = 0; k < kWalkChunks; ++k) {
-      const int ch = cb - k;
-      const size_t base = (size_t)(ch > 0 ? ch : 0) * p.TP;
-#pragma unroll
-      for (int i = 0; i < kWalkRows / kWave; ++i) {
-        const int r = e - (kWalkRows - 1) + i * kWave + lane;  // rows ascending
-        w[k][i] = ld_dev(db + base + (r > 0 ? r : 0));
-      }
+  for (int k = 0; k < 5; ++k) wvo[k] = 4 * lane + 256 * k;
+  int wlo = 0;  // lane s: first row of the window in ring slot s
+  // Window of chunk ch: rows [e - kWalkWin + 1, e] (clamped at row 0) into
+  // slot ch % kWalkSlots; placeholders for chunks before the first.
+  auto issue_win = [&](int ch, int e) __attribute__((always_inline)) {
+    const int slot = ch & (kWalkSlots - 1);
+    const int lo = max(e - kWalkWin + 1, 0);
+    wlo = lane == slot ? lo : wlo;
+    const uint32_t dst = lds_off(&L.u.walk.win[slot][0]);
+    if (ch >= 0) {
+      dma_words5(dst, sub_rsrc(db + (size_t)ch * p.TP, chunk_bytes, (uint64_t)lo * 4u), wvo);
+    } else {
+      dma_words5(dst, sub_rsrc(db, chunk_bytes, chunk_bytes), wvo);  // empty resource: reads 0
     }
-  };
-  auto stage = [&](const uint32_t (&w)[kWalkChunks][kWalkRows / kWave]) __attribute__((always_inline)) {
-#pragma unroll
-    for (int k = 0; k < kWalkChunks; ++k)
-#pragma unroll
-      for (int i = 0; i < kWalkRows / kWave; ++i) L.blk[k][i * kWave + lane] = w[k][i];
   };
   int idx = tx - 1;                  // entry row of the chunk being walked
   int cw = (ty - 1) / kChunk;        // chunk being walked
   int sh0 = 31 - (ty - 1) % kChunk;  // bits >= sh0 are columns not yet passed in chunk cw
+  for (int k = 0; k < kWalkAhead; ++k) issue_win(cw - k, idx);
   bool walking = idx > 0;
-  // Walks the kWalkChunks chunks staged in L.blk (rows [eb - kWalkRows + 1,
-  // eb] of chunks cb, cb-1, ...); clears `walking` when the walk is over.
-  auto walk_block = [&](int eb) __attribute__((always_inline)) {
-    for (int k = 0; k < kWalkChunks && walking; ++k) {
-      // Window of this chunk: lane l holds the word of row idx - l.
-      const int wr = idx - lane - (eb - (kWalkRows - 1));
-      const uint32_t W = L.blk[k][wr > 0 ? wr : 0];
-      int kk = 0, sh = sh0;
-      uint32_t pm = 0;  // bit p set: the kk-th recorded row starts at column 32cw + 31 - p
-      while (true) {
-        const uint32_t w = __builtin_amdgcn_readlane(W, kk);
-        const uint64_t t = (uint64_t)w & (~0ull << sh);
-        if (t == 0) break;  // the row continues left of this chunk (row 0 never steps)
-        const int pos = __builtin_ctzll(t);
-        pm |= 1u << pos;
-        sh = pos + 1;
-        kk += 1;
-      }
-      // Scatter: set bit p of pm belongs to the row (popcount of pm below p) under idx.
-      if (lane < kChunk && ((pm >> lane) & 1u))
-        mas_rs_lds[idx - (int)__builtin_popcount(pm & ((1u << lane) - 1u))] = cw * kChunk + 31 - lane;
-      idx -= kk;
-      sh0 = 0;
-      cw -= 1;
-      walking = idx > 0 && cw >= 0;
+  while (walking) {
+    vm_wait<5 * (kWalkAhead - 1)>();  // window of chunk cw (issued kWalkAhead chunks ago)
+    issue_win(cw - kWalkAhead, idx);
+    // Lane l holds the word of row idx - l.
+    const int slot = cw & (kWalkSlots - 1);
+    const int lo = __builtin_amdgcn_readlane(wlo, slot);
+    const int wr = idx - lane - lo;
+    const uint32_t W = L.u.walk.win[slot][wr > 0 ? wr : 0];
+    int kk = 0, sh = sh0;
+    uint32_t pm = 0;  // bit p set: the kk-th recorded row starts at column 32cw + 31 - p
+    while (true) {
+      const uint32_t w = __builtin_amdgcn_readlane(W, kk);
+      const uint64_t t = (uint64_t)w & (~0ull << sh);
+      if (t == 0) break;  // the row continues left of this chunk (row 0 never steps)
+      const int pos = __builtin_ctzll(t);
+      pm |= 1u << pos;
+      sh = pos + 1;
+      kk += 1;
     }
-  };
-  {
-    uint32_t wa[kWalkChunks][kWalkRows / kWave], wb[kWalkChunks][kWalkRows / kWave];
-    fetch(wa, cw, idx);
-    fetch(wb, cw - kWalkChunks, idx);
-    int ea = idx, eb_ = idx;  // band tops of the blocks held in wa / wb
-    while (walking) {
-      wave_lds_sync();
-      stage(wa);
-      wave_lds_sync();
-      const int e0 = idx;
-      fetch(wa, cw - 2 * kWalkChunks, e0);
-      walk_block(ea);
-      ea = e0;
-      if (!walking) break;
-      wave_lds_sync();
-      stage(wb);
-      wave_lds_sync();
-      const int e1 = idx;
-      fetch(wb, cw - 2 * kWalkChunks, e1);
-      walk_block(eb_);
-      eb_ = e1;
-    }
+    // Scatter: set bit p of pm belongs to the row (popcount of pm below p) under idx.
+    if (lane < kChunk && ((pm >> lane) & 1u)) rsl[idx - (int)__builtin_popcount(pm & ((1u << lane) - 1u))] = cw * kChunk + 31 - lane;
+    idx -= kk;
+    sh0 = 0;
+    cw -= 1;
+    walking = idx > 0 && cw >= 0;
   }
+  vm_wait<0>();  // no window load may land in LDS after this wave ends
   wave_lds_sync();
-  if (lane == 0) mas_rs_lds[0] = 0;
-  for (int i = tx + lane; i <= p.T; i += kWave) mas_rs_lds[i] = ty;
+  if (lane == 0) rsl[0] = 0;
+  for (int i = tx + lane; i <= p.T; i += kWave) rsl[i] = ty;
   wave_lds_sync();
-  for (int i = lane; i <= p.T; i += kWave) rs_out[i] = mas_rs_lds[i];
+  for (int i = lane; i <= p.T; i += kWave) rs_out[i] = rsl[i];
 
   if (!p.path) return;
-  // Ones of the item's path, once the zero fill has finished.
-  for (int z0 = 0; z0 < p.NZ; z0 += kWave) {
-    const int z = z0 + lane;
-    int spins = 0;
-    while (true) {
-      const bool ready = z >= p.NZ || (uint32_t)ld_dev(p.zprog + z) == tag;
-      if (__builtin_amdgcn_ballot_w64(!ready) == 0) break;
-      if (++spins > kSpinLimit) {
-        timed_out = true;
-        break;
-      }
-      __builtin_amdgcn_s_sleep(2);
-    }
-  }
+  // Ones of the item's path, once every wave holding rows below t_x has
+  // cleared its rows (this wave cleared its own during its steps).
+  wait_flags(p.zdone + (size_t)b * p.NW, g_last, tag, lane, timed_out);
   uint8_t* pb = p.path + (size_t)b * (size_t)p.T * (size_t)p.S;
   for (int i = lane; i < tx; i += kWave) {
-    const int lo = mas_rs_lds[i], hi = mas_rs_lds[i + 1];
+    const int lo = rsl[i], hi = rsl[i + 1];
     uint8_t* prow = pb + (size_t)i * (size_t)p.S;
     if (p.path16) {
       for (int j0 = lo & ~15; j0 < hi; j0 += 16) {
-        const uint4 x = path_piece(lo, hi, j0);
+        const uint4 pc = path_piece(lo, hi, j0);
         uint64_t* d = reinterpret_cast<uint64_t*>(prow + j0);
-        st_dev(d, ((uint64_t)x.y << 32) | x.x);
-        st_dev(d + 1, ((uint64_t)x.w << 32) | x.z);
+        st_dev(d, ((uint64_t)pc.y << 32) | pc.x);
+        st_dev(d + 1, ((uint64_t)pc.w << 32) | pc.z);
       }
     } else {
-      for (int j = lo; j < hi; ++j) __hip_atomic_store(prow + j, (uint8_t)1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      for (int j = lo; j < hi; ++j) st_dev(prow + j, (uint8_t)1);
     }
   }
 }
 
 template <bool ALIGNED>
-// Two waves per SIMD: a sweep workgroup and a zero-fill workgroup share a CU.
-__global__ void __launch_bounds__(kRowsPerBlock, 2) mas_kernel(KParams p) {
+// One workgroup per CU: the value-tile ring takes most of the LDS.
+__global__ void __launch_bounds__(kRowsPerBlock, 1) mas_kernel(KParams p) {
   __shared__ SweepLds L;
   const uint32_t gen = __hip_atomic_load(&p.hdr->gen, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   const uint32_t tag = call_tag(gen);
   bool timed_out = false;
-  int item = -1;
-  if ((int)blockIdx.x < p.NZ) {
-    zero_block(p, blockIdx.x, tag);
-  } else {
-    const int sid = blockIdx.x - p.NZ;
-    item = sid % p.B;
-    sweep_block<ALIGNED>(p, L, sid, tag, timed_out);
-  }
+  const int item = (int)blockIdx.x % p.B;
+  sweep_block<ALIGNED>(p, L, blockIdx.x, tag, timed_out);
   if (timed_out) {
-    if (p.status && item >= 0) p.status[item] = kItemSyncTimeout;
+    if (p.status) p.status[item] = kItemSyncTimeout;
     __hip_atomic_store(&p.hdr->error, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   }
   // The last wave of the call to finish advances the generation.
@@ -670,12 +884,11 @@ __global__ void __launch_bounds__(256) mas_zero_kernel(uint4* __restrict__ p, si
 
 // ---------------------------------------------------------------- launchers
 hipError_t launch_mas(const KParams& p, bool aligned, hipStream_t stream) {
-  const dim3 grid((unsigned)(p.NZ + p.B * p.NB)), block(kRowsPerBlock);
-  const size_t lds = ((size_t)p.T + 2 * kWave) * sizeof(int);
+  const dim3 grid((unsigned)(p.B * p.NB)), block(kRowsPerBlock);
   if (aligned)
-    hipLaunchKernelGGL(mas_kernel<true>, grid, block, lds, stream, p);
+    hipLaunchKernelGGL(mas_kernel<true>, grid, block, 0, stream, p);
   else
-    hipLaunchKernelGGL(mas_kernel<false>, grid, block, lds, stream, p);
+    hipLaunchKernelGGL(mas_kernel<false>, grid, block, 0, stream, p);
   return hipGetLastError();
 }
 

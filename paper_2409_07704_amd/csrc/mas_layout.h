@@ -17,7 +17,6 @@ constexpr int kRowsPerBlock = kWave * kWavesPerBlock;
 constexpr int kChunk = 32;                   // speech columns per decision word
 constexpr size_t kAlign = 256;
 constexpr int kMaxRows = 8192;               // largest T (the walker keeps row_start in LDS)
-constexpr int kMaxZero = 256;                // zero-fill workgroups of a launch
 
 // Decision bit of text row i at speech column j (j >= 1): 1 when the forward
 // max took the diagonal predecessor Q[i-1][j-1] (the backtrack then moves to
@@ -46,11 +45,10 @@ struct Layout {
   int32_t NB;      // workgroups per item = ceil(T / 256)
   int32_t NC;      // decision chunks per item = ceil(S / 32)
   int32_t TP;      // padded rows per item = 64 * NW
-  size_t off_done;   // uint32 [B][NW]   wave-finished flags (tag values)
+  size_t off_done;   // uint32 [2][B][NW] sweep-finished, then path-rows-cleared flags (tag values)
   size_t off_slots;  // uint64 [B][NW][NC*32] boundary hand-off words
   size_t off_dec;    // uint32 [B][NC][TP] decision words
   size_t off_rs;     // int32  [B][T+1] row_start table (mas_forward_ex)
-  size_t off_zprog;  // uint64 [kMaxZero] zero-fill progress words
   size_t bytes;
 };
 
@@ -71,15 +69,13 @@ __host__ inline bool make_layout(int32_t B, int32_t T, int32_t S, Layout* L) {
   if ((uint64_t)T * (uint64_t)S * 4u >= (1ull << 31)) return false;
   size_t off = sizeof(WsHeader);
   L->off_done = off;
-  off = round_up(off + (size_t)B * L->NW * sizeof(uint32_t), kAlign);
+  off = round_up(off + 2 * (size_t)B * L->NW * sizeof(uint32_t), kAlign);
   L->off_slots = off;
   off = round_up(off + (size_t)B * L->NW * (size_t)L->NC * kChunk * sizeof(uint64_t), kAlign);
   L->off_dec = off;
   off = round_up(off + (size_t)B * L->NC * (size_t)L->TP * sizeof(uint32_t), kAlign);
   L->off_rs = off;
   off = round_up(off + (size_t)B * ((size_t)T + 1) * sizeof(int32_t), kAlign);
-  L->off_zprog = off;
-  off = round_up(off + (size_t)kMaxZero * sizeof(uint64_t), kAlign);
   L->bytes = off;
   return true;
 }
