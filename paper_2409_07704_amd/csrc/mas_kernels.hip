@@ -52,29 +52,6 @@ typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
 __device__ __forceinline__ float neg_inf() { return -__builtin_inff(); }
 
-// 64-bit lane mask of (a < b); NaN compares false as in C.
-__device__ __forceinline__ uint64_t lt_mask(float a, float b) { return __builtin_amdgcn_ballot_w64(a < b); }
-
-// mask ? t : f, per lane, from an SGPR lane mask.
-__device__ __forceinline__ float select_mask(float f, float t, uint64_t m) {
-  float r;
-  asm("v_cndmask_b32_e64 %0, %1, %2, %3" : "=v"(r) : "v"(f), "v"(t), "s"(m));
-  return r;
-}
-
-// bits * 2 + (this lane's bit of m): shifts a decision into a lane's word.
-__device__ __forceinline__ uint32_t push_bit(uint32_t bits, uint64_t m) {
-  uint32_t r;
-  uint64_t carry;
-  asm("v_addc_co_u32_e64 %0, %1, %2, %2, %3" : "=v"(r), "=s"(carry) : "v"(bits), "s"(m));
-  return r;
-}
-
-// Lane l >= 1 receives src from lane l-1; lane 0 receives lane0 (DPP wave_shr:1).
-__device__ __forceinline__ float shift_rows(float src, float lane0) {
-  return __int_as_float(__builtin_amdgcn_update_dpp(__float_as_int(lane0), __float_as_int(src), 0x138, 0xF, 0xF, false));
-}
-
 // Keeps the compiler from moving LDS accesses across this point; LDS
 // operations of one wave execute in order, so no wait is needed.
 __device__ __forceinline__ void wave_lds_sync() {
@@ -170,9 +147,9 @@ __device__ __forceinline__ void dma_words8(uint32_t lds, __amdgpu_buffer_rsrc_t 
       : "memory", "m0", "scc");
 }
 
-// Five 4-byte loads, device-scope: load k brings the word at voff[k] of the
+// Six 4-byte loads, device-scope: load k brings the word at voff[k] of the
 // resource to LDS at lds + 256 k + 4 lane.
-__device__ __forceinline__ void dma_words5(uint32_t lds, __amdgpu_buffer_rsrc_t r, const int (&vo)[5]) {
+__device__ __forceinline__ void dma_words6(uint32_t lds, __amdgpu_buffer_rsrc_t r, const int (&vo)[6]) {
   asm volatile(
       "s_mov_b32 m0, %[l]\n\ts_nop 0\n\t"
       "buffer_load_dword %[v0], %[r], 0 offen sc1 lds\n\t"
@@ -183,9 +160,12 @@ __device__ __forceinline__ void dma_words5(uint32_t lds, __amdgpu_buffer_rsrc_t 
       "s_add_u32 m0, %[l], 0x300\n\ts_nop 0\n\t"
       "buffer_load_dword %[v3], %[r], 0 offen sc1 lds\n\t"
       "s_add_u32 m0, %[l], 0x400\n\ts_nop 0\n\t"
-      "buffer_load_dword %[v4], %[r], 0 offen sc1 lds"
+      "buffer_load_dword %[v4], %[r], 0 offen sc1 lds\n\t"
+      "s_add_u32 m0, %[l], 0x500\n\ts_nop 0\n\t"
+      "buffer_load_dword %[v5], %[r], 0 offen sc1 lds"
       :
-      : [l] "s"(lds), [r] "s"(r), [v0] "v"(vo[0]), [v1] "v"(vo[1]), [v2] "v"(vo[2]), [v3] "v"(vo[3]), [v4] "v"(vo[4])
+      : [l] "s"(lds), [r] "s"(r), [v0] "v"(vo[0]), [v1] "v"(vo[1]), [v2] "v"(vo[2]), [v3] "v"(vo[3]), [v4] "v"(vo[4]),
+        [v5] "v"(vo[5])
       : "memory", "m0", "scc");
 }
 
@@ -272,20 +252,87 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t sub_rsrc(const void* p, uint64
 // conflict-free for both the tile writes and the per-row reads.
 __device__ __forceinline__ int swz(int r) { return (r & 7) ^ ((r >> 3) & 1); }
 
-// One 32-column chunk of the recurrence for one row per lane.
-//   q   : this lane's Q at the column before the chunk (updated)
-//   v   : this lane's value[row][j0 .. j0+31]
-//   bd  : Q[row0-1][j0-1 .. j0+30] (the row above the wave), read by lane 0
-//   qc  : this lane's Q at every column of the chunk (out)
-//   bits: decisions of the chunk, first column in bit 31 (out)
-// MASKED handles the chunks that cross the triangle i > j (value not used
-// there, Q = -inf) and the first cell Q[0][0] = value[0][0].
-// FIRST: the wave holding row 0, whose row above is the virtual -inf row:
-// `diag` keeps -inf in lane 0 (DPP leaves lane 0 untouched), so bd is unused.
-template <bool MASKED, bool FIRST>
-__device__ __forceinline__ void sweep_chunk(float& q, float& diag, const f32x4 (&v4)[8], const float (&bd)[kChunk],
-                                            float (&qc)[kChunk], uint32_t& bits, int row, int j0) {
-  uint32_t w = 0;
+// The recurrence, one text row per lane, lane 0 carrying the row above the
+// wave.  Per column j (Algorithm 2's parallel step):
+//   t      = max(Q[r-1][j-1], Q[r][j-1])    v_max_f32 with DPP wave_shr:1
+//                                            (lane l reads lane l-1's Q);
+//   Q[r][j] = t + value[r][j]               one fp32 add;
+//   d      = sign(Q[r][j-1] - t)            1 iff the diagonal is strictly
+//                                            greater (-0 below +0, the order
+//                                            of v_max_f32 and of R2);
+//   bits   = bits << 1 | d                  v_alignbit (first column ends in
+//                                            bit 31 after 32 columns).
+// Lane 0 has no lane below it: DPP leaves its t untouched, and t is kept at
+// -0 in lane 0 for the whole sweep, so lane 0's Q becomes -0 + value = value
+// exactly (x + -0 = x for every x): lane 0's "values" are the Q of the row
+// above, handed down by the previous wave (or -inf above row 0).
+// A VALU write followed by a DPP read of the same register needs two wait
+// states: each column's add is followed by two other VALU instructions
+// before the next column reads it, and each block starts with s_nop 1.
+__device__ __forceinline__ void cols8(float& q, float& t, uint32_t& bits, float (&o)[8], const float* v) {
+  float u;
+  asm("s_nop 1\n\t"
+      "v_max_f32_dpp %[t], %[q], %[q] wave_shr:1 row_mask:0xf bank_mask:0xf\n\t"
+      "v_add_f32 %[o0], %[t], %[v0]\n\t"
+      "v_sub_f32 %[u], %[q], %[t]\n\t"
+      "v_alignbit_b32 %[b], %[b], %[u], 31\n\t"
+      "v_max_f32_dpp %[t], %[o0], %[o0] wave_shr:1 row_mask:0xf bank_mask:0xf\n\t"
+      "v_add_f32 %[o1], %[t], %[v1]\n\t"
+      "v_sub_f32 %[u], %[o0], %[t]\n\t"
+      "v_alignbit_b32 %[b], %[b], %[u], 31\n\t"
+      "v_max_f32_dpp %[t], %[o1], %[o1] wave_shr:1 row_mask:0xf bank_mask:0xf\n\t"
+      "v_add_f32 %[o2], %[t], %[v2]\n\t"
+      "v_sub_f32 %[u], %[o1], %[t]\n\t"
+      "v_alignbit_b32 %[b], %[b], %[u], 31\n\t"
+      "v_max_f32_dpp %[t], %[o2], %[o2] wave_shr:1 row_mask:0xf bank_mask:0xf\n\t"
+      "v_add_f32 %[o3], %[t], %[v3]\n\t"
+      "v_sub_f32 %[u], %[o2], %[t]\n\t"
+      "v_alignbit_b32 %[b], %[b], %[u], 31\n\t"
+      "v_max_f32_dpp %[t], %[o3], %[o3] wave_shr:1 row_mask:0xf bank_mask:0xf\n\t"
+      "v_add_f32 %[o4], %[t], %[v4]\n\t"
+      "v_sub_f32 %[u], %[o3], %[t]\n\t"
+      "v_alignbit_b32 %[b], %[b], %[u], 31\n\t"
+      "v_max_f32_dpp %[t], %[o4], %[o4] wave_shr:1 row_mask:0xf bank_mask:0xf\n\t"
+      "v_add_f32 %[o5], %[t], %[v5]\n\t"
+      "v_sub_f32 %[u], %[o4], %[t]\n\t"
+      "v_alignbit_b32 %[b], %[b], %[u], 31\n\t"
+      "v_max_f32_dpp %[t], %[o5], %[o5] wave_shr:1 row_mask:0xf bank_mask:0xf\n\t"
+      "v_add_f32 %[o6], %[t], %[v6]\n\t"
+      "v_sub_f32 %[u], %[o5], %[t]\n\t"
+      "v_alignbit_b32 %[b], %[b], %[u], 31\n\t"
+      "v_max_f32_dpp %[t], %[o6], %[o6] wave_shr:1 row_mask:0xf bank_mask:0xf\n\t"
+      "v_add_f32 %[o7], %[t], %[v7]\n\t"
+      "v_sub_f32 %[u], %[o6], %[t]\n\t"
+      "v_alignbit_b32 %[b], %[b], %[u], 31"
+      : [o0] "=&v"(o[0]), [o1] "=&v"(o[1]), [o2] "=&v"(o[2]), [o3] "=&v"(o[3]), [o4] "=&v"(o[4]), [o5] "=&v"(o[5]),
+        [o6] "=&v"(o[6]), [o7] "=&v"(o[7]), [t] "+v"(t), [b] "+v"(bits), [u] "=&v"(u)
+      : [q] "v"(q), [v0] "v"(v[0]), [v1] "v"(v[1]), [v2] "v"(v[2]), [v3] "v"(v[3]), [v4] "v"(v[4]), [v5] "v"(v[5]),
+        [v6] "v"(v[6]), [v7] "v"(v[7]));
+  q = o[7];
+}
+
+// One column of the same step (for the chunks that cross the masked triangle).
+__device__ __forceinline__ float col1(float q, float& t, uint32_t& bits, float v) {
+  float o, u;
+  asm("s_nop 1\n\t"
+      "v_max_f32_dpp %[t], %[q], %[q] wave_shr:1 row_mask:0xf bank_mask:0xf\n\t"
+      "v_add_f32 %[o], %[t], %[v]\n\t"
+      "v_sub_f32 %[u], %[q], %[t]\n\t"
+      "v_alignbit_b32 %[b], %[b], %[u], 31"
+      : [o] "=&v"(o), [t] "+v"(t), [b] "+v"(bits), [u] "=&v"(u)
+      : [q] "v"(q), [v] "v"(v));
+  return o;
+}
+
+// One 32-column chunk for lanes 1..63 (rows row0 + lane - 1) and the carried
+// row in lane 0.  v: this lane's 32 values (lane 0: the row above's Q);
+// qc: Q of every column (out); bits: decisions, first column in bit 31.
+// MASKED: the chunk crosses the triangle i > j, where Q is -inf (lane 0's
+// copies already are), and holds the first cell Q[0][0] = value[0][0] when
+// j0 == 0.
+template <bool MASKED>
+__device__ __forceinline__ void sweep_chunk(float& q, float& t, const f32x4 (&v4)[8], float (&qc)[kChunk], uint32_t& bits,
+                                            int lane, int row, int j0) {
   float v[kChunk];
 #pragma unroll
   for (int k = 0; k < 8; ++k) {
@@ -294,20 +341,26 @@ __device__ __forceinline__ void sweep_chunk(float& q, float& diag, const f32x4 (
     v[4 * k + 2] = v4[k].z;
     v[4 * k + 3] = v4[k].w;
   }
+  uint32_t w = bits;
+  if (!MASKED) {
 #pragma unroll
-  for (int m = 0; m < kChunk; ++m) {
-    const float stay = q;
-    diag = shift_rows(stay, FIRST ? diag : bd[m]);
-    const uint64_t d = lt_mask(stay, diag);
-    float qn = select_mask(stay, diag, d) + v[m];
-    if (MASKED) {
-      const int j = j0 + m;
-      qn = (row > j) ? neg_inf() : qn;
-      if (j == 0) qn = (row == 0) ? v[m] : neg_inf();
+    for (int k = 0; k < 4; ++k) {
+      float o[8];
+      cols8(q, t, w, o, v + 8 * k);
+#pragma unroll
+      for (int m = 0; m < 8; ++m) qc[8 * k + m] = o[m];
     }
-    w = push_bit(w, d);
-    qc[m] = qn;
-    q = qn;
+  } else {
+    const bool own = lane > 0;
+#pragma unroll
+    for (int m = 0; m < kChunk; ++m) {
+      const int j = j0 + m;
+      float qn = col1(q, t, w, v[m]);
+      qn = (own && row > j) ? neg_inf() : qn;
+      if (j == 0) qn = (own && row == 0) ? v[m] : qn;
+      qc[m] = qn;
+      q = qn;
+    }
   }
   bits = w;
 }
@@ -327,19 +380,27 @@ __device__ __forceinline__ uint4 path_piece(int lo, int hi, int j0) {
 
 // ---------------------------------------------------------------- LDS layout
 // The walk fetches each chunk's decision words kWalkAhead chunks before it
-// walks that chunk, as a window of kWalkWin rows below the walker's row at
-// fetch time: the path descends at most 32 rows per chunk and a chunk reads
-// the words of at most 32 rows below its entry row, so the window
-// 32 (kWalkAhead + 1) + 1 rows deep covers every word the chunk can need.
+// walks that chunk, as a window of kWalkWin words (lane-indexed, see
+// dec_index) below the walker's row at fetch time: the path descends at most
+// 32 rows per chunk and a chunk reads the words of at most 32 rows below its
+// entry row, so 32 (kWalkAhead + 1) + 1 rows (plus one carried-row slot per
+// 63 rows) cover every word the chunk can need.
 constexpr int kWalkAhead = 8;
-constexpr int kWalkWin = 5 * kWave;   // 320 rows: five 256-byte loads
+constexpr int kWalkWin = 6 * kWave;   // 384 words: six 256-byte loads
 constexpr int kWalkSlots = 16;        // window ring (power of two > kWalkAhead)
-static_assert(kWalkWin >= 32 * (kWalkAhead + 1) + 1, "walk window");
+static_assert(kWalkWin >= dec_index(32 * (kWalkAhead + 1) + 1) + 1, "walk window");
+
+// One hand-off slot between waves of a workgroup: the producer's last-row Q
+// over one chunk, then a tag (chunk + 1) written after the values.
+struct RingSlot {
+  f32x4 q[kChunk / 4];
+  int tag[4];
+};
 
 struct SweepLds {
   union {
-    // Value tiles: [wave][slot] 64 rows x 32 columns, 16-byte unit 8 r + s
-    // holds piece s ^ swz(r) of row r.
+    // Value tiles: [wave][slot] rows 63g .. 63g+63 x 32 columns, 16-byte unit
+    // 8 r + s holds piece s ^ swz(r) of tile row r.
     f32x4 tile[kWavesPerBlock][kStages][8 * kWave];
     // The walker's staging, once every sweep of its item (and so of its
     // workgroup) has finished.
@@ -348,16 +409,16 @@ struct SweepLds {
       int rs[kMaxRows + 2 * kWave];        // row_start under construction
     } walk;
   } u;
-  float ring[kWavesPerBlock - 1][kRing][kChunk];  // wave w -> w+1 boundary values
+  RingSlot ring[kWavesPerBlock - 1][kRing];       // wave w -> w+1 boundary rows
   uint64_t poll[kPollSlots][2 * kWave];           // polled boundary words (4 copies of 32)
-  f32x4 bout[kWavesPerBlock][kChunk / 4];         // boundary staging (global hand-off)
+  f32x4 stage[kWavesPerBlock][kChunk / 4];        // boundary row staging (global hand-off)
+  f32x4 ninf[kChunk / 4];                         // a chunk of -inf (the row above row 0)
   uint32_t dummy[kWavesPerBlock][kWave];          // target of placeholder loads
-  int prod[kWavesPerBlock];                       // chunks wave w has published (exclusive end)
   int cons[kWavesPerBlock];                       // next chunk wave w will consume
 };
 
 // ---------------------------------------------------------------- path clearing
-// The bytes [p0, p1) of the path that one wave clears: its 64 rows of its
+// The bytes [p0, p1) of the path that one wave clears: its 63 rows of its
 // item.  16-byte aligned pieces [a0, a1) go through the sweep schedule; the
 // unaligned head and tail are cleared up front with byte stores.
 struct ZeroPlan {
@@ -368,7 +429,7 @@ struct ZeroPlan {
 
 __device__ __forceinline__ ZeroPlan zero_plan(const KParams& p, int b, int g, int lane) {
   const uint64_t base = (uint64_t)b * (uint64_t)p.T * (uint64_t)p.S;  // offsets from p.path
-  const int r0 = min(g * kWave, p.T), r1 = min(g * kWave + kWave, p.T);
+  const int r0 = min(g * kRowsPerWave, p.T), r1 = min(g * kRowsPerWave + kRowsPerWave, p.T);
   const uint64_t p0 = base + (uint64_t)r0 * (uint64_t)p.S, p1 = base + (uint64_t)r1 * (uint64_t)p.S;
   const uint64_t pa = (uint64_t)(uintptr_t)p.path;
   const uint64_t a0 = ((pa + p0 + 15) & ~15ull) - pa, a1 = ((pa + p1) & ~15ull) - pa;
@@ -396,16 +457,17 @@ __device__ __forceinline__ void zero_rest(const ZeroPlan& z, uint64_t from, int 
 struct WaveCtx {
   int lane, wv, b, g, g_last, tx, ty, row, c_begin, c_end, out_mode;
   int prev_end;                     // chunks the previous wave computes (exclusive end)
+  int mask_end;                     // first chunk without a cell i > j of this wave
   bool zero;                        // this wave clears its path rows during its steps
   const float* slab;                // the item's value slab [T][S]
   uint64_t slab_bytes;
-  uint64_t row_off;                 // byte offset of this wave's first row in the slab
+  uint64_t row_off;                 // byte offset of the wave's first tile row in the slab
   const uint64_t* pslots;           // the previous wave's boundary words (IN == 2)
   uint64_t pslot_bytes;
   int voff[8];                      // per-lane byte offsets of the tile loads
   uint32_t tile0;                   // LDS offset of this wave's tile slot 0
   uint32_t dummy;                   // LDS offset of this wave's placeholder area
-  uint64_t decp;                    // &dec[b][0][row]
+  uint64_t decp;                    // &dec[b][0][64 g + lane]
   uint64_t slotp;                   // &slots[b][g][lane % 32] (boundary words out)
   ZeroPlan zp;
 };
@@ -418,11 +480,11 @@ struct WaveCtx {
 // whatever they hold never reaches a decision the walk reads or the score.
 __device__ __forceinline__ int chunk_end(int g, int tx, int ty) {
   const int by_len = (ty + kChunk - 1) / kChunk;
-  const int by_reach = (g * kWave + kWave - 1 + ty - tx) / kChunk + 1;
+  const int by_reach = (g * kRowsPerWave + kRowsPerWave - 1 + ty - tx) / kChunk + 1;
   return by_len < by_reach ? by_len : by_reach;
 }
 
-// Sweeps this wave's 64 rows over its chunks and returns the score candidate
+// Sweeps this wave's rows over its chunks and returns the score candidate
 // (Q at (row, t_y-1) of this lane; only meaningful for the wave holding row
 // t_x-1).  IN: where the row above the wave comes from — 0 nowhere (the wave
 // holds row 0), 1 the LDS ring of the previous wave of the workgroup, 2
@@ -434,9 +496,8 @@ __device__ __forceinline__ float sweep_rows(const KParams& p, SweepLds& L, const
   constexpr bool IN2 = IN == 2;
   const int lane = x.lane, wv = x.wv;
   const bool h = x.out_mode == 2, zero = x.zero;
-  float q = neg_inf();
-  float diag = neg_inf();  // lane 0 keeps -inf when IN == 0
   float score = neg_inf();
+  float t = -0.0f;  // lane 0 keeps -0 for the whole sweep (see cols8)
   const u32x4 zv = {0u, 0u, 0u, 0u};
   const int dvo = 4 * lane;  // placeholder loads read the slab's first 256 bytes
   const __amdgpu_buffer_rsrc_t drsrc = sub_rsrc(x.slab, x.slab_bytes, 0);
@@ -470,6 +531,37 @@ __device__ __forceinline__ float sweep_rows(const KParams& p, SweepLds& L, const
       ++zk;
     }
   };
+  // Boundary words of chunk c in poll slot c % 4, word lane % 32, once every
+  // one of them carries this call's tag (re-polled until then).
+  auto polled_word = [&](int c) __attribute__((always_inline)) -> uint64_t {
+    const int sl = c & (kPollSlots - 1);
+    uint64_t wd = L.poll[sl][lane & (kChunk - 1)];
+    int spins = 0;
+    while (__builtin_amdgcn_ballot_w64((uint32_t)(wd >> 32) != tag) != 0) {
+      if (++spins > kSpinLimit) {
+        timed_out = true;
+        break;
+      }
+      __builtin_amdgcn_s_sleep(1);
+      issue_poll(c);
+      vm_wait<0>();
+      wd = L.poll[sl][lane & (kChunk - 1)];
+    }
+    return wd;
+  };
+  // Ring slot of chunk c from the previous wave, once its tag says it is
+  // written (the tag is read before the values, and written after them).
+  auto ring_ready = [&](int c) __attribute__((always_inline)) {
+    const int* tg = &L.ring[wv - 1][c % kRing].tag[0];
+    int spins = 0;
+    while (lds_load(tg) != c + 1) {
+      if (++spins > kSpinLimit) {
+        timed_out = true;
+        break;
+      }
+      __builtin_amdgcn_s_sleep(1);
+    }
+  };
 
   // Pieces beyond what the steps will clear, up front.
   if (zero) zero_rest(x.zp, x.zp.a0 + (uint64_t)(kDepth + x.c_end - x.c_begin) * 2048u, lane);
@@ -484,89 +576,67 @@ __device__ __forceinline__ float sweep_rows(const KParams& p, SweepLds& L, const
     issue_zero();
   }
 
-  const int rsw = swz(lane);
-  int prod_seen = 0;               // last value read of the producer's counter
-  int cons_seen = x.c_begin + 2;   // last value read of the consumer's counter
+  // Lane 0's Q at the column before the first chunk: the previous wave's
+  // last row there (its chunk c_begin-1, always computed), or -inf.
+  float q = neg_inf();
+  if (IN == 1) {
+    ring_ready(x.c_begin - 1);
+    wave_lds_sync();
+    const f32x4 e = L.ring[wv - 1][(x.c_begin - 1) % kRing].q[kChunk / 4 - 1];
+    q = lane == 0 ? e.w : q;
+  } else if (IN == 2) {
+    vm_wait<0>();
+    const uint64_t wd = polled_word(x.c_begin - 1);
+    const float e = __int_as_float(__builtin_amdgcn_readlane((int)(uint32_t)wd, kChunk - 1));
+    q = lane == 0 ? e : q;
+  }
+  if (lane == 0) lds_store(&L.cons[wv], x.c_begin);
+
+  // This lane's 32 values come from its tile row (lanes 1..63: tile row
+  // lane-1) or, for lane 0, from the row above's 32 Q values.
+  const int tsw = lane > 0 ? swz(lane - 1) : 0;
+  const int trow = lane > 0 ? lane - 1 : 0;
+  // Lower bound of the consumer's counter: it starts at its own c_begin-1,
+  // which is at least this wave's c_begin+1 (63 rows span >= 63 columns).
+  int cons_seen = x.c_begin + 1;
   for (int c = x.c_begin; c < x.c_end; ++c) {
     wait_step<NL, IN2>(h, zero);
     if (IN2) issue_poll(c + 2);
     issue_tile(c + kDepth);
 
-    // This lane's row of the chunk, 32 values.
-    f32x4 v[8];
-    {
-      const f32x4* t = L.u.tile[wv][c & (kStages - 1)];
-#pragma unroll
-      for (int k = 0; k < 8; ++k) v[k] = t[8 * lane + (k ^ rsw)];
-    }
-    // Boundary column values bd[m] = Q[row0-1][j0-1+m].  The previous wave
-    // computes chunks below prev_end; past them its row cannot reach the end,
-    // so -inf stands in (bd[0] of chunk prev_end is its last real value).
-    float bd[kChunk];
-    if (IN == 1) {
-      const int need = c < x.prev_end ? c + 1 : x.prev_end;
-      int spins = 0;
-      while (prod_seen < need) {
-        prod_seen = lds_load(&L.prod[wv - 1]);
-        if (prod_seen >= need) break;
-        if (++spins > kSpinLimit) {
-          timed_out = true;
-          break;
-        }
-        __builtin_amdgcn_s_sleep(1);
-      }
-      wave_lds_sync();
-      const float* cur = L.ring[wv - 1][c % kRing];
-      bd[0] = c <= x.prev_end ? L.ring[wv - 1][(c + kRing - 1) % kRing][kChunk - 1] : neg_inf();
-      if (c < x.prev_end) {
-#pragma unroll
-        for (int m = 1; m < kChunk; ++m) bd[m] = cur[m - 1];
-      } else {
-#pragma unroll
-        for (int m = 1; m < kChunk; ++m) bd[m] = neg_inf();
-      }
-      wave_lds_sync();
-      if (lane == 0) lds_store(&L.cons[wv], c + 1);
-    } else if (IN == 2) {
-      // Lanes 0..31: word m of chunk c; lane 32: word 31 of chunk c-1.
-      const int wsl = lane < 32 ? (c & (kPollSlots - 1)) : ((c - 1) & (kPollSlots - 1));
-      const int wix = lane < 32 ? lane : kChunk - 1;
-      const bool check = lane < 32 ? c < x.prev_end : (lane == 32 && c <= x.prev_end);
-      uint64_t wd = L.poll[wsl][wix];
-      int spins = 0;
-      while (__builtin_amdgcn_ballot_w64(check && (uint32_t)(wd >> 32) != tag) != 0) {
-        if (++spins > kSpinLimit) {
-          timed_out = true;
-          break;
-        }
-        __builtin_amdgcn_s_sleep(1);
-        issue_poll(c - 1);
-        issue_poll(c);
-        vm_wait<0>();
-        wd = L.poll[wsl][wix];
-      }
-      // bd[0] = word 31 of chunk c-1 (lane 32), bd[m] = word m-1 of chunk c.
-      const float val = check ? __uint_as_float((uint32_t)wd) : neg_inf();
-      bd[0] = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(val), 32));
-      float* bf = reinterpret_cast<float*>(L.bout[wv]);
-      if (lane < kChunk) bf[lane] = val;
-      wave_lds_sync();
-#pragma unroll
-      for (int m = 1; m < kChunk; ++m) bd[m] = bf[m - 1];
-      wave_lds_sync();
+    // Source of lane 0's values for this chunk.
+    const f32x4* gsrc = L.ninf;
+    if (IN == 1 && c < x.prev_end) {
+      ring_ready(c);
+      gsrc = L.ring[wv - 1][c % kRing].q;
+    } else if (IN == 2 && c < x.prev_end) {
+      const uint64_t wd = polled_word(c);
+      float* sf = reinterpret_cast<float*>(L.stage[wv]);
+      if (lane < kChunk) sf[lane] = __uint_as_float((uint32_t)wd);
+      gsrc = L.stage[wv];
     }
     wave_lds_sync();
+    f32x4 v[8];
+    {
+      const f32x4* base = lane > 0 ? L.u.tile[wv][c & (kStages - 1)] + 8 * trow : gsrc;
+      const int sw = lane > 0 ? tsw : 0;
+#pragma unroll
+      for (int k = 0; k < 8; ++k) v[k] = base[k ^ sw];
+    }
+    wave_lds_sync();
+    if (IN == 1 && lane == 0) lds_store(&L.cons[wv], c + 1);
     float qc[kChunk];
-    uint32_t bits;
-    if (c < x.c_begin + 2)
-      sweep_chunk<true, IN == 0>(q, diag, v, bd, qc, bits, x.row, c * kChunk);
+    uint32_t bits = 0;
+    if (c < x.mask_end)
+      sweep_chunk<true>(q, t, v, qc, bits, lane, x.row, c * kChunk);
     else
-      sweep_chunk<false, IN == 0>(q, diag, v, bd, qc, bits, x.row, c * kChunk);
+      sweep_chunk<false>(q, t, v, qc, bits, lane, x.row, c * kChunk);
 
-    // Stores of the step: decision word, boundary words, path zeros.
+    // Stores of the step: decision word, boundary row, path zeros.
     vm_store32(x.decp + (uint64_t)c * (uint64_t)p.TP * 4u, bits);
     if (x.out_mode == 1) {
-      // Wait until the consumer no longer needs the ring slot, then publish.
+      // Wait until the consumer no longer needs the ring slot, then publish
+      // the values, then the tag.
       int spins = 0;
       while (cons_seen < c - (kRing - 2)) {
         cons_seen = lds_load(&L.cons[wv + 1]);
@@ -577,20 +647,20 @@ __device__ __forceinline__ float sweep_rows(const KParams& p, SweepLds& L, const
         }
         __builtin_amdgcn_s_sleep(1);
       }
+      RingSlot& rs = L.ring[wv][c % kRing];
       if (lane == kWave - 1) {
-        f32x4* dst = reinterpret_cast<f32x4*>(L.ring[wv][c % kRing]);
 #pragma unroll
-        for (int k = 0; k < kChunk / 4; ++k) dst[k] = f32x4{qc[4 * k], qc[4 * k + 1], qc[4 * k + 2], qc[4 * k + 3]};
+        for (int k = 0; k < kChunk / 4; ++k) rs.q[k] = f32x4{qc[4 * k], qc[4 * k + 1], qc[4 * k + 2], qc[4 * k + 3]};
       }
       wave_lds_sync();
-      if (lane == 0) lds_store(&L.prod[wv], c + 1);
+      if (lane == kWave - 1) lds_store(&rs.tag[0], c + 1);
     } else if (h) {
       if (lane == kWave - 1) {
 #pragma unroll
-        for (int k = 0; k < kChunk / 4; ++k) L.bout[wv][k] = f32x4{qc[4 * k], qc[4 * k + 1], qc[4 * k + 2], qc[4 * k + 3]};
+        for (int k = 0; k < kChunk / 4; ++k) L.stage[wv][k] = f32x4{qc[4 * k], qc[4 * k + 1], qc[4 * k + 2], qc[4 * k + 3]};
       }
       wave_lds_sync();
-      const float val = reinterpret_cast<const float*>(L.bout[wv])[lane & (kChunk - 1)];
+      const float val = reinterpret_cast<const float*>(L.stage[wv])[lane & (kChunk - 1)];
       const uint64_t word = ((uint64_t)tag << 32) | (uint64_t)__float_as_uint(val);
       vm_store64(x.slotp + (uint64_t)c * kChunk * 8u, word);
       wave_lds_sync();
@@ -635,16 +705,17 @@ __device__ __forceinline__ void sweep_block(const KParams& p, SweepLds& L, int s
   const int tx = p.t_x[b];
   const int ty = p.t_y[b];
   const int st = item_status(tx, ty, p.T, p.S);
-  const int c_begin = (g * kWave) / kChunk;
+  const int c_begin = (g * kRowsPerWave) / kChunk;
 
-  if (lane == 0) {
-    lds_store(&L.prod[wv], 0);
-    lds_store(&L.cons[wv], c_begin);
-  }
+  // Workgroup set-up: no ring slot is written yet; each wave's first chunk
+  // to consume (its carried row starts at chunk c_begin-1); the -inf chunk.
+  for (int i = threadIdx.x; i < (kWavesPerBlock - 1) * kRing; i += kThreadsPerBlock) lds_store(&L.ring[i / kRing][i % kRing].tag[0], 0);
+  if (lane == 0) lds_store(&L.cons[wv], c_begin - 1);
+  if (threadIdx.x < kChunk / 4) L.ninf[threadIdx.x] = f32x4{neg_inf(), neg_inf(), neg_inf(), neg_inf()};
   __syncthreads();
 
   int32_t* rs_out = p.row_start + (size_t)b * ((size_t)p.T + 1);
-  const bool has_rows = g * kWave < p.T;
+  const bool has_rows = g * kRowsPerWave < p.T;
   ZeroPlan zp{};
   if (p.path && has_rows) zp = zero_plan(p, b, g, lane);
   const bool clear = p.path && has_rows && zp.any;
@@ -659,7 +730,7 @@ __device__ __forceinline__ void sweep_block(const KParams& p, SweepLds& L, int s
     }
     return;
   }
-  const int g_last = (tx - 1) / kWave;
+  const int g_last = (tx - 1) / kRowsPerWave;
   if (g > g_last) {
     // No rows of the alignment here: clear the path rows once the item's
     // sweep is over (the HBM is less busy then).
@@ -682,23 +753,25 @@ __device__ __forceinline__ void sweep_block(const KParams& p, SweepLds& L, int s
   x.g_last = g_last;
   x.tx = tx;
   x.ty = ty;
-  x.row = g * kWave + lane;
+  x.row = g * kRowsPerWave + lane - 1;  // lane 0: the row above the wave
   x.c_begin = c_begin;
   x.c_end = chunk_end(g, tx, ty);
   x.prev_end = g > 0 ? chunk_end(g - 1, tx, ty) : 0;
+  x.mask_end = (g * kRowsPerWave + kRowsPerWave - 2) / kChunk + 1;  // last masked column: 63g + 61
   x.out_mode = g == g_last ? 0 : (wv < kWavesPerBlock - 1 ? 1 : 2);
   // The walker's wave clears its rows during its steps; the others after.
   x.zero = clear && g == g_last;
   x.zp = zp;
   x.slab = p.value + (size_t)b * (size_t)p.T * (size_t)p.S;
   x.slab_bytes = (uint64_t)p.T * (uint64_t)p.S * 4u;
-  x.row_off = (uint64_t)g * kWave * (uint64_t)p.S * 4u;
+  x.row_off = (uint64_t)g * kRowsPerWave * (uint64_t)p.S * 4u;
   const size_t slot_stride = (size_t)p.NC * kChunk;
   x.pslots = p.slots + ((size_t)b * p.NW + (g > 0 ? g - 1 : 0)) * slot_stride;
   x.pslot_bytes = slot_stride * 8u;
-  // Offsets relative to the wave's first row at the chunk's first column;
-  // rows past the slab fall outside the resource and read 0.  Tile rows
-  // below 64 and S * 4 * 64 < 2^31 keep them in range of an int.
+  // Tile rows 0..63 are item rows 63g .. 63g+63 (row 63 is not used); offsets
+  // are relative to the first tile row at the chunk's first column, and rows
+  // past the slab fall outside the resource and read 0.  Tile rows below 64
+  // and S * 4 * 64 < 2^31 keep them in range of an int.
   if (ALIGNED) {
     // Load q: lane L reads tile row 8q + L/8, piece (L%8) ^ swz(row).
 #pragma unroll
@@ -719,7 +792,7 @@ __device__ __forceinline__ void sweep_block(const KParams& p, SweepLds& L, int s
   }
   x.tile0 = lds_off(&L.u.tile[wv][0][0]);
   x.dummy = lds_off(&L.dummy[wv][0]);
-  x.decp = (uint64_t)(uintptr_t)(p.dec + (size_t)b * p.NC * (size_t)p.TP + x.row);
+  x.decp = (uint64_t)(uintptr_t)(p.dec + (size_t)b * p.NC * (size_t)p.TP + (size_t)g * kWave + lane);
   x.slotp = (uint64_t)(uintptr_t)(p.slots + ((size_t)b * p.NW + g) * slot_stride + (lane & (kChunk - 1)));
   const float score = g == 0 ? sweep_rows<ALIGNED, 0>(p, L, x, tag, timed_out)
                              : (wv > 0 ? sweep_rows<ALIGNED, 1>(p, L, x, tag, timed_out)
@@ -738,29 +811,28 @@ __device__ __forceinline__ void sweep_block(const KParams& p, SweepLds& L, int s
   }
 
   // ------------------------------------------------------------ backtrack
-  if (lane == ((tx - 1) & (kWave - 1)) && p.score) p.score[b] = score;
+  if (lane == (tx - 1) - g_last * kRowsPerWave + 1 && p.score) p.score[b] = score;
   wait_flags(p.done + (size_t)b * p.NW, g_last, tag, lane, timed_out);
   // Every sweep of this workgroup has finished (lower waves: flags above;
   // higher waves hold no rows of the alignment), so the tile area is free.
   int* rsl = L.u.walk.rs;
   const uint32_t* db = p.dec + (size_t)b * p.NC * (size_t)p.TP;
   const uint64_t chunk_bytes = (uint64_t)p.TP * 4u;
-  int wvo[5];
+  int wvo[6];
 #pragma unroll
-  for (int k = 0; k < 5; ++k) wvo[k] = 4 * lane + 256 * k;
-  int wlo = 0;  // lane s: first row of the window in ring slot s
-  // Window of chunk ch: rows [e - kWalkWin + 1, e] (clamped at row 0) into
-  // slot ch % kWalkSlots; placeholders for chunks before the first.
+  for (int k = 0; k < 6; ++k) wvo[k] = 4 * lane + 256 * k;
+  int wlo = 0;  // lane s: first decision index of the window in ring slot s
+  // Window of chunk ch: decision indices [dec_index(e) - kWalkWin + 1,
+  // dec_index(e)] (clamped at 0) into slot ch % kWalkSlots; placeholders for
+  // chunks before the first.
   auto issue_win = [&](int ch, int e) __attribute__((always_inline)) {
     const int slot = ch & (kWalkSlots - 1);
-    const int lo = max(e - kWalkWin + 1, 0);
+    const int lo = max(dec_index(e) - kWalkWin + 1, 0);
     wlo = lane == slot ? lo : wlo;
     const uint32_t dst = lds_off(&L.u.walk.win[slot][0]);
-    if (ch >= 0) {
-      dma_words5(dst, sub_rsrc(db + (size_t)ch * p.TP, chunk_bytes, (uint64_t)lo * 4u), wvo);
-    } else {
-      dma_words5(dst, sub_rsrc(db, chunk_bytes, chunk_bytes), wvo);  // empty resource: reads 0
-    }
+    const __amdgpu_buffer_rsrc_t rr = ch >= 0 ? sub_rsrc(db + (size_t)ch * p.TP, chunk_bytes, (uint64_t)lo * 4u)
+                                              : sub_rsrc(db, chunk_bytes, chunk_bytes);  // empty: reads 0
+    dma_words6(dst, rr, wvo);
   };
   int idx = tx - 1;                  // entry row of the chunk being walked
   int cw = (ty - 1) / kChunk;        // chunk being walked
@@ -768,20 +840,21 @@ __device__ __forceinline__ void sweep_block(const KParams& p, SweepLds& L, int s
   for (int k = 0; k < kWalkAhead; ++k) issue_win(cw - k, idx);
   bool walking = idx > 0;
   while (walking) {
-    vm_wait<5 * (kWalkAhead - 1)>();  // window of chunk cw (issued kWalkAhead chunks ago)
+    vm_wait<6 * (kWalkAhead - 1)>();  // window of chunk cw (issued kWalkAhead chunks ago)
     issue_win(cw - kWalkAhead, idx);
     // Lane l holds the word of row idx - l.
     const int slot = cw & (kWalkSlots - 1);
     const int lo = __builtin_amdgcn_readlane(wlo, slot);
-    const int wr = idx - lane - lo;
+    const int rr = idx - lane;
+    const int wr = dec_index(rr > 0 ? rr : 0) - lo;
     const uint32_t W = L.u.walk.win[slot][wr > 0 ? wr : 0];
     int kk = 0, sh = sh0;
     uint32_t pm = 0;  // bit p set: the kk-th recorded row starts at column 32cw + 31 - p
     while (true) {
       const uint32_t w = __builtin_amdgcn_readlane(W, kk);
-      const uint64_t t = (uint64_t)w & (~0ull << sh);
-      if (t == 0) break;  // the row continues left of this chunk (row 0 never steps)
-      const int pos = __builtin_ctzll(t);
+      const uint64_t tt = (uint64_t)w & (~0ull << sh);
+      if (tt == 0) break;  // the row continues left of this chunk (row 0 never steps)
+      const int pos = __builtin_ctzll(tt);
       pm |= 1u << pos;
       sh = pos + 1;
       kk += 1;
@@ -823,7 +896,7 @@ __device__ __forceinline__ void sweep_block(const KParams& p, SweepLds& L, int s
 
 template <bool ALIGNED>
 // One workgroup per CU: the value-tile ring takes most of the LDS.
-__global__ void __launch_bounds__(kRowsPerBlock, 1) mas_kernel(KParams p) {
+__global__ void __launch_bounds__(kThreadsPerBlock, 1) mas_kernel(KParams p) {
   __shared__ SweepLds L;
   const uint32_t gen = __hip_atomic_load(&p.hdr->gen, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   const uint32_t tag = call_tag(gen);
@@ -884,7 +957,7 @@ __global__ void __launch_bounds__(256) mas_zero_kernel(uint4* __restrict__ p, si
 
 // ---------------------------------------------------------------- launchers
 hipError_t launch_mas(const KParams& p, bool aligned, hipStream_t stream) {
-  const dim3 grid((unsigned)(p.B * p.NB)), block(kRowsPerBlock);
+  const dim3 grid((unsigned)(p.B * p.NB)), block(kThreadsPerBlock);
   if (aligned)
     hipLaunchKernelGGL(mas_kernel<true>, grid, block, 0, stream, p);
   else

@@ -1,7 +1,9 @@
 // Workspace and bit layout shared by the libmas kernels and host code.
 //
-// Rows of an item are processed by 64-lane waves, one text row per lane
-// (wave g of an item owns rows [64g, 64g+64)); four waves form a 256-thread
+// Rows of an item are processed by 64-lane waves.  Lane 0 of wave g carries
+// the row above the wave (row 63g-1, a copy handed down by the previous
+// wave; for g = 0 the virtual -inf row above row 0) and lanes 1..63 own
+// rows 63g .. 63g+62, one text row per lane.  Four waves form a 256-thread
 // workgroup.  Speech columns are processed in chunks of 32, and every lane
 // packs its row's 32 forward decisions of a chunk into one 32-bit word.
 #pragma once
@@ -12,21 +14,24 @@
 namespace mas {
 
 constexpr int kWave = 64;                    // lanes per wavefront (CDNA)
+constexpr int kRowsPerWave = kWave - 1;      // text rows a wave owns (lanes 1..63)
 constexpr int kWavesPerBlock = 4;            // one wave per SIMD of a CU
-constexpr int kRowsPerBlock = kWave * kWavesPerBlock;
+constexpr int kThreadsPerBlock = kWave * kWavesPerBlock;
 constexpr int kChunk = 32;                   // speech columns per decision word
 constexpr size_t kAlign = 256;
 constexpr int kMaxRows = 8192;               // largest T (the walker keeps row_start in LDS)
 
 // Decision bit of text row i at speech column j (j >= 1): 1 when the forward
 // max took the diagonal predecessor Q[i-1][j-1] (the backtrack then moves to
-// row i-1), 0 when it kept Q[i][j-1].  Stored as
-//   dec[b][c][i]  (uint32, c = j / 32, bit 31 - (j % 32)),
-// i.e. the first column of a chunk is the most significant bit.
+// row i-1), 0 when it kept Q[i][j-1].  Stored lane-indexed as
+//   dec[b][c][64 g + l]  (uint32, c = j / 32, bit 31 - (j % 32)),
+// for the lane l of wave g that owns row i (index i + i / 63 + 1; lane 0's
+// word is unused), i.e. the first column of a chunk is the most significant bit.
 __host__ __device__ constexpr int dec_bit(int j) { return 31 - (j % kChunk); }
+__host__ __device__ constexpr int dec_index(int i) { return i + i / kRowsPerWave + 1; }
 
 // Boundary hand-off between consecutive waves of an item: wave g publishes
-// Q[64g+63][j] for every column j it computes as one 64-bit word
+// Q[63g+62][j] (its last row) for every column j it computes as one 64-bit word
 // {low: fp32 bits, high: tag}.  The tag identifies the call (see WsHeader),
 // so stale words from earlier calls are never mistaken for fresh ones.
 struct WsHeader {
@@ -41,10 +46,10 @@ __host__ __device__ inline size_t round_up(size_t x, size_t a) { return (x + a -
 
 struct Layout {
   int32_t B, T, S;
-  int32_t NW;      // waves per item = ceil(T / 64)
-  int32_t NB;      // workgroups per item = ceil(T / 256)
+  int32_t NW;      // waves per item = ceil(T / 63)
+  int32_t NB;      // workgroups per item = ceil(NW / 4)
   int32_t NC;      // decision chunks per item = ceil(S / 32)
-  int32_t TP;      // padded rows per item = 64 * NW
+  int32_t TP;      // decision words per chunk of an item = 64 * NW
   size_t off_done;   // uint32 [2][B][NW] sweep-finished, then path-rows-cleared flags (tag values)
   size_t off_slots;  // uint64 [B][NW][NC*32] boundary hand-off words
   size_t off_dec;    // uint32 [B][NC][TP] decision words
@@ -58,8 +63,8 @@ __host__ inline bool make_layout(int32_t B, int32_t T, int32_t S, Layout* L) {
   L->B = B;
   L->T = T;
   L->S = S;
-  L->NW = (T + kWave - 1) / kWave;
-  L->NB = (T + kRowsPerBlock - 1) / kRowsPerBlock;
+  L->NW = (T + kRowsPerWave - 1) / kRowsPerWave;
+  L->NB = (L->NW + kWavesPerBlock - 1) / kWavesPerBlock;
   L->NC = (S + kChunk - 1) / kChunk;
   L->TP = L->NW * kWave;
   // Overflow guard: every product below stays far under 2^62 when these hold.

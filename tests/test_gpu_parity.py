@@ -91,6 +91,25 @@ def test_integer_ties(mas):
     assert_parity(mas, value, tx, ty, "integer-ties")
 
 
+def test_signed_zero_inputs(mas):
+    """Integer values with both signs of zero: exact ties between -0 and +0
+    partial sums, decided by the signed-zero order of the forward max."""
+    st = synth.Stream(123)
+    B, T, S = 16, 150, 260
+    value = st.randint(-1, 1, B * T * S).astype(np.float32)
+    neg = st.randint(0, 1, B * T * S).astype(bool)
+    value[(value == 0) & neg] = np.float32(-0.0)
+    value = value.reshape(B, T, S)
+    tx = st.randint(1, T, B)
+    ty = np.array([int(st.randint(int(a), S)[0]) for a in tx], np.int32)
+    assert (np.signbit(value) & (value == 0)).any()
+    assert_parity(mas, value, tx, ty, "signed-zeros")
+    # the exhaustive small shapes, all zeros of random sign
+    pairs = [(a, c) for a in range(1, 6) for c in range(a, 11)]
+    z = np.where(st.randint(0, 1, 40 * 5 * 10).astype(bool), np.float32(-0.0), np.float32(0.0)).reshape(40, 5, 10)
+    assert_parity(mas, z, np.array([a for a, _ in pairs], np.int32), np.array([c for _, c in pairs], np.int32), "zeros-40")
+
+
 @pytest.mark.parametrize(
     "B,T,S,seed",
     [(3, 33, 129, 1), (5, 65, 96, 2), (4, 257, 1001, 3), (2, 300, 301, 4), (6, 1, 77, 5), (3, 130, 4099, 6)],
