@@ -19,9 +19,9 @@ struct KParams {
   uint8_t* path;        // nullable [B][T][S]; null: no path is written
   WsHeader* hdr;
   uint32_t* done;       // [B][NW] sweep finished (decision words published)
-  uint32_t* zdone;      // [B][NW] this wave's path rows cleared
+  uint32_t* wdone;      // [B] walk finished (row_start published)
   uint64_t* slots;      // [B][NW][NC*32]
-  uint32_t* dec;        // [B][NC][TP]
+  uint32_t* dec;        // [B][NC][TP] decision words, row-indexed
   int32_t B, T, S, NW, NC, TP, NB;
   int32_t path16;       // path 16-byte aligned and S % 16 == 0
 };

@@ -147,26 +147,13 @@ __device__ __forceinline__ void dma_words8(uint32_t lds, __amdgpu_buffer_rsrc_t 
       : "memory", "m0", "scc");
 }
 
-// Six 4-byte loads, device-scope: load k brings the word at voff[k] of the
-// resource to LDS at lds + 256 k + 4 lane.
-__device__ __forceinline__ void dma_words6(uint32_t lds, __amdgpu_buffer_rsrc_t r, const int (&vo)[6]) {
-  asm volatile(
-      "s_mov_b32 m0, %[l]\n\ts_nop 0\n\t"
-      "buffer_load_dword %[v0], %[r], 0 offen sc1 lds\n\t"
-      "s_add_u32 m0, %[l], 0x100\n\ts_nop 0\n\t"
-      "buffer_load_dword %[v1], %[r], 0 offen sc1 lds\n\t"
-      "s_add_u32 m0, %[l], 0x200\n\ts_nop 0\n\t"
-      "buffer_load_dword %[v2], %[r], 0 offen sc1 lds\n\t"
-      "s_add_u32 m0, %[l], 0x300\n\ts_nop 0\n\t"
-      "buffer_load_dword %[v3], %[r], 0 offen sc1 lds\n\t"
-      "s_add_u32 m0, %[l], 0x400\n\ts_nop 0\n\t"
-      "buffer_load_dword %[v4], %[r], 0 offen sc1 lds\n\t"
-      "s_add_u32 m0, %[l], 0x500\n\ts_nop 0\n\t"
-      "buffer_load_dword %[v5], %[r], 0 offen sc1 lds"
-      :
-      : [l] "s"(lds), [r] "s"(r), [v0] "v"(vo[0]), [v1] "v"(vo[1]), [v2] "v"(vo[2]), [v3] "v"(vo[3]), [v4] "v"(vo[4]),
-        [v5] "v"(vo[5])
-      : "memory", "m0", "scc");
+// One 16-byte load per lane, device-scope: the bytes at voff of the resource
+// to LDS at lds + 16 lane.
+__device__ __forceinline__ void dma_piece(uint32_t lds, __amdgpu_buffer_rsrc_t r, int voff) {
+  asm volatile("s_mov_b32 m0, %[l]\n\ts_nop 0\n\tbuffer_load_dwordx4 %[v], %[r], 0 offen sc1 lds"
+               :
+               : [l] "s"(lds), [r] "s"(r), [v] "v"(voff)
+               : "memory", "m0");
 }
 
 // One 16-byte piece per lane, device-scope, to LDS at lds + 16 lane.
@@ -192,14 +179,15 @@ __device__ __forceinline__ void vm_store32(uint64_t a, uint32_t v) {
 __device__ __forceinline__ void vm_store64(uint64_t a, uint64_t v) {
   asm volatile("global_store_dwordx2 %0, %1, off sc1" ::"v"(a), "v"(v) : "memory");
 }
-// Two 16-byte zero stores (s_nop: a VALU write of store data needs one wait state).
+// Two 16-byte zero stores (s_nop: a VALU write of store data needs one wait
+// state).  Path bytes are only ever written by the wave that owns their row,
+// so these need no device-scope write-through.
 __device__ __forceinline__ void vm_zero2(uint64_t a0, uint64_t a1, u32x4 z) {
-  asm volatile("global_store_dwordx4 %0, %2, off sc1\n\tglobal_store_dwordx4 %1, %2, off sc1\n\ts_nop 0" ::"v"(a0), "v"(a1),
-               "v"(z)
+  asm volatile("global_store_dwordx4 %0, %2, off\n\tglobal_store_dwordx4 %1, %2, off\n\ts_nop 0" ::"v"(a0), "v"(a1), "v"(z)
                : "memory");
 }
 __device__ __forceinline__ void vm_zero1(uint64_t a, u32x4 z) {
-  asm volatile("global_store_dwordx4 %0, %1, off sc1\n\ts_nop 0" ::"v"(a), "v"(z) : "memory");
+  asm volatile("global_store_dwordx4 %0, %1, off\n\ts_nop 0" ::"v"(a), "v"(z) : "memory");
 }
 
 // Vector-memory operations of one sweep step, in issue order:
@@ -380,15 +368,17 @@ __device__ __forceinline__ uint4 path_piece(int lo, int hi, int j0) {
 
 // ---------------------------------------------------------------- LDS layout
 // The walk fetches each chunk's decision words kWalkAhead chunks before it
-// walks that chunk, as a window of kWalkWin words (lane-indexed, see
-// dec_index) below the walker's row at fetch time: the path descends at most
-// 32 rows per chunk and a chunk reads the words of at most 32 rows below its
-// entry row, so 32 (kWalkAhead + 1) + 1 rows (plus one carried-row slot per
-// 63 rows) cover every word the chunk can need.
-constexpr int kWalkAhead = 8;
-constexpr int kWalkWin = 6 * kWave;   // 384 words: six 256-byte loads
-constexpr int kWalkSlots = 16;        // window ring (power of two > kWalkAhead)
-static_assert(kWalkWin >= dec_index(32 * (kWalkAhead + 1) + 1) + 1, "walk window");
+// walks that chunk, as a window of kWalkWin rows below the walker's row e at
+// fetch time.  One chunk before walking it, the walker reads the 64 rows
+// below its current row from that window (a chunk holds at most 33 rows of
+// the path, and the current row is at most 32 rows into the 64); the current
+// row is then at least e - 32 (kWalkAhead - 1), as a chunk descends at most
+// 32 rows.
+constexpr int kWalkAhead = 14;
+constexpr int kWalkLoads = 2;                      // 1 KiB loads per window
+constexpr int kWalkWin = kWalkLoads * 4 * kWave;   // rows per window
+constexpr int kWalkSlots = 16;                 // window ring (power of two > kWalkAhead)
+static_assert(kWalkWin >= 32 * (kWalkAhead - 1) + kWave + 3, "walk window");
 
 // One hand-off slot between waves of a workgroup: the producer's last-row Q
 // over one chunk, then a tag (chunk + 1) written after the values.
@@ -439,9 +429,9 @@ __device__ __forceinline__ ZeroPlan zero_plan(const KParams& p, int b, int g, in
   z.last = pa + a1 - 16;
   // Unaligned head and tail bytes (at most 15 + 15; all bytes if no piece).
   const uint64_t h1 = z.any ? a0 : p1;
-  for (uint64_t o = p0 + lane; o < h1; o += kWave) st_dev(p.path + o, (uint8_t)0);
+  for (uint64_t o = p0 + lane; o < h1; o += kWave) p.path[o] = 0;
   if (z.any)
-    for (uint64_t o = a1 + lane; o < p1; o += kWave) st_dev(p.path + o, (uint8_t)0);
+    for (uint64_t o = a1 + lane; o < p1; o += kWave) p.path[o] = 0;
   return z;
 }
 
@@ -467,7 +457,7 @@ struct WaveCtx {
   int voff[8];                      // per-lane byte offsets of the tile loads
   uint32_t tile0;                   // LDS offset of this wave's tile slot 0
   uint32_t dummy;                   // LDS offset of this wave's placeholder area
-  uint64_t decp;                    // &dec[b][0][64 g + lane]
+  uint64_t decp;                    // &dec[b][0][row] (lane 0: the scratch word)
   uint64_t slotp;                   // &slots[b][g][lane % 32] (boundary words out)
   ZeroPlan zp;
 };
@@ -693,6 +683,126 @@ __device__ __forceinline__ void wait_flags(const uint32_t* flag, int n, uint32_t
   }
 }
 
+// ---------------------------------------------------------------- backtrack
+// One step of the walk inside a chunk, for row k >= 1 below the chunk's
+// first row (its word, shifted right by one, in CUR), with the word of row
+// k+1 read into NXT meanwhile.  q is the position of the previous row's
+// step: the row's own step is the lowest set bit of its word above q, at
+// q + 1 + ff1(word >> (q + 1)); none (shifted word zero, also for q = 31)
+// ends the chunk.  s_lshr sets SCC to (result != 0), s_ff1 leaves it, so the
+// s_addc adds the 1.
+#define MAS_WALK_STEP(CUR, NXT)                  \
+  "v_readlane_b32 %[" NXT "], %[wh], %[sl]\n\t" \
+  "s_add_u32 %[sl], %[sl], 1\n\t"               \
+  "s_lshr_b32 %[t], %[" CUR "], %[q]\n\t"       \
+  "s_cbranch_scc0 .Lmas_walk_end%=\n\t"    \
+  "s_ff1_i32_b32 %[t], %[t]\n\t"                \
+  "s_addc_u32 %[q], %[q], %[t]\n\t"             \
+  "s_bitset1_b32 %[pm], %[q]\n\t"
+#define MAS_WALK_STEP2 MAS_WALK_STEP("y", "x") MAS_WALK_STEP("x", "y")
+#define MAS_WALK_STEP8 MAS_WALK_STEP2 MAS_WALK_STEP2 MAS_WALK_STEP2 MAS_WALK_STEP2
+
+// The steps of one chunk.  Row k of the chunk (k = 0 at the row the path
+// enters the chunk in) is lane sl + k of w (and of wh = w >> 1).  The first
+// row's step is its lowest set bit at or above position q0 (the column the
+// path enters at); every later row's is its lowest set bit above the
+// previous row's.  Returns the set of step positions: bit p set means one
+// row starts at column 32c + 31 - p, the k-th lowest set bit for row k.  At
+// most 32 rows step (one per column), so the 33rd row is never looked at.
+__device__ __forceinline__ uint32_t walk_chunk(uint32_t w, uint32_t wh, int sl, int q0) {
+  uint32_t pm, t, x, y;
+  int q = q0;
+  asm volatile(
+      "s_mov_b32 %[pm], 0\n\t"
+      "v_readlane_b32 %[x], %[w], %[sl]\n\t"
+      "s_add_u32 %[sl], %[sl], 1\n\t"
+      "v_readlane_b32 %[y], %[wh], %[sl]\n\t"
+      "s_add_u32 %[sl], %[sl], 1\n\t"
+      "s_lshr_b32 %[t], %[x], %[q]\n\t"
+      "s_cbranch_scc0 .Lmas_walk_end%=\n\t"
+      "s_ff1_i32_b32 %[t], %[t]\n\t"
+      "s_add_u32 %[q], %[q], %[t]\n\t"
+      "s_bitset1_b32 %[pm], %[q]\n\t"
+      MAS_WALK_STEP8 MAS_WALK_STEP8 MAS_WALK_STEP8 MAS_WALK_STEP2 MAS_WALK_STEP2 MAS_WALK_STEP2
+      MAS_WALK_STEP("y", "x")
+      ".Lmas_walk_end%=:"
+      : [pm] "=&s"(pm), [t] "=&s"(t), [x] "=&s"(x), [y] "=&s"(y), [q] "+s"(q), [sl] "+s"(sl)
+      : [w] "v"(w), [wh] "v"(wh)
+      : "scc");
+  return pm;
+}
+#undef MAS_WALK_STEP8
+#undef MAS_WALK_STEP2
+#undef MAS_WALK_STEP
+
+// The walk of one item from (t_x-1, t_y-1) back to (0, 0) (Algorithm 1's
+// argmax loop, read off the decision words): in chunk c the path in row i
+// stays there until the nearest column to the left whose decision bit is
+// set, then continues one row up at the column before.  Builds row_start in
+// L.u.walk.rs: the first column of every row, with rs[0] = 0 and
+// rs[t_x .. T] = t_y.  Runs on the wave that holds row t_x-1, once every
+// wave of the item has published its words.
+__device__ __forceinline__ void walk(const KParams& p, SweepLds& L, int b, int tx, int ty, uint32_t tag, int lane,
+                                     bool& timed_out) {
+  const int g_last = (tx - 1) / kRowsPerWave;
+  wait_flags(p.done + (size_t)b * p.NW, g_last, tag, lane, timed_out);
+  // Every sweep of this workgroup has finished (lower waves: flags above;
+  // higher waves hold no rows of the alignment), so the tile area is free.
+  int* rsl = L.u.walk.rs;
+  const uint32_t* db = p.dec + (size_t)b * p.NC * (size_t)p.TP;
+  const uint64_t chunk_bytes = (uint64_t)p.TP * 4u;
+  const int wvo = 16 * lane;
+  int wlo = 0;  // lane s: first row of the window in ring slot s
+  // Window of chunk ch: kWalkWin rows from a 16-byte aligned row lo in
+  // [e - kWalkWin + 1, e - kWalkWin + 4] (or row 0) into slot ch % kWalkSlots;
+  // an empty resource (reads 0) for chunks before the first.
+  auto issue_win = [&](int ch, int e) __attribute__((always_inline)) {
+    const int slot = ch & (kWalkSlots - 1);
+    const int lo = max(e - kWalkWin + 4, 0) & ~3;
+    wlo = lane == slot ? lo : wlo;
+    const uint32_t dst = lds_off(&L.u.walk.win[slot][0]);
+    const __amdgpu_buffer_rsrc_t rr = ch >= 0 ? sub_rsrc(db + (size_t)ch * p.TP, chunk_bytes, (uint64_t)lo * 4u)
+                                              : sub_rsrc(db, chunk_bytes, chunk_bytes);
+#pragma unroll
+    for (int k = 0; k < kWalkLoads; ++k) dma_piece(dst + 1024 * k, rr, wvo + 1024 * k);
+  };
+  // Word of row e - lane of chunk ch (its window must be in LDS).
+  auto read_row = [&](int ch, int e) __attribute__((always_inline)) -> uint32_t {
+    const int slot = ch & (kWalkSlots - 1);
+    const int r = e - lane - __builtin_amdgcn_readlane(wlo, slot);
+    return L.u.walk.win[slot][r > 0 ? r : 0];
+  };
+  const uint32_t below = (1u << (lane & (kChunk - 1))) - 1u;  // positions below this lane's
+  int idx = tx - 1;                  // row of the path at the chunk's last column
+  int cw = (ty - 1) / kChunk;        // chunk being walked
+  int q0 = 31 - (ty - 1) % kChunk;   // position of the path's column in chunk cw
+  for (int k = 0; k < kWalkAhead; ++k) issue_win(cw - k, idx);
+  vm_wait<kWalkLoads * (kWalkAhead - 1)>();  // window of chunk cw
+  uint32_t W = read_row(cw, idx);    // rows e0 - lane of chunk cw
+  int off = 0;                       // lane of row idx in W: idx = e0 - off
+  bool walking = idx > 0;
+  while (walking) {
+    vm_wait<kWalkLoads * (kWalkAhead - 2)>();  // windows of chunks cw and cw-1
+    issue_win(cw - kWalkAhead, idx);
+    const uint32_t N = read_row(cw - 1, idx);  // the next chunk's rows below idx, read ahead
+    const uint32_t pm = walk_chunk(W, W >> 1, off, q0);
+    // Set bit p of pm belongs to the row (popcount of pm below p) under idx.
+    if (lane < kChunk && ((pm >> lane) & 1u)) rsl[idx - (int)__builtin_popcount(pm & below)] = cw * kChunk + 31 - lane;
+    const int kk = __builtin_popcount(pm);
+    idx -= kk;
+    q0 = 0;
+    cw -= 1;
+    W = N;
+    off = kk;
+    walking = idx > 0 && cw >= 0;
+  }
+  vm_wait<0>();  // no window load may land in LDS after this wave ends
+  wave_lds_sync();
+  if (lane == 0) rsl[0] = 0;
+  for (int i = tx + lane; i <= p.T; i += kWave) rsl[i] = ty;
+  wave_lds_sync();
+}
+
 template <bool ALIGNED>
 __device__ __forceinline__ void sweep_block(const KParams& p, SweepLds& L, int sid, uint32_t tag, bool& timed_out) {
   const int lane = threadIdx.x & (kWave - 1);
@@ -792,7 +902,7 @@ __device__ __forceinline__ void sweep_block(const KParams& p, SweepLds& L, int s
   }
   x.tile0 = lds_off(&L.u.tile[wv][0][0]);
   x.dummy = lds_off(&L.dummy[wv][0]);
-  x.decp = (uint64_t)(uintptr_t)(p.dec + (size_t)b * p.NC * (size_t)p.TP + (size_t)g * kWave + lane);
+  x.decp = (uint64_t)(uintptr_t)(p.dec + (size_t)b * p.NC * (size_t)p.TP + (lane > 0 ? (size_t)x.row : (size_t)p.TP - 1));
   x.slotp = (uint64_t)(uintptr_t)(p.slots + ((size_t)b * p.NW + g) * slot_stride + (lane & (kChunk - 1)));
   const float score = g == 0 ? sweep_rows<ALIGNED, 0>(p, L, x, tag, timed_out)
                              : (wv > 0 ? sweep_rows<ALIGNED, 1>(p, L, x, tag, timed_out)
@@ -800,96 +910,39 @@ __device__ __forceinline__ void sweep_block(const KParams& p, SweepLds& L, int s
 
   // Publish this wave's decision words to the item's walker.
   if (lane == 0) st_dev(p.done + (size_t)b * p.NW + g, tag);
-  if (g != g_last) {
-    // Then clear this wave's path rows, and say so.
-    if (clear) {
-      zero_rest(zp, zp.a0, lane);
-      asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-      if (lane == 0) st_dev(p.zdone + (size_t)b * p.NW + g, tag);
-    }
-    return;
-  }
-
-  // ------------------------------------------------------------ backtrack
-  if (lane == (tx - 1) - g_last * kRowsPerWave + 1 && p.score) p.score[b] = score;
-  wait_flags(p.done + (size_t)b * p.NW, g_last, tag, lane, timed_out);
-  // Every sweep of this workgroup has finished (lower waves: flags above;
-  // higher waves hold no rows of the alignment), so the tile area is free.
   int* rsl = L.u.walk.rs;
-  const uint32_t* db = p.dec + (size_t)b * p.NC * (size_t)p.TP;
-  const uint64_t chunk_bytes = (uint64_t)p.TP * 4u;
-  int wvo[6];
-#pragma unroll
-  for (int k = 0; k < 6; ++k) wvo[k] = 4 * lane + 256 * k;
-  int wlo = 0;  // lane s: first decision index of the window in ring slot s
-  // Window of chunk ch: decision indices [dec_index(e) - kWalkWin + 1,
-  // dec_index(e)] (clamped at 0) into slot ch % kWalkSlots; placeholders for
-  // chunks before the first.
-  auto issue_win = [&](int ch, int e) __attribute__((always_inline)) {
-    const int slot = ch & (kWalkSlots - 1);
-    const int lo = max(dec_index(e) - kWalkWin + 1, 0);
-    wlo = lane == slot ? lo : wlo;
-    const uint32_t dst = lds_off(&L.u.walk.win[slot][0]);
-    const __amdgpu_buffer_rsrc_t rr = ch >= 0 ? sub_rsrc(db + (size_t)ch * p.TP, chunk_bytes, (uint64_t)lo * 4u)
-                                              : sub_rsrc(db, chunk_bytes, chunk_bytes);  // empty: reads 0
-    dma_words6(dst, rr, wvo);
-  };
-  int idx = tx - 1;                  // entry row of the chunk being walked
-  int cw = (ty - 1) / kChunk;        // chunk being walked
-  int sh0 = 31 - (ty - 1) % kChunk;  // bits >= sh0 are columns not yet passed in chunk cw
-  for (int k = 0; k < kWalkAhead; ++k) issue_win(cw - k, idx);
-  bool walking = idx > 0;
-  while (walking) {
-    vm_wait<6 * (kWalkAhead - 1)>();  // window of chunk cw (issued kWalkAhead chunks ago)
-    issue_win(cw - kWalkAhead, idx);
-    // Lane l holds the word of row idx - l.
-    const int slot = cw & (kWalkSlots - 1);
-    const int lo = __builtin_amdgcn_readlane(wlo, slot);
-    const int rr = idx - lane;
-    const int wr = dec_index(rr > 0 ? rr : 0) - lo;
-    const uint32_t W = L.u.walk.win[slot][wr > 0 ? wr : 0];
-    int kk = 0, sh = sh0;
-    uint32_t pm = 0;  // bit p set: the kk-th recorded row starts at column 32cw + 31 - p
-    while (true) {
-      const uint32_t w = __builtin_amdgcn_readlane(W, kk);
-      const uint64_t tt = (uint64_t)w & (~0ull << sh);
-      if (tt == 0) break;  // the row continues left of this chunk (row 0 never steps)
-      const int pos = __builtin_ctzll(tt);
-      pm |= 1u << pos;
-      sh = pos + 1;
-      kk += 1;
-    }
-    // Scatter: set bit p of pm belongs to the row (popcount of pm below p) under idx.
-    if (lane < kChunk && ((pm >> lane) & 1u)) rsl[idx - (int)__builtin_popcount(pm & ((1u << lane) - 1u))] = cw * kChunk + 31 - lane;
-    idx -= kk;
-    sh0 = 0;
-    cw -= 1;
-    walking = idx > 0 && cw >= 0;
-  }
-  vm_wait<0>();  // no window load may land in LDS after this wave ends
-  wave_lds_sync();
-  if (lane == 0) rsl[0] = 0;
-  for (int i = tx + lane; i <= p.T; i += kWave) rsl[i] = ty;
-  wave_lds_sync();
-  for (int i = lane; i <= p.T; i += kWave) rs_out[i] = rsl[i];
-
-  if (!p.path) return;
-  // Ones of the item's path, once every wave holding rows below t_x has
-  // cleared its rows (this wave cleared its own during its steps).
-  wait_flags(p.zdone + (size_t)b * p.NW, g_last, tag, lane, timed_out);
-  uint8_t* pb = p.path + (size_t)b * (size_t)p.T * (size_t)p.S;
-  for (int i = lane; i < tx; i += kWave) {
-    const int lo = rsl[i], hi = rsl[i + 1];
-    uint8_t* prow = pb + (size_t)i * (size_t)p.S;
-    if (p.path16) {
-      for (int j0 = lo & ~15; j0 < hi; j0 += 16) {
-        const uint4 pc = path_piece(lo, hi, j0);
-        uint64_t* d = reinterpret_cast<uint64_t*>(prow + j0);
-        st_dev(d, ((uint64_t)pc.y << 32) | pc.x);
-        st_dev(d + 1, ((uint64_t)pc.w << 32) | pc.z);
+  if (g == g_last) {
+    if (lane == (tx - 1) - g_last * kRowsPerWave + 1 && p.score) p.score[b] = score;
+    walk(p, L, b, tx, ty, tag, lane, timed_out);
+    for (int i = lane; i <= p.T; i += kWave) st_dev(reinterpret_cast<uint32_t*>(rs_out + i), (uint32_t)rsl[i]);
+    if (!p.path) return;
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    if (lane == 0) st_dev(p.wdone + b, tag);
+  } else {
+    // Clear this wave's path rows while the walk runs, then wait for it.
+    if (!p.path) return;
+    if (clear) zero_rest(zp, zp.a0, lane);
+    int spins = 0;
+    while (ld_dev(p.wdone + b) != tag) {
+      if (++spins > kSpinLimit) {
+        timed_out = true;
+        break;
       }
+      __builtin_amdgcn_s_sleep(2);
+    }
+  }
+  // Ones of this wave's rows: lane l writes row 63g + l - 1, from row_start
+  // entries 63g + l - 1 (lane l-1's) and 63g + l (its own).
+  const int ri = min(g * kRowsPerWave + lane, p.T);
+  const int hi = g == g_last ? rsl[ri] : (int)ld_dev(reinterpret_cast<const uint32_t*>(rs_out + ri));
+  const int lo = __builtin_amdgcn_update_dpp(0, hi, 0x138, 0xF, 0xF, false);  // lane l-1's entry
+  const int row = g * kRowsPerWave + lane - 1;
+  if (lane > 0 && row < tx) {
+    uint8_t* prow = p.path + ((size_t)b * (size_t)p.T + (size_t)row) * (size_t)p.S;
+    if (p.path16) {
+      for (int j0 = lo & ~15; j0 < hi; j0 += 16) *reinterpret_cast<uint4*>(prow + j0) = path_piece(lo, hi, j0);
     } else {
-      for (int j = lo; j < hi; ++j) st_dev(prow + j, (uint8_t)1);
+      for (int j = lo; j < hi; ++j) prow[j] = 1;
     }
   }
 }

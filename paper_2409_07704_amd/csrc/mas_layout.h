@@ -23,12 +23,11 @@ constexpr int kMaxRows = 8192;               // largest T (the walker keeps row_
 
 // Decision bit of text row i at speech column j (j >= 1): 1 when the forward
 // max took the diagonal predecessor Q[i-1][j-1] (the backtrack then moves to
-// row i-1), 0 when it kept Q[i][j-1].  Stored lane-indexed as
-//   dec[b][c][64 g + l]  (uint32, c = j / 32, bit 31 - (j % 32)),
-// for the lane l of wave g that owns row i (index i + i / 63 + 1; lane 0's
-// word is unused), i.e. the first column of a chunk is the most significant bit.
+// row i-1), 0 when it kept Q[i][j-1].  Stored as
+//   dec[b][c][i]  (uint32, c = j / 32, bit 31 - (j % 32)),
+// i.e. the first column of a chunk is the most significant bit.  Word TP-1
+// of every chunk is a scratch slot (lane 0 of every wave stores there).
 __host__ __device__ constexpr int dec_bit(int j) { return 31 - (j % kChunk); }
-__host__ __device__ constexpr int dec_index(int i) { return i + i / kRowsPerWave + 1; }
 
 // Boundary hand-off between consecutive waves of an item: wave g publishes
 // Q[63g+62][j] (its last row) for every column j it computes as one 64-bit word
@@ -49,8 +48,8 @@ struct Layout {
   int32_t NW;      // waves per item = ceil(T / 63)
   int32_t NB;      // workgroups per item = ceil(NW / 4)
   int32_t NC;      // decision chunks per item = ceil(S / 32)
-  int32_t TP;      // decision words per chunk of an item = 64 * NW
-  size_t off_done;   // uint32 [2][B][NW] sweep-finished, then path-rows-cleared flags (tag values)
+  int32_t TP;      // decision words per chunk of an item (rows + scratch, multiple of 64)
+  size_t off_done;   // uint32 [B][NW] sweep-finished flags, then [B] walk-finished flags (tag values)
   size_t off_slots;  // uint64 [B][NW][NC*32] boundary hand-off words
   size_t off_dec;    // uint32 [B][NC][TP] decision words
   size_t off_rs;     // int32  [B][T+1] row_start table (mas_forward_ex)
@@ -66,7 +65,7 @@ __host__ inline bool make_layout(int32_t B, int32_t T, int32_t S, Layout* L) {
   L->NW = (T + kRowsPerWave - 1) / kRowsPerWave;
   L->NB = (L->NW + kWavesPerBlock - 1) / kWavesPerBlock;
   L->NC = (S + kChunk - 1) / kChunk;
-  L->TP = L->NW * kWave;
+  L->TP = (int32_t)round_up((size_t)L->NW * kRowsPerWave + 1, kWave);
   // Overflow guard: every product below stays far under 2^62 when these hold.
   if ((uint64_t)B * (uint64_t)L->NB > 0x7fffffffull) return false;  // grid size
   if ((uint64_t)B * (uint64_t)T * (uint64_t)S > (1ull << 46)) return false;
@@ -74,7 +73,7 @@ __host__ inline bool make_layout(int32_t B, int32_t T, int32_t S, Layout* L) {
   if ((uint64_t)T * (uint64_t)S * 4u >= (1ull << 31)) return false;
   size_t off = sizeof(WsHeader);
   L->off_done = off;
-  off = round_up(off + 2 * (size_t)B * L->NW * sizeof(uint32_t), kAlign);
+  off = round_up(off + ((size_t)B * L->NW + (size_t)B) * sizeof(uint32_t), kAlign);
   L->off_slots = off;
   off = round_up(off + (size_t)B * L->NW * (size_t)L->NC * kChunk * sizeof(uint64_t), kAlign);
   L->off_dec = off;
