@@ -73,7 +73,6 @@ __device__ __forceinline__ void lds_store(int* p, int v) { __hip_atomic_store(p,
 __device__ __forceinline__ uint32_t call_tag(uint32_t gen) { return 2u * gen + 1u; }
 
 constexpr int kSpinLimit = 1 << 21;  // bound of every device-side wait (~seconds)
-constexpr int kRing = 16;            // LDS hand-off ring depth (chunks)
 constexpr int kDepth = 3;            // value tiles in flight ahead of the one computed
 constexpr int kStages = 4;           // LDS tile slots per wave (kDepth + 1, a power of two)
 constexpr int kPollSlots = 4;        // LDS slots of polled boundary words
@@ -93,60 +92,59 @@ __device__ __forceinline__ void vm_wait() {
   asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
 }
 
-// One value tile, 16-byte variant: load q (q = 0..7) brings every lane's
-// 16-byte piece at byte offset voff[q] of the resource to LDS at
-// lds + 1024 q + 16 lane.  Eight operations.  (Offsets are kept in the
-// range-checked per-lane operand: the resource base moves per chunk.)
-__device__ __forceinline__ void dma_tile16(uint32_t lds, __amdgpu_buffer_rsrc_t r, const int (&vo)[8]) {
-  asm volatile(
-      "s_mov_b32 m0, %[l]\n\ts_nop 0\n\t"
-      "buffer_load_dwordx4 %[v0], %[r], 0 offen lds\n\t"
-      "s_add_u32 m0, %[l], 0x400\n\ts_nop 0\n\t"
-      "buffer_load_dwordx4 %[v1], %[r], 0 offen lds\n\t"
-      "s_add_u32 m0, %[l], 0x800\n\ts_nop 0\n\t"
-      "buffer_load_dwordx4 %[v2], %[r], 0 offen lds\n\t"
-      "s_add_u32 m0, %[l], 0xc00\n\ts_nop 0\n\t"
-      "buffer_load_dwordx4 %[v3], %[r], 0 offen lds\n\t"
-      "s_add_u32 m0, %[l], 0x1000\n\ts_nop 0\n\t"
-      "buffer_load_dwordx4 %[v4], %[r], 0 offen lds\n\t"
-      "s_add_u32 m0, %[l], 0x1400\n\ts_nop 0\n\t"
-      "buffer_load_dwordx4 %[v5], %[r], 0 offen lds\n\t"
-      "s_add_u32 m0, %[l], 0x1800\n\ts_nop 0\n\t"
-      "buffer_load_dwordx4 %[v6], %[r], 0 offen lds\n\t"
-      "s_add_u32 m0, %[l], 0x1c00\n\ts_nop 0\n\t"
-      "buffer_load_dwordx4 %[v7], %[r], 0 offen lds"
-      :
-      : [l] "s"(lds), [r] "s"(r), [v0] "v"(vo[0]), [v1] "v"(vo[1]), [v2] "v"(vo[2]), [v3] "v"(vo[3]),
-        [v4] "v"(vo[4]), [v5] "v"(vo[5]), [v6] "v"(vo[6]), [v7] "v"(vo[7])
-      : "memory", "m0", "scc");
+// A buffer resource that moves forward through a region: base and number of
+// bytes left, turned into a descriptor (raw buffer, 32-bit data format) at
+// each use.  Loads at offsets >= num_records return 0 and such stores are
+// dropped (the per-lane offset is range-checked, the scalar offset is not).
+constexpr int kRsrcWord3 = 0x00020000;
+// The count update is written as scalar instructions: the compiler turns
+// the saturating subtraction into a vector instruction otherwise, and the
+// descriptor must live in scalar registers.  Byte counts are below 2^31.
+struct Cursor {
+  const char* base;
+  int left;
+  __device__ __forceinline__ __amdgpu_buffer_rsrc_t rsrc() const {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<char*>(base), 0, left, kRsrcWord3);
+  }
+  __device__ __forceinline__ void advance(int step) {
+    base += step;
+    asm("s_sub_i32 %0, %0, %1\n\ts_max_i32 %0, %0, 0" : "+s"(left) : "s"(step) : "scc");
+  }
+};
+__device__ __forceinline__ Cursor make_cursor(const void* p, int bytes) { return Cursor{static_cast<const char*>(p), bytes}; }
+
+// Buffer resource over the bytes [off, total) of the region at p (empty
+// when off >= total; total < 2^31).
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t sub_rsrc(const void* p, uint64_t total, uint64_t off) {
+  const uint64_t o = off < total ? off : total;
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<char*>(static_cast<const char*>(p)) + o, 0, (int)(uint32_t)(total - o),
+                                           kRsrcWord3);
 }
 
-// Eight 4-byte loads: load k brings every lane's word at voff[k] of the
-// resource to LDS at lds + 256 k + 4 lane.
-__device__ __forceinline__ void dma_words8(uint32_t lds, __amdgpu_buffer_rsrc_t r, const int (&vo)[8]) {
-  asm volatile(
-      "s_mov_b32 m0, %[l]\n\ts_nop 0\n\t"
-      "buffer_load_dword %[v0], %[r], 0 offen lds\n\t"
-      "s_add_u32 m0, %[l], 0x100\n\ts_nop 0\n\t"
-      "buffer_load_dword %[v1], %[r], 0 offen lds\n\t"
-      "s_add_u32 m0, %[l], 0x200\n\ts_nop 0\n\t"
-      "buffer_load_dword %[v2], %[r], 0 offen lds\n\t"
-      "s_add_u32 m0, %[l], 0x300\n\ts_nop 0\n\t"
-      "buffer_load_dword %[v3], %[r], 0 offen lds\n\t"
-      "s_add_u32 m0, %[l], 0x400\n\ts_nop 0\n\t"
-      "buffer_load_dword %[v4], %[r], 0 offen lds\n\t"
-      "s_add_u32 m0, %[l], 0x500\n\ts_nop 0\n\t"
-      "buffer_load_dword %[v5], %[r], 0 offen lds\n\t"
-      "s_add_u32 m0, %[l], 0x600\n\ts_nop 0\n\t"
-      "buffer_load_dword %[v6], %[r], 0 offen lds\n\t"
-      "s_add_u32 m0, %[l], 0x700\n\ts_nop 0\n\t"
-      "buffer_load_dword %[v7], %[r], 0 offen lds"
-      :
-      : [l] "s"(lds), [r] "s"(r), [v0] "v"(vo[0]), [v1] "v"(vo[1]), [v2] "v"(vo[2]), [v3] "v"(vo[3]),
-        [v4] "v"(vo[4]), [v5] "v"(vo[5]), [v6] "v"(vo[6]), [v7] "v"(vo[7])
-      : "memory", "m0", "scc");
+// Loads into LDS (the lds flag): every lane's bytes at its voffset go to LDS
+// at M0 + size * lane.  A scalar write of M0 needs one wait state before
+// such a load.  OFF is added to the LDS base.
+template <int OFF>
+__device__ __forceinline__ void dma16(uint32_t lds, __amdgpu_buffer_rsrc_t r, int voff) {
+  asm volatile("s_add_u32 m0, %[l], %[o]\n\ts_nop 0\n\tbuffer_load_dwordx4 %[v], %[r], 0 offen lds"
+               :
+               : [l] "s"(lds), [o] "n"(OFF), [r] "s"(r), [v] "v"(voff)
+               : "memory", "m0", "scc");
 }
-
+template <int OFF>
+__device__ __forceinline__ void dma4(uint32_t lds, __amdgpu_buffer_rsrc_t r, int voff) {
+  asm volatile("s_add_u32 m0, %[l], %[o]\n\ts_nop 0\n\tbuffer_load_dword %[v], %[r], 0 offen lds"
+               :
+               : [l] "s"(lds), [o] "n"(OFF), [r] "s"(r), [v] "v"(voff)
+               : "memory", "m0", "scc");
+}
+// Device-scope (sc1) variants for data written by other workgroups.
+__device__ __forceinline__ void dma4_dev(uint32_t lds, __amdgpu_buffer_rsrc_t r, int voff) {
+  asm volatile("s_mov_b32 m0, %[l]\n\ts_nop 0\n\tbuffer_load_dword %[v], %[r], 0 offen sc1 lds"
+               :
+               : [l] "s"(lds), [r] "s"(r), [v] "v"(voff)
+               : "memory", "m0");
+}
 // One 16-byte load per lane, device-scope: the bytes at voff of the resource
 // to LDS at lds + 16 lane.
 __device__ __forceinline__ void dma_piece(uint32_t lds, __amdgpu_buffer_rsrc_t r, int voff) {
@@ -156,89 +154,21 @@ __device__ __forceinline__ void dma_piece(uint32_t lds, __amdgpu_buffer_rsrc_t r
                : "memory", "m0");
 }
 
-// One 16-byte piece per lane, device-scope, to LDS at lds + 16 lane.
-__device__ __forceinline__ void dma_poll(uint32_t lds, __amdgpu_buffer_rsrc_t r, int voff) {
-  asm volatile("s_mov_b32 m0, %[l]\n\ts_nop 0\n\tbuffer_load_dwordx4 %[v], %[r], 0 offen sc1 lds"
-               :
-               : [l] "s"(lds), [r] "s"(r), [v] "v"(voff)
-               : "memory", "m0");
-}
-
-// A placeholder operation that keeps a step's operation count when it has
-// nothing to store: one 4-byte load per lane into a scratch LDS area.
-__device__ __forceinline__ void dma_dummy(uint32_t lds, __amdgpu_buffer_rsrc_t r, int voff) {
-  asm volatile("s_mov_b32 m0, %[l]\n\ts_nop 0\n\tbuffer_load_dword %[v], %[r], 0 offen lds"
-               :
-               : [l] "s"(lds), [r] "s"(r), [v] "v"(voff)
-               : "memory", "m0");
-}
-
-__device__ __forceinline__ void vm_store32(uint64_t a, uint32_t v) {
-  asm volatile("global_store_dword %0, %1, off sc1" ::"v"(a), "v"(v) : "memory");
-}
-__device__ __forceinline__ void vm_store64(uint64_t a, uint64_t v) {
-  asm volatile("global_store_dwordx2 %0, %1, off sc1" ::"v"(a), "v"(v) : "memory");
-}
-// Two 16-byte zero stores (s_nop: a VALU write of store data needs one wait
-// state).  Path bytes are only ever written by the wave that owns their row,
-// so these need no device-scope write-through.
-__device__ __forceinline__ void vm_zero2(uint64_t a0, uint64_t a1, u32x4 z) {
-  asm volatile("global_store_dwordx4 %0, %2, off\n\tglobal_store_dwordx4 %1, %2, off\n\ts_nop 0" ::"v"(a0), "v"(a1), "v"(z)
+// Stores at voff + soff of a resource, device-scope (write-through).
+__device__ __forceinline__ void buf_store32(uint32_t v, int voff, __amdgpu_buffer_rsrc_t r, uint32_t soff) {
+  asm volatile("buffer_store_dword %[d], %[v], %[r], %[s] offen sc1" ::[d] "v"(v), [v] "v"(voff), [r] "s"(r), [s] "s"(soff)
                : "memory");
 }
+__device__ __forceinline__ void buf_store64(uint64_t v, int voff, __amdgpu_buffer_rsrc_t r, uint32_t soff) {
+  asm volatile("buffer_store_dwordx2 %[d], %[v], %[r], %[s] offen sc1" ::[d] "v"(v), [v] "v"(voff), [r] "s"(r), [s] "s"(soff)
+               : "memory");
+}
+// A 16-byte zero store (s_nop: a VALU write of store data needs one wait
+// state).  Path bytes are only ever written by the wave that owns their row,
+// so this needs no device-scope write-through.
 __device__ __forceinline__ void vm_zero1(uint64_t a, u32x4 z) {
   asm volatile("global_store_dwordx4 %0, %1, off\n\ts_nop 0" ::"v"(a), "v"(z) : "memory");
 }
-
-// Vector-memory operations of one sweep step, in issue order:
-//   [poll of chunk c+2]  (waves fed by another workgroup)
-//   tile of chunk c+kDepth (8 ops, or 32 for the 4-byte variant)
-//   decision word of chunk c (1)
-//   [boundary words of chunk c]  (waves that feed another workgroup)
-//   [2 zero stores]      (when the path is written)
-constexpr int step_ops(int nl, bool in2, bool h, bool z) { return (in2 ? 1 : 0) + nl + 1 + (h ? 1 : 0) + (z ? 2 : 0); }
-// Count for the wait at the start of step c: tile c was issued kDepth steps
-// earlier (followed by that step's stores and kDepth-1 whole steps), the
-// poll of chunk c two steps earlier (followed by that step's tile and stores
-// and one whole step).  Counts above 63 are clamped: at most 63 operations
-// are ever outstanding, so the clamped wait still covers the operation.
-constexpr int wait_count(int nl, bool in2, bool h, bool z) {
-  const int k = step_ops(nl, in2, h, z);
-  const int tail = 1 + (h ? 1 : 0) + (z ? 2 : 0);
-  const int n_tile = tail + (kDepth - 1) * k;
-  const int n_poll = nl + tail + k;
-  const int n = in2 && n_poll < n_tile ? n_poll : n_tile;
-  return n > 63 ? 63 : n;
-}
-
-template <int NL, bool IN2>
-__device__ __forceinline__ void wait_step(bool h, bool z) {
-  if (h) {
-    if (z)
-      vm_wait<wait_count(NL, IN2, true, true)>();
-    else
-      vm_wait<wait_count(NL, IN2, true, false)>();
-  } else {
-    if (z)
-      vm_wait<wait_count(NL, IN2, false, true)>();
-    else
-      vm_wait<wait_count(NL, IN2, false, false)>();
-  }
-}
-
-// Buffer resource over the bytes [off, total) of the region at p (empty
-// when off >= total; total < 2^31).  Loads outside a resource return 0.
-__device__ __forceinline__ __amdgpu_buffer_rsrc_t sub_rsrc(const void* p, uint64_t total, uint64_t off) {
-  const uint64_t o = off < total ? off : total;
-  return __builtin_amdgcn_make_buffer_rsrc(const_cast<char*>(static_cast<const char*>(p)) + o, 0, (int)(uint32_t)(total - o),
-                                           0x00020000);
-}
-
-// XOR swizzle of 16-byte slots inside a tile row: slot (r, p) holds piece
-// p ^ swz(r).  Distinct over 8 consecutive rows and over the 8 same-parity
-// rows of any 16 consecutive rows, so 8- and 16-lane LDS phases are
-// conflict-free for both the tile writes and the per-row reads.
-__device__ __forceinline__ int swz(int r) { return (r & 7) ^ ((r >> 3) & 1); }
 
 // The recurrence, one text row per lane, lane 0 carrying the row above the
 // wave.  Per column j (Algorithm 2's parallel step):
@@ -380,18 +310,29 @@ constexpr int kWalkWin = kWalkLoads * 4 * kWave;   // rows per window
 constexpr int kWalkSlots = 16;                 // window ring (power of two > kWalkAhead)
 static_assert(kWalkWin >= 32 * (kWalkAhead - 1) + kWave + 3, "walk window");
 
-// One hand-off slot between waves of a workgroup: the producer's last-row Q
-// over one chunk, then a tag (chunk + 1) written after the values.
-struct RingSlot {
-  f32x4 q[kChunk / 4];
-  int tag[4];
-};
+// Value tiles.  Each wave has kStages stages; the stage of chunk c is
+// (c - c_begin) % kStages (c_begin: the wave's first chunk).  A stage holds
+//   * 64 tile rows of 32 values: item rows 63g .. 63g+63 (row 63 unused), row
+//     r at byte 144 r.  The 16 bytes of padding per row put piece k of 16
+//     consecutive rows in distinct 4-bank groups of the 64-bank LDS
+//     (36 r mod 64 differs for r mod 16), so the per-row reads of a wave are
+//     conflict-free with one address per lane plus the piece offset;
+//   * the boundary row at kBoundOff: the 32 Q values of the row above the
+//     wave for the stage's chunk (word 2332 = 28 mod 64, a bank group that
+//     rows 0 .. 14 do not use), then its tag (chunk + 1) at kTagOff.  The
+//     previous wave of the workgroup writes it; a wave fed by another
+//     workgroup copies its polled words there; the first wave of an item
+//     fills it with -inf once.
+constexpr int kRowBytes = 144;
+constexpr int kBoundOff = 9328;
+constexpr int kTagOff = kBoundOff + 4 * kChunk;
+constexpr int kStageBytes = 9472;
+static_assert(64 * kRowBytes <= kBoundOff && kBoundOff % 16 == 0 && (kBoundOff / 4) % 64 == 28, "boundary slot");
+static_assert(kTagOff + 4 <= kStageBytes && kStageBytes % 256 == 0, "stage size");
 
 struct SweepLds {
   union {
-    // Value tiles: [wave][slot] rows 63g .. 63g+63 x 32 columns, 16-byte unit
-    // 8 r + s holds piece s ^ swz(r) of tile row r.
-    f32x4 tile[kWavesPerBlock][kStages][8 * kWave];
+    uint8_t tile[kWavesPerBlock][kStages][kStageBytes];
     // The walker's staging, once every sweep of its item (and so of its
     // workgroup) has finished.
     struct {
@@ -399,13 +340,12 @@ struct SweepLds {
       int rs[kMaxRows + 2 * kWave];        // row_start under construction
     } walk;
   } u;
-  RingSlot ring[kWavesPerBlock - 1][kRing];       // wave w -> w+1 boundary rows
-  uint64_t poll[kPollSlots][2 * kWave];           // polled boundary words (4 copies of 32)
-  f32x4 stage[kWavesPerBlock][kChunk / 4];        // boundary row staging (global hand-off)
-  f32x4 ninf[kChunk / 4];                         // a chunk of -inf (the row above row 0)
-  uint32_t dummy[kWavesPerBlock][kWave];          // target of placeholder loads
-  int cons[kWavesPerBlock];                       // next chunk wave w will consume
+  uint32_t poll[kPollSlots][kWave];        // polled boundary words {value, tag} x 32 (wave 0)
+  f32x4 ostage[kChunk / 4];                // last row of wave 3 before its global hand-off
+  uint32_t dummy[kWavesPerBlock][kWave];   // target of placeholder loads and idle lanes' writes
+  int cons[kWavesPerBlock];                // next chunk wave w will consume
 };
+static_assert(sizeof(SweepLds) <= 160 * 1024, "LDS");
 
 // ---------------------------------------------------------------- path clearing
 // The bytes [p0, p1) of the path that one wave clears: its 63 rows of its
@@ -445,21 +385,10 @@ __device__ __forceinline__ void zero_rest(const ZeroPlan& z, uint64_t from, int 
 // ---------------------------------------------------------------- sweep
 // Per-wave constants of the sweep.
 struct WaveCtx {
-  int lane, wv, b, g, g_last, tx, ty, row, c_begin, c_end, out_mode;
-  int prev_end;                     // chunks the previous wave computes (exclusive end)
-  int mask_end;                     // first chunk without a cell i > j of this wave
-  bool zero;                        // this wave clears its path rows during its steps
-  const float* slab;                // the item's value slab [T][S]
-  uint64_t slab_bytes;
-  uint64_t row_off;                 // byte offset of the wave's first tile row in the slab
-  const uint64_t* pslots;           // the previous wave's boundary words (IN == 2)
-  uint64_t pslot_bytes;
-  int voff[8];                      // per-lane byte offsets of the tile loads
-  uint32_t tile0;                   // LDS offset of this wave's tile slot 0
-  uint32_t dummy;                   // LDS offset of this wave's placeholder area
-  uint64_t decp;                    // &dec[b][0][row] (lane 0: the scratch word)
-  uint64_t slotp;                   // &slots[b][g][lane % 32] (boundary words out)
-  ZeroPlan zp;
+  int lane, wv, b, g, g_last, tx, ty, row, c_begin, c_end;
+  int prev_end;    // chunks the previous wave computes (exclusive end)
+  int mask_end;    // first chunk without a cell i > j of this wave
+  int next_begin;  // the next wave's first chunk
 };
 
 // Chunks of wave g worth computing: from the first chunk holding a cell with
@@ -474,77 +403,136 @@ __device__ __forceinline__ int chunk_end(int g, int tx, int ty) {
   return by_len < by_reach ? by_len : by_reach;
 }
 
+// Vector-memory operations of one sweep step, in issue order:
+//   [poll of chunk c+2]        (IN == 2)
+//   tile of chunk c+kDepth     (NL loads)
+//   decision words of chunk c  (1 store)
+//   [boundary words of c]      (OUT == 2: 1 store)
+constexpr int step_ops(int nl, bool in2, bool out2) { return (in2 ? 1 : 0) + nl + 1 + (out2 ? 1 : 0); }
+// Count for the wait at the start of step c: tile c was issued kDepth steps
+// earlier (followed by that step's stores and kDepth-1 whole steps), the
+// poll of chunk c two steps earlier (followed by that step's tile and stores
+// and one whole step).  Counts above 63 are clamped: a wave has at most 63
+// operations outstanding (issue stalls at the counter's limit), so anything
+// issued earlier than that has completed.
+constexpr int wait_count(int nl, bool in2, bool out2) {
+  const int k = step_ops(nl, in2, out2);
+  const int tail = 1 + (out2 ? 1 : 0);
+  const int n_tile = tail + (kDepth - 1) * k;
+  const int n_poll = nl + tail + k;
+  const int n = in2 && n_poll < n_tile ? n_poll : n_tile;
+  return n > 63 ? 63 : n;
+}
+
+// The 4-byte tile loads K .. N-1 (load k fills LDS bytes 256 k .. 256 k + 255).
+template <int K, int N>
+__device__ __forceinline__ void dma4_loads(uint32_t dst, __amdgpu_buffer_rsrc_t r, const int* vo) {
+  if constexpr (K < N) {
+    dma4<256 * K>(dst, r, vo[K]);
+    dma4_loads<K + 1, N>(dst, r, vo);
+  }
+}
+// The 16-byte tile loads K .. N-1 (load k fills LDS bytes 1024 k .. 1024 k + 1023).
+template <int K, int N>
+__device__ __forceinline__ void dma16_loads(uint32_t dst, __amdgpu_buffer_rsrc_t r, const int* vo) {
+  if constexpr (K < N) {
+    dma16<1024 * K>(dst, r, vo[K]);
+    dma16_loads<K + 1, N>(dst, r, vo);
+  }
+}
+
+// Byte offset of (tile row r, byte e of the row's 128) in the value slab
+// relative to the tile's first row, or an offset no resource covers.
+__device__ __forceinline__ int tile_voff(int r, int e, int S) {
+  const uint64_t o = (uint64_t)r * (uint64_t)S * 4u + (uint64_t)e;
+  return o < 0x80000000ull ? (int)o : -16;
+}
+
 // Sweeps this wave's rows over its chunks and returns the score candidate
 // (Q at (row, t_y-1) of this lane; only meaningful for the wave holding row
 // t_x-1).  IN: where the row above the wave comes from — 0 nowhere (the wave
-// holds row 0), 1 the LDS ring of the previous wave of the workgroup, 2
-// global boundary words of the previous workgroup.  out_mode: 0 no
-// consumer, 1 LDS ring, 2 global boundary words.
-template <bool ALIGNED, int IN>
+// holds row 0), 1 the previous wave of the workgroup, 2 global boundary words
+// of the previous workgroup.  OUT: 0 no consumer, 1 the next wave of the
+// workgroup, 2 global boundary words for the next workgroup.
+template <bool ALIGNED, int IN, int OUT>
 __device__ __forceinline__ float sweep_rows(const KParams& p, SweepLds& L, const WaveCtx& x, uint32_t tag, bool& timed_out) {
-  constexpr int NL = ALIGNED ? 8 : 32;
-  constexpr bool IN2 = IN == 2;
+  constexpr int NL = ALIGNED ? 9 : 36;  // tile loads per chunk (padding slots included)
+  constexpr bool IN2 = IN == 2, OUT2 = OUT == 2;
   const int lane = x.lane, wv = x.wv;
-  const bool h = x.out_mode == 2, zero = x.zero;
-  float score = neg_inf();
   float t = -0.0f;  // lane 0 keeps -0 for the whole sweep (see cols8)
-  const u32x4 zv = {0u, 0u, 0u, 0u};
-  const int dvo = 4 * lane;  // placeholder loads read the slab's first 256 bytes
-  const __amdgpu_buffer_rsrc_t drsrc = sub_rsrc(x.slab, x.slab_bytes, 0);
 
-  // Tile of chunk c into its slot.
-  auto issue_tile = [&](int c) __attribute__((always_inline)) {
-    const uint32_t dst = x.tile0 + (uint32_t)((c & (kStages - 1)) * 8 * kWave * 16);
-    const uint64_t off = x.row_off + (uint64_t)c * (kChunk * 4);
-    if (ALIGNED) {
-      dma_tile16(dst, sub_rsrc(x.slab, x.slab_bytes, off), x.voff);
-    } else {
-      // Four groups of 8 loads; group hh covers tile rows 16hh .. 16hh+15.
+  // Value tiles: a resource from the wave's first tile row at the next chunk
+  // to load; rows past the slab fall outside it and read 0.
+  const float* slab = p.value + (size_t)x.b * (size_t)p.T * (size_t)p.S;
+  const uint32_t slab_bytes = (uint32_t)((uint64_t)p.T * (uint64_t)p.S * 4u);
+  const uint32_t first = (uint32_t)((uint64_t)x.g * kRowsPerWave * (uint64_t)p.S * 4u) + (uint32_t)x.c_begin * (kChunk * 4);
+  Cursor vr = make_cursor(reinterpret_cast<const char*>(slab), (int)slab_bytes);
+  vr.advance((int)first);
+  // Per-lane load offsets: load k, lane L fills stage slot 64 k + L (16-byte
+  // slots, nine per row: eight pieces and the padding) or word 64 k + L
+  // (4-byte words, 36 per row).
+  int voff[NL];
 #pragma unroll
-      for (int hh = 0; hh < 4; ++hh)
-        dma_words8(dst + hh * 2048, sub_rsrc(x.slab, x.slab_bytes, off + (uint64_t)hh * 16u * (uint64_t)p.S * 4u), x.voff);
+  for (int k = 0; k < NL; ++k) {
+    if (ALIGNED) {
+      const int sl = 64 * k + lane, r = sl / 9, pc = sl % 9;
+      voff[k] = pc < 8 ? tile_voff(r, 16 * pc, p.S) : -16;
+    } else {
+      const int w = 64 * k + lane, r = w / 36, wi = w % 36;
+      voff[k] = wi < 32 ? tile_voff(r, 4 * wi, p.S) : -16;
     }
-  };
-  // Boundary words of chunk c (32 u64 = 256 bytes, 4 copies) into poll slot c % 4.
-  const int pvo = 16 * (lane & 15);
-  auto issue_poll = [&](int c) __attribute__((always_inline)) {
-    dma_poll(lds_off(&L.poll[c & (kPollSlots - 1)][0]), sub_rsrc(x.pslots, x.pslot_bytes, (uint64_t)c * kChunk * 8u), pvo);
-  };
-  int zk = 0;  // zero steps issued
-  auto issue_zero = [&]() __attribute__((always_inline)) {
-    if (zero) {
-      uint64_t a0 = x.zp.a0 + (uint64_t)zk * 2048u + 16u * (uint64_t)lane;
-      uint64_t a1 = a0 + 1024u;
-      a0 = a0 < x.zp.last ? a0 : x.zp.last;
-      a1 = a1 < x.zp.last ? a1 : x.zp.last;
-      vm_zero2(a0, a1, zv);
-      ++zk;
-    }
-  };
-  // Boundary words of chunk c in poll slot c % 4, word lane % 32, once every
-  // one of them carries this call's tag (re-polled until then).
+  }
+  // LDS: tile0 is this wave's stage 0 as an LDS address (for M0); the C++
+  // accesses use byte offsets from the start of L (where the tiles begin).
+  char* const Lc = reinterpret_cast<char*>(&L);
+  const uint32_t tile_rel = (uint32_t)wv * (kStages * kStageBytes);
+  const uint32_t tile0 = lds_off(&L.u.tile[wv][0][0]);
+  // Lane l reads tile row l-1 of a stage; lane 0 reads the boundary row.
+  const uint32_t rbase = tile_rel + (lane > 0 ? (uint32_t)(lane - 1) * kRowBytes : (uint32_t)kBoundOff);
+  // Placeholder loads (steps with no store yet) read the slab's first 256 bytes.
+  const uint32_t dummy = lds_off(&L.dummy[wv][0]);
+  const __amdgpu_buffer_rsrc_t drsrc = make_cursor(slab, min((int)slab_bytes, 256)).rsrc();
+  // Decision words: dec[b][c][row], lane 0 into the chunk's scratch word.
+  const __amdgpu_buffer_rsrc_t dr = make_cursor(p.dec + (size_t)x.b * p.NC * (size_t)p.TP, p.NC * p.TP * 4).rsrc();
+  const int dvo = 4 * (lane > 0 ? x.row : p.TP - 1);
+  const uint32_t dstride = (uint32_t)p.TP * 4u;
+  // Boundary words of this wave (OUT == 2) and of the previous one (IN == 2).
+  const size_t slot_stride = (size_t)p.NC * kChunk;
+  const int slot_bytes = (int)(slot_stride * 8u);
+  const __amdgpu_buffer_rsrc_t sr = make_cursor(p.slots + ((size_t)x.b * p.NW + x.g) * slot_stride, slot_bytes).rsrc();
+  const int svo = lane < kChunk ? 8 * lane : -16;
+  const uint64_t* pslots = p.slots + ((size_t)x.b * p.NW + (x.g > 0 ? x.g - 1 : 0)) * slot_stride;
+  Cursor pr = make_cursor(pslots, slot_bytes);
+  if (IN2) pr.advance((x.c_begin - 1) * 256);  // first poll: chunk c_begin-1
+
+  // Boundary words of chunk c are in poll slot c % 4 once all carry this
+  // call's tag (re-polled until then); lane L's word is L % 32.
   auto polled_word = [&](int c) __attribute__((always_inline)) -> uint64_t {
-    const int sl = c & (kPollSlots - 1);
-    uint64_t wd = L.poll[sl][lane & (kChunk - 1)];
+    const uint64_t* pw = reinterpret_cast<const uint64_t*>(&L.poll[c & (kPollSlots - 1)][0]);
+    uint64_t wd = pw[lane & (kChunk - 1)];
     int spins = 0;
-    while (__builtin_amdgcn_ballot_w64((uint32_t)(wd >> 32) != tag) != 0) {
+    while (true) {
+      // Lanes still seeing an old tag, as an opaque scalar: branching on the
+      // ballot directly lets the compiler treat the loop as divergent.
+      uint64_t stale = __builtin_amdgcn_ballot_w64((uint32_t)(wd >> 32) != tag);
+      asm volatile("" : "+s"(stale));
+      if (stale == 0) break;
       if (++spins > kSpinLimit) {
         timed_out = true;
         break;
       }
       __builtin_amdgcn_s_sleep(1);
-      issue_poll(c);
+      dma4_dev(lds_off(&L.poll[c & (kPollSlots - 1)][0]), make_cursor(pslots + (size_t)c * kChunk, kChunk * 8u).rsrc(), 4 * lane);
       vm_wait<0>();
-      wd = L.poll[sl][lane & (kChunk - 1)];
+      wd = pw[lane & (kChunk - 1)];
     }
     return wd;
   };
-  // Ring slot of chunk c from the previous wave, once its tag says it is
-  // written (the tag is read before the values, and written after them).
-  auto ring_ready = [&](int c) __attribute__((always_inline)) {
-    const int* tg = &L.ring[wv - 1][c % kRing].tag[0];
+  // Waits for the boundary row of chunk c in the stage at byte offset so.
+  auto bound_ready = [&](int c, uint32_t so) __attribute__((always_inline)) {
+    const int* tg = reinterpret_cast<const int*>(Lc + tile_rel + so + kTagOff);
     int spins = 0;
-    while (lds_load(tg) != c + 1) {
+    while (__builtin_amdgcn_readfirstlane(lds_load(tg)) != c + 1) {
       if (++spins > kSpinLimit) {
         timed_out = true;
         break;
@@ -553,116 +541,147 @@ __device__ __forceinline__ float sweep_rows(const KParams& p, SweepLds& L, const
     }
   };
 
-  // Pieces beyond what the steps will clear, up front.
-  if (zero) zero_rest(x.zp, x.zp.a0 + (uint64_t)(kDepth + x.c_end - x.c_begin) * 2048u, lane);
+  if (IN == 0) {
+    // The row above row 0 is -inf in every stage.
+    if (lane < kChunk) {
+#pragma unroll
+      for (int st = 0; st < kStages; ++st)
+        reinterpret_cast<float*>(&L.u.tile[wv][st][kBoundOff])[lane] = neg_inf();
+    }
+  }
 
   // Prologue: kDepth placeholder steps with the steady-state operation
   // sequence, so that the loop's wait counts hold from its first step.
-  for (int c = x.c_begin - kDepth; c < x.c_begin; ++c) {
-    if (IN2) issue_poll(c + 2);  // chunks c_begin-1 .. c_begin+1
-    issue_tile(c + kDepth);
-    dma_dummy(x.dummy, drsrc, dvo);
-    if (h) dma_dummy(x.dummy, drsrc, dvo);
-    issue_zero();
+#pragma unroll
+  for (int k = 0; k < kDepth; ++k) {
+    if (IN2) {
+      dma4_dev(lds_off(&L.poll[(x.c_begin - 1 + k) & (kPollSlots - 1)][0]), pr.rsrc(), 4 * lane);
+      pr.advance(256);
+    }
+    if (ALIGNED)
+      dma16_loads<0, NL>(tile0 + k * kStageBytes, vr.rsrc(), voff);
+    else
+      dma4_loads<0, NL>(tile0 + k * kStageBytes, vr.rsrc(), voff);
+    vr.advance(kChunk * 4);
+    dma4<0>(dummy, drsrc, 4 * lane);
+    if (OUT2) dma4<0>(dummy, drsrc, 4 * lane);
   }
 
   // Lane 0's Q at the column before the first chunk: the previous wave's
   // last row there (its chunk c_begin-1, always computed), or -inf.
   float q = neg_inf();
   if (IN == 1) {
-    ring_ready(x.c_begin - 1);
+    bound_ready(x.c_begin - 1, (kStages - 1) * kStageBytes);
     wave_lds_sync();
-    const f32x4 e = L.ring[wv - 1][(x.c_begin - 1) % kRing].q[kChunk / 4 - 1];
-    q = lane == 0 ? e.w : q;
+    const float e = reinterpret_cast<const float*>(&L.u.tile[wv][kStages - 1][kBoundOff])[kChunk - 1];
+    q = lane == 0 ? e : q;
+    wave_lds_sync();
+    if (lane == 0) lds_store(&L.cons[wv], x.c_begin);
   } else if (IN == 2) {
     vm_wait<0>();
     const uint64_t wd = polled_word(x.c_begin - 1);
     const float e = __int_as_float(__builtin_amdgcn_readlane((int)(uint32_t)wd, kChunk - 1));
     q = lane == 0 ? e : q;
   }
-  if (lane == 0) lds_store(&L.cons[wv], x.c_begin);
 
-  // This lane's 32 values come from its tile row (lanes 1..63: tile row
-  // lane-1) or, for lane 0, from the row above's 32 Q values.
-  const int tsw = lane > 0 ? swz(lane - 1) : 0;
-  const int trow = lane > 0 ? lane - 1 : 0;
+  // Stage offsets: so of chunk c (the one computed), sd of chunk c+kDepth,
+  // sn of chunk c in the next wave's stages.
+  uint32_t so = 0, sd = (kStages - 1) * kStageBytes;
+  uint32_t sn = (uint32_t)((x.c_begin - x.next_begin) & (kStages - 1)) * kStageBytes;
+  const uint32_t tile_next = tile_rel + kStages * kStageBytes;
+  // Lane 0 publishes the consumed-chunk counter; the other lanes write
+  // their own dummy words (one store, no exec change).
+  int* const cons_ptr = lane == 0 ? &L.cons[wv] : reinterpret_cast<int*>(&L.dummy[wv][lane]);
   // Lower bound of the consumer's counter: it starts at its own c_begin-1,
   // which is at least this wave's c_begin+1 (63 rows span >= 63 columns).
   int cons_seen = x.c_begin + 1;
+  float qc[kChunk];
+  uint32_t soff = (uint32_t)x.c_begin * dstride;
   for (int c = x.c_begin; c < x.c_end; ++c) {
-    wait_step<NL, IN2>(h, zero);
-    if (IN2) issue_poll(c + 2);
-    issue_tile(c + kDepth);
+    vm_wait<wait_count(NL, IN2, OUT2)>();
+    if (IN2) {
+      dma4_dev(lds_off(&L.poll[(c + 2) & (kPollSlots - 1)][0]), pr.rsrc(), 4 * lane);
+      pr.advance(256);
+    }
+    if (ALIGNED)
+      dma16_loads<0, NL>(tile0 + sd, vr.rsrc(), voff);
+    else
+      dma4_loads<0, NL>(tile0 + sd, vr.rsrc(), voff);
+    vr.advance(kChunk * 4);
 
-    // Source of lane 0's values for this chunk.
-    const f32x4* gsrc = L.ninf;
-    if (IN == 1 && c < x.prev_end) {
-      ring_ready(c);
-      gsrc = L.ring[wv - 1][c % kRing].q;
-    } else if (IN == 2 && c < x.prev_end) {
+    // The row above: from the previous wave, or copied from the polled
+    // words.  Beyond the previous wave's chunks the slot holds stale values:
+    // they only reach cells that cannot reach (t_x-1, t_y-1).
+    if (IN == 1 && c < x.prev_end) bound_ready(c, so);
+    if (IN == 2 && c < x.prev_end) {
       const uint64_t wd = polled_word(c);
-      float* sf = reinterpret_cast<float*>(L.stage[wv]);
-      if (lane < kChunk) sf[lane] = __uint_as_float((uint32_t)wd);
-      gsrc = L.stage[wv];
+      reinterpret_cast<float*>(Lc + tile_rel + so + kBoundOff)[lane & (kChunk - 1)] = __uint_as_float((uint32_t)wd);
     }
     wave_lds_sync();
     f32x4 v[8];
     {
-      const f32x4* base = lane > 0 ? L.u.tile[wv][c & (kStages - 1)] + 8 * trow : gsrc;
-      const int sw = lane > 0 ? tsw : 0;
+      const f32x4* base = reinterpret_cast<const f32x4*>(Lc + rbase + so);
 #pragma unroll
-      for (int k = 0; k < 8; ++k) v[k] = base[k ^ sw];
+      for (int k = 0; k < 8; ++k) v[k] = base[k];
     }
-    wave_lds_sync();
-    if (IN == 1 && lane == 0) lds_store(&L.cons[wv], c + 1);
-    float qc[kChunk];
     uint32_t bits = 0;
     if (c < x.mask_end)
       sweep_chunk<true>(q, t, v, qc, bits, lane, x.row, c * kChunk);
     else
       sweep_chunk<false>(q, t, v, qc, bits, lane, x.row, c * kChunk);
-
-    // Stores of the step: decision word, boundary row, path zeros.
-    vm_store32(x.decp + (uint64_t)c * (uint64_t)p.TP * 4u, bits);
-    if (x.out_mode == 1) {
-      // Wait until the consumer no longer needs the ring slot, then publish
-      // the values, then the tag.
+    buf_store32(bits, dvo, dr, soff);
+    soff += dstride;
+    if (IN == 1) {
+      // The reads of this chunk's slot are done: the previous wave may
+      // reuse it for chunk c + kStages.
+      wave_lds_sync();
+      lds_store(cons_ptr, c + 1);
+    }
+    if (OUT == 1) {
+      // Wait until the consumer no longer needs the slot, then publish the
+      // values, then the tag.
       int spins = 0;
-      while (cons_seen < c - (kRing - 2)) {
-        cons_seen = lds_load(&L.cons[wv + 1]);
-        if (cons_seen >= c - (kRing - 2)) break;
+      while (cons_seen < c - (kStages - 1)) {
+        cons_seen = __builtin_amdgcn_readfirstlane(lds_load(&L.cons[wv + 1]));
+        if (cons_seen >= c - (kStages - 1)) break;
         if (++spins > kSpinLimit) {
           timed_out = true;
           break;
         }
         __builtin_amdgcn_s_sleep(1);
       }
-      RingSlot& rs = L.ring[wv][c % kRing];
+      if (lane == kWave - 1) {
+        f32x4* dst = reinterpret_cast<f32x4*>(Lc + tile_next + sn + kBoundOff);
+#pragma unroll
+        for (int k = 0; k < kChunk / 4; ++k) dst[k] = f32x4{qc[4 * k], qc[4 * k + 1], qc[4 * k + 2], qc[4 * k + 3]};
+      }
+      // Values before the tag (the LDS executes one wave's operations in
+      // order; the fence keeps the compiler from reordering them).  Kept out
+      // of the lane-63 branch: inside it, the compiler makes the whole chunk
+      // loop divergent for the waves that feed no other wave of the group.
+      wave_lds_sync();
+      if (lane == kWave - 1) lds_store(reinterpret_cast<int*>(Lc + tile_next + sn + kTagOff), c + 1);
+      sn = sn == (kStages - 1) * kStageBytes ? 0u : sn + kStageBytes;
+    } else if (OUT == 2) {
       if (lane == kWave - 1) {
 #pragma unroll
-        for (int k = 0; k < kChunk / 4; ++k) rs.q[k] = f32x4{qc[4 * k], qc[4 * k + 1], qc[4 * k + 2], qc[4 * k + 3]};
+        for (int k = 0; k < kChunk / 4; ++k) L.ostage[k] = f32x4{qc[4 * k], qc[4 * k + 1], qc[4 * k + 2], qc[4 * k + 3]};
       }
       wave_lds_sync();
-      if (lane == kWave - 1) lds_store(&rs.tag[0], c + 1);
-    } else if (h) {
-      if (lane == kWave - 1) {
-#pragma unroll
-        for (int k = 0; k < kChunk / 4; ++k) L.stage[wv][k] = f32x4{qc[4 * k], qc[4 * k + 1], qc[4 * k + 2], qc[4 * k + 3]};
-      }
-      wave_lds_sync();
-      const float val = reinterpret_cast<const float*>(L.stage[wv])[lane & (kChunk - 1)];
-      const uint64_t word = ((uint64_t)tag << 32) | (uint64_t)__float_as_uint(val);
-      vm_store64(x.slotp + (uint64_t)c * kChunk * 8u, word);
+      const float val = reinterpret_cast<const float*>(L.ostage)[lane & (kChunk - 1)];
+      buf_store64(((uint64_t)tag << 32) | (uint64_t)__float_as_uint(val), svo, sr, (uint32_t)c * 256u);
       wave_lds_sync();
     }
-    issue_zero();
-    if (x.g == x.g_last && c == x.c_end - 1) {
-      const int m_last = (x.ty - 1) % kChunk;
-#pragma unroll
-      for (int m = 0; m < kChunk; ++m) score = (m == m_last) ? qc[m] : score;
-    }
+    so = so == (kStages - 1) * kStageBytes ? 0u : so + kStageBytes;
+    sd = sd == (kStages - 1) * kStageBytes ? 0u : sd + kStageBytes;
   }
   vm_wait<0>();
+  float score = neg_inf();
+  if (OUT == 0) {
+    const int m_last = (x.ty - 1) % kChunk;
+#pragma unroll
+    for (int m = 0; m < kChunk; ++m) score = (m == m_last) ? qc[m] : score;
+  }
   return score;
 }
 
@@ -817,11 +836,12 @@ __device__ __forceinline__ void sweep_block(const KParams& p, SweepLds& L, int s
   const int st = item_status(tx, ty, p.T, p.S);
   const int c_begin = (g * kRowsPerWave) / kChunk;
 
-  // Workgroup set-up: no ring slot is written yet; each wave's first chunk
-  // to consume (its carried row starts at chunk c_begin-1); the -inf chunk.
-  for (int i = threadIdx.x; i < (kWavesPerBlock - 1) * kRing; i += kThreadsPerBlock) lds_store(&L.ring[i / kRing][i % kRing].tag[0], 0);
+  // Workgroup set-up: no boundary row is written yet (the LDS holds
+  // whatever earlier workgroups left); each wave's first chunk to consume
+  // (its carried row comes from chunk c_begin-1).
+  if (threadIdx.x < kWavesPerBlock * kStages)
+    lds_store(reinterpret_cast<int*>(&L.u.tile[threadIdx.x / kStages][threadIdx.x % kStages][kTagOff]), 0);
   if (lane == 0) lds_store(&L.cons[wv], c_begin - 1);
-  if (threadIdx.x < kChunk / 4) L.ninf[threadIdx.x] = f32x4{neg_inf(), neg_inf(), neg_inf(), neg_inf()};
   __syncthreads();
 
   int32_t* rs_out = p.row_start + (size_t)b * ((size_t)p.T + 1);
@@ -854,6 +874,10 @@ __device__ __forceinline__ void sweep_block(const KParams& p, SweepLds& L, int s
     return;
   }
   if (g == 0 && lane == 0 && p.status) p.status[b] = kItemOk;
+  // The walker's wave clears its rows first: it waits for the waves above
+  // it anyway (for g_last > 0), and the walk then ends with only the ones
+  // left to write.  The other waves clear theirs after their sweep.
+  if (clear && g == g_last) zero_rest(zp, zp.a0, lane);
 
   WaveCtx x;
   x.lane = lane;
@@ -868,45 +892,17 @@ __device__ __forceinline__ void sweep_block(const KParams& p, SweepLds& L, int s
   x.c_end = chunk_end(g, tx, ty);
   x.prev_end = g > 0 ? chunk_end(g - 1, tx, ty) : 0;
   x.mask_end = (g * kRowsPerWave + kRowsPerWave - 2) / kChunk + 1;  // last masked column: 63g + 61
-  x.out_mode = g == g_last ? 0 : (wv < kWavesPerBlock - 1 ? 1 : 2);
-  // The walker's wave clears its rows during its steps; the others after.
-  x.zero = clear && g == g_last;
-  x.zp = zp;
-  x.slab = p.value + (size_t)b * (size_t)p.T * (size_t)p.S;
-  x.slab_bytes = (uint64_t)p.T * (uint64_t)p.S * 4u;
-  x.row_off = (uint64_t)g * kRowsPerWave * (uint64_t)p.S * 4u;
-  const size_t slot_stride = (size_t)p.NC * kChunk;
-  x.pslots = p.slots + ((size_t)b * p.NW + (g > 0 ? g - 1 : 0)) * slot_stride;
-  x.pslot_bytes = slot_stride * 8u;
-  // Tile rows 0..63 are item rows 63g .. 63g+63 (row 63 is not used); offsets
-  // are relative to the first tile row at the chunk's first column, and rows
-  // past the slab fall outside the resource and read 0.  Tile rows below 64
-  // and S * 4 * 64 < 2^31 keep them in range of an int.
-  if (ALIGNED) {
-    // Load q: lane L reads tile row 8q + L/8, piece (L%8) ^ swz(row).
-#pragma unroll
-    for (int q = 0; q < 8; ++q) {
-      const int tr = 8 * q + (lane >> 3);
-      const int pc = (lane & 7) ^ swz(tr);
-      x.voff[q] = (tr * p.S + 4 * pc) * 4;
-    }
+  x.next_begin = ((g + 1) * kRowsPerWave) / kChunk;
+  float score;
+  if (g == g_last) {
+    score = g == 0 ? sweep_rows<ALIGNED, 0, 0>(p, L, x, tag, timed_out)
+                   : (wv > 0 ? sweep_rows<ALIGNED, 1, 0>(p, L, x, tag, timed_out) : sweep_rows<ALIGNED, 2, 0>(p, L, x, tag, timed_out));
+  } else if (wv < kWavesPerBlock - 1) {
+    score = g == 0 ? sweep_rows<ALIGNED, 0, 1>(p, L, x, tag, timed_out)
+                   : (wv > 0 ? sweep_rows<ALIGNED, 1, 1>(p, L, x, tag, timed_out) : sweep_rows<ALIGNED, 2, 1>(p, L, x, tag, timed_out));
   } else {
-    // Load k of group hh: lane L writes LDS word 64k + L of the group, i.e.
-    // tile row 16hh + 2k + L/32, slot (L%32)/4, word L%4 (swz has period 16).
-#pragma unroll
-    for (int k = 0; k < 8; ++k) {
-      const int tr = 2 * k + (lane >> 5);
-      const int pc = ((lane & 31) >> 2) ^ swz(tr);
-      x.voff[k] = (tr * p.S + 4 * pc + (lane & 3)) * 4;
-    }
+    score = sweep_rows<ALIGNED, 1, 2>(p, L, x, tag, timed_out);
   }
-  x.tile0 = lds_off(&L.u.tile[wv][0][0]);
-  x.dummy = lds_off(&L.dummy[wv][0]);
-  x.decp = (uint64_t)(uintptr_t)(p.dec + (size_t)b * p.NC * (size_t)p.TP + (lane > 0 ? (size_t)x.row : (size_t)p.TP - 1));
-  x.slotp = (uint64_t)(uintptr_t)(p.slots + ((size_t)b * p.NW + g) * slot_stride + (lane & (kChunk - 1)));
-  const float score = g == 0 ? sweep_rows<ALIGNED, 0>(p, L, x, tag, timed_out)
-                             : (wv > 0 ? sweep_rows<ALIGNED, 1>(p, L, x, tag, timed_out)
-                                       : sweep_rows<ALIGNED, 2>(p, L, x, tag, timed_out));
 
   // Publish this wave's decision words to the item's walker.
   if (lane == 0) st_dev(p.done + (size_t)b * p.NW + g, tag);
