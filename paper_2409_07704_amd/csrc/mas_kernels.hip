@@ -73,6 +73,7 @@ __device__ __forceinline__ void lds_store(int* p, int v) { __hip_atomic_store(p,
 __device__ __forceinline__ uint32_t call_tag(uint32_t gen) { return 2u * gen + 1u; }
 
 constexpr int kSpinLimit = 1 << 21;  // bound of every device-side wait (~seconds)
+constexpr int kOnesPerLane = 128;    // path bytes a lane writes for its own row before the wave helps
 constexpr int kDepth = 3;            // value tiles in flight ahead of the one computed
 constexpr int kStages = 4;           // LDS tile slots per wave (kDepth + 1, a power of two)
 constexpr int kPollSlots = 4;        // LDS slots of polled boundary words
@@ -927,18 +928,40 @@ __device__ __forceinline__ void sweep_block(const KParams& p, SweepLds& L, int s
       __builtin_amdgcn_s_sleep(2);
     }
   }
-  // Ones of this wave's rows: lane l writes row 63g + l - 1, from row_start
-  // entries 63g + l - 1 (lane l-1's) and 63g + l (its own).
+  // Ones of this wave's rows: lane l's row 63g + l - 1 has columns [lo, hi),
+  // from row_start entries 63g + l - 1 (lane l-1's) and 63g + l (its own).
+  // Each lane writes the first kOnesPerLane bytes of its row's ones (one
+  // 16-byte piece or one byte at a time); rows with more (a long stay in one
+  // row) are finished by the whole wave, one such row at a time, 64 pieces
+  // or bytes per store.
   const int ri = min(g * kRowsPerWave + lane, p.T);
   const int hi = g == g_last ? rsl[ri] : (int)ld_dev(reinterpret_cast<const uint32_t*>(rs_out + ri));
   const int lo = __builtin_amdgcn_update_dpp(0, hi, 0x138, 0xF, 0xF, false);  // lane l-1's entry
   const int row = g * kRowsPerWave + lane - 1;
-  if (lane > 0 && row < tx) {
-    uint8_t* prow = p.path + ((size_t)b * (size_t)p.T + (size_t)row) * (size_t)p.S;
+  const bool mine = lane > 0 && row < tx;
+  uint8_t* const item_path = p.path + (size_t)b * (size_t)p.T * (size_t)p.S;
+  const int start = p.path16 ? (lo & ~15) : lo;
+  const int split = mine ? min(hi, start + kOnesPerLane) : start;  // own part: [start, split)
+  if (mine) {
+    uint8_t* prow = item_path + (size_t)row * (size_t)p.S;
     if (p.path16) {
-      for (int j0 = lo & ~15; j0 < hi; j0 += 16) *reinterpret_cast<uint4*>(prow + j0) = path_piece(lo, hi, j0);
+      for (int j0 = start; j0 < split; j0 += 16) *reinterpret_cast<uint4*>(prow + j0) = path_piece(lo, hi, j0);
     } else {
-      for (int j = lo; j < hi; ++j) prow[j] = 1;
+      for (int j = start; j < split; ++j) prow[j] = 1;
+    }
+  }
+  uint64_t rest = __builtin_amdgcn_ballot_w64(mine && split < hi);
+  while (rest) {
+    const int l = __builtin_ctzll(rest);
+    rest &= rest - 1;
+    const int a = __builtin_amdgcn_readlane(split, l), e = __builtin_amdgcn_readlane(hi, l);
+    uint8_t* prow = item_path + (size_t)(g * kRowsPerWave + l - 1) * (size_t)p.S;
+    if (p.path16) {
+      // a is a multiple of 16 and at least lo: every piece from a on holds
+      // ones up to e.
+      for (int j0 = a + 16 * lane; j0 < e; j0 += 16 * kWave) *reinterpret_cast<uint4*>(prow + j0) = path_piece(a, e, j0);
+    } else {
+      for (int j = a + lane; j < e; j += kWave) prow[j] = 1;
     }
   }
 }
