@@ -39,8 +39,7 @@ static mas_status run(const float* value, const int32_t* t_x, const int32_t* t_y
   p.TP = L.TP;
   p.NB = L.NB;
   p.path16 = path && (L.S % 16 == 0) && ((uintptr_t)path % 16 == 0);
-  const bool aligned = (L.S % 4 == 0) && ((uintptr_t)value % 16 == 0);
-  return launch_mas(p, aligned, stream) == hipSuccess ? MAS_OK : MAS_ERR_HIP;
+  return launch_mas(p, stream) == hipSuccess ? MAS_OK : MAS_ERR_HIP;
 }
 }  // namespace mas
 

@@ -27,9 +27,8 @@ struct KParams {
 };
 
 // Forward sweep, backtrack and (when p.path) the dense path, in one launch:
-// one 256-thread workgroup per 256 text rows of every item.  `aligned`:
-// S % 4 == 0 and value 16-byte aligned.
-hipError_t launch_mas(const KParams& p, bool aligned, hipStream_t stream);
+// one 256-thread workgroup per 252 text rows of every item.
+hipError_t launch_mas(const KParams& p, hipStream_t stream);
 // Dense [B, T, S] u8 path from row_start [B, T+1].
 hipError_t launch_path(const int32_t* row_start, int32_t B, int32_t T, int32_t S, uint8_t* path, hipStream_t stream);
 // Zero-fill of `bytes` (a multiple of 16) at a 16-byte aligned pointer.

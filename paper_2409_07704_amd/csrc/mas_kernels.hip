@@ -49,6 +49,7 @@ namespace mas {
 
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 
 __device__ __forceinline__ float neg_inf() { return -__builtin_inff(); }
 
@@ -74,10 +75,10 @@ __device__ __forceinline__ uint32_t call_tag(uint32_t gen) { return 2u * gen + 1
 
 constexpr int kSpinLimit = 1 << 21;  // bound of every device-side wait (~seconds)
 constexpr int kOnesPerLane = 128;    // path bytes a lane writes for its own row before the wave helps
-constexpr int kDepth = 3;            // value tiles in flight ahead of the one computed
-constexpr int kStages = 4;           // LDS tile slots per wave (kDepth + 1, a power of two)
+constexpr int kGroup = 4;            // chunks per value load (512 contiguous bytes of each row)
+constexpr int kSlots = 4;            // boundary-row slots per wave (a power of two, = kGroup)
 constexpr int kPollSlots = 4;        // LDS slots of polled boundary words
-static_assert(kStages == kDepth + 1 && (kStages & (kStages - 1)) == 0, "tile ring");
+static_assert((kSlots & (kSlots - 1)) == 0 && kSlots == kGroup, "slot ring");
 
 // ---------------------------------------------------------------- vector memory (inline asm)
 // Byte offset of a __shared__ object inside the workgroup's LDS allocation.
@@ -98,18 +99,28 @@ __device__ __forceinline__ void vm_wait() {
 // each use.  Loads at offsets >= num_records return 0 and such stores are
 // dropped (the per-lane offset is range-checked, the scalar offset is not).
 constexpr int kRsrcWord3 = 0x00020000;
-// The count update is written as scalar instructions: the compiler turns
-// the saturating subtraction into a vector instruction otherwise, and the
-// descriptor must live in scalar registers.  Byte counts are below 2^31.
+// The compiler computes the saturating count update with a vector
+// instruction; the descriptor must live in scalar registers, so the count
+// is read back as a wave-uniform value.  Byte counts are below 2^31.
 struct Cursor {
   const char* base;
   int left;
   __device__ __forceinline__ __amdgpu_buffer_rsrc_t rsrc() const {
     return __builtin_amdgcn_make_buffer_rsrc(const_cast<char*>(base), 0, left, kRsrcWord3);
   }
+  // The same, with every field read back as wave-uniform: for inline
+  // assembly operands that must be scalar registers (under scalar-register
+  // pressure the compiler may keep a uniform pointer in vector registers).
+  __device__ __forceinline__ __amdgpu_buffer_rsrc_t rsrc_s() const {
+    const uint64_t a = (uint64_t)(uintptr_t)base;
+    const uint64_t lo = (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)a);
+    const uint64_t hi = (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)(a >> 32));
+    return __builtin_amdgcn_make_buffer_rsrc(reinterpret_cast<char*>((uintptr_t)(lo | hi << 32)), 0,
+                                             __builtin_amdgcn_readfirstlane(left), kRsrcWord3);
+  }
   __device__ __forceinline__ void advance(int step) {
     base += step;
-    asm("s_sub_i32 %0, %0, %1\n\ts_max_i32 %0, %0, 0" : "+s"(left) : "s"(step) : "scc");
+    left = __builtin_amdgcn_readfirstlane(max(left - step, 0));
   }
 };
 __device__ __forceinline__ Cursor make_cursor(const void* p, int bytes) { return Cursor{static_cast<const char*>(p), bytes}; }
@@ -124,21 +135,7 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t sub_rsrc(const void* p, uint64
 
 // Loads into LDS (the lds flag): every lane's bytes at its voffset go to LDS
 // at M0 + size * lane.  A scalar write of M0 needs one wait state before
-// such a load.  OFF is added to the LDS base.
-template <int OFF>
-__device__ __forceinline__ void dma16(uint32_t lds, __amdgpu_buffer_rsrc_t r, int voff) {
-  asm volatile("s_add_u32 m0, %[l], %[o]\n\ts_nop 0\n\tbuffer_load_dwordx4 %[v], %[r], 0 offen lds"
-               :
-               : [l] "s"(lds), [o] "n"(OFF), [r] "s"(r), [v] "v"(voff)
-               : "memory", "m0", "scc");
-}
-template <int OFF>
-__device__ __forceinline__ void dma4(uint32_t lds, __amdgpu_buffer_rsrc_t r, int voff) {
-  asm volatile("s_add_u32 m0, %[l], %[o]\n\ts_nop 0\n\tbuffer_load_dword %[v], %[r], 0 offen lds"
-               :
-               : [l] "s"(lds), [o] "n"(OFF), [r] "s"(r), [v] "v"(voff)
-               : "memory", "m0", "scc");
-}
+// such a load.
 // Device-scope (sc1) variants for data written by other workgroups.
 __device__ __forceinline__ void dma4_dev(uint32_t lds, __amdgpu_buffer_rsrc_t r, int voff) {
   asm volatile("s_mov_b32 m0, %[l]\n\ts_nop 0\n\tbuffer_load_dword %[v], %[r], 0 offen sc1 lds"
@@ -311,29 +308,33 @@ constexpr int kWalkWin = kWalkLoads * 4 * kWave;   // rows per window
 constexpr int kWalkSlots = 16;                 // window ring (power of two > kWalkAhead)
 static_assert(kWalkWin >= 32 * (kWalkAhead - 1) + kWave + 3, "walk window");
 
-// Value tiles.  Each wave has kStages stages; the stage of chunk c is
-// (c - c_begin) % kStages (c_begin: the wave's first chunk).  A stage holds
-//   * 64 tile rows of 32 values: item rows 63g .. 63g+63 (row 63 unused), row
-//     r at byte 144 r.  The 16 bytes of padding per row put piece k of 16
-//     consecutive rows in distinct 4-bank groups of the 64-bank LDS
-//     (36 r mod 64 differs for r mod 16), so the per-row reads of a wave are
-//     conflict-free with one address per lane plus the piece offset;
-//   * the boundary row at kBoundOff: the 32 Q values of the row above the
-//     wave for the stage's chunk (word 2332 = 28 mod 64, a bank group that
-//     rows 0 .. 14 do not use), then its tag (chunk + 1) at kTagOff.  The
-//     previous wave of the workgroup writes it; a wave fed by another
-//     workgroup copies its polled words there; the first wave of an item
-//     fills it with -inf once.
+// Per-wave LDS region (kWaveLds bytes):
+//   * kGroup value tiles, one per chunk of the current group of kGroup
+//     chunks: 64 rows of 32 values, item rows 63g .. 63g+63 (row 63 unused),
+//     row r at byte 144 r of its tile.  The 16 bytes of padding per row put
+//     piece k of 16 consecutive rows in distinct 4-bank groups of the
+//     64-bank LDS (36 r mod 64 differs for r mod 16), so the per-row reads of
+//     a wave are conflict-free with one address per lane plus the piece
+//     offset;
+//   * kSlots boundary slots at kBoundOff + 256 k: the 32 Q values of the row
+//     above the wave for chunk c in slot (c - c_begin) % kSlots (word
+//     9244 + 64 k = 28 mod 64, a bank group rows 0 .. 14 do not use), then
+//     its tag (chunk + 1).  The previous wave of the workgroup writes them; a
+//     wave fed by another workgroup copies its polled words there; the first
+//     wave of an item fills them with -inf once.
 constexpr int kRowBytes = 144;
-constexpr int kBoundOff = 9328;
-constexpr int kTagOff = kBoundOff + 4 * kChunk;
-constexpr int kStageBytes = 9472;
-static_assert(64 * kRowBytes <= kBoundOff && kBoundOff % 16 == 0 && (kBoundOff / 4) % 64 == 28, "boundary slot");
-static_assert(kTagOff + 4 <= kStageBytes && kStageBytes % 256 == 0, "stage size");
+constexpr int kTileBytes = 64 * kRowBytes;
+constexpr int kBoundOff = kGroup * kTileBytes + 112;
+constexpr int kSlotBytes = 256;
+constexpr int kTagOff = 4 * kChunk;  // inside a slot
+constexpr int kWaveLds = 37888;
+static_assert(kBoundOff % 16 == 0 && (kBoundOff / 4) % 64 == 28, "boundary slot");
+static_assert(kBoundOff + (kSlots - 1) * kSlotBytes + kTagOff + 4 <= kWaveLds && kWaveLds % 256 == 0, "wave region");
+static_assert(kBoundOff + (kSlots - 1) * kSlotBytes + kTagOff + 4 <= kWaveLds && kWaveLds % 256 == 0, "wave region");
 
 struct SweepLds {
   union {
-    uint8_t tile[kWavesPerBlock][kStages][kStageBytes];
+    uint8_t tile[kWavesPerBlock][kWaveLds];
     // The walker's staging, once every sweep of its item (and so of its
     // workgroup) has finished.
     struct {
@@ -404,50 +405,25 @@ __device__ __forceinline__ int chunk_end(int g, int tx, int ty) {
   return by_len < by_reach ? by_len : by_reach;
 }
 
-// Vector-memory operations of one sweep step, in issue order:
-//   [poll of chunk c+2]        (IN == 2)
-//   tile of chunk c+kDepth     (NL loads)
-//   decision words of chunk c  (1 store)
-//   [boundary words of c]      (OUT == 2: 1 store)
-constexpr int step_ops(int nl, bool in2, bool out2) { return (in2 ? 1 : 0) + nl + 1 + (out2 ? 1 : 0); }
-// Count for the wait at the start of step c: tile c was issued kDepth steps
-// earlier (followed by that step's stores and kDepth-1 whole steps), the
-// poll of chunk c two steps earlier (followed by that step's tile and stores
-// and one whole step).  Counts above 63 are clamped: a wave has at most 63
-// operations outstanding (issue stalls at the counter's limit), so anything
-// issued earlier than that has completed.
-constexpr int wait_count(int nl, bool in2, bool out2) {
-  const int k = step_ops(nl, in2, out2);
-  const int tail = 1 + (out2 ? 1 : 0);
-  const int n_tile = tail + (kDepth - 1) * k;
-  const int n_poll = nl + tail + k;
-  const int n = in2 && n_poll < n_tile ? n_poll : n_tile;
-  return n > 63 ? 63 : n;
-}
-
-// The 4-byte tile loads K .. N-1 (load k fills LDS bytes 256 k .. 256 k + 255).
-template <int K, int N>
-__device__ __forceinline__ void dma4_loads(uint32_t dst, __amdgpu_buffer_rsrc_t r, const int* vo) {
-  if constexpr (K < N) {
-    dma4<256 * K>(dst, r, vo[K]);
-    dma4_loads<K + 1, N>(dst, r, vo);
-  }
-}
-// The 16-byte tile loads K .. N-1 (load k fills LDS bytes 1024 k .. 1024 k + 1023).
-template <int K, int N>
-__device__ __forceinline__ void dma16_loads(uint32_t dst, __amdgpu_buffer_rsrc_t r, const int* vo) {
-  if constexpr (K < N) {
-    dma16<1024 * K>(dst, r, vo[K]);
-    dma16_loads<K + 1, N>(dst, r, vo);
-  }
-}
-
-// Byte offset of (tile row r, byte e of the row's 128) in the value slab
-// relative to the tile's first row, or an offset no resource covers.
+// Byte offset of (tile row r, byte e of the row) in the value slab relative
+// to the tile's first row, or INT_MIN: as an unsigned offset it stays at or
+// above 2^31, outside every resource, after adding up to 2^31 - 1.
 __device__ __forceinline__ int tile_voff(int r, int e, int S) {
   const uint64_t o = (uint64_t)r * (uint64_t)S * 4u + (uint64_t)e;
-  return o < 0x80000000ull ? (int)o : -16;
+  return o < 0x80000000ull ? (int)o : (int)0x80000000u;
 }
+
+__device__ __forceinline__ f32x4 load16(__amdgpu_buffer_rsrc_t r, int voff) {
+  return __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(r, voff, 0, 0));
+}
+
+template <int V>
+struct IntC {
+  static constexpr int value = V;
+};
+
+// Cache policy of hand-off data between workgroups: sc1 (device scope).
+constexpr int kPolicyDev = 16;
 
 // Sweeps this wave's rows over its chunks and returns the score candidate
 // (Q at (row, t_y-1) of this lane; only meaningful for the wave holding row
@@ -455,48 +431,61 @@ __device__ __forceinline__ int tile_voff(int r, int e, int S) {
 // holds row 0), 1 the previous wave of the workgroup, 2 global boundary words
 // of the previous workgroup.  OUT: 0 no consumer, 1 the next wave of the
 // workgroup, 2 global boundary words for the next workgroup.
-template <bool ALIGNED, int IN, int OUT>
+//
+// Value tiles travel HBM -> registers -> LDS in groups of kGroup chunks
+// (512 contiguous bytes of each row: DRAM serves longer runs of a row
+// faster than scattered 128-byte pieces).  While the kGroup tiles of one
+// group sit in LDS and are swept, the next group is in flight in registers.
+// Lane L loads piece L % 8 of chunk j of tile rows 8q + L/8 (q = 0..7):
+// 16 bytes each, eight lanes per 128-byte row segment.  The compiler sees
+// these loads and waits for them right before writing them to LDS.
+template <int IN, int OUT>
 __device__ __forceinline__ float sweep_rows(const KParams& p, SweepLds& L, const WaveCtx& x, uint32_t tag, bool& timed_out) {
-  constexpr int NL = ALIGNED ? 9 : 36;  // tile loads per chunk (padding slots included)
   constexpr bool IN2 = IN == 2, OUT2 = OUT == 2;
   const int lane = x.lane, wv = x.wv;
   float t = -0.0f;  // lane 0 keeps -0 for the whole sweep (see cols8)
 
+  // LDS: byte offsets from the start of L (where the wave regions begin).
+  char* const Lc = reinterpret_cast<char*>(&L);
+  const uint32_t wbase = (uint32_t)wv * kWaveLds;
+  const uint32_t nbase = wbase + kWaveLds;  // the next wave's region
+  auto slot_ptr = [&](uint32_t base, int k) __attribute__((always_inline)) -> char* {
+    return Lc + base + kBoundOff + (uint32_t)(k & (kSlots - 1)) * kSlotBytes;
+  };
+
   // Value tiles: a resource from the wave's first tile row at the next chunk
   // to load; rows past the slab fall outside it and read 0.
   const float* slab = p.value + (size_t)x.b * (size_t)p.T * (size_t)p.S;
-  const uint32_t slab_bytes = (uint32_t)((uint64_t)p.T * (uint64_t)p.S * 4u);
-  const uint32_t first = (uint32_t)((uint64_t)x.g * kRowsPerWave * (uint64_t)p.S * 4u) + (uint32_t)x.c_begin * (kChunk * 4);
-  Cursor vr = make_cursor(reinterpret_cast<const char*>(slab), (int)slab_bytes);
-  vr.advance((int)first);
-  // Per-lane load offsets: load k, lane L fills stage slot 64 k + L (16-byte
-  // slots, nine per row: eight pieces and the padding) or word 64 k + L
-  // (4-byte words, 36 per row).
-  int voff[NL];
+  const int slab_bytes = (int)((uint64_t)p.T * (uint64_t)p.S * 4u);
+  Cursor vr = make_cursor(slab, slab_bytes);
+  vr.advance((int)((uint64_t)x.g * kRowsPerWave * (uint64_t)p.S * 4u) + x.c_begin * (kChunk * 4));
+  int voff[8];
 #pragma unroll
-  for (int k = 0; k < NL; ++k) {
-    if (ALIGNED) {
-      const int sl = 64 * k + lane, r = sl / 9, pc = sl % 9;
-      voff[k] = pc < 8 ? tile_voff(r, 16 * pc, p.S) : -16;
-    } else {
-      const int w = 64 * k + lane, r = w / 36, wi = w % 36;
-      voff[k] = wi < 32 ? tile_voff(r, 4 * wi, p.S) : -16;
-    }
-  }
-  // LDS: tile0 is this wave's stage 0 as an LDS address (for M0); the C++
-  // accesses use byte offsets from the start of L (where the tiles begin).
-  char* const Lc = reinterpret_cast<char*>(&L);
-  const uint32_t tile_rel = (uint32_t)wv * (kStages * kStageBytes);
-  const uint32_t tile0 = lds_off(&L.u.tile[wv][0][0]);
-  // Lane l reads tile row l-1 of a stage; lane 0 reads the boundary row.
-  const uint32_t rbase = tile_rel + (lane > 0 ? (uint32_t)(lane - 1) * kRowBytes : (uint32_t)kBoundOff);
-  // Placeholder loads (steps with no store yet) read the slab's first 256 bytes.
-  const uint32_t dummy = lds_off(&L.dummy[wv][0]);
-  const __amdgpu_buffer_rsrc_t drsrc = make_cursor(slab, min((int)slab_bytes, 256)).rsrc();
+  for (int q = 0; q < 8; ++q) voff[q] = tile_voff(8 * q + (lane >> 3), 16 * (lane & 7), p.S);
+  // Where lane L's pieces go: row 8q + L/8, piece L % 8 (q * 1152 bytes apart).
+  f32x4* const tile_w = reinterpret_cast<f32x4*>(Lc + wbase + (uint32_t)(lane >> 3) * kRowBytes + 16u * (uint32_t)(lane & 7));
+  // Lane l >= 1 reads tile row l-1; lane 0 reads the chunk's boundary slot.
+  const f32x4* const tile_r = reinterpret_cast<const f32x4*>(Lc + wbase + (uint32_t)(lane > 0 ? lane - 1 : 0) * kRowBytes);
+  f32x4 buf[kGroup][8];
+  auto load_group = [&]() __attribute__((always_inline)) {
+    const __amdgpu_buffer_rsrc_t r = vr.rsrc();
+#pragma unroll
+    for (int q = 0; q < 8; ++q)
+#pragma unroll
+      for (int j = 0; j < kGroup; ++j) buf[j][q] = load16(r, voff[q] + j * (kChunk * 4));
+    vr.advance(kGroup * kChunk * 4);
+  };
+  auto put_group = [&]() __attribute__((always_inline)) {
+#pragma unroll
+    for (int j = 0; j < kGroup; ++j)
+#pragma unroll
+      for (int q = 0; q < 8; ++q) tile_w[j * (kTileBytes / 16) + q * (8 * kRowBytes / 16)] = buf[j][q];
+  };
+
   // Decision words: dec[b][c][row], lane 0 into the chunk's scratch word.
   const __amdgpu_buffer_rsrc_t dr = make_cursor(p.dec + (size_t)x.b * p.NC * (size_t)p.TP, p.NC * p.TP * 4).rsrc();
   const int dvo = 4 * (lane > 0 ? x.row : p.TP - 1);
-  const uint32_t dstride = (uint32_t)p.TP * 4u;
+  const int dstride = p.TP * 4;
   // Boundary words of this wave (OUT == 2) and of the previous one (IN == 2).
   const size_t slot_stride = (size_t)p.NC * kChunk;
   const int slot_bytes = (int)(slot_stride * 8u);
@@ -506,6 +495,12 @@ __device__ __forceinline__ float sweep_rows(const KParams& p, SweepLds& L, const
   Cursor pr = make_cursor(pslots, slot_bytes);
   if (IN2) pr.advance((x.c_begin - 1) * 256);  // first poll: chunk c_begin-1
 
+  // Boundary words of chunk c (256 bytes) into poll slot c % 4.  These
+  // loads are the only vector-memory operations the compiler does not see:
+  // the wait before reading a poll slot counts them by hand.
+  auto issue_poll = [&](int c, __amdgpu_buffer_rsrc_t r) __attribute__((always_inline)) {
+    dma4_dev(lds_off(&L.poll[c & (kPollSlots - 1)][0]), r, 4 * lane);
+  };
   // Boundary words of chunk c are in poll slot c % 4 once all carry this
   // call's tag (re-polled until then); lane L's word is L % 32.
   auto polled_word = [&](int c) __attribute__((always_inline)) -> uint64_t {
@@ -523,15 +518,17 @@ __device__ __forceinline__ float sweep_rows(const KParams& p, SweepLds& L, const
         break;
       }
       __builtin_amdgcn_s_sleep(1);
-      dma4_dev(lds_off(&L.poll[c & (kPollSlots - 1)][0]), make_cursor(pslots + (size_t)c * kChunk, kChunk * 8u).rsrc(), 4 * lane);
+      // (c is uniform; saying so keeps the descriptor in scalar registers.)
+      const int cu = __builtin_amdgcn_readfirstlane(c);
+      issue_poll(cu, make_cursor(pslots + (size_t)cu * kChunk, kChunk * 8).rsrc_s());
       vm_wait<0>();
       wd = pw[lane & (kChunk - 1)];
     }
     return wd;
   };
-  // Waits for the boundary row of chunk c in the stage at byte offset so.
-  auto bound_ready = [&](int c, uint32_t so) __attribute__((always_inline)) {
-    const int* tg = reinterpret_cast<const int*>(Lc + tile_rel + so + kTagOff);
+  // Waits for the boundary row of chunk c in this wave's slot k.
+  auto bound_ready = [&](int c, int k) __attribute__((always_inline)) {
+    const int* tg = reinterpret_cast<const int*>(slot_ptr(wbase, k) + kTagOff);
     int spins = 0;
     while (__builtin_amdgcn_readfirstlane(lds_load(tg)) != c + 1) {
       if (++spins > kSpinLimit) {
@@ -543,38 +540,30 @@ __device__ __forceinline__ float sweep_rows(const KParams& p, SweepLds& L, const
   };
 
   if (IN == 0) {
-    // The row above row 0 is -inf in every stage.
+    // The row above row 0 is -inf in every slot.
     if (lane < kChunk) {
 #pragma unroll
-      for (int st = 0; st < kStages; ++st)
-        reinterpret_cast<float*>(&L.u.tile[wv][st][kBoundOff])[lane] = neg_inf();
+      for (int k = 0; k < kSlots; ++k) reinterpret_cast<float*>(slot_ptr(wbase, k))[lane] = neg_inf();
     }
   }
-
-  // Prologue: kDepth placeholder steps with the steady-state operation
-  // sequence, so that the loop's wait counts hold from its first step.
+  if (IN2) {
+    // Polls of chunks c_begin-1 .. c_begin+1 (the loop polls two ahead).
 #pragma unroll
-  for (int k = 0; k < kDepth; ++k) {
-    if (IN2) {
-      dma4_dev(lds_off(&L.poll[(x.c_begin - 1 + k) & (kPollSlots - 1)][0]), pr.rsrc(), 4 * lane);
+    for (int k = 0; k < 3; ++k) {
+      issue_poll(x.c_begin - 1 + k, pr.rsrc_s());
       pr.advance(256);
     }
-    if (ALIGNED)
-      dma16_loads<0, NL>(tile0 + k * kStageBytes, vr.rsrc(), voff);
-    else
-      dma4_loads<0, NL>(tile0 + k * kStageBytes, vr.rsrc(), voff);
-    vr.advance(kChunk * 4);
-    dma4<0>(dummy, drsrc, 4 * lane);
-    if (OUT2) dma4<0>(dummy, drsrc, 4 * lane);
   }
+  // The first group in flight.
+  load_group();
 
   // Lane 0's Q at the column before the first chunk: the previous wave's
   // last row there (its chunk c_begin-1, always computed), or -inf.
   float q = neg_inf();
   if (IN == 1) {
-    bound_ready(x.c_begin - 1, (kStages - 1) * kStageBytes);
+    bound_ready(x.c_begin - 1, -1);
     wave_lds_sync();
-    const float e = reinterpret_cast<const float*>(&L.u.tile[wv][kStages - 1][kBoundOff])[kChunk - 1];
+    const float e = reinterpret_cast<const float*>(slot_ptr(wbase, -1))[kChunk - 1];
     q = lane == 0 ? e : q;
     wave_lds_sync();
     if (lane == 0) lds_store(&L.cons[wv], x.c_begin);
@@ -585,96 +574,107 @@ __device__ __forceinline__ float sweep_rows(const KParams& p, SweepLds& L, const
     q = lane == 0 ? e : q;
   }
 
-  // Stage offsets: so of chunk c (the one computed), sd of chunk c+kDepth,
-  // sn of chunk c in the next wave's stages.
-  uint32_t so = 0, sd = (kStages - 1) * kStageBytes;
-  uint32_t sn = (uint32_t)((x.c_begin - x.next_begin) & (kStages - 1)) * kStageBytes;
-  const uint32_t tile_next = tile_rel + kStages * kStageBytes;
   // Lane 0 publishes the consumed-chunk counter; the other lanes write
   // their own dummy words (one store, no exec change).
   int* const cons_ptr = lane == 0 ? &L.cons[wv] : reinterpret_cast<int*>(&L.dummy[wv][lane]);
   // Lower bound of the consumer's counter: it starts at its own c_begin-1,
   // which is at least this wave's c_begin+1 (63 rows span >= 63 columns).
   int cons_seen = x.c_begin + 1;
+  const int dk = x.c_begin - x.next_begin;  // the next wave's slot of chunk c: c - c_begin + dk
   float qc[kChunk];
-  uint32_t soff = (uint32_t)x.c_begin * dstride;
-  for (int c = x.c_begin; c < x.c_end; ++c) {
-    vm_wait<wait_count(NL, IN2, OUT2)>();
+  int soff = x.c_begin * dstride;
+  // One chunk, at position J of its group: its tile and its boundary slot
+  // are number J.
+  auto step = [&](auto pos_c, int c) __attribute__((always_inline)) {
+    constexpr int J = decltype(pos_c)::value;
+    const int k = c - x.c_begin;  // k % kSlots == J
     if (IN2) {
-      dma4_dev(lds_off(&L.poll[(c + 2) & (kPollSlots - 1)][0]), pr.rsrc(), 4 * lane);
+      // Poll of chunk c: issued two steps ago, followed by the rest of that
+      // step and the next one (the group's loads come first in position 0),
+      // and nothing of this one yet.
+      constexpr int tail = 1 + (OUT2 ? 1 : 0);
+      constexpr int n = tail + (((J - 2) & (kGroup - 1)) == 0 ? 8 * kGroup : 0) + 1 + tail +
+                        (((J - 1) & (kGroup - 1)) == 0 ? 8 * kGroup : 0);
+      vm_wait<n>();
+      issue_poll(c + 2, pr.rsrc_s());
       pr.advance(256);
     }
-    if (ALIGNED)
-      dma16_loads<0, NL>(tile0 + sd, vr.rsrc(), voff);
-    else
-      dma4_loads<0, NL>(tile0 + sd, vr.rsrc(), voff);
-    vr.advance(kChunk * 4);
-
+    if (J == 0) {
+      // The group's tiles into LDS (the previous group's reads are done),
+      // the next group into flight.
+      wave_lds_sync();
+      put_group();
+      load_group();
+    }
     // The row above: from the previous wave, or copied from the polled
     // words.  Beyond the previous wave's chunks the slot holds stale values:
     // they only reach cells that cannot reach (t_x-1, t_y-1).
-    if (IN == 1 && c < x.prev_end) bound_ready(c, so);
-    if (IN == 2 && c < x.prev_end) {
+    if (IN == 1 && c < x.prev_end) bound_ready(c, k);
+    if (IN2 && c < x.prev_end) {
       const uint64_t wd = polled_word(c);
-      reinterpret_cast<float*>(Lc + tile_rel + so + kBoundOff)[lane & (kChunk - 1)] = __uint_as_float((uint32_t)wd);
+      reinterpret_cast<float*>(slot_ptr(wbase, k))[lane & (kChunk - 1)] = __uint_as_float((uint32_t)wd);
     }
     wave_lds_sync();
     f32x4 v[8];
     {
-      const f32x4* base = reinterpret_cast<const f32x4*>(Lc + rbase + so);
+      const f32x4* src = lane > 0 ? tile_r + J * (kTileBytes / 16) : reinterpret_cast<const f32x4*>(slot_ptr(wbase, J));
 #pragma unroll
-      for (int k = 0; k < 8; ++k) v[k] = base[k];
+      for (int m = 0; m < 8; ++m) v[m] = src[m];
     }
     uint32_t bits = 0;
     if (c < x.mask_end)
       sweep_chunk<true>(q, t, v, qc, bits, lane, x.row, c * kChunk);
     else
       sweep_chunk<false>(q, t, v, qc, bits, lane, x.row, c * kChunk);
-    buf_store32(bits, dvo, dr, soff);
+    __builtin_amdgcn_raw_buffer_store_b32(bits, dr, dvo, soff, kPolicyDev);
     soff += dstride;
     if (IN == 1) {
       // The reads of this chunk's slot are done: the previous wave may
-      // reuse it for chunk c + kStages.
-      wave_lds_sync();
+      // reuse it for chunk c + kSlots.
       lds_store(cons_ptr, c + 1);
     }
     if (OUT == 1) {
       // Wait until the consumer no longer needs the slot, then publish the
       // values, then the tag.
       int spins = 0;
-      while (cons_seen < c - (kStages - 1)) {
+      while (cons_seen < c - (kSlots - 1)) {
         cons_seen = __builtin_amdgcn_readfirstlane(lds_load(&L.cons[wv + 1]));
-        if (cons_seen >= c - (kStages - 1)) break;
+        if (cons_seen >= c - (kSlots - 1)) break;
         if (++spins > kSpinLimit) {
           timed_out = true;
           break;
         }
         __builtin_amdgcn_s_sleep(1);
       }
+      char* const ns = slot_ptr(nbase, k + dk);
       if (lane == kWave - 1) {
-        f32x4* dst = reinterpret_cast<f32x4*>(Lc + tile_next + sn + kBoundOff);
+        f32x4* dst = reinterpret_cast<f32x4*>(ns);
 #pragma unroll
-        for (int k = 0; k < kChunk / 4; ++k) dst[k] = f32x4{qc[4 * k], qc[4 * k + 1], qc[4 * k + 2], qc[4 * k + 3]};
+        for (int m = 0; m < kChunk / 4; ++m) dst[m] = f32x4{qc[4 * m], qc[4 * m + 1], qc[4 * m + 2], qc[4 * m + 3]};
       }
       // Values before the tag (the LDS executes one wave's operations in
       // order; the fence keeps the compiler from reordering them).  Kept out
       // of the lane-63 branch: inside it, the compiler makes the whole chunk
       // loop divergent for the waves that feed no other wave of the group.
       wave_lds_sync();
-      if (lane == kWave - 1) lds_store(reinterpret_cast<int*>(Lc + tile_next + sn + kTagOff), c + 1);
-      sn = sn == (kStages - 1) * kStageBytes ? 0u : sn + kStageBytes;
-    } else if (OUT == 2) {
+      if (lane == kWave - 1) lds_store(reinterpret_cast<int*>(ns + kTagOff), c + 1);
+    } else if (OUT2) {
       if (lane == kWave - 1) {
 #pragma unroll
-        for (int k = 0; k < kChunk / 4; ++k) L.ostage[k] = f32x4{qc[4 * k], qc[4 * k + 1], qc[4 * k + 2], qc[4 * k + 3]};
+        for (int m = 0; m < kChunk / 4; ++m) L.ostage[m] = f32x4{qc[4 * m], qc[4 * m + 1], qc[4 * m + 2], qc[4 * m + 3]};
       }
       wave_lds_sync();
       const float val = reinterpret_cast<const float*>(L.ostage)[lane & (kChunk - 1)];
-      buf_store64(((uint64_t)tag << 32) | (uint64_t)__float_as_uint(val), svo, sr, (uint32_t)c * 256u);
+      const uint64_t word = ((uint64_t)tag << 32) | (uint64_t)__float_as_uint(val);
+      __builtin_amdgcn_raw_buffer_store_b64(__builtin_bit_cast(u32x2, word), sr, svo, c * 256, kPolicyDev);
       wave_lds_sync();
     }
-    so = so == (kStages - 1) * kStageBytes ? 0u : so + kStageBytes;
-    sd = sd == (kStages - 1) * kStageBytes ? 0u : sd + kStageBytes;
+  };
+  for (int c = x.c_begin; c < x.c_end; c += kGroup) {
+    step(IntC<0>(), c);
+    if (c + 1 < x.c_end) step(IntC<1>(), c + 1);
+    if (c + 2 < x.c_end) step(IntC<2>(), c + 2);
+    if (c + 3 < x.c_end) step(IntC<3>(), c + 3);
   }
   vm_wait<0>();
   float score = neg_inf();
@@ -823,7 +823,6 @@ __device__ __forceinline__ void walk(const KParams& p, SweepLds& L, int b, int t
   wave_lds_sync();
 }
 
-template <bool ALIGNED>
 __device__ __forceinline__ void sweep_block(const KParams& p, SweepLds& L, int sid, uint32_t tag, bool& timed_out) {
   const int lane = threadIdx.x & (kWave - 1);
   // The wave index is uniform across a wave; saying so keeps everything
@@ -840,8 +839,8 @@ __device__ __forceinline__ void sweep_block(const KParams& p, SweepLds& L, int s
   // Workgroup set-up: no boundary row is written yet (the LDS holds
   // whatever earlier workgroups left); each wave's first chunk to consume
   // (its carried row comes from chunk c_begin-1).
-  if (threadIdx.x < kWavesPerBlock * kStages)
-    lds_store(reinterpret_cast<int*>(&L.u.tile[threadIdx.x / kStages][threadIdx.x % kStages][kTagOff]), 0);
+  if (threadIdx.x < kWavesPerBlock * kSlots)
+    lds_store(reinterpret_cast<int*>(&L.u.tile[threadIdx.x / kSlots][kBoundOff + (threadIdx.x % kSlots) * kSlotBytes + kTagOff]), 0);
   if (lane == 0) lds_store(&L.cons[wv], c_begin - 1);
   __syncthreads();
 
@@ -896,13 +895,13 @@ __device__ __forceinline__ void sweep_block(const KParams& p, SweepLds& L, int s
   x.next_begin = ((g + 1) * kRowsPerWave) / kChunk;
   float score;
   if (g == g_last) {
-    score = g == 0 ? sweep_rows<ALIGNED, 0, 0>(p, L, x, tag, timed_out)
-                   : (wv > 0 ? sweep_rows<ALIGNED, 1, 0>(p, L, x, tag, timed_out) : sweep_rows<ALIGNED, 2, 0>(p, L, x, tag, timed_out));
+    score = g == 0 ? sweep_rows<0, 0>(p, L, x, tag, timed_out)
+                   : (wv > 0 ? sweep_rows<1, 0>(p, L, x, tag, timed_out) : sweep_rows<2, 0>(p, L, x, tag, timed_out));
   } else if (wv < kWavesPerBlock - 1) {
-    score = g == 0 ? sweep_rows<ALIGNED, 0, 1>(p, L, x, tag, timed_out)
-                   : (wv > 0 ? sweep_rows<ALIGNED, 1, 1>(p, L, x, tag, timed_out) : sweep_rows<ALIGNED, 2, 1>(p, L, x, tag, timed_out));
+    score = g == 0 ? sweep_rows<0, 1>(p, L, x, tag, timed_out)
+                   : (wv > 0 ? sweep_rows<1, 1>(p, L, x, tag, timed_out) : sweep_rows<2, 1>(p, L, x, tag, timed_out));
   } else {
-    score = sweep_rows<ALIGNED, 1, 2>(p, L, x, tag, timed_out);
+    score = sweep_rows<1, 2>(p, L, x, tag, timed_out);
   }
 
   // Publish this wave's decision words to the item's walker.
@@ -966,15 +965,14 @@ __device__ __forceinline__ void sweep_block(const KParams& p, SweepLds& L, int s
   }
 }
 
-template <bool ALIGNED>
-// One workgroup per CU: the value-tile ring takes most of the LDS.
+// One workgroup per CU.
 __global__ void __launch_bounds__(kThreadsPerBlock, 1) mas_kernel(KParams p) {
   __shared__ SweepLds L;
   const uint32_t gen = __hip_atomic_load(&p.hdr->gen, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   const uint32_t tag = call_tag(gen);
   bool timed_out = false;
   const int item = (int)blockIdx.x % p.B;
-  sweep_block<ALIGNED>(p, L, blockIdx.x, tag, timed_out);
+  sweep_block(p, L, blockIdx.x, tag, timed_out);
   if (timed_out) {
     if (p.status) p.status[item] = kItemSyncTimeout;
     __hip_atomic_store(&p.hdr->error, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -1028,12 +1026,9 @@ __global__ void __launch_bounds__(256) mas_zero_kernel(uint4* __restrict__ p, si
 }
 
 // ---------------------------------------------------------------- launchers
-hipError_t launch_mas(const KParams& p, bool aligned, hipStream_t stream) {
+hipError_t launch_mas(const KParams& p, hipStream_t stream) {
   const dim3 grid((unsigned)(p.B * p.NB)), block(kThreadsPerBlock);
-  if (aligned)
-    hipLaunchKernelGGL(mas_kernel<true>, grid, block, 0, stream, p);
-  else
-    hipLaunchKernelGGL(mas_kernel<false>, grid, block, 0, stream, p);
+  hipLaunchKernelGGL(mas_kernel, grid, block, 0, stream, p);
   return hipGetLastError();
 }
 
