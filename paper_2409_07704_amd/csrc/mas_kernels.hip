@@ -126,11 +126,11 @@ struct Cursor {
 __device__ __forceinline__ Cursor make_cursor(const void* p, int bytes) { return Cursor{static_cast<const char*>(p), bytes}; }
 
 // Buffer resource over the bytes [off, total) of the region at p (empty
-// when off >= total; total < 2^31).
+// when off >= total; total < 2^31).  Every field is read back as
+// wave-uniform, so the descriptor can feed inline-assembly scalar operands.
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t sub_rsrc(const void* p, uint64_t total, uint64_t off) {
   const uint64_t o = off < total ? off : total;
-  return __builtin_amdgcn_make_buffer_rsrc(const_cast<char*>(static_cast<const char*>(p)) + o, 0, (int)(uint32_t)(total - o),
-                                           kRsrcWord3);
+  return Cursor{static_cast<const char*>(p) + o, (int)(uint32_t)(total - o)}.rsrc_s();
 }
 
 // Loads into LDS (the lds flag): every lane's bytes at its voffset go to LDS
@@ -138,6 +138,7 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t sub_rsrc(const void* p, uint64
 // such a load.
 // Device-scope (sc1) variants for data written by other workgroups.
 __device__ __forceinline__ void dma4_dev(uint32_t lds, __amdgpu_buffer_rsrc_t r, int voff) {
+  lds = __builtin_amdgcn_readfirstlane(lds);
   asm volatile("s_mov_b32 m0, %[l]\n\ts_nop 0\n\tbuffer_load_dword %[v], %[r], 0 offen sc1 lds"
                :
                : [l] "s"(lds), [r] "s"(r), [v] "v"(voff)
@@ -146,6 +147,7 @@ __device__ __forceinline__ void dma4_dev(uint32_t lds, __amdgpu_buffer_rsrc_t r,
 // One 16-byte load per lane, device-scope: the bytes at voff of the resource
 // to LDS at lds + 16 lane.
 __device__ __forceinline__ void dma_piece(uint32_t lds, __amdgpu_buffer_rsrc_t r, int voff) {
+  lds = __builtin_amdgcn_readfirstlane(lds);
   asm volatile("s_mov_b32 m0, %[l]\n\ts_nop 0\n\tbuffer_load_dwordx4 %[v], %[r], 0 offen sc1 lds"
                :
                : [l] "s"(lds), [r] "s"(r), [v] "v"(voff)
