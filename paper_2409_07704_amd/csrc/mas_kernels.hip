@@ -1,47 +1,43 @@
 // libmas kernels for gfx950 (MI355X): batched monotonic alignment search
-// (Super-MAS Sec. 2, Algorithm 1; column-parallel forward loop of
+// (Super-MAS Sec. 2, Algorithm 1; the column-parallel forward loop of
 // Algorithm 2) and the dense path writer.
 //
-// One launch computes everything (mas_kernel).  A workgroup owns 256 text
-// rows of one item: four waves, one text row per lane, 64 rows per wave.  A
-// wave walks the speech axis in chunks of 32 columns.
-//   * The recurrence's only cross-row dependency, the diagonal predecessor
-//     Q[i-1][j-1], crosses lanes with one DPP wave_shr:1 per column, crosses
-//     waves of a workgroup through an LDS ring, and crosses workgroups
-//     through 64-bit {value, tag} words in global memory.  Wave g starts at
-//     chunk floor(64g / 32): all earlier cells of its rows lie in the masked
-//     triangle i > j, so waves are naturally skewed by 64 columns.
-//   * Value tiles (64 rows x 32 columns) travel HBM -> LDS by buffer loads
-//     with the lds flag, three chunks ahead, eight coalesced 16-byte pieces
-//     per lane, into an XOR-swizzled layout from which each lane reads its
-//     own row's 32 values.
-//   * Q is never materialised: each lane keeps its row's previous column in
-//     a register.  Each column's 64-row decision mask is the compare's SGPR
-//     mask; every lane shifts its bit into a 32-bit word (v_addc with the
-//     mask as carry-in), stored once per chunk.
-//   * The dense path is cleared by the same waves: each wave zeroes its own
-//     64 rows of the path, two 1 KiB stores per chunk step.
-//   * The wave owning row t_x-1 then walks the decision words backwards from
-//     (t_x-1, t_y-1), four chunks per block (words fetched two blocks ahead,
-//     staged in LDS; one find-first-set per row change), builds row_start
-//     in LDS and writes the item's ones into the cleared path.
+// One launch computes everything (mas_kernel).  A workgroup owns 252 text
+// rows of one item and has eight waves:
+//   * four sweep waves (one per SIMD): wave w owns 63 rows, one text row per
+//     lane in lanes 1..63, and lane 0 carries a copy of the row above the
+//     wave.  A wave walks the speech axis in chunks of 32 columns.  The
+//     diagonal predecessor Q[i-1][j-1] crosses lanes with one DPP wave_shr:1
+//     per column, crosses waves of the workgroup through LDS ring slots, and
+//     crosses workgroups through 64-bit {value, tag} words in global memory.
+//     Wave g starts at chunk floor(63g / 32): every earlier cell of its rows
+//     lies in the masked triangle i > j.
+//   * four loader waves: loader w moves sweep wave w's value tiles (64 rows x
+//     32 columns) from HBM into an LDS ring by buffer loads with the lds flag,
+//     up to four chunks ahead, and publishes each tile once it has landed.
+//     The sweep waves issue no loads of values; they read their tiles from LDS
+//     while the next chunk's reads are already in flight.  Afterwards the
+//     loader writes zeros over its sweep wave's path rows.
+// The sweep wave holding row t_x-1 walks the decision words back from
+// (t_x-1, t_y-1) once every wave of the item has published them; its loader
+// stages the decision words of upcoming chunks in LDS.  The walker then
+// writes the ones of the alignment over the zeroed rows.
 //
-// Vector-memory accounting: gfx9 retires a wave's vector-memory operations
-// (loads and stores alike) in issue order, so "the operation issued N
-// operations ago has completed" is s_waitcnt vmcnt(N).  Every vector-memory
-// operation of the sweep loop is issued from inline assembly in a fixed
-// sequence per step, and each step waits with a count derived from that
-// sequence; the compiler neither sees these operations nor inserts waits
-// for them.  Loads that feed the loop write LDS, never registers, so no
-// register is written behind the compiler's back.
+// Every wait is bounded, and a wave only waits on waves of its own workgroup
+// or of workgroups with lower ids, which the hardware dispatches first:
+// workgroup (band r, item b) has id r * B + b.
 //
-// Memory ordering across workgroups: data handed between workgroups
-// (decision words, boundary words, flags, path bytes) is written with
-// device-scope write-through stores and read with device-scope loads, and a
-// wave waits for all its stores (vmcnt(0)) before raising a flag, so no cache
-// write-back or invalidation is needed.
+// Memory ordering across workgroups: data handed between workgroups (decision
+// words, boundary words, flags, path bytes) is written with device-scope
+// (write-through) stores and read with device-scope loads, and a wave waits
+// for its stores (vmcnt(0)) before raising a flag, so no cache write-back or
+// invalidation is needed.  Path zeros and ones for the same bytes come from
+// different workgroups: both go through to memory, the zeros before the
+// cleared flag that the writer of the ones waits for.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
+
+#include <type_traits>
 
 #include "mas_internal.h"
 
@@ -50,6 +46,7 @@ namespace mas {
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+typedef int i32x4 __attribute__((ext_vector_type(4)));
 
 __device__ __forceinline__ float neg_inf() { return -__builtin_inff(); }
 
@@ -62,134 +59,193 @@ __device__ __forceinline__ void wave_lds_sync() {
 }
 
 // Device-scope (write-through) stores and loads of data shared across
-// workgroups, outside the sweep loop.
+// workgroups.
 __device__ __forceinline__ void st_dev(uint32_t* p, uint32_t v) { __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT); }
-__device__ __forceinline__ void st_dev(uint64_t* p, uint64_t v) { __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT); }
 __device__ __forceinline__ void st_dev(uint8_t* p, uint8_t v) { __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT); }
 __device__ __forceinline__ uint32_t ld_dev(const uint32_t* p) { return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT); }
 
 __device__ __forceinline__ int lds_load(const int* p) { return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP); }
 __device__ __forceinline__ void lds_store(int* p, int v) { __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP); }
+__device__ __forceinline__ long long lds_load(const long long* p) { return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP); }
+__device__ __forceinline__ void lds_store(long long* p, long long v) { __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP); }
 
 __device__ __forceinline__ uint32_t call_tag(uint32_t gen) { return 2u * gen + 1u; }
+__device__ __forceinline__ int uni(int v) { return __builtin_amdgcn_readfirstlane(v); }
 
-constexpr int kSpinLimit = 1 << 21;  // bound of every device-side wait (~seconds)
-constexpr int kOnesPerLane = 128;    // path bytes a lane writes for its own row before the wave helps
-constexpr int kGroup = 4;            // chunks per value load (512 contiguous bytes of each row)
-constexpr int kSlots = 4;            // boundary-row slots per wave (a power of two, = kGroup)
-constexpr int kPollSlots = 4;        // LDS slots of polled boundary words
-static_assert((kSlots & (kSlots - 1)) == 0 && kSlots == kGroup, "slot ring");
+constexpr int kSpinLimit = 1 << 20;  // bound of every device-side wait
+constexpr int kOnesPerLane = 128;    // path bytes a lane writes for one row before the wave helps
+constexpr int kLoaders = 4;          // loader waves per workgroup
+constexpr int kThreads = kThreadsPerBlock + kLoaders * kWave;
+constexpr int kRing = 4;             // tile and boundary slots per sweep wave
+constexpr int kPollAhead = 4;        // boundary polls in flight (first wave of a workgroup)
+constexpr int kPolicyDev = 16;       // cache policy sc1: device scope (write-through stores)
 
-// ---------------------------------------------------------------- vector memory (inline asm)
-// Byte offset of a __shared__ object inside the workgroup's LDS allocation.
+// ---------------------------------------------------------------- LDS layout
+// Sweep wave w owns kRing slots of kSlotStride bytes.  Slot k holds
+//   * the value tile of one chunk: 64 tile rows (item rows 63g .. 63g+63; the
+//     last one is loaded but unused) of 128 bytes.  Piece p (16 bytes,
+//     columns 4p .. 4p+3) of tile row r sits at position p ^ swz(r) of the
+//     row, swz(r) = (r >> 1) & 7: for any piece, 16 consecutive rows then
+//     occupy 16 distinct four-bank groups of the 64-bank LDS, so the reads of
+//     a wave (lane l reads row l-1) are conflict-free;
+//   * at kBoundOff, the chunk's boundary row: Q of the row above the wave
+//     for the chunk's 32 columns (lane 0's values).
+// Chunk c uses slot (c - c_begin) % kRing of its wave.
+constexpr int kTileBytes = kWave * kChunk * 4;  // 8192
+constexpr int kBoundOff = kTileBytes;
+constexpr int kSlotStride = kTileBytes + 256;
+constexpr int kWaveRegion = kRing * kSlotStride;
+__host__ __device__ constexpr int swz(int r) { return (r >> 1) & 7; }
+
+// The walk reuses the slot area: decision-word windows of kWinRows rows for
+// kNWin chunks, and the row_start table under construction.
+constexpr int kWinRows = 1024;
+constexpr int kNWin = 24;
+constexpr int kWinAhead = 14;  // windows in flight (4 loads each: at most 63 outstanding)
+static_assert(kWinRows >= 32 * (kNWin - 1) + kWave + 96, "a window covers the rows the walk can reach");
+// Walker position: (chunk << 32) | row, or -1 once the walk is over.
+__device__ __forceinline__ long long walk_pos(int chunk, int row) { return ((long long)chunk << 32) | (uint32_t)row; }
+
+struct SweepLds {
+  union {
+    uint8_t ring[kWavesPerBlock][kWaveRegion];
+    struct {
+      uint32_t win[kNWin][kWinRows];
+      int rs[kMaxRows + 1 + kWave];
+    } walk;
+  } u;
+  f32x4 ostage[1][kChunk / 4];  // last row of wave 3 before its global hand-off
+  uint32_t poll[kPollAhead][kWave];  // polled boundary words {value, tag} x 32 (wave 0)
+  // Mailbox of sweep wave w, read with one 16-byte load per chunk:
+  //   .x ready: value tiles of chunks < ready are in w's slots (loader w);
+  //   .y prod:  boundary rows of chunks < prod are in w's slots (wave w-1);
+  //   .z cnext: progress of wave w+1: it has read every chunk < cnext, whose
+  //             slots are free again (written by wave w+1).
+  // Wave 0's own progress goes to cons0.
+  i32x4 box[kWavesPerBlock];
+  int cons0;
+  int wlo[kNWin];               // first row of each walk window (T > kWinRows)
+  int wready;                   // walk windows in LDS: chunks >= wready
+  long long wpos;               // walker position (walk_pos), or -1 once the walk is over
+};
+static_assert(sizeof(SweepLds) <= 160 * 1024, "LDS");
+
 template <typename T>
 __device__ __forceinline__ uint32_t lds_off(T* p) {
   return (uint32_t)(uintptr_t)(__attribute__((address_space(3))) T*)p;
 }
 
+// ---------------------------------------------------------------- vector memory
 // Waits until at most N vector-memory operations of this wave are outstanding.
 template <int N>
 __device__ __forceinline__ void vm_wait() {
   static_assert(N >= 0 && N <= 63, "vmcnt is a 6-bit counter");
   asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
 }
+// The same for a count known only at run time (n in [0, 63]; more waits for 0).
+__device__ __forceinline__ void vm_wait_n(int n) {
+  switch (n) {
+#define MAS_VMW(k) \
+  case k:          \
+    vm_wait<k>();  \
+    break;
+    MAS_VMW(0) MAS_VMW(1) MAS_VMW(2) MAS_VMW(3) MAS_VMW(4) MAS_VMW(5) MAS_VMW(6) MAS_VMW(7) MAS_VMW(8)
+    MAS_VMW(9) MAS_VMW(10) MAS_VMW(11) MAS_VMW(12) MAS_VMW(13) MAS_VMW(14) MAS_VMW(15) MAS_VMW(16)
+    MAS_VMW(17) MAS_VMW(18) MAS_VMW(19) MAS_VMW(20) MAS_VMW(21) MAS_VMW(22) MAS_VMW(23) MAS_VMW(24)
+    MAS_VMW(25) MAS_VMW(26) MAS_VMW(27) MAS_VMW(28) MAS_VMW(29) MAS_VMW(30) MAS_VMW(31) MAS_VMW(32)
+    MAS_VMW(33) MAS_VMW(34) MAS_VMW(35) MAS_VMW(36) MAS_VMW(37) MAS_VMW(38) MAS_VMW(39) MAS_VMW(40)
+    MAS_VMW(41) MAS_VMW(42) MAS_VMW(43) MAS_VMW(44) MAS_VMW(45) MAS_VMW(46) MAS_VMW(47) MAS_VMW(48)
+    MAS_VMW(49) MAS_VMW(50) MAS_VMW(51) MAS_VMW(52) MAS_VMW(53) MAS_VMW(54) MAS_VMW(55) MAS_VMW(56)
+    MAS_VMW(57) MAS_VMW(58) MAS_VMW(59) MAS_VMW(60) MAS_VMW(61) MAS_VMW(62) MAS_VMW(63)
+#undef MAS_VMW
+    default:
+      vm_wait<0>();
+  }
+}
 
 // A buffer resource that moves forward through a region: base and number of
-// bytes left, turned into a descriptor (raw buffer, 32-bit data format) at
-// each use.  Loads at offsets >= num_records return 0 and such stores are
-// dropped (the per-lane offset is range-checked, the scalar offset is not).
+// bytes left.  Loads at per-lane offsets >= the count return 0 and such
+// stores are dropped (the per-lane offset is range-checked, the scalar offset
+// is not).  rsrc_s() reads every field back as wave-uniform, so the
+// descriptor can feed scalar operands of inline assembly.
 constexpr int kRsrcWord3 = 0x00020000;
-// The compiler computes the saturating count update with a vector
-// instruction; the descriptor must live in scalar registers, so the count
-// is read back as a wave-uniform value.  Byte counts are below 2^31.
 struct Cursor {
   const char* base;
   int left;
   __device__ __forceinline__ __amdgpu_buffer_rsrc_t rsrc() const {
     return __builtin_amdgcn_make_buffer_rsrc(const_cast<char*>(base), 0, left, kRsrcWord3);
   }
-  // The same, with every field read back as wave-uniform: for inline
-  // assembly operands that must be scalar registers (under scalar-register
-  // pressure the compiler may keep a uniform pointer in vector registers).
   __device__ __forceinline__ __amdgpu_buffer_rsrc_t rsrc_s() const {
     const uint64_t a = (uint64_t)(uintptr_t)base;
-    const uint64_t lo = (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)a);
-    const uint64_t hi = (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)(a >> 32));
-    return __builtin_amdgcn_make_buffer_rsrc(reinterpret_cast<char*>((uintptr_t)(lo | hi << 32)), 0,
-                                             __builtin_amdgcn_readfirstlane(left), kRsrcWord3);
+    const uint64_t lo = (uint32_t)uni((int)(uint32_t)a);
+    const uint64_t hi = (uint32_t)uni((int)(uint32_t)(a >> 32));
+    return __builtin_amdgcn_make_buffer_rsrc(reinterpret_cast<char*>((uintptr_t)(lo | hi << 32)), 0, uni(left), kRsrcWord3);
   }
   __device__ __forceinline__ void advance(int step) {
     base += step;
-    left = __builtin_amdgcn_readfirstlane(max(left - step, 0));
+    left = uni(max(left - step, 0));
   }
 };
-__device__ __forceinline__ Cursor make_cursor(const void* p, int bytes) { return Cursor{static_cast<const char*>(p), bytes}; }
-
-// Buffer resource over the bytes [off, total) of the region at p (empty
-// when off >= total; total < 2^31).  Every field is read back as
-// wave-uniform, so the descriptor can feed inline-assembly scalar operands.
-__device__ __forceinline__ __amdgpu_buffer_rsrc_t sub_rsrc(const void* p, uint64_t total, uint64_t off) {
-  const uint64_t o = off < total ? off : total;
-  return Cursor{static_cast<const char*>(p) + o, (int)(uint32_t)(total - o)}.rsrc_s();
+__device__ __forceinline__ Cursor make_cursor(const void* p, uint64_t bytes) {
+  return Cursor{static_cast<const char*>(p), (int)(bytes < 0x7fffffffull ? bytes : 0x7fffffffull)};
 }
 
-// Loads into LDS (the lds flag): every lane's bytes at its voffset go to LDS
-// at M0 + size * lane.  A scalar write of M0 needs one wait state before
-// such a load.
-// Device-scope (sc1) variants for data written by other workgroups.
-__device__ __forceinline__ void dma4_dev(uint32_t lds, __amdgpu_buffer_rsrc_t r, int voff) {
-  lds = __builtin_amdgcn_readfirstlane(lds);
-  asm volatile("s_mov_b32 m0, %[l]\n\ts_nop 0\n\tbuffer_load_dword %[v], %[r], 0 offen sc1 lds"
+// Loads into LDS: every lane's bytes at its voffset go to LDS at
+// M0 + size * lane.  A scalar write of M0 needs one wait state before the
+// load.  dma16 / dma4: read-only input (default cache policy); dma16_dev /
+// dma4_dev: data written by other workgroups (device scope).
+__device__ __forceinline__ void dma16(uint32_t lds, __amdgpu_buffer_rsrc_t r, int voff) {
+  lds = uni(lds);
+  asm volatile("s_mov_b32 m0, %[l]\n\ts_nop 0\n\tbuffer_load_dwordx4 %[v], %[r], 0 offen lds"
                :
                : [l] "s"(lds), [r] "s"(r), [v] "v"(voff)
                : "memory", "m0");
 }
-// One 16-byte load per lane, device-scope: the bytes at voff of the resource
-// to LDS at lds + 16 lane.
-__device__ __forceinline__ void dma_piece(uint32_t lds, __amdgpu_buffer_rsrc_t r, int voff) {
-  lds = __builtin_amdgcn_readfirstlane(lds);
+__device__ __forceinline__ void dma16_dev(uint32_t lds, __amdgpu_buffer_rsrc_t r, int voff) {
+  lds = uni(lds);
   asm volatile("s_mov_b32 m0, %[l]\n\ts_nop 0\n\tbuffer_load_dwordx4 %[v], %[r], 0 offen sc1 lds"
                :
                : [l] "s"(lds), [r] "s"(r), [v] "v"(voff)
                : "memory", "m0");
 }
-
-// Stores at voff + soff of a resource, device-scope (write-through).
-__device__ __forceinline__ void buf_store32(uint32_t v, int voff, __amdgpu_buffer_rsrc_t r, uint32_t soff) {
-  asm volatile("buffer_store_dword %[d], %[v], %[r], %[s] offen sc1" ::[d] "v"(v), [v] "v"(voff), [r] "s"(r), [s] "s"(soff)
-               : "memory");
+__device__ __forceinline__ void dma4_dev(uint32_t lds, __amdgpu_buffer_rsrc_t r, int voff) {
+  lds = uni(lds);
+  asm volatile("s_mov_b32 m0, %[l]\n\ts_nop 0\n\tbuffer_load_dword %[v], %[r], 0 offen sc1 lds"
+               :
+               : [l] "s"(lds), [r] "s"(r), [v] "v"(voff)
+               : "memory", "m0");
 }
-__device__ __forceinline__ void buf_store64(uint64_t v, int voff, __amdgpu_buffer_rsrc_t r, uint32_t soff) {
-  asm volatile("buffer_store_dwordx2 %[d], %[v], %[r], %[s] offen sc1" ::[d] "v"(v), [v] "v"(voff), [r] "s"(r), [s] "s"(soff)
-               : "memory");
-}
-// A 16-byte zero store (s_nop: a VALU write of store data needs one wait
-// state).  Path bytes are only ever written by the wave that owns their row,
-// so this needs no device-scope write-through.
-__device__ __forceinline__ void vm_zero1(uint64_t a, u32x4 z) {
-  asm volatile("global_store_dwordx4 %0, %1, off\n\ts_nop 0" ::"v"(a), "v"(z) : "memory");
+__device__ __forceinline__ void dma4(uint32_t lds, __amdgpu_buffer_rsrc_t r, int voff) {
+  lds = uni(lds);
+  asm volatile("s_mov_b32 m0, %[l]\n\ts_nop 0\n\tbuffer_load_dword %[v], %[r], 0 offen lds"
+               :
+               : [l] "s"(lds), [r] "s"(r), [v] "v"(voff)
+               : "memory", "m0");
 }
 
-// The recurrence, one text row per lane, lane 0 carrying the row above the
-// wave.  Per column j (Algorithm 2's parallel step):
-//   t      = max(Q[r-1][j-1], Q[r][j-1])    v_max_f32 with DPP wave_shr:1
+// ---------------------------------------------------------------- recurrence
+// One text row per lane, lane 0 carrying the row above the wave.  Per column
+// j (Algorithm 2's parallel step):
+//   t       = max(Q[r-1][j-1], Q[r][j-1])   v_max_f32 with DPP wave_shr:1
 //                                            (lane l reads lane l-1's Q);
-//   Q[r][j] = t + value[r][j]               one fp32 add;
-//   d      = sign(Q[r][j-1] - t)            1 iff the diagonal is strictly
-//                                            greater (-0 below +0, the order
-//                                            of v_max_f32 and of R2);
-//   bits   = bits << 1 | d                  v_alignbit (first column ends in
-//                                            bit 31 after 32 columns).
+//   Q[r][j] = t + value[r][j]                one fp32 add;
+//   d       = sign(Q[r][j-1] - t)            1 iff the diagonal is strictly
+//                                            greater (-0 below +0: the order
+//                                            of v_max_f32);
+//   bits    = bits << 1 | d                  v_alignbit (the chunk's first
+//                                            column ends in bit 31).
 // Lane 0 has no lane below it: DPP leaves its t untouched, and t is kept at
 // -0 in lane 0 for the whole sweep, so lane 0's Q becomes -0 + value = value
-// exactly (x + -0 = x for every x): lane 0's "values" are the Q of the row
-// above, handed down by the previous wave (or -inf above row 0).
+// exactly: lane 0's "values" are the Q of the row above, handed down by the
+// previous wave (or -inf above row 0).
 // A VALU write followed by a DPP read of the same register needs two wait
 // states: each column's add is followed by two other VALU instructions
 // before the next column reads it, and each block starts with s_nop 1.
+// (asm volatile: the compute must stay between the LDS reads issued before
+// it and the wait after it.)
 __device__ __forceinline__ void cols8(float& q, float& t, uint32_t& bits, float (&o)[8], const float* v) {
   float u;
-  asm("s_nop 1\n\t"
+  asm volatile("s_nop 1\n\t"
       "v_max_f32_dpp %[t], %[q], %[q] wave_shr:1 row_mask:0xf bank_mask:0xf\n\t"
       "v_add_f32 %[o0], %[t], %[v0]\n\t"
       "v_sub_f32 %[u], %[q], %[t]\n\t"
@@ -232,7 +288,7 @@ __device__ __forceinline__ void cols8(float& q, float& t, uint32_t& bits, float 
 // One column of the same step (for the chunks that cross the masked triangle).
 __device__ __forceinline__ float col1(float q, float& t, uint32_t& bits, float v) {
   float o, u;
-  asm("s_nop 1\n\t"
+  asm volatile("s_nop 1\n\t"
       "v_max_f32_dpp %[t], %[q], %[q] wave_shr:1 row_mask:0xf bank_mask:0xf\n\t"
       "v_add_f32 %[o], %[t], %[v]\n\t"
       "v_sub_f32 %[u], %[q], %[t]\n\t"
@@ -243,7 +299,7 @@ __device__ __forceinline__ float col1(float q, float& t, uint32_t& bits, float v
 }
 
 // One 32-column chunk for lanes 1..63 (rows row0 + lane - 1) and the carried
-// row in lane 0.  v: this lane's 32 values (lane 0: the row above's Q);
+// row in lane 0.  v4: this lane's 32 values (lane 0: the row above's Q);
 // qc: Q of every column (out); bits: decisions, first column in bit 31.
 // MASKED: the chunk crosses the triangle i > j, where Q is -inf (lane 0's
 // copies already are), and holds the first cell Q[0][0] = value[0][0] when
@@ -259,7 +315,7 @@ __device__ __forceinline__ void sweep_chunk(float& q, float& t, const f32x4 (&v4
     v[4 * k + 2] = v4[k].z;
     v[4 * k + 3] = v4[k].w;
   }
-  uint32_t w = bits;
+  uint32_t w = 0;
   if (!MASKED) {
 #pragma unroll
     for (int k = 0; k < 4; ++k) {
@@ -296,100 +352,9 @@ __device__ __forceinline__ uint4 path_piece(int lo, int hi, int j0) {
   return make_uint4((uint32_t)m0, (uint32_t)(m0 >> 32), (uint32_t)m1, (uint32_t)(m1 >> 32));
 }
 
-// ---------------------------------------------------------------- LDS layout
-// The walk fetches each chunk's decision words kWalkAhead chunks before it
-// walks that chunk, as a window of kWalkWin rows below the walker's row e at
-// fetch time.  One chunk before walking it, the walker reads the 64 rows
-// below its current row from that window (a chunk holds at most 33 rows of
-// the path, and the current row is at most 32 rows into the 64); the current
-// row is then at least e - 32 (kWalkAhead - 1), as a chunk descends at most
-// 32 rows.
-constexpr int kWalkAhead = 14;
-constexpr int kWalkLoads = 2;                      // 1 KiB loads per window
-constexpr int kWalkWin = kWalkLoads * 4 * kWave;   // rows per window
-constexpr int kWalkSlots = 16;                 // window ring (power of two > kWalkAhead)
-static_assert(kWalkWin >= 32 * (kWalkAhead - 1) + kWave + 3, "walk window");
-
-// Per-wave LDS region (kWaveLds bytes):
-//   * kGroup value tiles, one per chunk of the current group of kGroup
-//     chunks: 64 rows of 32 values, item rows 63g .. 63g+63 (row 63 unused),
-//     row r at byte 144 r of its tile.  The 16 bytes of padding per row put
-//     piece k of 16 consecutive rows in distinct 4-bank groups of the
-//     64-bank LDS (36 r mod 64 differs for r mod 16), so the per-row reads of
-//     a wave are conflict-free with one address per lane plus the piece
-//     offset;
-//   * kSlots boundary slots at kBoundOff + 256 k: the 32 Q values of the row
-//     above the wave for chunk c in slot (c - c_begin) % kSlots (word
-//     9244 + 64 k = 28 mod 64, a bank group rows 0 .. 14 do not use), then
-//     its tag (chunk + 1).  The previous wave of the workgroup writes them; a
-//     wave fed by another workgroup copies its polled words there; the first
-//     wave of an item fills them with -inf once.
-constexpr int kRowBytes = 144;
-constexpr int kTileBytes = 64 * kRowBytes;
-constexpr int kBoundOff = kGroup * kTileBytes + 112;
-constexpr int kSlotBytes = 256;
-constexpr int kTagOff = 4 * kChunk;  // inside a slot
-constexpr int kWaveLds = 37888;
-static_assert(kBoundOff % 16 == 0 && (kBoundOff / 4) % 64 == 28, "boundary slot");
-static_assert(kBoundOff + (kSlots - 1) * kSlotBytes + kTagOff + 4 <= kWaveLds && kWaveLds % 256 == 0, "wave region");
-static_assert(kBoundOff + (kSlots - 1) * kSlotBytes + kTagOff + 4 <= kWaveLds && kWaveLds % 256 == 0, "wave region");
-
-struct SweepLds {
-  union {
-    uint8_t tile[kWavesPerBlock][kWaveLds];
-    // The walker's staging, once every sweep of its item (and so of its
-    // workgroup) has finished.
-    struct {
-      uint32_t win[kWalkSlots][kWalkWin];  // decision-word windows of upcoming chunks
-      int rs[kMaxRows + 2 * kWave];        // row_start under construction
-    } walk;
-  } u;
-  uint32_t poll[kPollSlots][kWave];        // polled boundary words {value, tag} x 32 (wave 0)
-  f32x4 ostage[kChunk / 4];                // last row of wave 3 before its global hand-off
-  uint32_t dummy[kWavesPerBlock][kWave];   // target of placeholder loads and idle lanes' writes
-  int cons[kWavesPerBlock];                // next chunk wave w will consume
-};
-static_assert(sizeof(SweepLds) <= 160 * 1024, "LDS");
-
-// ---------------------------------------------------------------- path clearing
-// The bytes [p0, p1) of the path that one wave clears: its 63 rows of its
-// item.  16-byte aligned pieces [a0, a1) go through the sweep schedule; the
-// unaligned head and tail are cleared up front with byte stores.
-struct ZeroPlan {
-  uint64_t a0;    // address of the first aligned piece
-  uint64_t last;  // address of the last aligned piece (a1 - 16)
-  bool any;       // at least one aligned piece
-};
-
-__device__ __forceinline__ ZeroPlan zero_plan(const KParams& p, int b, int g, int lane) {
-  const uint64_t base = (uint64_t)b * (uint64_t)p.T * (uint64_t)p.S;  // offsets from p.path
-  const int r0 = min(g * kRowsPerWave, p.T), r1 = min(g * kRowsPerWave + kRowsPerWave, p.T);
-  const uint64_t p0 = base + (uint64_t)r0 * (uint64_t)p.S, p1 = base + (uint64_t)r1 * (uint64_t)p.S;
-  const uint64_t pa = (uint64_t)(uintptr_t)p.path;
-  const uint64_t a0 = ((pa + p0 + 15) & ~15ull) - pa, a1 = ((pa + p1) & ~15ull) - pa;
-  ZeroPlan z;
-  z.any = a1 > a0 && a1 - a0 >= 16;
-  z.a0 = pa + a0;
-  z.last = pa + a1 - 16;
-  // Unaligned head and tail bytes (at most 15 + 15; all bytes if no piece).
-  const uint64_t h1 = z.any ? a0 : p1;
-  for (uint64_t o = p0 + lane; o < h1; o += kWave) p.path[o] = 0;
-  if (z.any)
-    for (uint64_t o = a1 + lane; o < p1; o += kWave) p.path[o] = 0;
-  return z;
-}
-
-// Clears the aligned pieces from address `from` to the last one with 1 KiB
-// stores (outside the sweep schedule).
-__device__ __forceinline__ void zero_rest(const ZeroPlan& z, uint64_t from, int lane) {
-  const u32x4 zero = {0u, 0u, 0u, 0u};
-  for (uint64_t a = from + 16u * (uint64_t)lane; a <= z.last; a += 16u * kWave) vm_zero1(a, zero);
-}
-
-// ---------------------------------------------------------------- sweep
-// Per-wave constants of the sweep.
+// ---------------------------------------------------------------- per-wave context
 struct WaveCtx {
-  int lane, wv, b, g, g_last, tx, ty, row, c_begin, c_end;
+  int lane, w, b, g, g_last, tx, ty, row, c_begin, c_end;
   int prev_end;    // chunks the previous wave computes (exclusive end)
   int mask_end;    // first chunk without a cell i > j of this wave
   int next_begin;  // the next wave's first chunk
@@ -401,291 +366,29 @@ struct WaveCtx {
 // row r is useful up to column r + t_y - t_x).  Cells outside only feed
 // cells outside (a reachable cell's two predecessors are reachable), so
 // whatever they hold never reaches a decision the walk reads or the score.
+__device__ __forceinline__ int chunk_begin(int g) { return (g * kRowsPerWave) / kChunk; }
 __device__ __forceinline__ int chunk_end(int g, int tx, int ty) {
   const int by_len = (ty + kChunk - 1) / kChunk;
   const int by_reach = (g * kRowsPerWave + kRowsPerWave - 1 + ty - tx) / kChunk + 1;
   return by_len < by_reach ? by_len : by_reach;
 }
 
-// Byte offset of (tile row r, byte e of the row) in the value slab relative
-// to the tile's first row, or INT_MIN: as an unsigned offset it stays at or
-// above 2^31, outside every resource, after adding up to 2^31 - 1.
-__device__ __forceinline__ int tile_voff(int r, int e, int S) {
-  const uint64_t o = (uint64_t)r * (uint64_t)S * 4u + (uint64_t)e;
-  return o < 0x80000000ull ? (int)o : (int)0x80000000u;
-}
-
-__device__ __forceinline__ f32x4 load16(__amdgpu_buffer_rsrc_t r, int voff) {
-  return __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(r, voff, 0, 0));
-}
-
-template <int V>
-struct IntC {
-  static constexpr int value = V;
-};
-
-// Cache policy of hand-off data between workgroups: sc1 (device scope).
-constexpr int kPolicyDev = 16;
-
-// Sweeps this wave's rows over its chunks and returns the score candidate
-// (Q at (row, t_y-1) of this lane; only meaningful for the wave holding row
-// t_x-1).  IN: where the row above the wave comes from — 0 nowhere (the wave
-// holds row 0), 1 the previous wave of the workgroup, 2 global boundary words
-// of the previous workgroup.  OUT: 0 no consumer, 1 the next wave of the
-// workgroup, 2 global boundary words for the next workgroup.
-//
-// Value tiles travel HBM -> registers -> LDS in groups of kGroup chunks
-// (512 contiguous bytes of each row: DRAM serves longer runs of a row
-// faster than scattered 128-byte pieces).  While the kGroup tiles of one
-// group sit in LDS and are swept, the next group is in flight in registers.
-// Lane L loads piece L % 8 of chunk j of tile rows 8q + L/8 (q = 0..7):
-// 16 bytes each, eight lanes per 128-byte row segment.  The compiler sees
-// these loads and waits for them right before writing them to LDS.
-template <int IN, int OUT>
-__device__ __forceinline__ float sweep_rows(const KParams& p, SweepLds& L, const WaveCtx& x, uint32_t tag, bool& timed_out) {
-  constexpr bool IN2 = IN == 2, OUT2 = OUT == 2;
-  const int lane = x.lane, wv = x.wv;
-  float t = -0.0f;  // lane 0 keeps -0 for the whole sweep (see cols8)
-
-  // LDS: byte offsets from the start of L (where the wave regions begin).
-  char* const Lc = reinterpret_cast<char*>(&L);
-  const uint32_t wbase = (uint32_t)wv * kWaveLds;
-  const uint32_t nbase = wbase + kWaveLds;  // the next wave's region
-  auto slot_ptr = [&](uint32_t base, int k) __attribute__((always_inline)) -> char* {
-    return Lc + base + kBoundOff + (uint32_t)(k & (kSlots - 1)) * kSlotBytes;
-  };
-
-  // Value tiles: a resource from the wave's first tile row at the next chunk
-  // to load; rows past the slab fall outside it and read 0.
-  const float* slab = p.value + (size_t)x.b * (size_t)p.T * (size_t)p.S;
-  const int slab_bytes = (int)((uint64_t)p.T * (uint64_t)p.S * 4u);
-  Cursor vr = make_cursor(slab, slab_bytes);
-  vr.advance((int)((uint64_t)x.g * kRowsPerWave * (uint64_t)p.S * 4u) + x.c_begin * (kChunk * 4));
-  int voff[8];
-#pragma unroll
-  for (int q = 0; q < 8; ++q) voff[q] = tile_voff(8 * q + (lane >> 3), 16 * (lane & 7), p.S);
-  // Where lane L's pieces go: row 8q + L/8, piece L % 8 (q * 1152 bytes apart).
-  f32x4* const tile_w = reinterpret_cast<f32x4*>(Lc + wbase + (uint32_t)(lane >> 3) * kRowBytes + 16u * (uint32_t)(lane & 7));
-  // Lane l >= 1 reads tile row l-1; lane 0 reads the chunk's boundary slot.
-  const f32x4* const tile_r = reinterpret_cast<const f32x4*>(Lc + wbase + (uint32_t)(lane > 0 ? lane - 1 : 0) * kRowBytes);
-  f32x4 buf[kGroup][8];
-  auto load_group = [&]() __attribute__((always_inline)) {
-    const __amdgpu_buffer_rsrc_t r = vr.rsrc();
-#pragma unroll
-    for (int q = 0; q < 8; ++q)
-#pragma unroll
-      for (int j = 0; j < kGroup; ++j) buf[j][q] = load16(r, voff[q] + j * (kChunk * 4));
-    vr.advance(kGroup * kChunk * 4);
-  };
-  auto put_group = [&]() __attribute__((always_inline)) {
-#pragma unroll
-    for (int j = 0; j < kGroup; ++j)
-#pragma unroll
-      for (int q = 0; q < 8; ++q) tile_w[j * (kTileBytes / 16) + q * (8 * kRowBytes / 16)] = buf[j][q];
-  };
-
-  // Decision words: dec[b][c][row], lane 0 into the chunk's scratch word.
-  const __amdgpu_buffer_rsrc_t dr = make_cursor(p.dec + (size_t)x.b * p.NC * (size_t)p.TP, p.NC * p.TP * 4).rsrc();
-  const int dvo = 4 * (lane > 0 ? x.row : p.TP - 1);
-  const int dstride = p.TP * 4;
-  // Boundary words of this wave (OUT == 2) and of the previous one (IN == 2).
-  const size_t slot_stride = (size_t)p.NC * kChunk;
-  const int slot_bytes = (int)(slot_stride * 8u);
-  const __amdgpu_buffer_rsrc_t sr = make_cursor(p.slots + ((size_t)x.b * p.NW + x.g) * slot_stride, slot_bytes).rsrc();
-  const int svo = lane < kChunk ? 8 * lane : -16;
-  const uint64_t* pslots = p.slots + ((size_t)x.b * p.NW + (x.g > 0 ? x.g - 1 : 0)) * slot_stride;
-  Cursor pr = make_cursor(pslots, slot_bytes);
-  if (IN2) pr.advance((x.c_begin - 1) * 256);  // first poll: chunk c_begin-1
-
-  // Boundary words of chunk c (256 bytes) into poll slot c % 4.  These
-  // loads are the only vector-memory operations the compiler does not see:
-  // the wait before reading a poll slot counts them by hand.
-  auto issue_poll = [&](int c, __amdgpu_buffer_rsrc_t r) __attribute__((always_inline)) {
-    dma4_dev(lds_off(&L.poll[c & (kPollSlots - 1)][0]), r, 4 * lane);
-  };
-  // Boundary words of chunk c are in poll slot c % 4 once all carry this
-  // call's tag (re-polled until then); lane L's word is L % 32.
-  auto polled_word = [&](int c) __attribute__((always_inline)) -> uint64_t {
-    const uint64_t* pw = reinterpret_cast<const uint64_t*>(&L.poll[c & (kPollSlots - 1)][0]);
-    uint64_t wd = pw[lane & (kChunk - 1)];
-    int spins = 0;
-    while (true) {
-      // Lanes still seeing an old tag, as an opaque scalar: branching on the
-      // ballot directly lets the compiler treat the loop as divergent.
-      uint64_t stale = __builtin_amdgcn_ballot_w64((uint32_t)(wd >> 32) != tag);
-      asm volatile("" : "+s"(stale));
-      if (stale == 0) break;
-      if (++spins > kSpinLimit) {
-        timed_out = true;
-        break;
-      }
-      __builtin_amdgcn_s_sleep(1);
-      // (c is uniform; saying so keeps the descriptor in scalar registers.)
-      const int cu = __builtin_amdgcn_readfirstlane(c);
-      issue_poll(cu, make_cursor(pslots + (size_t)cu * kChunk, kChunk * 8).rsrc_s());
-      vm_wait<0>();
-      wd = pw[lane & (kChunk - 1)];
-    }
-    return wd;
-  };
-  // Waits for the boundary row of chunk c in this wave's slot k.
-  auto bound_ready = [&](int c, int k) __attribute__((always_inline)) {
-    const int* tg = reinterpret_cast<const int*>(slot_ptr(wbase, k) + kTagOff);
-    int spins = 0;
-    while (__builtin_amdgcn_readfirstlane(lds_load(tg)) != c + 1) {
-      if (++spins > kSpinLimit) {
-        timed_out = true;
-        break;
-      }
-      __builtin_amdgcn_s_sleep(1);
-    }
-  };
-
-  if (IN == 0) {
-    // The row above row 0 is -inf in every slot.
-    if (lane < kChunk) {
-#pragma unroll
-      for (int k = 0; k < kSlots; ++k) reinterpret_cast<float*>(slot_ptr(wbase, k))[lane] = neg_inf();
-    }
-  }
-  if (IN2) {
-    // Polls of chunks c_begin-1 .. c_begin+1 (the loop polls two ahead).
-#pragma unroll
-    for (int k = 0; k < 3; ++k) {
-      issue_poll(x.c_begin - 1 + k, pr.rsrc_s());
-      pr.advance(256);
-    }
-  }
-  // The first group in flight.
-  load_group();
-
-  // Lane 0's Q at the column before the first chunk: the previous wave's
-  // last row there (its chunk c_begin-1, always computed), or -inf.
-  float q = neg_inf();
-  if (IN == 1) {
-    bound_ready(x.c_begin - 1, -1);
-    wave_lds_sync();
-    const float e = reinterpret_cast<const float*>(slot_ptr(wbase, -1))[kChunk - 1];
-    q = lane == 0 ? e : q;
-    wave_lds_sync();
-    if (lane == 0) lds_store(&L.cons[wv], x.c_begin);
-  } else if (IN == 2) {
-    vm_wait<0>();
-    const uint64_t wd = polled_word(x.c_begin - 1);
-    const float e = __int_as_float(__builtin_amdgcn_readlane((int)(uint32_t)wd, kChunk - 1));
-    q = lane == 0 ? e : q;
-  }
-
-  // Lane 0 publishes the consumed-chunk counter; the other lanes write
-  // their own dummy words (one store, no exec change).
-  int* const cons_ptr = lane == 0 ? &L.cons[wv] : reinterpret_cast<int*>(&L.dummy[wv][lane]);
-  // Lower bound of the consumer's counter: it starts at its own c_begin-1,
-  // which is at least this wave's c_begin+1 (63 rows span >= 63 columns).
-  int cons_seen = x.c_begin + 1;
-  const int dk = x.c_begin - x.next_begin;  // the next wave's slot of chunk c: c - c_begin + dk
-  float qc[kChunk];
-  int soff = x.c_begin * dstride;
-  // One chunk, at position J of its group: its tile and its boundary slot
-  // are number J.
-  auto step = [&](auto pos_c, int c) __attribute__((always_inline)) {
-    constexpr int J = decltype(pos_c)::value;
-    const int k = c - x.c_begin;  // k % kSlots == J
-    if (IN2) {
-      // Poll of chunk c: issued two steps ago, followed by the rest of that
-      // step and the next one (the group's loads come first in position 0),
-      // and nothing of this one yet.
-      constexpr int tail = 1 + (OUT2 ? 1 : 0);
-      constexpr int n = tail + (((J - 2) & (kGroup - 1)) == 0 ? 8 * kGroup : 0) + 1 + tail +
-                        (((J - 1) & (kGroup - 1)) == 0 ? 8 * kGroup : 0);
-      vm_wait<n>();
-      issue_poll(c + 2, pr.rsrc_s());
-      pr.advance(256);
-    }
-    if (J == 0) {
-      // The group's tiles into LDS (the previous group's reads are done),
-      // the next group into flight.
-      wave_lds_sync();
-      put_group();
-      load_group();
-    }
-    // The row above: from the previous wave, or copied from the polled
-    // words.  Beyond the previous wave's chunks the slot holds stale values:
-    // they only reach cells that cannot reach (t_x-1, t_y-1).
-    if (IN == 1 && c < x.prev_end) bound_ready(c, k);
-    if (IN2 && c < x.prev_end) {
-      const uint64_t wd = polled_word(c);
-      reinterpret_cast<float*>(slot_ptr(wbase, k))[lane & (kChunk - 1)] = __uint_as_float((uint32_t)wd);
-    }
-    wave_lds_sync();
-    f32x4 v[8];
-    {
-      const f32x4* src = lane > 0 ? tile_r + J * (kTileBytes / 16) : reinterpret_cast<const f32x4*>(slot_ptr(wbase, J));
-#pragma unroll
-      for (int m = 0; m < 8; ++m) v[m] = src[m];
-    }
-    uint32_t bits = 0;
-    if (c < x.mask_end)
-      sweep_chunk<true>(q, t, v, qc, bits, lane, x.row, c * kChunk);
-    else
-      sweep_chunk<false>(q, t, v, qc, bits, lane, x.row, c * kChunk);
-    __builtin_amdgcn_raw_buffer_store_b32(bits, dr, dvo, soff, kPolicyDev);
-    soff += dstride;
-    if (IN == 1) {
-      // The reads of this chunk's slot are done: the previous wave may
-      // reuse it for chunk c + kSlots.
-      lds_store(cons_ptr, c + 1);
-    }
-    if (OUT == 1) {
-      // Wait until the consumer no longer needs the slot, then publish the
-      // values, then the tag.
-      int spins = 0;
-      while (cons_seen < c - (kSlots - 1)) {
-        cons_seen = __builtin_amdgcn_readfirstlane(lds_load(&L.cons[wv + 1]));
-        if (cons_seen >= c - (kSlots - 1)) break;
-        if (++spins > kSpinLimit) {
-          timed_out = true;
-          break;
-        }
-        __builtin_amdgcn_s_sleep(1);
-      }
-      char* const ns = slot_ptr(nbase, k + dk);
-      if (lane == kWave - 1) {
-        f32x4* dst = reinterpret_cast<f32x4*>(ns);
-#pragma unroll
-        for (int m = 0; m < kChunk / 4; ++m) dst[m] = f32x4{qc[4 * m], qc[4 * m + 1], qc[4 * m + 2], qc[4 * m + 3]};
-      }
-      // Values before the tag (the LDS executes one wave's operations in
-      // order; the fence keeps the compiler from reordering them).  Kept out
-      // of the lane-63 branch: inside it, the compiler makes the whole chunk
-      // loop divergent for the waves that feed no other wave of the group.
-      wave_lds_sync();
-      if (lane == kWave - 1) lds_store(reinterpret_cast<int*>(ns + kTagOff), c + 1);
-    } else if (OUT2) {
-      if (lane == kWave - 1) {
-#pragma unroll
-        for (int m = 0; m < kChunk / 4; ++m) L.ostage[m] = f32x4{qc[4 * m], qc[4 * m + 1], qc[4 * m + 2], qc[4 * m + 3]};
-      }
-      wave_lds_sync();
-      const float val = reinterpret_cast<const float*>(L.ostage)[lane & (kChunk - 1)];
-      const uint64_t word = ((uint64_t)tag << 32) | (uint64_t)__float_as_uint(val);
-      __builtin_amdgcn_raw_buffer_store_b64(__builtin_bit_cast(u32x2, word), sr, svo, c * 256, kPolicyDev);
-      wave_lds_sync();
-    }
-  };
-  for (int c = x.c_begin; c < x.c_end; c += kGroup) {
-    step(IntC<0>(), c);
-    if (c + 1 < x.c_end) step(IntC<1>(), c + 1);
-    if (c + 2 < x.c_end) step(IntC<2>(), c + 2);
-    if (c + 3 < x.c_end) step(IntC<3>(), c + 3);
-  }
-  vm_wait<0>();
-  float score = neg_inf();
-  if (OUT == 0) {
-    const int m_last = (x.ty - 1) % kChunk;
-#pragma unroll
-    for (int m = 0; m < kChunk; ++m) score = (m == m_last) ? qc[m] : score;
-  }
-  return score;
+__device__ __forceinline__ WaveCtx make_ctx(int b, int g, int w, int lane, int tx, int ty) {
+  WaveCtx x;
+  x.lane = lane;
+  x.w = w;
+  x.b = b;
+  x.g = g;
+  x.tx = tx;
+  x.ty = ty;
+  x.g_last = (tx - 1) / kRowsPerWave;
+  x.row = g * kRowsPerWave + lane - 1;  // lane 0: the row above the wave
+  x.c_begin = chunk_begin(g);
+  x.c_end = chunk_end(g, tx, ty);
+  x.prev_end = g > 0 ? chunk_end(g - 1, tx, ty) : 0;
+  x.mask_end = (g * kRowsPerWave + kRowsPerWave - 2) / kChunk + 1;  // last masked column: 63g + 61
+  x.next_begin = chunk_begin(g + 1);
+  return x;
 }
 
 // Waits (bounded) until flag[k] == tag for every k in [0, n).
@@ -693,15 +396,433 @@ __device__ __forceinline__ void wait_flags(const uint32_t* flag, int n, uint32_t
   for (int k0 = 0; k0 < n; k0 += kWave) {
     const int k = k0 + lane;
     int spins = 0;
-    while (true) {
+    while (!timed_out) {
       const bool ready = k >= n || ld_dev(flag + k) == tag;
       if (__builtin_amdgcn_ballot_w64(!ready) == 0) break;
-      if (++spins > kSpinLimit) {
-        timed_out = true;
-        break;
-      }
-      __builtin_amdgcn_s_sleep(1);
+      if (++spins > kSpinLimit) timed_out = true;
+      __builtin_amdgcn_s_sleep(2);
     }
+  }
+}
+
+// Spins (bounded) until the LDS word *p >= v; returns the last value read.
+__device__ __forceinline__ int wait_at_least(const int* p, int v, bool& timed_out) {
+  int seen = uni(lds_load(p));
+  int spins = 0;
+  while (seen < v && !timed_out) {
+    if (++spins > kSpinLimit) timed_out = true;
+    __builtin_amdgcn_s_sleep(1);
+    seen = uni(lds_load(p));
+  }
+  return seen;
+}
+
+// Spins (bounded) until the LDS word *p == v.
+__device__ __forceinline__ void wait_equal(const int* p, int v, bool& timed_out) {
+  int spins = 0;
+  while (uni(lds_load(p)) != v && !timed_out) {
+    if (++spins > kSpinLimit) timed_out = true;
+    __builtin_amdgcn_s_sleep(1);
+  }
+}
+
+using lds_cchar = const __attribute__((address_space(3))) char;
+
+// The LDS reads of the next chunk in slot K of a sweep wave: the wave's
+// mailbox (ready, prod, cnext), then the lane's 8 pieces (byte offsets a[m]
+// from the base of the shared block).  The empty asm statement with a memory
+// clobber keeps the mailbox read ahead of the piece reads in issue order, and
+// one wave's LDS reads execute in issue order, so pieces that the mailbox
+// reports as delivered are read after their delivery.  These are ordinary
+// loads for the compiler, which waits for each before its first use; callers
+// pin them ahead of the compute with a scheduling barrier.
+template <int K>
+__device__ __forceinline__ void read_ahead(lds_cchar* Lb, uint32_t box_off, const uint32_t (&a)[8], f32x4 (&v)[8],
+                                           i32x4& mb) {
+  mb = *reinterpret_cast<const __attribute__((address_space(3))) i32x4*>(Lb + box_off);
+  asm volatile("" ::: "memory");
+#pragma unroll
+  for (int m = 0; m < 8; ++m)
+    v[m] = *reinterpret_cast<const __attribute__((address_space(3))) f32x4*>(Lb + a[m] + (uint32_t)(K * kSlotStride));
+}
+// s_waitcnt lgkmcnt(0) as a real instruction (vmcnt and expcnt at their
+// maxima), which the compiler's own wait placement takes into account.
+__device__ __forceinline__ void lgkm_wait0() { __builtin_amdgcn_s_waitcnt(0xC07F); }
+
+// LDS stores without a branch: one lane (lane 0) writes v at addr; lanes
+// 56..63 write f at their own addr (16 bytes each).  On this LDS every store
+// instruction costs about the same whatever the number of active lanes, and
+// a store from all lanes to one address serialises.
+__device__ __forceinline__ void lds_put(uint32_t addr, int v) {
+  uint64_t sv;
+  asm volatile("s_mov_b64 %[sv], exec\n\ts_mov_b64 exec, 1\n\tds_write_b32 %[a], %[v]\n\ts_mov_b64 exec, %[sv]"
+               : [sv] "=&s"(sv)
+               : [a] "v"(addr), [v] "v"(v)
+               : "memory");
+}
+__device__ __forceinline__ void lds_put64(uint32_t addr, long long v) {
+  uint64_t sv;
+  asm volatile("s_mov_b64 %[sv], exec\n\ts_mov_b64 exec, 1\n\tds_write_b64 %[a], %[v]\n\ts_mov_b64 exec, %[sv]"
+               : [sv] "=&s"(sv)
+               : [a] "v"(addr), [v] "v"(v)
+               : "memory");
+}
+__device__ __forceinline__ void lds_put_hi8(uint32_t addr, f32x4 f) {
+  uint64_t sv;
+  asm volatile("s_mov_b64 %[sv], exec\n\ts_mov_b64 exec, %[m]\n\tds_write_b128 %[a], %[f]\n\ts_mov_b64 exec, %[sv]"
+               : [sv] "=&s"(sv)
+               : [m] "s"(0xff00000000000000ull), [a] "v"(addr), [f] "v"(f)
+               : "memory");
+}
+template <int N>
+__device__ __forceinline__ float dpp_row_shl(float old, float src) {
+  return __int_as_float(__builtin_amdgcn_update_dpp(__float_as_int(old), __float_as_int(src), 0x100 | N, 0xf, 0xf, false));
+}
+// Lanes 56..63 receive lane 63's q[4k .. 4k+3] (k = lane - 56), gathered by
+// DPP row shifts inside the last 16-lane row: lane 56+k reads lane 63 with
+// row_shl:(7-k); a lane whose source lies past the end of the row keeps its
+// value, so the shifts run from the smallest up.
+__device__ __forceinline__ f32x4 gather_last_row(const float (&q)[kChunk]) {
+  f32x4 f = {q[28], q[29], q[30], q[31]};
+#define MAS_GATHER(K)                                      \
+  f.x = dpp_row_shl<7 - K>(f.x, q[4 * K + 0]);             \
+  f.y = dpp_row_shl<7 - K>(f.y, q[4 * K + 1]);             \
+  f.z = dpp_row_shl<7 - K>(f.z, q[4 * K + 2]);             \
+  f.w = dpp_row_shl<7 - K>(f.w, q[4 * K + 3]);
+  MAS_GATHER(6) MAS_GATHER(5) MAS_GATHER(4) MAS_GATHER(3) MAS_GATHER(2) MAS_GATHER(1) MAS_GATHER(0)
+#undef MAS_GATHER
+  return f;
+}
+
+// ---------------------------------------------------------------- sweep wave
+// Sweeps the wave's rows over its chunks and returns the score candidate
+// (Q at (row, t_y-1) of this lane; only meaningful for the wave holding row
+// t_x-1).  IN: where the row above the wave comes from — 0 nowhere (the wave
+// holds row 0: -inf), 1 the previous wave of the workgroup (its slots, with
+// tags), 2 the global boundary words of the previous workgroup (polled by
+// this wave kPollAhead chunks ahead and copied into its own slots).  OUT: 0
+// no consumer, 1 the next wave of the workgroup, 2 global boundary words for
+// the next workgroup (staged in LDS, stored one chunk later).
+//
+// Step c computes chunk c from registers while the LDS reads of chunk c+1
+// (its tile, its boundary row, the loader's ready count and the boundary
+// tag) are in flight; after the compute the step checks the count and tag
+// and only falls back to waiting when they were not there yet.
+template <int IN, int OUT>
+__device__ __forceinline__ float sweep_wave(const KParams& p, SweepLds& L, const WaveCtx& x, uint32_t tag, bool& timed_out) {
+  constexpr bool IN1 = IN == 1, IN2 = IN == 2;
+  const int lane = x.lane, w = x.w;
+  float t = -0.0f;  // lane 0 keeps -0 for the whole sweep (see cols8)
+  char* const Lc = reinterpret_cast<char*>(&L);
+  const uint32_t wbase = (uint32_t)w * kWaveRegion;
+  auto bound_ptr = [&](int k) __attribute__((always_inline)) -> float* {
+    return reinterpret_cast<float*>(Lc + wbase + (uint32_t)k * kSlotStride + kBoundOff);
+  };
+  // Per-lane LDS byte offsets of the 8 pieces of slot 0: lanes 1..63 read
+  // tile row lane-1 (swizzled), lane 0 reads the boundary row.
+  uint32_t ra[8];
+  {
+    const int r = lane > 0 ? lane - 1 : 0;
+#pragma unroll
+    for (int m = 0; m < 8; ++m)
+      ra[m] = lane > 0 ? wbase + (uint32_t)(r * 128 + 16 * (m ^ swz(r))) : wbase + (uint32_t)(kBoundOff + 16 * m);
+  }
+  // Mailboxes: this wave's, the next wave's (OUT1: its prod), and where this
+  // wave's progress goes (the previous wave's mailbox, or cons0).
+  const uint32_t box_off = (uint32_t)((const char*)&L.box[w] - Lc);
+  lds_cchar* const Lb = (lds_cchar*)Lc;
+  const uint32_t next_prod = lds_off(&L.box[w < kWavesPerBlock - 1 ? w + 1 : w]) + 4u;
+  const uint32_t my_cons = w > 0 ? lds_off(&L.box[w - 1]) + 8u : lds_off(&L.cons0);
+  const int* const my_box = reinterpret_cast<const int*>(&L.box[w]);
+
+  // Decision words: dec[b][c][row], lane 0 into the chunk's scratch word.
+  const __amdgpu_buffer_rsrc_t dr =
+      make_cursor(p.dec + (size_t)x.b * p.NC * (size_t)p.TP, (uint64_t)p.NC * p.TP * 4u).rsrc();
+  const int dvo = 4 * (lane > 0 ? x.row : p.TP - 1);
+  const int dstride = p.TP * 4;
+  // Global boundary words: this wave's (OUT2) and the previous wave's (IN2),
+  // word 32c + l for column 32c + l; lanes 0..31 move one word each.
+  const size_t slot_words = (size_t)p.NC * kChunk;
+  const __amdgpu_buffer_rsrc_t sr =
+      make_cursor(p.slots + ((size_t)x.b * p.NW + x.g) * slot_words, slot_words * 8u).rsrc();
+  const uint64_t* const pslots = p.slots + ((size_t)x.b * p.NW + (x.g > 0 ? x.g - 1 : 0)) * slot_words;
+  const int pslot_bytes = (int)(slot_words * 8u);
+  auto word_off = [&](int c) __attribute__((always_inline)) -> int {
+    return lane < kChunk ? c * (kChunk * 8) + 8 * lane : -1;  // -1: out of range, dropped / 0
+  };
+
+  // IN2: the boundary words of chunk c (256 bytes: {value, tag} for its 32
+  // columns), polled kPollAhead chunks ahead by LDS-DMA into poll slot
+  // (c - c_begin + 1) % kPollAhead, then checked and copied into the chunk's
+  // slot right before the wave reads it.  The wave counts its own
+  // vector-memory operations (these polls and its decision stores; it issues
+  // no others) so that it can wait for one poll and not for later ones.
+  uint32_t n_vm = 0;               // vector-memory operations issued
+  uint32_t poll_seq[kPollAhead];   // n_vm of each slot's poll
+  const uint32_t poll_lds = lds_off(&L.poll[0][0]);
+  auto issue_poll = [&](int c, int k) __attribute__((always_inline)) {
+    dma4_dev(poll_lds + (uint32_t)k * (kWave * 4), Cursor{reinterpret_cast<const char*>(pslots), pslot_bytes}.rsrc_s(),
+             c * (kChunk * 8) + 4 * lane);
+    poll_seq[k] = n_vm++;
+  };
+  // Makes the boundary row of chunk c (polled into poll slot pk) available in
+  // slot k.
+  auto deliver = [&](int c, int k, int pk) __attribute__((always_inline)) {
+    vm_wait_n((int)(n_vm - 1u - poll_seq[pk]));
+    const uint64_t* pw = reinterpret_cast<const uint64_t*>(&L.poll[pk][0]);
+    uint64_t wd = pw[lane & (kChunk - 1)];
+    int spins = 0;
+    while (!timed_out) {
+      uint64_t stale = __builtin_amdgcn_ballot_w64(lane < kChunk && (uint32_t)(wd >> 32) != tag);
+      asm volatile("" : "+s"(stale));
+      if (stale == 0) break;
+      if (++spins > kSpinLimit) timed_out = true;
+      __builtin_amdgcn_s_sleep(1);
+      issue_poll(uni(c), pk);
+      vm_wait<0>();
+      wd = pw[lane & (kChunk - 1)];
+    }
+    if (lane < kChunk) bound_ptr(k)[lane] = __uint_as_float((uint32_t)wd);
+  };
+
+  if (IN == 0) {
+    // The row above row 0 is -inf in every slot.
+    if (lane < kChunk) {
+#pragma unroll
+      for (int k = 0; k < kRing; ++k) bound_ptr(k)[lane] = neg_inf();
+    }
+  }
+  // IN2 prologue: polls of chunks c_begin-1 .. c_begin-1+kPollAhead-1.
+  if (IN2) {
+#pragma unroll
+    for (int k = 0; k < kPollAhead; ++k) issue_poll(x.c_begin - 1 + k, k);
+  }
+
+  // Lane 0's Q at the column before the first chunk: the previous wave's
+  // last row there (its chunk c_begin-1, always computed), or -inf.  It
+  // sits in slot kRing-1 (chunk c_begin-1).
+  float q = neg_inf();
+  if (IN1) {
+    wait_at_least(my_box + 1, x.c_begin, timed_out);
+  } else if (IN2) {
+    deliver(x.c_begin - 1, kRing - 1, 0);
+    issue_poll(x.c_begin - 1 + kPollAhead, 0);
+  }
+  if (IN != 0) {
+    wave_lds_sync();
+    const float e = bound_ptr(kRing - 1)[kChunk - 1];
+    q = lane == 0 ? e : q;
+    wave_lds_sync();
+    lds_put(my_cons, x.c_begin);
+  }
+
+  // The first chunk's tile and boundary row.  Values alternate between two
+  // register sets by ring position: chunk c uses set (c - c_begin) % 2.
+  f32x4 va[8], vb[8];
+  wait_at_least(my_box + 0, x.c_begin + 1, timed_out);
+  if (IN1 && x.c_begin < x.prev_end) {
+    wait_at_least(my_box + 1, x.c_begin + 1, timed_out);
+  } else if (IN2 && x.c_begin < x.prev_end) {
+    deliver(x.c_begin, 0, 1);
+    issue_poll(x.c_begin + kPollAhead, 1);
+  }
+  int cons_seen;  // the consumer's progress as last read (OUT1)
+  {
+    // (Through the same inline-assembly reads as the loop: values the
+    // compiler loaded itself would make it wait for LDS inside the loop.)
+    i32x4 mb;
+    read_ahead<0>(Lb, box_off, ra, va, mb);
+    cons_seen = uni(mb.z);
+  }
+  lds_put(my_cons, x.c_begin + 1);
+
+  float qc[kChunk];
+  int soff = x.c_begin * dstride;
+  float score = neg_inf();
+  const int m_last = (x.ty - 1) % kChunk;
+
+  // The last row of chunk cp (in lane 63's qc) for the next wave: gathered
+  // into lanes 56..63 and stored with one LDS write.  OUT1: into the next
+  // wave's slot for chunk cp (once it has read chunk cp-4 from that slot),
+  // then its mailbox's prod; OUT2: into the staging row, read back by lanes
+  // 0..31 (returned) for the global store.  Issued at the start of the
+  // following step, ahead of that step's reads and compute, so the wave
+  // never waits for these LDS writes to complete.
+  auto hand_off = [&](int cp) __attribute__((always_inline)) -> float {
+    float ov = 0.0f;
+    if (OUT == 1 && cp >= x.next_begin - 1) {
+      if (cons_seen < cp - (kRing - 1)) cons_seen = wait_at_least(my_box + 2, cp - (kRing - 1), timed_out);
+      const int kn = (cp - x.next_begin) & (kRing - 1);
+      const uint32_t ns = wbase + kWaveRegion + (uint32_t)kn * kSlotStride + kBoundOff;
+      lds_put_hi8(ns + 16u * (uint32_t)(lane - (kWave - 8)), gather_last_row(qc));
+      lds_put(next_prod, cp + 1);
+    } else if (OUT == 2 && cp >= x.next_begin - 1) {
+      float* const stage = reinterpret_cast<float*>(&L.ostage[0][0]);
+      lds_put_hi8(lds_off(stage) + 16u * (uint32_t)(lane - (kWave - 8)), gather_last_row(qc));
+      wave_lds_sync();
+      ov = stage[lane & (kChunk - 1)];
+    }
+    return ov;
+  };
+  auto relay = [&](int cp, float ov) __attribute__((always_inline)) {
+    if (OUT == 2 && cp >= x.next_begin - 1) {
+      const uint64_t word = ((uint64_t)tag << 32) | (uint64_t)__float_as_uint(ov);
+      __builtin_amdgcn_raw_buffer_store_b64(__builtin_bit_cast(u32x2, word), sr, word_off(cp), 0, kPolicyDev);
+    }
+  };
+
+  // Chunk c at ring position J = (c - c_begin) % kRing, its values in vc,
+  // the next chunk's read into vn.
+  auto step = [&](auto pos_c, int c, f32x4 (&vc)[8], f32x4 (&vn)[8]) __attribute__((always_inline)) {
+    constexpr int J = decltype(pos_c)::value;
+    constexpr int J1 = (J + 1) & (kRing - 1);
+    const bool has_next = c + 1 < x.c_end;
+    const bool need_prod = IN1 && c + 1 < x.prev_end;
+    // IN2: the boundary row of chunk c+1 into slot J1, and the poll of chunk
+    // c+1+kPollAhead into the freed poll slot.
+    if (IN2 && has_next && c + 1 < x.prev_end) {
+      constexpr int PK = (J + 2) & (kPollAhead - 1);
+      deliver(c + 1, J1, PK);
+      issue_poll(c + 1 + kPollAhead, PK);
+    }
+    // The previous chunk's last row to the next wave.
+    const float ov = c > x.c_begin ? hand_off(c - 1) : 0.0f;
+    // Reads of chunk c+1, in flight during the compute of chunk c: the
+    // mailbox first, then the values (one LDS queue per wave: in order).
+    i32x4 mb = {1 << 30, 1 << 30, 0, 0};
+    if (has_next) read_ahead<J1>(Lb, box_off, ra, vn, mb);
+    __builtin_amdgcn_sched_barrier(0);
+
+    uint32_t bits = 0;
+    if (c < x.mask_end)
+      sweep_chunk<true>(q, t, vc, qc, bits, lane, x.row, c * kChunk);
+    else
+      sweep_chunk<false>(q, t, vc, qc, bits, lane, x.row, c * kChunk);
+    __builtin_amdgcn_sched_barrier(0);
+    __builtin_amdgcn_raw_buffer_store_b32(bits, dr, dvo, soff, kPolicyDev);
+    ++n_vm;
+    soff += dstride;
+    if (c > x.c_begin) relay(c - 1, ov);
+    if (OUT == 0 && c == x.c_end - 1) {
+#pragma unroll
+      for (int m = 0; m < kChunk; ++m) score = (m == m_last) ? qc[m] : score;
+    }
+
+    if (has_next) {
+      // The reads of chunk c+1 are usable if the tile and the boundary row
+      // were there when they were issued; otherwise wait and read again.
+      if (OUT == 1) cons_seen = max(cons_seen, uni(mb.z));
+      if (uni(mb.x) < c + 2 || (need_prod && uni(mb.y) < c + 2)) {
+        wait_at_least(my_box + 0, c + 2, timed_out);
+        if (need_prod) wait_at_least(my_box + 1, c + 2, timed_out);
+        read_ahead<J1>(Lb, box_off, ra, vn, mb);
+        lgkm_wait0();
+      }
+      lds_put(my_cons, c + 2);
+    }
+  };
+  for (int c = x.c_begin; c < x.c_end; c += kRing) {
+    step(std::integral_constant<int, 0>(), c, va, vb);
+    if (c + 1 < x.c_end) step(std::integral_constant<int, 1>(), c + 1, vb, va);
+    if (c + 2 < x.c_end) step(std::integral_constant<int, 2>(), c + 2, va, vb);
+    if (c + 3 < x.c_end) step(std::integral_constant<int, 3>(), c + 3, vb, va);
+  }
+  // The last chunk's row.
+  {
+    const float ov = hand_off(x.c_end - 1);
+    relay(x.c_end - 1, ov);
+  }
+  vm_wait<0>();
+  return score;
+}
+
+// ---------------------------------------------------------------- loader wave
+// Value tiles of sweep wave w, chunks [c_begin, c_end), each into the slot
+// its sweep wave has handed back.  ALIGNED (value 16-byte aligned, S % 4 ==
+// 0): lane L of load k (k = 0..7) fetches tile row 8k + L/8, piece
+// (L % 8) ^ swz(row), so each load covers eight 128-byte row segments and
+// lands as eight contiguous swizzled LDS rows; up to kRing tiles in flight.
+// Otherwise 4-byte loads of the same layout, one tile in flight.
+template <bool ALIGNED>
+__device__ __forceinline__ void load_tiles(const KParams& p, SweepLds& L, const WaveCtx& x, bool& timed_out) {
+  const int lane = x.lane, w = x.w;
+  const float* slab = p.value + (size_t)x.b * (size_t)p.T * (size_t)p.S;
+  const uint64_t slab_bytes = (uint64_t)p.T * (uint64_t)p.S * 4u;
+  Cursor vr = make_cursor(slab, slab_bytes);
+  vr.advance((int)((uint64_t)x.g * kRowsPerWave * (uint64_t)p.S * 4u) + x.c_begin * (kChunk * 4));
+  const uint32_t ring = lds_off(&L.u.ring[w][0]);
+  constexpr int kOps = ALIGNED ? 8 : 32;  // loads per tile
+  constexpr int kInflight = ALIGNED ? kRing : 1;
+  // Per-lane byte offsets, relative to the chunk's first tile row; rows past
+  // 2^31 bytes fall outside every resource.
+  int voff[kOps];
+#pragma unroll
+  for (int k = 0; k < kOps; ++k) {
+    const int r = ALIGNED ? 8 * k + (lane >> 3) : 2 * k + (lane >> 5);
+    const int pos = ALIGNED ? (lane & 7) : ((lane & 31) >> 2);
+    const uint32_t elem = ALIGNED ? 0u : 4u * (uint32_t)(lane & 3);
+    const uint64_t o = (uint64_t)r * (uint64_t)p.S * 4u + 16u * (uint32_t)(pos ^ swz(r)) + elem;
+    voff[k] = o < 0x80000000ull ? (int)o : (int)0x80000000u;
+  }
+  int issued = x.c_begin, readied = x.c_begin;
+  // The sweep wave's progress (its slots below it are free again).
+  const int* const progress = w > 0 ? reinterpret_cast<const int*>(&L.box[w - 1]) + 2 : &L.cons0;
+  const uint32_t ready_addr = lds_off(&L.box[w]);
+  int cons = x.c_begin - 1;
+  while (readied < x.c_end && !timed_out) {
+    // Issue while slots are free (the slot of chunk c held chunk c-4).
+    while (issued < x.c_end && issued - readied < kInflight) {
+      if (issued > cons + kRing - 1) {
+        cons = uni(lds_load(progress));
+        if (issued > cons + kRing - 1) break;
+      }
+      const __amdgpu_buffer_rsrc_t r = vr.rsrc_s();
+      const uint32_t dst = ring + (uint32_t)((issued - x.c_begin) & (kRing - 1)) * kSlotStride;
+#pragma unroll
+      for (int k = 0; k < kOps; ++k) {
+        if (ALIGNED)
+          dma16(dst + 1024u * k, r, voff[k]);
+        else
+          dma4(dst + 256u * k, r, voff[k]);
+      }
+      vr.advance(kChunk * 4);
+      ++issued;
+    }
+    if (issued == readied) {
+      // Nothing in flight and no free slot: wait for the sweep wave.
+      cons = wait_at_least(progress, issued - (kRing - 1), timed_out);
+      continue;
+    }
+    // The oldest tile in flight has landed once at most the younger ones
+    // are outstanding.
+    vm_wait_n(kOps * (issued - readied - 1));
+    ++readied;
+    lds_put(ready_addr, readied);
+  }
+  vm_wait<0>();
+}
+
+// Zeros over the path rows of wave g of item b (device-scope stores: the
+// walker of the item writes the ones over some of them later, from another
+// workgroup).
+__device__ __forceinline__ void clear_rows(const KParams& p, int b, int g, int lane) {
+  const int r0 = min(g * kRowsPerWave, p.T), r1 = min(g * kRowsPerWave + kRowsPerWave, p.T);
+  if (r1 <= r0) return;
+  const uint64_t base = (uint64_t)b * (uint64_t)p.T * (uint64_t)p.S;
+  const uint64_t p0 = base + (uint64_t)r0 * (uint64_t)p.S, p1 = base + (uint64_t)r1 * (uint64_t)p.S;
+  const uint64_t pa = (uint64_t)(uintptr_t)p.path;
+  const uint64_t a0 = ((pa + p0 + 15) & ~15ull) - pa, a1 = ((pa + p1) & ~15ull) - pa;
+  const bool any = a1 > a0 && a1 - a0 >= 16;
+  // Unaligned head and tail bytes (all bytes when no aligned piece).
+  const uint64_t h1 = any ? a0 : p1;
+  for (uint64_t o = p0 + lane; o < h1; o += kWave) st_dev(p.path + o, (uint8_t)0);
+  if (any) {
+    for (uint64_t o = a1 + lane; o < p1; o += kWave) st_dev(p.path + o, (uint8_t)0);
+    // 16-byte pieces [a0, a1) through a resource over them (< 2^31 bytes).
+    const __amdgpu_buffer_rsrc_t r = make_cursor(p.path + a0, a1 - a0).rsrc();
+    const u32x4 zero = {0u, 0u, 0u, 0u};
+    const int n = (int)(a1 - a0);
+    for (int o = 16 * lane; o < n; o += 16 * kWave) __builtin_amdgcn_raw_buffer_store_b128(zero, r, o, 0, kPolicyDev);
   }
 }
 
@@ -717,7 +838,7 @@ __device__ __forceinline__ void wait_flags(const uint32_t* flag, int n, uint32_t
   "v_readlane_b32 %[" NXT "], %[wh], %[sl]\n\t" \
   "s_add_u32 %[sl], %[sl], 1\n\t"               \
   "s_lshr_b32 %[t], %[" CUR "], %[q]\n\t"       \
-  "s_cbranch_scc0 .Lmas_walk_end%=\n\t"    \
+  "s_cbranch_scc0 .Lmas_walk_end%=\n\t"         \
   "s_ff1_i32_b32 %[t], %[t]\n\t"                \
   "s_addc_u32 %[q], %[q], %[t]\n\t"             \
   "s_bitset1_b32 %[pm], %[q]\n\t"
@@ -757,231 +878,276 @@ __device__ __forceinline__ uint32_t walk_chunk(uint32_t w, uint32_t wh, int sl, 
 #undef MAS_WALK_STEP2
 #undef MAS_WALK_STEP
 
+// Loader side of the walk: the decision words of chunks C-1 down to 0, a
+// window of kWinRows rows per chunk, kWinAhead windows in flight, into slot
+// ch % kNWin once the walker has moved past the chunk that slot held.  When
+// T exceeds kWinRows a window ends 63 rows above the walker's row at issue
+// time: the walk cannot descend past the window before it reaches the chunk.
+// Stops early once the walker has reached row 0.
+__device__ __forceinline__ void load_windows(const KParams& p, SweepLds& L, int b, int ty, int lane, bool& timed_out) {
+  const int C = (ty + kChunk - 1) / kChunk;
+  const uint32_t* db = p.dec + (size_t)b * p.NC * (size_t)p.TP;
+  const uint64_t chunk_bytes = (uint64_t)p.TP * 4u;
+  const uint32_t win0 = lds_off(&L.u.walk.win[0][0]);
+  int issued = C - 1, readied = C;  // windows of chunks > issued are issued, >= readied ready
+  long long wpos = lds_load(&L.wpos);
+  int spins = 0;
+  while (readied > 0 && wpos >= 0 && !timed_out) {
+    while (issued >= 0 && readied - 1 - issued < kWinAhead) {
+      if ((int)(wpos >> 32) > issued + kNWin) {
+        wpos = lds_load(&L.wpos);
+        if (wpos < 0 || (int)(wpos >> 32) > issued + kNWin) break;
+      }
+      const int e = uni((int)(uint32_t)wpos);
+      const int lo = p.T <= kWinRows ? 0 : (max(e - (kWinRows - 64), 0) & ~3);
+      const int slot = issued % kNWin;
+      if (p.T > kWinRows) lds_put(lds_off(&L.wlo[slot]), lo);
+      const Cursor cr = make_cursor(db + (size_t)issued * p.TP + lo, chunk_bytes - (uint64_t)lo * 4u);
+      const __amdgpu_buffer_rsrc_t r = cr.rsrc_s();
+#pragma unroll
+      for (int k = 0; k < kWinRows / 256; ++k)
+        dma16_dev(win0 + (uint32_t)slot * (kWinRows * 4) + 1024u * k, r, 16 * lane + 1024 * k);
+      --issued;
+    }
+    if (readied - 1 == issued) {
+      // Nothing in flight: wait for the walker to free a slot.
+      if (++spins > kSpinLimit) timed_out = true;
+      __builtin_amdgcn_s_sleep(1);
+      wpos = lds_load(&L.wpos);
+      continue;
+    }
+    vm_wait_n((kWinRows / 256) * (readied - 2 - issued));
+    --readied;
+    lds_put(lds_off(&L.wready), readied);
+  }
+  vm_wait<0>();
+}
+
 // The walk of one item from (t_x-1, t_y-1) back to (0, 0) (Algorithm 1's
 // argmax loop, read off the decision words): in chunk c the path in row i
 // stays there until the nearest column to the left whose decision bit is
 // set, then continues one row up at the column before.  Builds row_start in
 // L.u.walk.rs: the first column of every row, with rs[0] = 0 and
-// rs[t_x .. T] = t_y.  Runs on the wave that holds row t_x-1, once every
-// wave of the item has published its words.
-__device__ __forceinline__ void walk(const KParams& p, SweepLds& L, int b, int tx, int ty, uint32_t tag, int lane,
-                                     bool& timed_out) {
-  const int g_last = (tx - 1) / kRowsPerWave;
-  wait_flags(p.done + (size_t)b * p.NW, g_last, tag, lane, timed_out);
-  // Every sweep of this workgroup has finished (lower waves: flags above;
-  // higher waves hold no rows of the alignment), so the tile area is free.
+// rs[t_x .. T] = t_y.  Runs on the sweep wave that holds row t_x-1; its
+// loader stages the windows.
+__device__ __forceinline__ void walk(const KParams& p, SweepLds& L, int tx, int ty, int lane, bool& timed_out) {
   int* rsl = L.u.walk.rs;
-  const uint32_t* db = p.dec + (size_t)b * p.NC * (size_t)p.TP;
-  const uint64_t chunk_bytes = (uint64_t)p.TP * 4u;
-  const int wvo = 16 * lane;
-  int wlo = 0;  // lane s: first row of the window in ring slot s
-  // Window of chunk ch: kWalkWin rows from a 16-byte aligned row lo in
-  // [e - kWalkWin + 1, e - kWalkWin + 4] (or row 0) into slot ch % kWalkSlots;
-  // an empty resource (reads 0) for chunks before the first.
-  auto issue_win = [&](int ch, int e) __attribute__((always_inline)) {
-    const int slot = ch & (kWalkSlots - 1);
-    const int lo = max(e - kWalkWin + 4, 0) & ~3;
-    wlo = lane == slot ? lo : wlo;
-    const uint32_t dst = lds_off(&L.u.walk.win[slot][0]);
-    const __amdgpu_buffer_rsrc_t rr = ch >= 0 ? sub_rsrc(db + (size_t)ch * p.TP, chunk_bytes, (uint64_t)lo * 4u)
-                                              : sub_rsrc(db, chunk_bytes, chunk_bytes);
-#pragma unroll
-    for (int k = 0; k < kWalkLoads; ++k) dma_piece(dst + 1024 * k, rr, wvo + 1024 * k);
-  };
+  const uint32_t below = (1u << (lane & (kChunk - 1))) - 1u;  // positions below this lane's
+  int idx = tx - 1;                   // row of the path at the chunk's last column
+  int cw = (ty - 1) / kChunk;         // chunk being walked
+  int q0 = 31 - (ty - 1) % kChunk;    // position of the path's column in chunk cw
   // Word of row e - lane of chunk ch (its window must be in LDS).
+  const bool banded = p.T > kWinRows;  // windows start at row 0 otherwise
   auto read_row = [&](int ch, int e) __attribute__((always_inline)) -> uint32_t {
-    const int slot = ch & (kWalkSlots - 1);
-    const int r = e - lane - __builtin_amdgcn_readlane(wlo, slot);
+    const int slot = ch % kNWin;
+    const int r = e - lane - (banded ? lds_load(&L.wlo[slot]) : 0);
     return L.u.walk.win[slot][r > 0 ? r : 0];
   };
-  const uint32_t below = (1u << (lane & (kChunk - 1))) - 1u;  // positions below this lane's
-  int idx = tx - 1;                  // row of the path at the chunk's last column
-  int cw = (ty - 1) / kChunk;        // chunk being walked
-  int q0 = 31 - (ty - 1) % kChunk;   // position of the path's column in chunk cw
-  for (int k = 0; k < kWalkAhead; ++k) issue_win(cw - k, idx);
-  vm_wait<kWalkLoads * (kWalkAhead - 1)>();  // window of chunk cw
-  uint32_t W = read_row(cw, idx);    // rows e0 - lane of chunk cw
-  int off = 0;                       // lane of row idx in W: idx = e0 - off
-  bool walking = idx > 0;
-  while (walking) {
-    vm_wait<kWalkLoads * (kWalkAhead - 2)>();  // windows of chunks cw and cw-1
-    issue_win(cw - kWalkAhead, idx);
-    const uint32_t N = read_row(cw - 1, idx);  // the next chunk's rows below idx, read ahead
-    const uint32_t pm = walk_chunk(W, W >> 1, off, q0);
-    // Set bit p of pm belongs to the row (popcount of pm below p) under idx.
-    if (lane < kChunk && ((pm >> lane) & 1u)) rsl[idx - (int)__builtin_popcount(pm & below)] = cw * kChunk + 31 - lane;
-    const int kk = __builtin_popcount(pm);
-    idx -= kk;
-    q0 = 0;
-    cw -= 1;
-    W = N;
-    off = kk;
-    walking = idx > 0 && cw >= 0;
+  auto window_ready = [&](int ch) __attribute__((always_inline)) {
+    int spins = 0;
+    while (uni(lds_load(&L.wready)) > ch && !timed_out) {
+      if (++spins > kSpinLimit) timed_out = true;
+      __builtin_amdgcn_s_sleep(1);
+    }
+  };
+  if (idx > 0) {
+    lds_put64(lds_off(&L.wpos), walk_pos(cw, idx));
+    window_ready(cw);
+    wave_lds_sync();
+    uint32_t W = read_row(cw, idx);  // rows idx - lane of chunk cw
+    int off = 0;                     // lane of the current row in W
+    bool walking = true;
+    while (walking) {
+      // The next chunk's rows below idx, read ahead; checked after the steps.
+      uint32_t N = 0;
+      int rdy = 0;
+      if (cw > 0) {
+        rdy = lds_load(&L.wready);
+        wave_lds_sync();
+        N = read_row(cw - 1, idx);
+      }
+      const uint32_t pm = walk_chunk(W, W >> 1, off, q0);
+      // Set bit q of pm belongs to the row (popcount of pm below q) under idx.
+      const int ri = idx - (int)__builtin_popcount(pm & below);
+      if (lane < kChunk && ((pm >> lane) & 1u) && ri >= 0) rsl[ri] = cw * kChunk + 31 - lane;
+      const int kk = __builtin_popcount(pm);
+      if (cw > 0 && uni(rdy) > cw - 1) {
+        window_ready(cw - 1);
+        wave_lds_sync();
+        N = read_row(cw - 1, idx);
+      }
+      idx -= kk;
+      q0 = 0;
+      cw -= 1;
+      W = N;
+      off = kk;
+      walking = idx > 0 && cw >= 0;
+      // Windows of chunks above cw are no longer needed.
+      lds_put64(lds_off(&L.wpos), walk_pos(max(cw, 0), max(idx, 0)));
+    }
   }
-  vm_wait<0>();  // no window load may land in LDS after this wave ends
   wave_lds_sync();
+  lds_put64(lds_off(&L.wpos), -1ll);
   if (lane == 0) rsl[0] = 0;
   for (int i = tx + lane; i <= p.T; i += kWave) rsl[i] = ty;
   wave_lds_sync();
 }
 
-__device__ __forceinline__ void sweep_block(const KParams& p, SweepLds& L, int sid, uint32_t tag, bool& timed_out) {
-  const int lane = threadIdx.x & (kWave - 1);
-  // The wave index is uniform across a wave; saying so keeps everything
-  // derived from it (chunk indices, modes, loop bounds) in scalar registers.
-  const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
-  const int b = sid % p.B;
-  const int r = sid / p.B;
-  const int g = r * kWavesPerBlock + wv;  // wave index inside the item
-  const int tx = p.t_x[b];
-  const int ty = p.t_y[b];
-  const int st = item_status(tx, ty, p.T, p.S);
-  const int c_begin = (g * kRowsPerWave) / kChunk;
-
-  // Workgroup set-up: no boundary row is written yet (the LDS holds
-  // whatever earlier workgroups left); each wave's first chunk to consume
-  // (its carried row comes from chunk c_begin-1).
-  if (threadIdx.x < kWavesPerBlock * kSlots)
-    lds_store(reinterpret_cast<int*>(&L.u.tile[threadIdx.x / kSlots][kBoundOff + (threadIdx.x % kSlots) * kSlotBytes + kTagOff]), 0);
-  if (lane == 0) lds_store(&L.cons[wv], c_begin - 1);
-  __syncthreads();
-
-  int32_t* rs_out = p.row_start + (size_t)b * ((size_t)p.T + 1);
-  const bool has_rows = g * kRowsPerWave < p.T;
-  ZeroPlan zp{};
-  if (p.path && has_rows) zp = zero_plan(p, b, g, lane);
-  const bool clear = p.path && has_rows && zp.any;
-  if (st != kItemOk) {
-    if (clear) zero_rest(zp, zp.a0, lane);
-    if (g == 0) {
-      for (int i = lane; i <= p.T; i += kWave) rs_out[i] = 0;
-      if (lane == 0) {
-        if (p.score) p.score[b] = neg_inf();
-        if (p.status) p.status[b] = st;
-      }
-    }
-    return;
-  }
-  const int g_last = (tx - 1) / kRowsPerWave;
-  if (g > g_last) {
-    // No rows of the alignment here: clear the path rows once the item's
-    // sweep is over (the HBM is less busy then).
-    if (clear) {
-      if (lane == 0) {
-        int spins = 0;
-        while (ld_dev(p.done + (size_t)b * p.NW + g_last) != tag && ++spins <= kSpinLimit) __builtin_amdgcn_s_sleep(8);
-      }
-      zero_rest(zp, zp.a0, lane);
-    }
-    return;
-  }
-  if (g == 0 && lane == 0 && p.status) p.status[b] = kItemOk;
-  // The walker's wave clears its rows first: it waits for the waves above
-  // it anyway (for g_last > 0), and the walk then ends with only the ones
-  // left to write.  The other waves clear theirs after their sweep.
-  if (clear && g == g_last) zero_rest(zp, zp.a0, lane);
-
-  WaveCtx x;
-  x.lane = lane;
-  x.wv = wv;
-  x.b = b;
-  x.g = g;
-  x.g_last = g_last;
-  x.tx = tx;
-  x.ty = ty;
-  x.row = g * kRowsPerWave + lane - 1;  // lane 0: the row above the wave
-  x.c_begin = c_begin;
-  x.c_end = chunk_end(g, tx, ty);
-  x.prev_end = g > 0 ? chunk_end(g - 1, tx, ty) : 0;
-  x.mask_end = (g * kRowsPerWave + kRowsPerWave - 2) / kChunk + 1;  // last masked column: 63g + 61
-  x.next_begin = ((g + 1) * kRowsPerWave) / kChunk;
-  float score;
-  if (g == g_last) {
-    score = g == 0 ? sweep_rows<0, 0>(p, L, x, tag, timed_out)
-                   : (wv > 0 ? sweep_rows<1, 0>(p, L, x, tag, timed_out) : sweep_rows<2, 0>(p, L, x, tag, timed_out));
-  } else if (wv < kWavesPerBlock - 1) {
-    score = g == 0 ? sweep_rows<0, 1>(p, L, x, tag, timed_out)
-                   : (wv > 0 ? sweep_rows<1, 1>(p, L, x, tag, timed_out) : sweep_rows<2, 1>(p, L, x, tag, timed_out));
-  } else {
-    score = sweep_rows<1, 2>(p, L, x, tag, timed_out);
-  }
-
-  // Publish this wave's decision words to the item's walker.
-  if (lane == 0) st_dev(p.done + (size_t)b * p.NW + g, tag);
-  int* rsl = L.u.walk.rs;
-  if (g == g_last) {
-    if (lane == (tx - 1) - g_last * kRowsPerWave + 1 && p.score) p.score[b] = score;
-    walk(p, L, b, tx, ty, tag, lane, timed_out);
-    for (int i = lane; i <= p.T; i += kWave) st_dev(reinterpret_cast<uint32_t*>(rs_out + i), (uint32_t)rsl[i]);
-    if (!p.path) return;
-    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-    if (lane == 0) st_dev(p.wdone + b, tag);
-  } else {
-    // Clear this wave's path rows while the walk runs, then wait for it.
-    if (!p.path) return;
-    if (clear) zero_rest(zp, zp.a0, lane);
-    int spins = 0;
-    while (ld_dev(p.wdone + b) != tag) {
-      if (++spins > kSpinLimit) {
-        timed_out = true;
-        break;
-      }
-      __builtin_amdgcn_s_sleep(2);
-    }
-  }
-  // Ones of this wave's rows: lane l's row 63g + l - 1 has columns [lo, hi),
-  // from row_start entries 63g + l - 1 (lane l-1's) and 63g + l (its own).
-  // Each lane writes the first kOnesPerLane bytes of its row's ones (one
-  // 16-byte piece or one byte at a time); rows with more (a long stay in one
-  // row) are finished by the whole wave, one such row at a time, 64 pieces
-  // or bytes per store.
-  const int ri = min(g * kRowsPerWave + lane, p.T);
-  const int hi = g == g_last ? rsl[ri] : (int)ld_dev(reinterpret_cast<const uint32_t*>(rs_out + ri));
-  const int lo = __builtin_amdgcn_update_dpp(0, hi, 0x138, 0xF, 0xF, false);  // lane l-1's entry
-  const int row = g * kRowsPerWave + lane - 1;
-  const bool mine = lane > 0 && row < tx;
+// The ones of the item's alignment (rows < t_x) over the zeroed path, from
+// the finished row_start table: row i holds ones at [rs[i], rs[i+1]).  Lane l
+// writes rows l, l+64, ...: the first kOnesPerLane bytes of each; the rest of
+// a longer row (a long stay) is written by the whole wave afterwards.
+__device__ __forceinline__ void write_ones(const KParams& p, const int* rsl, int b, int tx, int lane) {
   uint8_t* const item_path = p.path + (size_t)b * (size_t)p.T * (size_t)p.S;
-  const int start = p.path16 ? (lo & ~15) : lo;
-  const int split = mine ? min(hi, start + kOnesPerLane) : start;  // own part: [start, split)
-  if (mine) {
-    uint8_t* prow = item_path + (size_t)row * (size_t)p.S;
-    if (p.path16) {
-      for (int j0 = start; j0 < split; j0 += 16) *reinterpret_cast<uint4*>(prow + j0) = path_piece(lo, hi, j0);
-    } else {
-      for (int j = start; j < split; ++j) prow[j] = 1;
+  const __amdgpu_buffer_rsrc_t r = make_cursor(item_path, (uint64_t)p.T * p.S).rsrc();
+  for (int i0 = 0; i0 < tx; i0 += kWave) {
+    const int i = i0 + lane;
+    const bool mine = i < tx;
+    // (Clamped to the row: the table is built by the walk, never trusted blindly.)
+    const int lo = mine ? min(max(rsl[i], 0), p.S) : 0, hi = mine ? min(max(rsl[i + 1], 0), p.S) : 0;
+    const int start = p.path16 ? (lo & ~15) : lo;
+    const int split = mine ? min(hi, start + kOnesPerLane) : start;
+    const int rowoff = i * p.S;
+    if (mine) {
+      if (p.path16) {
+        for (int j0 = start; j0 < split; j0 += 16)
+          __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, path_piece(lo, hi, j0)), r, rowoff + j0, 0, kPolicyDev);
+      } else {
+        for (int j = start; j < split; ++j) st_dev(item_path + rowoff + j, (uint8_t)1);
+      }
     }
-  }
-  uint64_t rest = __builtin_amdgcn_ballot_w64(mine && split < hi);
-  while (rest) {
-    const int l = __builtin_ctzll(rest);
-    rest &= rest - 1;
-    const int a = __builtin_amdgcn_readlane(split, l), e = __builtin_amdgcn_readlane(hi, l);
-    uint8_t* prow = item_path + (size_t)(g * kRowsPerWave + l - 1) * (size_t)p.S;
-    if (p.path16) {
-      // a is a multiple of 16 and at least lo: every piece from a on holds
-      // ones up to e.
-      for (int j0 = a + 16 * lane; j0 < e; j0 += 16 * kWave) *reinterpret_cast<uint4*>(prow + j0) = path_piece(a, e, j0);
-    } else {
-      for (int j = a + lane; j < e; j += kWave) prow[j] = 1;
+    uint64_t rest = __builtin_amdgcn_ballot_w64(mine && split < hi);
+    while (rest) {
+      const int l = __builtin_ctzll(rest);
+      rest &= rest - 1;
+      const int a = __builtin_amdgcn_readlane(split, l), e = __builtin_amdgcn_readlane(hi, l);
+      const int ro = (i0 + l) * p.S;
+      if (p.path16) {
+        // a is a multiple of 16 and at least lo: every piece from a on holds
+        // ones up to e.
+        for (int j0 = a + 16 * lane; j0 < e; j0 += 16 * kWave)
+          __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, path_piece(a, e, j0)), r, ro + j0, 0, kPolicyDev);
+      } else {
+        for (int j = a + lane; j < e; j += kWave) st_dev(item_path + ro + j, (uint8_t)1);
+      }
     }
   }
 }
 
-// One workgroup per CU.
-__global__ void __launch_bounds__(kThreadsPerBlock, 1) mas_kernel(KParams p) {
+// ---------------------------------------------------------------- roles
+__device__ __forceinline__ void sweep_role(const KParams& p, SweepLds& L, const WaveCtx& x, uint32_t tag, bool& timed_out) {
+  const int lane = x.lane, b = x.b, g = x.g, w = x.w, g_last = x.g_last;
+  if (g > g_last) return;  // no rows of the alignment here
+  if (g == 0 && lane == 0 && p.status) p.status[b] = kItemOk;
+  float score;
+  if (g == g_last) {
+    score = g == 0 ? sweep_wave<0, 0>(p, L, x, tag, timed_out)
+                   : (w > 0 ? sweep_wave<1, 0>(p, L, x, tag, timed_out) : sweep_wave<2, 0>(p, L, x, tag, timed_out));
+  } else if (w < kWavesPerBlock - 1) {
+    score = g == 0 ? sweep_wave<0, 1>(p, L, x, tag, timed_out)
+                   : (w > 0 ? sweep_wave<1, 1>(p, L, x, tag, timed_out) : sweep_wave<2, 1>(p, L, x, tag, timed_out));
+  } else {
+    score = sweep_wave<1, 2>(p, L, x, tag, timed_out);
+  }
+  // Publish this wave's decision words (its stores are complete).
+  if (lane == 0) st_dev(p.done + (size_t)b * p.NW + g, tag);
+  if (g != g_last) return;
+
+  // The walker.
+  if (lane == (x.tx - 1) - g_last * kRowsPerWave + 1 && p.score) p.score[b] = score;
+  walk(p, L, x.tx, x.ty, lane, timed_out);
+  int32_t* rs_out = p.row_start + (size_t)b * ((size_t)p.T + 1);
+  for (int i = lane; i <= p.T; i += kWave) st_dev(reinterpret_cast<uint32_t*>(rs_out + i), (uint32_t)L.u.walk.rs[i]);
+  if (!p.path) return;
+  wait_flags(p.cleared + (size_t)b * p.NW, g_last + 1, tag, lane, timed_out);
+  write_ones(p, L.u.walk.rs, b, x.tx, lane);
+}
+
+template <bool ALIGNED>
+__device__ __forceinline__ void loader_role(const KParams& p, SweepLds& L, const WaveCtx& x, uint32_t tag, bool& timed_out) {
+  const int lane = x.lane, b = x.b, g = x.g, g_last = x.g_last;
+  if (g <= g_last) load_tiles<ALIGNED>(p, L, x, timed_out);
+  if (p.path && g * kRowsPerWave < p.T) {
+    // Rows past the alignment are cleared once the item's sweep is over,
+    // when the HBM is less busy.
+    if (g > g_last) wait_flags(p.done + (size_t)b * p.NW + g_last, 1, tag, lane, timed_out);
+    clear_rows(p, b, g, lane);
+    vm_wait<0>();
+    if (lane == 0) st_dev(p.cleared + (size_t)b * p.NW + g, tag);
+  }
+  if (g != g_last) return;
+  // The walker's loader: decision words of every wave of the item.
+  wait_flags(p.done + (size_t)b * p.NW, g_last + 1, tag, lane, timed_out);
+  load_windows(p, L, b, x.ty, lane, timed_out);
+}
+
+// Items with invalid lengths: an all-zero slab, zero row_start, score -inf.
+__device__ __forceinline__ void invalid_item(const KParams& p, int b, int g, bool is_loader, int lane, int st) {
+  if (is_loader) {
+    if (p.path) clear_rows(p, b, g, lane);
+    return;
+  }
+  if (g == 0) {
+    int32_t* rs_out = p.row_start + (size_t)b * ((size_t)p.T + 1);
+    for (int i = lane; i <= p.T; i += kWave) rs_out[i] = 0;
+    if (lane == 0) {
+      if (p.score) p.score[b] = neg_inf();
+      if (p.status) p.status[b] = st;
+    }
+  }
+}
+
+// Eight waves per workgroup, one workgroup per CU.
+template <bool ALIGNED>
+__global__ void __launch_bounds__(kThreads, 1) mas_kernel(KParams p) {
   __shared__ SweepLds L;
   const uint32_t gen = __hip_atomic_load(&p.hdr->gen, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   const uint32_t tag = call_tag(gen);
   bool timed_out = false;
-  const int item = (int)blockIdx.x % p.B;
-  sweep_block(p, L, blockIdx.x, tag, timed_out);
+  const int sid = blockIdx.x;
+  const int b = sid % p.B;
+  const int r = sid / p.B;
+  const int lane = threadIdx.x & (kWave - 1);
+  const int wv = uni(threadIdx.x / kWave);
+  const int w = wv & (kWavesPerBlock - 1);
+  const bool is_loader = wv >= kWavesPerBlock;
+  const int g = r * kWavesPerBlock + w;
+  const int tx = p.t_x[b];
+  const int ty = p.t_y[b];
+  const int st = item_status(tx, ty, p.T, p.S);
+
+  // Workgroup set-up: the LDS holds whatever earlier workgroups left.
+  if (threadIdx.x < kWavesPerBlock) {
+    // Nothing loaded or delivered yet; every wave's progress is just below
+    // its first chunk (it first reads the boundary row of chunk c_begin-1).
+    const int gg = r * kWavesPerBlock + (int)threadIdx.x;
+    L.box[threadIdx.x] = i32x4{chunk_begin(gg), chunk_begin(gg) - 1, chunk_begin(gg + 1) - 1, 0};
+  }
+  if (threadIdx.x == 0) {
+    L.cons0 = chunk_begin(r * kWavesPerBlock) - 1;
+    lds_store(&L.wready, 1 << 30);
+    // Walker not started: at chunk C (every window slot free), row t_x-1.
+    lds_store(&L.wpos, walk_pos((ty + kChunk - 1) / kChunk, max(tx - 1, 0)));
+  }
+  __syncthreads();
+
+  if (st != kItemOk) {
+    invalid_item(p, b, g, is_loader, lane, st);
+  } else {
+    const WaveCtx x = make_ctx(b, g, w, lane, tx, ty);
+    if (is_loader)
+      loader_role<ALIGNED>(p, L, x, tag, timed_out);
+    else
+      sweep_role(p, L, x, tag, timed_out);
+  }
   if (timed_out) {
-    if (p.status) p.status[item] = kItemSyncTimeout;
+    if (p.status) p.status[b] = kItemSyncTimeout;
     __hip_atomic_store(&p.hdr->error, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   }
   // The last wave of the call to finish advances the generation.
-  if ((threadIdx.x & (kWave - 1)) == 0) {
-    const uint32_t total = gridDim.x * kWavesPerBlock;
+  vm_wait<0>();
+  if (lane == 0) {
+    const uint32_t total = gridDim.x * (kThreads / kWave);
     const uint32_t prev = __hip_atomic_fetch_add(&p.hdr->exit_count, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     if (prev == total - 1) {
       __hip_atomic_store(&p.hdr->exit_count, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -1029,8 +1195,12 @@ __global__ void __launch_bounds__(256) mas_zero_kernel(uint4* __restrict__ p, si
 
 // ---------------------------------------------------------------- launchers
 hipError_t launch_mas(const KParams& p, hipStream_t stream) {
-  const dim3 grid((unsigned)(p.B * p.NB)), block(kThreadsPerBlock);
-  hipLaunchKernelGGL(mas_kernel, grid, block, 0, stream, p);
+  const dim3 grid((unsigned)(p.B * p.NB)), block(kThreads);
+  const bool aligned = (p.S % 4 == 0) && ((uintptr_t)p.value % 16 == 0);
+  if (aligned)
+    hipLaunchKernelGGL(mas_kernel<true>, grid, block, 0, stream, p);
+  else
+    hipLaunchKernelGGL(mas_kernel<false>, grid, block, 0, stream, p);
   return hipGetLastError();
 }
 

@@ -49,7 +49,7 @@ struct Layout {
   int32_t NB;      // workgroups per item = ceil(NW / 4)
   int32_t NC;      // decision chunks per item = ceil(S / 32)
   int32_t TP;      // decision words per chunk of an item (rows + scratch, multiple of 64)
-  size_t off_done;   // uint32 [B][NW] sweep-finished flags, then [B] walk-finished flags (tag values)
+  size_t off_done;   // uint32 [B][NW] sweep-finished flags, then [B][NW] path-rows-cleared flags (tag values)
   size_t off_slots;  // uint64 [B][NW][NC*32] boundary hand-off words
   size_t off_dec;    // uint32 [B][NC][TP] decision words
   size_t off_rs;     // int32  [B][T+1] row_start table (mas_forward_ex)
@@ -73,7 +73,7 @@ __host__ inline bool make_layout(int32_t B, int32_t T, int32_t S, Layout* L) {
   if ((uint64_t)T * (uint64_t)S * 4u >= (1ull << 31)) return false;
   size_t off = sizeof(WsHeader);
   L->off_done = off;
-  off = round_up(off + ((size_t)B * L->NW + (size_t)B) * sizeof(uint32_t), kAlign);
+  off = round_up(off + 2 * (size_t)B * L->NW * sizeof(uint32_t), kAlign);
   L->off_slots = off;
   off = round_up(off + (size_t)B * L->NW * (size_t)L->NC * kChunk * sizeof(uint64_t), kAlign);
   L->off_dec = off;

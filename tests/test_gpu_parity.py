@@ -137,6 +137,18 @@ def test_many_waves_per_item(mas):
     assert_parity(mas, value, tx, ty, "many-waves")
 
 
+def test_full_length_batch(mas):
+    """Every item spans the whole padded extent (t_x = T, t_y = S) at the
+    largest workload shape: every workgroup of the grid carries a sweep, so
+    each one depends on a chain of others across the whole launch."""
+    st = synth.Stream(77)
+    B, T, S = 64, 1024, 4096
+    value = st.normal_f32(B * T * S).reshape(B, T, S) * np.float32(4.0) - np.float32(2.0)
+    tx = np.full(B, T, np.int32)
+    ty = np.full(B, S, np.int32)
+    assert_parity(mas, value, tx, ty, "full-length-b64-t1024-s4096")
+
+
 def test_unaligned_value_pointer(mas):
     value, tx, ty = synth.generate("tts-b16-t128-s512")
     B, T, S = value.shape
