@@ -101,7 +101,9 @@ __host__ __device__ constexpr int swz(int r) { return (r >> 1) & 7; }
 // kNWin chunks, and the row_start table under construction.
 constexpr int kWinRows = 1024;
 constexpr int kNWin = 24;
-constexpr int kWinAhead = 14;  // windows in flight (4 loads each: at most 63 outstanding)
+constexpr int kWinLoaders = 4;  // loader waves staging windows: loader k takes chunks C-1-k, C-1-k-4, ...
+constexpr int kWinAhead = 6;    // windows in flight per loader (4 loads each)
+static_assert(kWinLoaders * kWinAhead <= kNWin, "windows in flight fit the slots");
 static_assert(kWinRows >= 32 * (kNWin - 1) + kWave + 96, "a window covers the rows the walk can reach");
 // Walker position: (chunk << 32) | row, or -1 once the walk is over.
 __device__ __forceinline__ long long walk_pos(int chunk, int row) { return ((long long)chunk << 32) | (uint32_t)row; }
@@ -125,7 +127,8 @@ struct SweepLds {
   i32x4 box[kWavesPerBlock];
   int cons0;
   int wlo[kNWin];               // first row of each walk window (T > kWinRows)
-  int wready;                   // walk windows in LDS: chunks >= wready
+  i32x4 wready;                 // window loader k: its windows of chunks >= wready[k] are in LDS
+  int zdone;                    // helper waves done writing zeros (walker's workgroup)
   long long wpos;               // walker position (walk_pos), or -1 once the walk is over
 };
 static_assert(sizeof(SweepLds) <= 160 * 1024, "LDS");
@@ -142,25 +145,35 @@ __device__ __forceinline__ void vm_wait() {
   static_assert(N >= 0 && N <= 63, "vmcnt is a 6-bit counter");
   asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
 }
-// The same for a count known only at run time (n in [0, 63]; more waits for 0).
-__device__ __forceinline__ void vm_wait_n(int n) {
-  switch (n) {
-#define MAS_VMW(k) \
-  case k:          \
-    vm_wait<k>();  \
-    break;
-    MAS_VMW(0) MAS_VMW(1) MAS_VMW(2) MAS_VMW(3) MAS_VMW(4) MAS_VMW(5) MAS_VMW(6) MAS_VMW(7) MAS_VMW(8)
-    MAS_VMW(9) MAS_VMW(10) MAS_VMW(11) MAS_VMW(12) MAS_VMW(13) MAS_VMW(14) MAS_VMW(15) MAS_VMW(16)
-    MAS_VMW(17) MAS_VMW(18) MAS_VMW(19) MAS_VMW(20) MAS_VMW(21) MAS_VMW(22) MAS_VMW(23) MAS_VMW(24)
-    MAS_VMW(25) MAS_VMW(26) MAS_VMW(27) MAS_VMW(28) MAS_VMW(29) MAS_VMW(30) MAS_VMW(31) MAS_VMW(32)
-    MAS_VMW(33) MAS_VMW(34) MAS_VMW(35) MAS_VMW(36) MAS_VMW(37) MAS_VMW(38) MAS_VMW(39) MAS_VMW(40)
-    MAS_VMW(41) MAS_VMW(42) MAS_VMW(43) MAS_VMW(44) MAS_VMW(45) MAS_VMW(46) MAS_VMW(47) MAS_VMW(48)
-    MAS_VMW(49) MAS_VMW(50) MAS_VMW(51) MAS_VMW(52) MAS_VMW(53) MAS_VMW(54) MAS_VMW(55) MAS_VMW(56)
-    MAS_VMW(57) MAS_VMW(58) MAS_VMW(59) MAS_VMW(60) MAS_VMW(61) MAS_VMW(62) MAS_VMW(63)
-#undef MAS_VMW
-    default:
-      vm_wait<0>();
+// The same for a count known only at run time (n >= 0): waits until at most
+// k operations are outstanding for the largest k <= n of a fixed set, which
+// is at least as strict.  Compile-time branches only (a switch would become a
+// jump table read through the scalar cache on every call).
+__device__ __forceinline__ void vm_wait_le(int n) {
+  if (n >= 16) {
+    if (n >= 48) vm_wait<48>();
+    else if (n >= 32) vm_wait<32>();
+    else if (n >= 24) vm_wait<24>();
+    else vm_wait<16>();
+  } else if (n >= 4) {
+    if (n >= 12) vm_wait<12>();
+    else if (n >= 8) vm_wait<8>();
+    else if (n >= 6) vm_wait<6>();
+    else vm_wait<4>();
+  } else {
+    if (n >= 3) vm_wait<3>();
+    else if (n >= 2) vm_wait<2>();
+    else if (n >= 1) vm_wait<1>();
+    else vm_wait<0>();
   }
+}
+// vm_wait_le with the call site's usual count first.
+template <int USUAL>
+__device__ __forceinline__ void vm_wait_usual(int n) {
+  if (n == USUAL)
+    vm_wait<USUAL>();
+  else
+    vm_wait_le(n);
 }
 
 // A buffer resource that moves forward through a region: base and number of
@@ -568,7 +581,7 @@ __device__ __forceinline__ float sweep_wave(const KParams& p, SweepLds& L, const
   // Makes the boundary row of chunk c (polled into poll slot pk) available in
   // slot k.
   auto deliver = [&](int c, int k, int pk) __attribute__((always_inline)) {
-    vm_wait_n((int)(n_vm - 1u - poll_seq[pk]));
+    vm_wait_usual<2 * kPollAhead - 1>((int)(n_vm - 1u - poll_seq[pk]));
     const uint64_t* pw = reinterpret_cast<const uint64_t*>(&L.poll[pk][0]);
     uint64_t wd = pw[lane & (kChunk - 1)];
     int spins = 0;
@@ -795,18 +808,18 @@ __device__ __forceinline__ void load_tiles(const KParams& p, SweepLds& L, const 
     }
     // The oldest tile in flight has landed once at most the younger ones
     // are outstanding.
-    vm_wait_n(kOps * (issued - readied - 1));
+    vm_wait_usual<kOps * (kInflight - 1)>(kOps * (issued - readied - 1));
     ++readied;
     lds_put(ready_addr, readied);
   }
   vm_wait<0>();
 }
 
-// Zeros over the path rows of wave g of item b (device-scope stores: the
-// walker of the item writes the ones over some of them later, from another
-// workgroup).
-__device__ __forceinline__ void clear_rows(const KParams& p, int b, int g, int lane) {
-  const int r0 = min(g * kRowsPerWave, p.T), r1 = min(g * kRowsPerWave + kRowsPerWave, p.T);
+// Zeros over path rows [r0, r1) of item b, clamped to [0, T) (device-scope
+// stores: the walker of the item writes the ones over some of them later).
+__device__ __forceinline__ void clear_rows(const KParams& p, int b, int r0, int r1, int lane) {
+  r0 = max(min(r0, p.T), 0);
+  r1 = max(min(r1, p.T), r0);
   if (r1 <= r0) return;
   const uint64_t base = (uint64_t)b * (uint64_t)p.T * (uint64_t)p.S;
   const uint64_t p0 = base + (uint64_t)r0 * (uint64_t)p.S, p1 = base + (uint64_t)r1 * (uint64_t)p.S;
@@ -824,6 +837,9 @@ __device__ __forceinline__ void clear_rows(const KParams& p, int b, int g, int l
     const int n = (int)(a1 - a0);
     for (int o = 16 * lane; o < n; o += 16 * kWave) __builtin_amdgcn_raw_buffer_store_b128(zero, r, o, 0, kPolicyDev);
   }
+}
+__device__ __forceinline__ void clear_group(const KParams& p, int b, int g, int lane) {
+  clear_rows(p, b, g * kRowsPerWave, g * kRowsPerWave + kRowsPerWave, lane);
 }
 
 // ---------------------------------------------------------------- backtrack
@@ -878,22 +894,27 @@ __device__ __forceinline__ uint32_t walk_chunk(uint32_t w, uint32_t wh, int sl, 
 #undef MAS_WALK_STEP2
 #undef MAS_WALK_STEP
 
-// Loader side of the walk: the decision words of chunks C-1 down to 0, a
-// window of kWinRows rows per chunk, kWinAhead windows in flight, into slot
-// ch % kNWin once the walker has moved past the chunk that slot held.  When
-// T exceeds kWinRows a window ends 63 rows above the walker's row at issue
-// time: the walk cannot descend past the window before it reaches the chunk.
-// Stops early once the walker has reached row 0.
-__device__ __forceinline__ void load_windows(const KParams& p, SweepLds& L, int b, int ty, int lane, bool& timed_out) {
+// Loader side of the walk: loader k (of kWinLoaders) stages the decision
+// words of chunks C-1-k, C-1-k-4, ... down to 0, a window of kWinRows rows per
+// chunk, kWinAhead windows in flight, into slot ch % kNWin once the walker
+// has moved past the chunk that slot held, and publishes the lowest chunk of
+// its sequence staged so far in wready[k].  When T exceeds kWinRows a window
+// ends 63 rows above the walker's row at issue time: the walk cannot descend
+// past the window before it reaches the chunk.  Stops early once the walker
+// has reached row 0.
+__device__ __forceinline__ void load_windows(const KParams& p, SweepLds& L, int b, int ty, int k, int lane, bool& timed_out) {
   const int C = (ty + kChunk - 1) / kChunk;
   const uint32_t* db = p.dec + (size_t)b * p.NC * (size_t)p.TP;
   const uint64_t chunk_bytes = (uint64_t)p.TP * 4u;
   const uint32_t win0 = lds_off(&L.u.walk.win[0][0]);
-  int issued = C - 1, readied = C;  // windows of chunks > issued are issued, >= readied ready
+  const uint32_t ready_addr = lds_off(&L.wready) + 4u * (uint32_t)k;
+  constexpr int kStep = kWinLoaders;
+  // Own chunks above `issued` are issued; own chunks >= `readied` are staged.
+  int issued = C - 1 - k, readied = C - 1 - k + kStep;
   long long wpos = lds_load(&L.wpos);
   int spins = 0;
-  while (readied > 0 && wpos >= 0 && !timed_out) {
-    while (issued >= 0 && readied - 1 - issued < kWinAhead) {
+  while (readied - kStep >= 0 && wpos >= 0 && !timed_out) {
+    while (issued >= 0 && readied - kStep - issued < kStep * kWinAhead) {
       if ((int)(wpos >> 32) > issued + kNWin) {
         wpos = lds_load(&L.wpos);
         if (wpos < 0 || (int)(wpos >> 32) > issued + kNWin) break;
@@ -905,22 +926,49 @@ __device__ __forceinline__ void load_windows(const KParams& p, SweepLds& L, int 
       const Cursor cr = make_cursor(db + (size_t)issued * p.TP + lo, chunk_bytes - (uint64_t)lo * 4u);
       const __amdgpu_buffer_rsrc_t r = cr.rsrc_s();
 #pragma unroll
-      for (int k = 0; k < kWinRows / 256; ++k)
-        dma16_dev(win0 + (uint32_t)slot * (kWinRows * 4) + 1024u * k, r, 16 * lane + 1024 * k);
-      --issued;
+      for (int q = 0; q < kWinRows / 256; ++q)
+        dma16_dev(win0 + (uint32_t)slot * (kWinRows * 4) + 1024u * q, r, 16 * lane + 1024 * q);
+      issued -= kStep;
     }
-    if (readied - 1 == issued) {
+    const int inflight = (readied - kStep - issued) / kStep;
+    if (inflight == 0) {
       // Nothing in flight: wait for the walker to free a slot.
       if (++spins > kSpinLimit) timed_out = true;
       __builtin_amdgcn_s_sleep(1);
       wpos = lds_load(&L.wpos);
       continue;
     }
-    vm_wait_n((kWinRows / 256) * (readied - 2 - issued));
-    --readied;
-    lds_put(lds_off(&L.wready), readied);
+    vm_wait_usual<(kWinRows / 256) * (kWinAhead - 1)>((kWinRows / 256) * (inflight - 1));
+    readied -= kStep;
+    lds_put(ready_addr, readied);
   }
   vm_wait<0>();
+}
+
+// Lane l of v becomes x (x and l wave-uniform, l in [0, 63]); the lane
+// select goes through M0 (one VALU operand may read one SGPR besides M0).
+template <typename T>
+__device__ __forceinline__ void write_lane(T& v, T x, int l) {
+  asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tv_writelane_b32 %0, %1, m0" : "+v"(v) : "s"(x), "s"(l) : "m0");
+}
+
+// Row starts from the walk's records of up to 64 chunks: lane k holds the
+// record of chunk base + k (valid when lo <= chunk <= hi): the set pm of its
+// step positions and the row e the path entered it in.  The k-th lowest set
+// bit p of pm is where row e - k begins: column 32 * chunk + 31 - p.  Steps
+// from row 0 or below (possible only as the walk stops) are not rows.
+__device__ __forceinline__ void flush_records(int* rsl, int base, int lo, int hi, uint32_t pm, int e, int lane) {
+  const int c = base + lane;
+  uint32_t m = (c >= lo && c <= hi) ? pm : 0u;
+  int r = e;
+  while (__builtin_amdgcn_ballot_w64(m != 0u) != 0) {
+    if (m != 0u) {
+      const int bit = __builtin_ctz(m);
+      if (r >= 1) rsl[r] = c * kChunk + (kChunk - 1) - bit;
+      --r;
+      m &= m - 1u;
+    }
+  }
 }
 
 // The walk of one item from (t_x-1, t_y-1) back to (0, 0) (Algorithm 1's
@@ -930,60 +978,99 @@ __device__ __forceinline__ void load_windows(const KParams& p, SweepLds& L, int 
 // L.u.walk.rs: the first column of every row, with rs[0] = 0 and
 // rs[t_x .. T] = t_y.  Runs on the sweep wave that holds row t_x-1; its
 // loader stages the windows.
+//
+// Per chunk the wave runs the scalar step chain (walk_chunk) on the words of
+// rows idx, idx-1, ... (lane k: row idx - k) while the LDS read of the next
+// chunk's words, at the same rows, is in flight: the path descends at most
+// 32 rows per chunk, so those 64 rows cover the next chunk too.  Each chunk's
+// step set and entry row go into lane (chunk % 64) of two registers; every 64
+// chunks the lanes turn them into row starts in parallel.
 __device__ __forceinline__ void walk(const KParams& p, SweepLds& L, int tx, int ty, int lane, bool& timed_out) {
   int* rsl = L.u.walk.rs;
-  const uint32_t below = (1u << (lane & (kChunk - 1))) - 1u;  // positions below this lane's
-  int idx = tx - 1;                   // row of the path at the chunk's last column
-  int cw = (ty - 1) / kChunk;         // chunk being walked
-  int q0 = 31 - (ty - 1) % kChunk;    // position of the path's column in chunk cw
-  // Word of row e - lane of chunk ch (its window must be in LDS).
   const bool banded = p.T > kWinRows;  // windows start at row 0 otherwise
-  auto read_row = [&](int ch, int e) __attribute__((always_inline)) -> uint32_t {
-    const int slot = ch % kNWin;
-    const int r = e - lane - (banded ? lds_load(&L.wlo[slot]) : 0);
-    return L.u.walk.win[slot][r > 0 ? r : 0];
+  int idx = tx - 1;                    // row of the path at the chunk's last column
+  int cw = (ty - 1) / kChunk;          // chunk being walked
+  const int c_top = cw;
+  int q0 = 31 - (ty - 1) % kChunk;     // position of the path's column in chunk cw
+  int slot = cw % kNWin;               // window slot of chunk cw
+  // The staging progress of the window loaders as last read; chunk c's
+  // window comes from loader (c_top - c) % kWinLoaders.
+  int kn0 = 1 << 30, kn1 = 1 << 30, kn2 = 1 << 30, kn3 = 1 << 30;
+  // Windows of every chunk >= ch are staged: each loader's chunk among ch ..
+  // ch+3 (if it has one) is.
+  auto staged = [&](int ch) __attribute__((always_inline)) -> bool {
+    const int c0 = ch + ((c_top - ch) & 3), c1 = ch + ((c_top - 1 - ch) & 3);
+    const int c2 = ch + ((c_top - 2 - ch) & 3), c3 = ch + ((c_top - 3 - ch) & 3);
+    return (c0 > c_top || kn0 <= c0) && (c1 > c_top || kn1 <= c1) && (c2 > c_top || kn2 <= c2) &&
+           (c3 > c_top || kn3 <= c3);
   };
-  auto window_ready = [&](int ch) __attribute__((always_inline)) {
+  // Waits (bounded) until the windows of chunks >= ch are in LDS.
+  auto ensure = [&](int ch) __attribute__((always_inline)) {
     int spins = 0;
-    while (uni(lds_load(&L.wready)) > ch && !timed_out) {
+    while (!staged(ch) && !timed_out) {
+      const i32x4 r = *reinterpret_cast<const volatile i32x4*>(&L.wready);
+      kn0 = uni(r.x);
+      kn1 = uni(r.y);
+      kn2 = uni(r.z);
+      kn3 = uni(r.w);
+      if (staged(ch)) break;
       if (++spins > kSpinLimit) timed_out = true;
       __builtin_amdgcn_s_sleep(1);
     }
   };
+  // Word of row e - lane from window slot sl (clamped into the window).
+  auto row_word = [&](int sl, int e) __attribute__((always_inline)) -> uint32_t {
+    const int r = e - lane - (banded ? lds_load(&L.wlo[sl]) : 0);
+    return L.u.walk.win[sl][min(max(r, 0), kWinRows - 1)];
+  };
   if (idx > 0) {
-    lds_put64(lds_off(&L.wpos), walk_pos(cw, idx));
-    window_ready(cw);
-    wave_lds_sync();
-    uint32_t W = read_row(cw, idx);  // rows idx - lane of chunk cw
-    int off = 0;                     // lane of the current row in W
-    bool walking = true;
-    while (walking) {
-      // The next chunk's rows below idx, read ahead; checked after the steps.
-      uint32_t N = 0;
-      int rdy = 0;
-      if (cw > 0) {
-        rdy = lds_load(&L.wready);
-        wave_lds_sync();
-        N = read_row(cw - 1, idx);
-      }
-      const uint32_t pm = walk_chunk(W, W >> 1, off, q0);
-      // Set bit q of pm belongs to the row (popcount of pm below q) under idx.
-      const int ri = idx - (int)__builtin_popcount(pm & below);
-      if (lane < kChunk && ((pm >> lane) & 1u) && ri >= 0) rsl[ri] = cw * kChunk + 31 - lane;
+    ensure(cw);
+    uint32_t Wa = row_word(slot, idx), Wb = 0;
+    uint32_t rec_pm = 0;  // lane k: steps of chunk (64-aligned base) + k
+    int rec_e = 0;        // lane k: its entry row
+    int off = 0;          // lane of row idx in the current words
+    bool more = true;
+    // One chunk on the words in Wc, the next chunk's read into Wn; false once
+    // the walk is over or the chunk was the last of its block.
+    auto chunk = [&](uint32_t& Wc, uint32_t& Wn) __attribute__((always_inline)) -> bool {
+      const int nslot = slot == 0 ? kNWin - 1 : slot - 1;
+      if (cw > 0) Wn = row_word(nslot, idx);
+      __builtin_amdgcn_sched_barrier(0);
+      // (readfirstlane: the compiler treats asm results as per-lane values)
+      const uint32_t pm = (uint32_t)uni((int)walk_chunk(Wc, Wc >> 1, uni(off), uni(q0)));
+      __builtin_amdgcn_sched_barrier(0);
       const int kk = __builtin_popcount(pm);
-      if (cw > 0 && uni(rdy) > cw - 1) {
-        window_ready(cw - 1);
-        wave_lds_sync();
-        N = read_row(cw - 1, idx);
-      }
+      write_lane(rec_pm, pm, uni(cw & (kWave - 1)));
+      write_lane(rec_e, uni(idx), uni(cw & (kWave - 1)));
       idx -= kk;
+      more = idx > 0 && cw > 0;
+      off = kk;
       q0 = 0;
       cw -= 1;
-      W = N;
-      off = kk;
-      walking = idx > 0 && cw >= 0;
-      // Windows of chunks above cw are no longer needed.
-      lds_put64(lds_off(&L.wpos), walk_pos(max(cw, 0), max(idx, 0)));
+      slot = nslot;
+      return more && (cw & 7) != 7;
+    };
+    // Blocks of chunks down to a multiple of 8: the windows a block reads are
+    // checked once, and the walker's position is published once per block
+    // (the loader refills slots of chunks above it).  The chunk loop holds
+    // no inner loop, so the compiler waits for each read only where its
+    // words are used, one chunk after it was issued.
+    while (more) {
+      lds_put64(lds_off(&L.wpos), walk_pos(cw, idx));
+      ensure(max((cw & ~7) - 1, 0));
+      bool in_b = false;  // the next chunk's words are in Wb
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        if (!chunk(Wa, Wb)) {
+          in_b = true;
+          break;
+        }
+        if (!chunk(Wb, Wa)) break;
+      }
+      if (in_b) Wa = Wb;
+      // Records are complete for every 64-aligned group the walk has left.
+      if (!more || ((cw + 1) & (kWave - 1)) == 0)
+        flush_records(rsl, (cw + 1) & ~(kWave - 1), cw + 1, c_top, rec_pm, rec_e, lane);
     }
   }
   wave_lds_sync();
@@ -1035,23 +1122,46 @@ __device__ __forceinline__ void write_ones(const KParams& p, const int* rsl, int
 }
 
 // ---------------------------------------------------------------- roles
+// The workgroup of the wave holding row t_x-1 walks the item: that wave walks,
+// the workgroup's four loaders stage the decision windows, and its other
+// three sweep waves write the zeros of the workgroup's path rows while the
+// walk runs (each its own rows and a third of the walker's).  In every other
+// workgroup the loaders write the zeros of their sweep waves' rows.
+__device__ __forceinline__ bool walker_workgroup(const WaveCtx& x) {
+  return x.g / kWavesPerBlock == x.g_last / kWavesPerBlock;
+}
+
 __device__ __forceinline__ void sweep_role(const KParams& p, SweepLds& L, const WaveCtx& x, uint32_t tag, bool& timed_out) {
   const int lane = x.lane, b = x.b, g = x.g, w = x.w, g_last = x.g_last;
-  if (g > g_last) return;  // no rows of the alignment here
-  if (g == 0 && lane == 0 && p.status) p.status[b] = kItemOk;
-  float score;
-  if (g == g_last) {
-    score = g == 0 ? sweep_wave<0, 0>(p, L, x, tag, timed_out)
-                   : (w > 0 ? sweep_wave<1, 0>(p, L, x, tag, timed_out) : sweep_wave<2, 0>(p, L, x, tag, timed_out));
-  } else if (w < kWavesPerBlock - 1) {
-    score = g == 0 ? sweep_wave<0, 1>(p, L, x, tag, timed_out)
-                   : (w > 0 ? sweep_wave<1, 1>(p, L, x, tag, timed_out) : sweep_wave<2, 1>(p, L, x, tag, timed_out));
-  } else {
-    score = sweep_wave<1, 2>(p, L, x, tag, timed_out);
+  float score = neg_inf();
+  if (g <= g_last) {
+    if (g == 0 && lane == 0 && p.status) p.status[b] = kItemOk;
+    if (g == g_last) {
+      score = g == 0 ? sweep_wave<0, 0>(p, L, x, tag, timed_out)
+                     : (w > 0 ? sweep_wave<1, 0>(p, L, x, tag, timed_out) : sweep_wave<2, 0>(p, L, x, tag, timed_out));
+    } else if (w < kWavesPerBlock - 1) {
+      score = g == 0 ? sweep_wave<0, 1>(p, L, x, tag, timed_out)
+                     : (w > 0 ? sweep_wave<1, 1>(p, L, x, tag, timed_out) : sweep_wave<2, 1>(p, L, x, tag, timed_out));
+    } else {
+      score = sweep_wave<1, 2>(p, L, x, tag, timed_out);
+    }
+    // Publish this wave's decision words (its stores are complete).
+    if (lane == 0) st_dev(p.done + (size_t)b * p.NW + g, tag);
   }
-  // Publish this wave's decision words (its stores are complete).
-  if (lane == 0) st_dev(p.done + (size_t)b * p.NW + g, tag);
-  if (g != g_last) return;
+  if (!walker_workgroup(x)) return;
+  const int w_last = g_last % kWavesPerBlock;
+  if (g != g_last) {
+    // Helper: zeros over this wave's rows and a third of the walker's.
+    if (p.path) {
+      clear_group(p, b, g, lane);
+      const int h = w < w_last ? w : w - 1;
+      const int r0 = g_last * kRowsPerWave + h * (kRowsPerWave / 3);
+      clear_rows(p, b, r0, r0 + kRowsPerWave / 3, lane);
+      vm_wait<0>();
+    }
+    if (lane == 0) __hip_atomic_fetch_add(&L.zdone, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+    return;
+  }
 
   // The walker.
   if (lane == (x.tx - 1) - g_last * kRowsPerWave + 1 && p.score) p.score[b] = score;
@@ -1059,7 +1169,9 @@ __device__ __forceinline__ void sweep_role(const KParams& p, SweepLds& L, const 
   int32_t* rs_out = p.row_start + (size_t)b * ((size_t)p.T + 1);
   for (int i = lane; i <= p.T; i += kWave) st_dev(reinterpret_cast<uint32_t*>(rs_out + i), (uint32_t)L.u.walk.rs[i]);
   if (!p.path) return;
-  wait_flags(p.cleared + (size_t)b * p.NW, g_last + 1, tag, lane, timed_out);
+  // Zeros first: the loaders' in earlier workgroups, the helpers' here.
+  wait_flags(p.cleared + (size_t)b * p.NW, g_last - w_last, tag, lane, timed_out);
+  wait_equal(&L.zdone, kWavesPerBlock - 1, timed_out);
   write_ones(p, L.u.walk.rs, b, x.tx, lane);
 }
 
@@ -1067,24 +1179,27 @@ template <bool ALIGNED>
 __device__ __forceinline__ void loader_role(const KParams& p, SweepLds& L, const WaveCtx& x, uint32_t tag, bool& timed_out) {
   const int lane = x.lane, b = x.b, g = x.g, g_last = x.g_last;
   if (g <= g_last) load_tiles<ALIGNED>(p, L, x, timed_out);
+  if (walker_workgroup(x)) {
+    // Decision windows for the walk, once every wave of the item has
+    // published its words.
+    wait_flags(p.done + (size_t)b * p.NW, g_last + 1, tag, lane, timed_out);
+    load_windows(p, L, b, x.ty, x.w, lane, timed_out);
+    return;
+  }
   if (p.path && g * kRowsPerWave < p.T) {
     // Rows past the alignment are cleared once the item's sweep is over,
     // when the HBM is less busy.
     if (g > g_last) wait_flags(p.done + (size_t)b * p.NW + g_last, 1, tag, lane, timed_out);
-    clear_rows(p, b, g, lane);
+    clear_group(p, b, g, lane);
     vm_wait<0>();
     if (lane == 0) st_dev(p.cleared + (size_t)b * p.NW + g, tag);
   }
-  if (g != g_last) return;
-  // The walker's loader: decision words of every wave of the item.
-  wait_flags(p.done + (size_t)b * p.NW, g_last + 1, tag, lane, timed_out);
-  load_windows(p, L, b, x.ty, lane, timed_out);
 }
 
 // Items with invalid lengths: an all-zero slab, zero row_start, score -inf.
 __device__ __forceinline__ void invalid_item(const KParams& p, int b, int g, bool is_loader, int lane, int st) {
   if (is_loader) {
-    if (p.path) clear_rows(p, b, g, lane);
+    if (p.path) clear_group(p, b, g, lane);
     return;
   }
   if (g == 0) {
@@ -1125,7 +1240,8 @@ __global__ void __launch_bounds__(kThreads, 1) mas_kernel(KParams p) {
   }
   if (threadIdx.x == 0) {
     L.cons0 = chunk_begin(r * kWavesPerBlock) - 1;
-    lds_store(&L.wready, 1 << 30);
+    L.wready = i32x4{1 << 30, 1 << 30, 1 << 30, 1 << 30};
+    L.zdone = 0;
     // Walker not started: at chunk C (every window slot free), row t_x-1.
     lds_store(&L.wpos, walk_pos((ty + kChunk - 1) / kChunk, max(tx - 1, 0)));
   }
