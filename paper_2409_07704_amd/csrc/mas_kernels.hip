@@ -77,7 +77,6 @@ constexpr int kOnesPerLane = 128;    // path bytes a lane writes for one row bef
 constexpr int kLoaders = 4;          // loader waves per workgroup
 constexpr int kThreads = kThreadsPerBlock + kLoaders * kWave;
 constexpr int kRing = 4;             // tile and boundary slots per sweep wave
-constexpr int kPollAhead = 4;        // boundary polls in flight (first wave of a workgroup)
 constexpr int kPolicyDev = 16;       // cache policy sc1: device scope (write-through stores)
 
 // ---------------------------------------------------------------- LDS layout
@@ -116,8 +115,6 @@ struct SweepLds {
       int rs[kMaxRows + 1 + kWave];
     } walk;
   } u;
-  f32x4 ostage[1][kChunk / 4];  // last row of wave 3 before its global hand-off
-  uint32_t poll[kPollAhead][kWave];  // polled boundary words {value, tag} x 32 (wave 0)
   // Mailbox of sweep wave w, read with one 16-byte load per chunk:
   //   .x ready: value tiles of chunks < ready are in w's slots (loader w);
   //   .y prod:  boundary rows of chunks < prod are in w's slots (wave w-1);
@@ -129,6 +126,7 @@ struct SweepLds {
   int wlo[kNWin];               // first row of each walk window (T > kWinRows)
   i32x4 wready;                 // window loader k: its windows of chunks >= wready[k] are in LDS
   int zdone;                    // helper waves done writing zeros (walker's workgroup)
+  f32x4 sink[kWavesPerBlock][kChunk / 4 + 1];  // target of hand-offs nobody reads (a fixed LDS op count per step)
   long long wpos;               // walker position (walk_pos), or -1 once the walk is over
 };
 static_assert(sizeof(SweepLds) <= 160 * 1024, "LDS");
@@ -513,14 +511,14 @@ __device__ __forceinline__ f32x4 gather_last_row(const float (&q)[kChunk]) {
 // t_x-1).  IN: where the row above the wave comes from — 0 nowhere (the wave
 // holds row 0: -inf), 1 the previous wave of the workgroup (its slots, with
 // tags), 2 the global boundary words of the previous workgroup (polled by
-// this wave kPollAhead chunks ahead and copied into its own slots).  OUT: 0
-// no consumer, 1 the next wave of the workgroup, 2 global boundary words for
-// the next workgroup (staged in LDS, stored one chunk later).
+// this wave one chunk ahead and copied into its own slots).  OUT: 0 no
+// consumer, 1 the next wave of the workgroup, 2 global boundary words for the
+// next workgroup.
 //
 // Step c computes chunk c from registers while the LDS reads of chunk c+1
-// (its tile, its boundary row, the loader's ready count and the boundary
-// tag) are in flight; after the compute the step checks the count and tag
-// and only falls back to waiting when they were not there yet.
+// (its tile, its boundary row and its mailbox) are in flight, hands the
+// chunk's last row to the consumer, and then checks the mailbox: it only
+// waits when the tile or the boundary row of chunk c+1 was not there yet.
 template <int IN, int OUT>
 __device__ __forceinline__ float sweep_wave(const KParams& p, SweepLds& L, const WaveCtx& x, uint32_t tag, bool& timed_out) {
   constexpr bool IN1 = IN == 1, IN2 = IN == 2;
@@ -553,49 +551,35 @@ __device__ __forceinline__ float sweep_wave(const KParams& p, SweepLds& L, const
       make_cursor(p.dec + (size_t)x.b * p.NC * (size_t)p.TP, (uint64_t)p.NC * p.TP * 4u).rsrc();
   const int dvo = 4 * (lane > 0 ? x.row : p.TP - 1);
   const int dstride = p.TP * 4;
-  // Global boundary words: this wave's (OUT2) and the previous wave's (IN2),
-  // word 32c + l for column 32c + l; lanes 0..31 move one word each.
+  // Global boundary words: this wave's (OUT2) and the previous wave's (IN2):
+  // word 32c + j = {Q of the wave's last row at column 32c + j, tag}.
   const size_t slot_words = (size_t)p.NC * kChunk;
   const __amdgpu_buffer_rsrc_t sr =
       make_cursor(p.slots + ((size_t)x.b * p.NW + x.g) * slot_words, slot_words * 8u).rsrc();
   const uint64_t* const pslots = p.slots + ((size_t)x.b * p.NW + (x.g > 0 ? x.g - 1 : 0)) * slot_words;
-  const int pslot_bytes = (int)(slot_words * 8u);
-  auto word_off = [&](int c) __attribute__((always_inline)) -> int {
-    return lane < kChunk ? c * (kChunk * 8) + 8 * lane : -1;  // -1: out of range, dropped / 0
-  };
 
-  // IN2: the boundary words of chunk c (256 bytes: {value, tag} for its 32
-  // columns), polled kPollAhead chunks ahead by LDS-DMA into poll slot
-  // (c - c_begin + 1) % kPollAhead, then checked and copied into the chunk's
-  // slot right before the wave reads it.  The wave counts its own
-  // vector-memory operations (these polls and its decision stores; it issues
-  // no others) so that it can wait for one poll and not for later ones.
-  uint32_t n_vm = 0;               // vector-memory operations issued
-  uint32_t poll_seq[kPollAhead];   // n_vm of each slot's poll
-  const uint32_t poll_lds = lds_off(&L.poll[0][0]);
-  auto issue_poll = [&](int c, int k) __attribute__((always_inline)) {
-    dma4_dev(poll_lds + (uint32_t)k * (kWave * 4), Cursor{reinterpret_cast<const char*>(pslots), pslot_bytes}.rsrc_s(),
-             c * (kChunk * 8) + 4 * lane);
-    poll_seq[k] = n_vm++;
+  // IN2: the boundary words of chunk c (256 bytes: lane l < 32 loads column
+  // 32c + l; lanes 32..63 load the same words again).  A device-scope load
+  // issued one step before the words are needed; when their tags are not all
+  // this call's, the wave loads them again until they are.  Then lanes 0..31
+  // write the values into the chunk's slot.
+  uint64_t pw = 0;
+  auto poll = [&](int c) __attribute__((always_inline)) {
+    pw = __hip_atomic_load(pslots + (size_t)c * kChunk + (lane & (kChunk - 1)), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   };
-  // Makes the boundary row of chunk c (polled into poll slot pk) available in
-  // slot k.
-  auto deliver = [&](int c, int k, int pk) __attribute__((always_inline)) {
-    vm_wait_usual<2 * kPollAhead - 1>((int)(n_vm - 1u - poll_seq[pk]));
-    const uint64_t* pw = reinterpret_cast<const uint64_t*>(&L.poll[pk][0]);
-    uint64_t wd = pw[lane & (kChunk - 1)];
+  // (The reload waits for itself inside the assembly and writes pw in place,
+  // so the usual path keeps a single wait for the poll of the step before.)
+  auto deliver = [&](int c, int k) __attribute__((always_inline)) {
+    const uint64_t* const src = pslots + (size_t)c * kChunk + (lane & (kChunk - 1));
     int spins = 0;
     while (!timed_out) {
-      uint64_t stale = __builtin_amdgcn_ballot_w64(lane < kChunk && (uint32_t)(wd >> 32) != tag);
+      uint64_t stale = __builtin_amdgcn_ballot_w64((uint32_t)(pw >> 32) != tag);
       asm volatile("" : "+s"(stale));
       if (stale == 0) break;
       if (++spins > kSpinLimit) timed_out = true;
-      __builtin_amdgcn_s_sleep(1);
-      issue_poll(uni(c), pk);
-      vm_wait<0>();
-      wd = pw[lane & (kChunk - 1)];
+      asm volatile("global_load_dwordx2 %0, %1, off sc1\n\ts_waitcnt vmcnt(0)" : "+v"(pw) : "v"(src) : "memory");
     }
-    if (lane < kChunk) bound_ptr(k)[lane] = __uint_as_float((uint32_t)wd);
+    if (lane < kChunk) bound_ptr(k)[lane] = __uint_as_float((uint32_t)pw);
   };
 
   if (IN == 0) {
@@ -605,11 +589,6 @@ __device__ __forceinline__ float sweep_wave(const KParams& p, SweepLds& L, const
       for (int k = 0; k < kRing; ++k) bound_ptr(k)[lane] = neg_inf();
     }
   }
-  // IN2 prologue: polls of chunks c_begin-1 .. c_begin-1+kPollAhead-1.
-  if (IN2) {
-#pragma unroll
-    for (int k = 0; k < kPollAhead; ++k) issue_poll(x.c_begin - 1 + k, k);
-  }
 
   // Lane 0's Q at the column before the first chunk: the previous wave's
   // last row there (its chunk c_begin-1, always computed), or -inf.  It
@@ -618,8 +597,8 @@ __device__ __forceinline__ float sweep_wave(const KParams& p, SweepLds& L, const
   if (IN1) {
     wait_at_least(my_box + 1, x.c_begin, timed_out);
   } else if (IN2) {
-    deliver(x.c_begin - 1, kRing - 1, 0);
-    issue_poll(x.c_begin - 1 + kPollAhead, 0);
+    poll(x.c_begin - 1);
+    deliver(x.c_begin - 1, kRing - 1);
   }
   if (IN != 0) {
     wave_lds_sync();
@@ -636,8 +615,9 @@ __device__ __forceinline__ float sweep_wave(const KParams& p, SweepLds& L, const
   if (IN1 && x.c_begin < x.prev_end) {
     wait_at_least(my_box + 1, x.c_begin + 1, timed_out);
   } else if (IN2 && x.c_begin < x.prev_end) {
-    deliver(x.c_begin, 0, 1);
-    issue_poll(x.c_begin + kPollAhead, 1);
+    poll(x.c_begin);
+    deliver(x.c_begin, 0);
+    if (x.c_begin + 1 < x.prev_end) poll(x.c_begin + 1);
   }
   int cons_seen;  // the consumer's progress as last read (OUT1)
   {
@@ -649,38 +629,36 @@ __device__ __forceinline__ float sweep_wave(const KParams& p, SweepLds& L, const
   }
   lds_put(my_cons, x.c_begin + 1);
 
-  float qc[kChunk];
+  float qc[kChunk] = {};
   int soff = x.c_begin * dstride;
   float score = neg_inf();
   const int m_last = (x.ty - 1) % kChunk;
 
-  // The last row of chunk cp (in lane 63's qc) for the next wave: gathered
-  // into lanes 56..63 and stored with one LDS write.  OUT1: into the next
-  // wave's slot for chunk cp (once it has read chunk cp-4 from that slot),
-  // then its mailbox's prod; OUT2: into the staging row, read back by lanes
-  // 0..31 (returned) for the global store.  Issued at the start of the
-  // following step, ahead of that step's reads and compute, so the wave
-  // never waits for these LDS writes to complete.
-  auto hand_off = [&](int cp) __attribute__((always_inline)) -> float {
-    float ov = 0.0f;
-    if (OUT == 1 && cp >= x.next_begin - 1) {
-      if (cons_seen < cp - (kRing - 1)) cons_seen = wait_at_least(my_box + 2, cp - (kRing - 1), timed_out);
+  // The last row of chunk cp (in lane 63's qc) for the next wave, right
+  // after its compute: gathered into lanes 56..63 (four columns each).  OUT1:
+  // one LDS write into the next wave's slot for chunk cp (once it has read
+  // chunk cp-4 from that slot), then its mailbox's prod.  Chunks the next
+  // wave does not read (cp < next_begin - 1) go to this wave's sink, so that
+  // every step issues the same LDS operations and the compiler's waits stay
+  // exact.  OUT2: two device-scope 16-byte stores per lane of {value, tag}
+  // pairs; lanes outside 56..63 get offsets past the resource (dropped).
+  const uint32_t sink = lds_off(&L.sink[w][0]);
+  auto hand_off = [&](int cp) __attribute__((always_inline)) {
+    const bool real = cp >= x.next_begin - 1;
+    if (OUT == 1) {
+      if (real && cons_seen < cp - (kRing - 1)) cons_seen = wait_at_least(my_box + 2, cp - (kRing - 1), timed_out);
       const int kn = (cp - x.next_begin) & (kRing - 1);
-      const uint32_t ns = wbase + kWaveRegion + (uint32_t)kn * kSlotStride + kBoundOff;
+      const uint32_t ns = real ? wbase + kWaveRegion + (uint32_t)kn * kSlotStride + kBoundOff : sink;
       lds_put_hi8(ns + 16u * (uint32_t)(lane - (kWave - 8)), gather_last_row(qc));
-      lds_put(next_prod, cp + 1);
-    } else if (OUT == 2 && cp >= x.next_begin - 1) {
-      float* const stage = reinterpret_cast<float*>(&L.ostage[0][0]);
-      lds_put_hi8(lds_off(stage) + 16u * (uint32_t)(lane - (kWave - 8)), gather_last_row(qc));
-      wave_lds_sync();
-      ov = stage[lane & (kChunk - 1)];
-    }
-    return ov;
-  };
-  auto relay = [&](int cp, float ov) __attribute__((always_inline)) {
-    if (OUT == 2 && cp >= x.next_begin - 1) {
-      const uint64_t word = ((uint64_t)tag << 32) | (uint64_t)__float_as_uint(ov);
-      __builtin_amdgcn_raw_buffer_store_b64(__builtin_bit_cast(u32x2, word), sr, word_off(cp), 0, kPolicyDev);
+      lds_put(real ? next_prod : sink + 128u, cp + 1);
+    } else if (OUT == 2 && real) {
+      const f32x4 f = gather_last_row(qc);
+      const bool mine = lane >= kWave - 8;
+      const int o = cp * (kChunk * 8) + 32 * (lane - (kWave - 8));
+      const u32x4 lo = {__float_as_uint(f.x), tag, __float_as_uint(f.y), tag};
+      const u32x4 hi = {__float_as_uint(f.z), tag, __float_as_uint(f.w), tag};
+      __builtin_amdgcn_raw_buffer_store_b128(lo, sr, mine ? o : -1, 0, kPolicyDev);
+      __builtin_amdgcn_raw_buffer_store_b128(hi, sr, mine ? o + 16 : -1, 0, kPolicyDev);
     }
   };
 
@@ -692,18 +670,16 @@ __device__ __forceinline__ float sweep_wave(const KParams& p, SweepLds& L, const
     const bool has_next = c + 1 < x.c_end;
     const bool need_prod = IN1 && c + 1 < x.prev_end;
     // IN2: the boundary row of chunk c+1 into slot J1, and the poll of chunk
-    // c+1+kPollAhead into the freed poll slot.
+    // c+2 (used at the next step).
     if (IN2 && has_next && c + 1 < x.prev_end) {
-      constexpr int PK = (J + 2) & (kPollAhead - 1);
-      deliver(c + 1, J1, PK);
-      issue_poll(c + 1 + kPollAhead, PK);
+      deliver(c + 1, J1);
+      if (c + 2 < x.prev_end) poll(c + 2);
     }
-    // The previous chunk's last row to the next wave.
-    const float ov = c > x.c_begin ? hand_off(c - 1) : 0.0f;
     // Reads of chunk c+1, in flight during the compute of chunk c: the
     // mailbox first, then the values (one LDS queue per wave: in order).
-    i32x4 mb = {1 << 30, 1 << 30, 0, 0};
-    if (has_next) read_ahead<J1>(Lb, box_off, ra, vn, mb);
+    // After the last chunk they read the next slot's stale contents, unused.
+    i32x4 mb;
+    read_ahead<J1>(Lb, box_off, ra, vn, mb);
     __builtin_amdgcn_sched_barrier(0);
 
     uint32_t bits = 0;
@@ -712,10 +688,9 @@ __device__ __forceinline__ float sweep_wave(const KParams& p, SweepLds& L, const
     else
       sweep_chunk<false>(q, t, vc, qc, bits, lane, x.row, c * kChunk);
     __builtin_amdgcn_sched_barrier(0);
+    hand_off(c);
     __builtin_amdgcn_raw_buffer_store_b32(bits, dr, dvo, soff, kPolicyDev);
-    ++n_vm;
     soff += dstride;
-    if (c > x.c_begin) relay(c - 1, ov);
     if (OUT == 0 && c == x.c_end - 1) {
 #pragma unroll
       for (int m = 0; m < kChunk; ++m) score = (m == m_last) ? qc[m] : score;
@@ -740,13 +715,42 @@ __device__ __forceinline__ float sweep_wave(const KParams& p, SweepLds& L, const
     if (c + 2 < x.c_end) step(std::integral_constant<int, 2>(), c + 2, va, vb);
     if (c + 3 < x.c_end) step(std::integral_constant<int, 3>(), c + 3, vb, va);
   }
-  // The last chunk's row.
-  {
-    const float ov = hand_off(x.c_end - 1);
-    relay(x.c_end - 1, ov);
-  }
   vm_wait<0>();
   return score;
+}
+
+// ---------------------------------------------------------------- scheduling
+// Critical-path-first start.  Every item runs as its own chain of waves, and
+// the launch ends with the longest chain; HBM bandwidth, shared by every item
+// sweeping at the same time, is the resource they compete for.  So each item
+// waits, before loading more than its first tiles, for a share of the time by
+// which its estimated run is shorter than the batch's longest: long items
+// sweep first with little contention and short ones fill in behind them.
+// Estimates are in wall-clock ticks (100 MHz) of one item running alone:
+// kTicksPerChunk per 32 columns and kTicksPerGroup per 63 rows, fitted to
+// measured single-item runs.  Batches larger than kDelayMaxBatch start at
+// once (every workgroup would read every length), and no delay exceeds
+// kDelayMaxTicks (1 ms, far below the bound of any device-side wait).
+constexpr int kTicksPerChunk = 75;
+constexpr int kTicksPerGroup = 480;
+constexpr int kDelayPercent = 80;
+constexpr int kDelayMaxBatch = 1024;
+constexpr int kDelayMaxTicks = 100000;
+
+__device__ __forceinline__ int est_ticks(int tx, int ty, int T, int S) {
+  if (item_status(tx, ty, T, S) != kItemOk) return 0;
+  return kTicksPerChunk * ((ty + kChunk - 1) / kChunk) + kTicksPerGroup * ((tx + kRowsPerWave - 1) / kRowsPerWave);
+}
+
+// Start delay of item b in ticks (wave-uniform).
+__device__ __forceinline__ int start_delay(const KParams& p, int b, int lane) {
+  if (p.B > kDelayMaxBatch) return 0;
+  int m = 0;
+  for (int i = lane; i < p.B; i += kWave) m = max(m, est_ticks(p.t_x[i], p.t_y[i], p.T, p.S));
+#pragma unroll
+  for (int off = kWave / 2; off >= 1; off >>= 1) m = max(m, __shfl_xor(m, off));
+  const int mine = est_ticks(p.t_x[b], p.t_y[b], p.T, p.S);
+  return uni(min((m - mine) / 100 * kDelayPercent, kDelayMaxTicks));
 }
 
 // ---------------------------------------------------------------- loader wave
@@ -778,6 +782,7 @@ __device__ __forceinline__ void load_tiles(const KParams& p, SweepLds& L, const 
     voff[k] = o < 0x80000000ull ? (int)o : (int)0x80000000u;
   }
   int issued = x.c_begin, readied = x.c_begin;
+  bool held = x.g != 0;  // the item's first group waits for its start once its first tiles are in flight
   // The sweep wave's progress (its slots below it are free again).
   const int* const progress = w > 0 ? reinterpret_cast<const int*>(&L.box[w - 1]) + 2 : &L.cons0;
   const uint32_t ready_addr = lds_off(&L.box[w]);
@@ -800,6 +805,14 @@ __device__ __forceinline__ void load_tiles(const KParams& p, SweepLds& L, const 
       }
       vr.advance(kChunk * 4);
       ++issued;
+    }
+    if (!held) {
+      held = true;
+      const int delay = start_delay(p, x.b, lane);
+      if (delay > 0) {
+        const uint64_t until = wall_clock64() + (uint64_t)delay;
+        while (wall_clock64() < until) __builtin_amdgcn_s_sleep(127);
+      }
     }
     if (issued == readied) {
       // Nothing in flight and no free slot: wait for the sweep wave.
