@@ -1094,13 +1094,17 @@ __device__ __forceinline__ void walk(const KParams& p, SweepLds& L, int tx, int 
 }
 
 // The ones of the item's alignment (rows < t_x) over the zeroed path, from
-// the finished row_start table: row i holds ones at [rs[i], rs[i+1]).  Lane l
-// writes rows l, l+64, ...: the first kOnesPerLane bytes of each; the rest of
-// a longer row (a long stay) is written by the whole wave afterwards.
-__device__ __forceinline__ void write_ones(const KParams& p, const int* rsl, int b, int tx, int lane) {
+// the finished row_start table: row i holds ones at [rs[i], rs[i+1]).  The
+// eight waves of the walker's workgroup share the rows: wave k takes blocks
+// of 64 rows k, k+8, ...; lane l of a block writes its row's first
+// kOnesPerLane bytes, and the rest of a longer row (a long stay) is written
+// by the whole wave afterwards.
+constexpr int kOnesGo = 1 << 20;  // zdone value that lets the workgroup write the ones
+__device__ __forceinline__ void write_ones(const KParams& p, const int* rsl, int b, int tx, int k, int lane) {
   uint8_t* const item_path = p.path + (size_t)b * (size_t)p.T * (size_t)p.S;
   const __amdgpu_buffer_rsrc_t r = make_cursor(item_path, (uint64_t)p.T * p.S).rsrc();
-  for (int i0 = 0; i0 < tx; i0 += kWave) {
+  constexpr int kWaves = kThreads / kWave;
+  for (int i0 = k * kWave; i0 < tx; i0 += kWaves * kWave) {
     const int i = i0 + lane;
     const bool mine = i < tx;
     // (Clamped to the row: the table is built by the walk, never trusted blindly.)
@@ -1173,6 +1177,10 @@ __device__ __forceinline__ void sweep_role(const KParams& p, SweepLds& L, const 
       vm_wait<0>();
     }
     if (lane == 0) __hip_atomic_fetch_add(&L.zdone, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+    if (p.path) {
+      wait_at_least(&L.zdone, kOnesGo, timed_out);
+      write_ones(p, L.u.walk.rs, b, x.tx, w, lane);
+    }
     return;
   }
 
@@ -1182,10 +1190,12 @@ __device__ __forceinline__ void sweep_role(const KParams& p, SweepLds& L, const 
   int32_t* rs_out = p.row_start + (size_t)b * ((size_t)p.T + 1);
   for (int i = lane; i <= p.T; i += kWave) st_dev(reinterpret_cast<uint32_t*>(rs_out + i), (uint32_t)L.u.walk.rs[i]);
   if (!p.path) return;
-  // Zeros first: the loaders' in earlier workgroups, the helpers' here.
+  // Zeros first: the loaders' in earlier workgroups, the helpers' here; then
+  // the whole workgroup writes the ones.
   wait_flags(p.cleared + (size_t)b * p.NW, g_last - w_last, tag, lane, timed_out);
   wait_equal(&L.zdone, kWavesPerBlock - 1, timed_out);
-  write_ones(p, L.u.walk.rs, b, x.tx, lane);
+  if (lane == 0) lds_store(&L.zdone, kOnesGo);
+  write_ones(p, L.u.walk.rs, b, x.tx, w, lane);
 }
 
 template <bool ALIGNED>
@@ -1197,6 +1207,10 @@ __device__ __forceinline__ void loader_role(const KParams& p, SweepLds& L, const
     // published its words.
     wait_flags(p.done + (size_t)b * p.NW, g_last + 1, tag, lane, timed_out);
     load_windows(p, L, b, x.ty, x.w, lane, timed_out);
+    if (p.path) {
+      wait_at_least(&L.zdone, kOnesGo, timed_out);
+      write_ones(p, L.u.walk.rs, b, x.tx, kWavesPerBlock + x.w, lane);
+    }
     return;
   }
   if (p.path && g * kRowsPerWave < p.T) {
@@ -1273,10 +1287,12 @@ __global__ void __launch_bounds__(kThreads, 1) mas_kernel(KParams p) {
     if (p.status) p.status[b] = kItemSyncTimeout;
     __hip_atomic_store(&p.hdr->error, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   }
-  // The last wave of the call to finish advances the generation.
+  // The last workgroup of the call to finish advances the generation (one
+  // counter update per workgroup: updates of one word serialise).
   vm_wait<0>();
-  if (lane == 0) {
-    const uint32_t total = gridDim.x * (kThreads / kWave);
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    const uint32_t total = gridDim.x;
     const uint32_t prev = __hip_atomic_fetch_add(&p.hdr->exit_count, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     if (prev == total - 1) {
       __hip_atomic_store(&p.hdr->exit_count, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);

@@ -35,7 +35,7 @@ __host__ __device__ constexpr int dec_bit(int j) { return 31 - (j % kChunk); }
 // so stale words from earlier calls are never mistaken for fresh ones.
 struct WsHeader {
   uint32_t gen;         // call generation; tag of a call = 2 * gen + 1
-  uint32_t exit_count;  // waves that finished the current call
+  uint32_t exit_count;  // workgroups that finished the current call
   uint32_t error;       // sticky: non-zero once a device-side wait timed out
   uint32_t pad[61];
 };
