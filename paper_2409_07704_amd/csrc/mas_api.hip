@@ -28,7 +28,7 @@ static mas_status run(const float* value, const int32_t* t_x, const int32_t* t_y
   p.path = path;
   p.hdr = reinterpret_cast<WsHeader*>(base);
   p.done = reinterpret_cast<uint32_t*>(base + L.off_done);
-  p.cleared = p.done + (size_t)L.B * L.NW;
+  p.walked = p.done + (size_t)L.B * L.NW;
   p.slots = reinterpret_cast<uint64_t*>(base + L.off_slots);
   p.dec = reinterpret_cast<uint32_t*>(base + L.off_dec);
   p.B = L.B;

@@ -19,7 +19,7 @@ struct KParams {
   uint8_t* path;        // nullable [B][T][S]; null: no path is written
   WsHeader* hdr;
   uint32_t* done;       // [B][NW] sweep finished (decision words published)
-  uint32_t* cleared;    // [B][NW] path rows of the wave written with zeros
+  uint32_t* walked;     // [B] row_start published (tag values)
   uint64_t* slots;      // [B][NW][NC*32]
   uint32_t* dec;        // [B][NC][TP] decision words, row-indexed
   int32_t B, T, S, NW, NC, TP, NB;
@@ -28,7 +28,7 @@ struct KParams {
 
 // Forward sweep, backtrack and (when p.path) the dense path, in one launch:
 // one 512-thread workgroup (four sweep waves, four loader waves) per 252 text
-// rows of every item.
+// rows of every item, then (when p.path) the path-writer workgroups.
 hipError_t launch_mas(const KParams& p, hipStream_t stream);
 // Dense [B, T, S] u8 path from row_start [B, T+1].
 hipError_t launch_path(const int32_t* row_start, int32_t B, int32_t T, int32_t S, uint8_t* path, hipStream_t stream);

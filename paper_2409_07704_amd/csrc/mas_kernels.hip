@@ -16,24 +16,24 @@
 //     32 columns) from HBM into an LDS ring by buffer loads with the lds flag,
 //     up to four chunks ahead, and publishes each tile once it has landed.
 //     The sweep waves issue no loads of values; they read their tiles from LDS
-//     while the next chunk's reads are already in flight.  Afterwards the
-//     loader writes zeros over its sweep wave's path rows.
+//     while the next chunk's reads are already in flight.
 // The sweep wave holding row t_x-1 walks the decision words back from
-// (t_x-1, t_y-1) once every wave of the item has published them; its loader
-// stages the decision words of upcoming chunks in LDS.  The walker then
-// writes the ones of the alignment over the zeroed rows.
+// (t_x-1, t_y-1) once every wave of the item has published them, while the
+// four loaders of its workgroup stage the decision words of upcoming chunks
+// in LDS, and publishes the item's row_start table.  Path-writer workgroups,
+// last in the grid, then write the item's dense path from that table, every
+// byte once (zeros and ones in one pass).
 //
 // Every wait is bounded, and a wave only waits on waves of its own workgroup
 // or of workgroups with lower ids, which the hardware dispatches first:
-// workgroup (band r, item b) has id r * B + b.
+// workgroup (band r, item b) has id r * B + b, and path writer (part k, item
+// b) has id B * NB + k * B + b.
 //
 // Memory ordering across workgroups: data handed between workgroups (decision
-// words, boundary words, flags, path bytes) is written with device-scope
+// words, boundary words, row_start, flags) is written with device-scope
 // (write-through) stores and read with device-scope loads, and a wave waits
 // for its stores (vmcnt(0)) before raising a flag, so no cache write-back or
-// invalidation is needed.  Path zeros and ones for the same bytes come from
-// different workgroups: both go through to memory, the zeros before the
-// cleared flag that the writer of the ones waits for.
+// invalidation is needed.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -61,7 +61,6 @@ __device__ __forceinline__ void wave_lds_sync() {
 // Device-scope (write-through) stores and loads of data shared across
 // workgroups.
 __device__ __forceinline__ void st_dev(uint32_t* p, uint32_t v) { __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT); }
-__device__ __forceinline__ void st_dev(uint8_t* p, uint8_t v) { __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT); }
 __device__ __forceinline__ uint32_t ld_dev(const uint32_t* p) { return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT); }
 
 __device__ __forceinline__ int lds_load(const int* p) { return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP); }
@@ -73,7 +72,6 @@ __device__ __forceinline__ uint32_t call_tag(uint32_t gen) { return 2u * gen + 1
 __device__ __forceinline__ int uni(int v) { return __builtin_amdgcn_readfirstlane(v); }
 
 constexpr int kSpinLimit = 1 << 20;  // bound of every device-side wait
-constexpr int kOnesPerLane = 128;    // path bytes a lane writes for one row before the wave helps
 constexpr int kLoaders = 4;          // loader waves per workgroup
 constexpr int kThreads = kThreadsPerBlock + kLoaders * kWave;
 constexpr int kRing = 4;             // tile and boundary slots per sweep wave
@@ -125,7 +123,6 @@ struct SweepLds {
   int cons0;
   int wlo[kNWin];               // first row of each walk window (T > kWinRows)
   i32x4 wready;                 // window loader k: its windows of chunks >= wready[k] are in LDS
-  int zdone;                    // helper waves done writing zeros (walker's workgroup)
   f32x4 sink[kWavesPerBlock][kChunk / 4 + 1];  // target of hand-offs nobody reads (a fixed LDS op count per step)
   long long wpos;               // walker position (walk_pos), or -1 once the walk is over
 };
@@ -828,33 +825,6 @@ __device__ __forceinline__ void load_tiles(const KParams& p, SweepLds& L, const 
   vm_wait<0>();
 }
 
-// Zeros over path rows [r0, r1) of item b, clamped to [0, T) (device-scope
-// stores: the walker of the item writes the ones over some of them later).
-__device__ __forceinline__ void clear_rows(const KParams& p, int b, int r0, int r1, int lane) {
-  r0 = max(min(r0, p.T), 0);
-  r1 = max(min(r1, p.T), r0);
-  if (r1 <= r0) return;
-  const uint64_t base = (uint64_t)b * (uint64_t)p.T * (uint64_t)p.S;
-  const uint64_t p0 = base + (uint64_t)r0 * (uint64_t)p.S, p1 = base + (uint64_t)r1 * (uint64_t)p.S;
-  const uint64_t pa = (uint64_t)(uintptr_t)p.path;
-  const uint64_t a0 = ((pa + p0 + 15) & ~15ull) - pa, a1 = ((pa + p1) & ~15ull) - pa;
-  const bool any = a1 > a0 && a1 - a0 >= 16;
-  // Unaligned head and tail bytes (all bytes when no aligned piece).
-  const uint64_t h1 = any ? a0 : p1;
-  for (uint64_t o = p0 + lane; o < h1; o += kWave) st_dev(p.path + o, (uint8_t)0);
-  if (any) {
-    for (uint64_t o = a1 + lane; o < p1; o += kWave) st_dev(p.path + o, (uint8_t)0);
-    // 16-byte pieces [a0, a1) through a resource over them (< 2^31 bytes).
-    const __amdgpu_buffer_rsrc_t r = make_cursor(p.path + a0, a1 - a0).rsrc();
-    const u32x4 zero = {0u, 0u, 0u, 0u};
-    const int n = (int)(a1 - a0);
-    for (int o = 16 * lane; o < n; o += 16 * kWave) __builtin_amdgcn_raw_buffer_store_b128(zero, r, o, 0, kPolicyDev);
-  }
-}
-__device__ __forceinline__ void clear_group(const KParams& p, int b, int g, int lane) {
-  clear_rows(p, b, g * kRowsPerWave, g * kRowsPerWave + kRowsPerWave, lane);
-}
-
 // ---------------------------------------------------------------- backtrack
 // One step of the walk inside a chunk, for row k >= 1 below the chunk's
 // first row (its word, shifted right by one, in CUR), with the word of row
@@ -1093,148 +1063,122 @@ __device__ __forceinline__ void walk(const KParams& p, SweepLds& L, int tx, int 
   wave_lds_sync();
 }
 
-// The ones of the item's alignment (rows < t_x) over the zeroed path, from
-// the finished row_start table: row i holds ones at [rs[i], rs[i+1]).  The
-// eight waves of the walker's workgroup share the rows: wave k takes blocks
-// of 64 rows k, k+8, ...; lane l of a block writes its row's first
-// kOnesPerLane bytes, and the rest of a longer row (a long stay) is written
-// by the whole wave afterwards.
-constexpr int kOnesGo = 1 << 20;  // zdone value that lets the workgroup write the ones
-__device__ __forceinline__ void write_ones(const KParams& p, const int* rsl, int b, int tx, int k, int lane) {
+// ---------------------------------------------------------------- path writer
+// The dense path of item b (Sec. 2: the alignment as a 0/1 matrix of the
+// input's size) from its published row_start table: row i holds ones at
+// columns [rs[i], rs[i+1]) and zeros elsewhere (rows t_x .. T-1 and invalid
+// items: all zeros).  kPathParts workgroups per item each write a contiguous
+// share of the rows once the item's walker has published, each wave an
+// eighth of that share.  path16: per row, zero pieces by plain 16-byte
+// stores (the pieces holding ones are skipped: offset past the resource),
+// then the few pieces holding ones; otherwise bytes.  (Bounds are clamped to
+// the row: the table is read back from memory, never trusted blindly.)
+__device__ __forceinline__ void path_writer(const KParams& p, int k, uint32_t tag, int wv, int lane, bool& timed_out) {
+  const int b = k % p.B, part = k / p.B;
+  constexpr int kWaves = kThreads / kWave;
+  const int q0 = (int)((int64_t)p.T * part / kPathParts), q1 = (int)((int64_t)p.T * (part + 1) / kPathParts);
+  const int per = (q1 - q0 + kWaves - 1) / kWaves;
+  const int r0 = min(q0 + wv * per, q1), r1 = min(r0 + per, q1);
+  if (r1 <= r0) return;
+  wait_flags(p.walked + b, 1, tag, lane, timed_out);
+  const uint32_t* const rs = reinterpret_cast<const uint32_t*>(p.row_start) + (size_t)b * ((size_t)p.T + 1);
   uint8_t* const item_path = p.path + (size_t)b * (size_t)p.T * (size_t)p.S;
   const __amdgpu_buffer_rsrc_t r = make_cursor(item_path, (uint64_t)p.T * p.S).rsrc();
-  constexpr int kWaves = kThreads / kWave;
-  for (int i0 = k * kWave; i0 < tx; i0 += kWaves * kWave) {
-    const int i = i0 + lane;
-    const bool mine = i < tx;
-    // (Clamped to the row: the table is built by the walk, never trusted blindly.)
-    const int lo = mine ? min(max(rsl[i], 0), p.S) : 0, hi = mine ? min(max(rsl[i + 1], 0), p.S) : 0;
-    const int start = p.path16 ? (lo & ~15) : lo;
-    const int split = mine ? min(hi, start + kOnesPerLane) : start;
-    const int rowoff = i * p.S;
-    if (mine) {
+  const u32x4 zero = {0u, 0u, 0u, 0u};
+  for (int i0 = r0; i0 < r1; i0 += kWave) {
+    const int n = min(kWave, r1 - i0);
+    const int v = (int)ld_dev(rs + min(i0 + lane, p.T));
+    const int vlast = (int)ld_dev(rs + min(i0 + kWave, p.T));
+    for (int k2 = 0; k2 < n; ++k2) {
+      const int a = __builtin_amdgcn_readlane(v, k2);
+      const int e = k2 + 1 < kWave ? __builtin_amdgcn_readlane(v, k2 + 1) : vlast;
+      const int lo = min(max(a, 0), p.S), hi = min(max(e, lo), p.S);
+      const int row = i0 + k2;
       if (p.path16) {
-        for (int j0 = start; j0 < split; j0 += 16)
-          __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, path_piece(lo, hi, j0)), r, rowoff + j0, 0, kPolicyDev);
+        const int plo = lo >> 4, phi = hi > lo ? (hi + 15) >> 4 : plo;  // pieces holding ones
+        for (int pc = lane; pc < p.S / 16; pc += kWave)
+          __builtin_amdgcn_raw_buffer_store_b128(zero, r, (pc < plo || pc >= phi) ? row * p.S + 16 * pc : -1, 0, 0);
+        for (int pc = plo + lane; pc < phi; pc += kWave)
+          __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, path_piece(lo, hi, 16 * pc)), r, row * p.S + 16 * pc, 0, 0);
       } else {
-        for (int j = start; j < split; ++j) st_dev(item_path + rowoff + j, (uint8_t)1);
-      }
-    }
-    uint64_t rest = __builtin_amdgcn_ballot_w64(mine && split < hi);
-    while (rest) {
-      const int l = __builtin_ctzll(rest);
-      rest &= rest - 1;
-      const int a = __builtin_amdgcn_readlane(split, l), e = __builtin_amdgcn_readlane(hi, l);
-      const int ro = (i0 + l) * p.S;
-      if (p.path16) {
-        // a is a multiple of 16 and at least lo: every piece from a on holds
-        // ones up to e.
-        for (int j0 = a + 16 * lane; j0 < e; j0 += 16 * kWave)
-          __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, path_piece(a, e, j0)), r, ro + j0, 0, kPolicyDev);
-      } else {
-        for (int j = a + lane; j < e; j += kWave) st_dev(item_path + ro + j, (uint8_t)1);
+        uint8_t* const rowp = item_path + (size_t)row * p.S;
+        for (int j = lane; j < p.S; j += kWave) rowp[j] = (uint8_t)(j >= lo && j < hi);
       }
     }
   }
 }
 
 // ---------------------------------------------------------------- roles
-// The workgroup of the wave holding row t_x-1 walks the item: that wave walks,
-// the workgroup's four loaders stage the decision windows, and its other
-// three sweep waves write the zeros of the workgroup's path rows while the
-// walk runs (each its own rows and a third of the walker's).  In every other
-// workgroup the loaders write the zeros of their sweep waves' rows.
+// The workgroup of the wave holding row t_x-1 walks the item: that wave walks
+// and publishes row_start, the workgroup's four loaders stage the decision
+// windows.
 __device__ __forceinline__ bool walker_workgroup(const WaveCtx& x) {
   return x.g / kWavesPerBlock == x.g_last / kWavesPerBlock;
 }
 
 __device__ __forceinline__ void sweep_role(const KParams& p, SweepLds& L, const WaveCtx& x, uint32_t tag, bool& timed_out) {
   const int lane = x.lane, b = x.b, g = x.g, w = x.w, g_last = x.g_last;
-  float score = neg_inf();
-  if (g <= g_last) {
-    if (g == 0 && lane == 0 && p.status) p.status[b] = kItemOk;
-    if (g == g_last) {
-      score = g == 0 ? sweep_wave<0, 0>(p, L, x, tag, timed_out)
-                     : (w > 0 ? sweep_wave<1, 0>(p, L, x, tag, timed_out) : sweep_wave<2, 0>(p, L, x, tag, timed_out));
-    } else if (w < kWavesPerBlock - 1) {
-      score = g == 0 ? sweep_wave<0, 1>(p, L, x, tag, timed_out)
-                     : (w > 0 ? sweep_wave<1, 1>(p, L, x, tag, timed_out) : sweep_wave<2, 1>(p, L, x, tag, timed_out));
-    } else {
-      score = sweep_wave<1, 2>(p, L, x, tag, timed_out);
-    }
-    // Publish this wave's decision words (its stores are complete).
-    if (lane == 0) st_dev(p.done + (size_t)b * p.NW + g, tag);
+  if (g > g_last) return;  // no rows of the alignment here
+  if (g == 0 && lane == 0 && p.status) p.status[b] = kItemOk;
+  float score;
+  if (g == g_last) {
+    score = g == 0 ? sweep_wave<0, 0>(p, L, x, tag, timed_out)
+                   : (w > 0 ? sweep_wave<1, 0>(p, L, x, tag, timed_out) : sweep_wave<2, 0>(p, L, x, tag, timed_out));
+  } else if (w < kWavesPerBlock - 1) {
+    score = g == 0 ? sweep_wave<0, 1>(p, L, x, tag, timed_out)
+                   : (w > 0 ? sweep_wave<1, 1>(p, L, x, tag, timed_out) : sweep_wave<2, 1>(p, L, x, tag, timed_out));
+  } else {
+    score = sweep_wave<1, 2>(p, L, x, tag, timed_out);
   }
-  if (!walker_workgroup(x)) return;
-  const int w_last = g_last % kWavesPerBlock;
-  if (g != g_last) {
-    // Helper: zeros over this wave's rows and a third of the walker's.
-    if (p.path) {
-      clear_group(p, b, g, lane);
-      const int h = w < w_last ? w : w - 1;
-      const int r0 = g_last * kRowsPerWave + h * (kRowsPerWave / 3);
-      clear_rows(p, b, r0, r0 + kRowsPerWave / 3, lane);
-      vm_wait<0>();
-    }
-    if (lane == 0) __hip_atomic_fetch_add(&L.zdone, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
-    if (p.path) {
-      wait_at_least(&L.zdone, kOnesGo, timed_out);
-      write_ones(p, L.u.walk.rs, b, x.tx, w, lane);
-    }
-    return;
-  }
+  // Publish this wave's decision words (its stores are complete).
+  if (lane == 0) st_dev(p.done + (size_t)b * p.NW + g, tag);
+  if (g != g_last) return;
 
   // The walker.
   if (lane == (x.tx - 1) - g_last * kRowsPerWave + 1 && p.score) p.score[b] = score;
   walk(p, L, x.tx, x.ty, lane, timed_out);
   int32_t* rs_out = p.row_start + (size_t)b * ((size_t)p.T + 1);
   for (int i = lane; i <= p.T; i += kWave) st_dev(reinterpret_cast<uint32_t*>(rs_out + i), (uint32_t)L.u.walk.rs[i]);
-  if (!p.path) return;
-  // Zeros first: the loaders' in earlier workgroups, the helpers' here; then
-  // the whole workgroup writes the ones.
-  wait_flags(p.cleared + (size_t)b * p.NW, g_last - w_last, tag, lane, timed_out);
-  wait_equal(&L.zdone, kWavesPerBlock - 1, timed_out);
-  if (lane == 0) lds_store(&L.zdone, kOnesGo);
-  write_ones(p, L.u.walk.rs, b, x.tx, w, lane);
+  vm_wait<0>();
+  if (lane == 0) st_dev(p.walked + b, tag);
 }
 
 template <bool ALIGNED>
 __device__ __forceinline__ void loader_role(const KParams& p, SweepLds& L, const WaveCtx& x, uint32_t tag, bool& timed_out) {
   const int lane = x.lane, b = x.b, g = x.g, g_last = x.g_last;
   if (g <= g_last) load_tiles<ALIGNED>(p, L, x, timed_out);
-  if (walker_workgroup(x)) {
-    // Decision windows for the walk, once every wave of the item has
-    // published its words.
-    wait_flags(p.done + (size_t)b * p.NW, g_last + 1, tag, lane, timed_out);
-    load_windows(p, L, b, x.ty, x.w, lane, timed_out);
-    if (p.path) {
-      wait_at_least(&L.zdone, kOnesGo, timed_out);
-      write_ones(p, L.u.walk.rs, b, x.tx, kWavesPerBlock + x.w, lane);
-    }
-    return;
-  }
-  if (p.path && g * kRowsPerWave < p.T) {
-    // Rows past the alignment are cleared once the item's sweep is over,
-    // when the HBM is less busy.
-    if (g > g_last) wait_flags(p.done + (size_t)b * p.NW + g_last, 1, tag, lane, timed_out);
-    clear_group(p, b, g, lane);
-    vm_wait<0>();
-    if (lane == 0) st_dev(p.cleared + (size_t)b * p.NW + g, tag);
-  }
+  if (!walker_workgroup(x)) return;
+  // Decision windows for the walk, once every wave of the item has published
+  // its words.
+  wait_flags(p.done + (size_t)b * p.NW, g_last + 1, tag, lane, timed_out);
+  load_windows(p, L, b, x.ty, x.w, lane, timed_out);
 }
 
 // Items with invalid lengths: an all-zero slab, zero row_start, score -inf.
-__device__ __forceinline__ void invalid_item(const KParams& p, int b, int g, bool is_loader, int lane, int st) {
-  if (is_loader) {
-    if (p.path) clear_group(p, b, g, lane);
-    return;
+__device__ __forceinline__ void invalid_item(const KParams& p, int b, int g, bool is_loader, int lane, int st, uint32_t tag) {
+  if (is_loader || g != 0) return;
+  int32_t* rs_out = p.row_start + (size_t)b * ((size_t)p.T + 1);
+  for (int i = lane; i <= p.T; i += kWave) st_dev(reinterpret_cast<uint32_t*>(rs_out + i), 0u);
+  if (lane == 0) {
+    if (p.score) p.score[b] = neg_inf();
+    if (p.status) p.status[b] = st;
   }
-  if (g == 0) {
-    int32_t* rs_out = p.row_start + (size_t)b * ((size_t)p.T + 1);
-    for (int i = lane; i <= p.T; i += kWave) rs_out[i] = 0;
-    if (lane == 0) {
-      if (p.score) p.score[b] = neg_inf();
-      if (p.status) p.status[b] = st;
+  // The path writers write the all-zero slab from this table.
+  vm_wait<0>();
+  if (lane == 0) st_dev(p.walked + b, tag);
+}
+
+// The last workgroup of the call to finish advances the generation (one
+// counter update per workgroup: updates of one word serialise).
+__device__ __forceinline__ void finish_call(const KParams& p, uint32_t gen) {
+  vm_wait<0>();
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    const uint32_t total = gridDim.x;
+    const uint32_t prev = __hip_atomic_fetch_add(&p.hdr->exit_count, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (prev == total - 1) {
+      __hip_atomic_store(&p.hdr->exit_count, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      __hip_atomic_store(&p.hdr->gen, gen + 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }
   }
 }
@@ -1247,6 +1191,13 @@ __global__ void __launch_bounds__(kThreads, 1) mas_kernel(KParams p) {
   const uint32_t tag = call_tag(gen);
   bool timed_out = false;
   const int sid = blockIdx.x;
+  if (sid >= p.B * p.NB) {
+    // A path writer.
+    path_writer(p, sid - p.B * p.NB, tag, uni(threadIdx.x / kWave), threadIdx.x & (kWave - 1), timed_out);
+    if (timed_out) __hip_atomic_store(&p.hdr->error, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    finish_call(p, gen);
+    return;
+  }
   const int b = sid % p.B;
   const int r = sid / p.B;
   const int lane = threadIdx.x & (kWave - 1);
@@ -1268,14 +1219,13 @@ __global__ void __launch_bounds__(kThreads, 1) mas_kernel(KParams p) {
   if (threadIdx.x == 0) {
     L.cons0 = chunk_begin(r * kWavesPerBlock) - 1;
     L.wready = i32x4{1 << 30, 1 << 30, 1 << 30, 1 << 30};
-    L.zdone = 0;
     // Walker not started: at chunk C (every window slot free), row t_x-1.
     lds_store(&L.wpos, walk_pos((ty + kChunk - 1) / kChunk, max(tx - 1, 0)));
   }
   __syncthreads();
 
   if (st != kItemOk) {
-    invalid_item(p, b, g, is_loader, lane, st);
+    invalid_item(p, b, g, is_loader, lane, st, tag);
   } else {
     const WaveCtx x = make_ctx(b, g, w, lane, tx, ty);
     if (is_loader)
@@ -1287,18 +1237,7 @@ __global__ void __launch_bounds__(kThreads, 1) mas_kernel(KParams p) {
     if (p.status) p.status[b] = kItemSyncTimeout;
     __hip_atomic_store(&p.hdr->error, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   }
-  // The last workgroup of the call to finish advances the generation (one
-  // counter update per workgroup: updates of one word serialise).
-  vm_wait<0>();
-  __syncthreads();
-  if (threadIdx.x == 0) {
-    const uint32_t total = gridDim.x;
-    const uint32_t prev = __hip_atomic_fetch_add(&p.hdr->exit_count, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    if (prev == total - 1) {
-      __hip_atomic_store(&p.hdr->exit_count, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      __hip_atomic_store(&p.hdr->gen, gen + 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    }
-  }
+  finish_call(p, gen);
 }
 
 // ---------------------------------------------------------------- path writer
@@ -1340,7 +1279,7 @@ __global__ void __launch_bounds__(256) mas_zero_kernel(uint4* __restrict__ p, si
 
 // ---------------------------------------------------------------- launchers
 hipError_t launch_mas(const KParams& p, hipStream_t stream) {
-  const dim3 grid((unsigned)(p.B * p.NB)), block(kThreads);
+  const dim3 grid((unsigned)(p.B * p.NB + (p.path ? p.B * kPathParts : 0))), block(kThreads);
   const bool aligned = (p.S % 4 == 0) && ((uintptr_t)p.value % 16 == 0);
   if (aligned)
     hipLaunchKernelGGL(mas_kernel<true>, grid, block, 0, stream, p);

@@ -33,6 +33,10 @@ __host__ __device__ constexpr int dec_bit(int j) { return 31 - (j % kChunk); }
 // Q[63g+62][j] (its last row) for every column j it computes as one 64-bit word
 // {low: fp32 bits, high: tag}.  The tag identifies the call (see WsHeader),
 // so stale words from earlier calls are never mistaken for fresh ones.
+// Path-writer workgroups per item (the dense path of an item is written by
+// this many workgroups once its row_start table is published).
+constexpr int kPathParts = 8;
+
 struct WsHeader {
   uint32_t gen;         // call generation; tag of a call = 2 * gen + 1
   uint32_t exit_count;  // workgroups that finished the current call
@@ -49,7 +53,7 @@ struct Layout {
   int32_t NB;      // workgroups per item = ceil(NW / 4)
   int32_t NC;      // decision chunks per item = ceil(S / 32)
   int32_t TP;      // decision words per chunk of an item (rows + scratch, multiple of 64)
-  size_t off_done;   // uint32 [B][NW] sweep-finished flags, then [B][NW] path-rows-cleared flags (tag values)
+  size_t off_done;   // uint32 [B][NW] sweep-finished flags, then [B] row_start-published flags (tag values)
   size_t off_slots;  // uint64 [B][NW][NC*32] boundary hand-off words
   size_t off_dec;    // uint32 [B][NC][TP] decision words
   size_t off_rs;     // int32  [B][T+1] row_start table (mas_forward_ex)
@@ -67,13 +71,13 @@ __host__ inline bool make_layout(int32_t B, int32_t T, int32_t S, Layout* L) {
   L->NC = (S + kChunk - 1) / kChunk;
   L->TP = (int32_t)round_up((size_t)L->NW * kRowsPerWave + 1, kWave);
   // Overflow guard: every product below stays far under 2^62 when these hold.
-  if ((uint64_t)B * (uint64_t)L->NB > 0x7fffffffull) return false;  // grid size
+  if ((uint64_t)B * (uint64_t)(L->NB + kPathParts) > 0x7fffffffull) return false;  // grid size
   if ((uint64_t)B * (uint64_t)T * (uint64_t)S > (1ull << 46)) return false;
   // One item's value slab is addressed with signed 32-bit byte offsets.
   if ((uint64_t)T * (uint64_t)S * 4u >= (1ull << 31)) return false;
   size_t off = sizeof(WsHeader);
   L->off_done = off;
-  off = round_up(off + 2 * (size_t)B * L->NW * sizeof(uint32_t), kAlign);
+  off = round_up(off + (size_t)B * (L->NW + 1) * sizeof(uint32_t), kAlign);
   L->off_slots = off;
   off = round_up(off + (size_t)B * L->NW * (size_t)L->NC * kChunk * sizeof(uint64_t), kAlign);
   L->off_dec = off;
