@@ -28,7 +28,7 @@ static mas_status run(const float* value, const int32_t* t_x, const int32_t* t_y
   p.path = path;
   p.hdr = reinterpret_cast<WsHeader*>(base);
   p.done = reinterpret_cast<uint32_t*>(base + L.off_done);
-  p.walked = p.done + (size_t)L.B * L.NW;
+  p.order = reinterpret_cast<uint64_t*>(base + L.off_order);
   p.slots = reinterpret_cast<uint64_t*>(base + L.off_slots);
   p.dec = reinterpret_cast<uint32_t*>(base + L.off_dec);
   p.B = L.B;
@@ -38,6 +38,7 @@ static mas_status run(const float* value, const int32_t* t_x, const int32_t* t_y
   p.NC = L.NC;
   p.TP = L.TP;
   p.NB = L.NB;
+  p.ntile = (L.T + kPathTileRows - 1) / kPathTileRows;
   p.path16 = path && (L.S % 16 == 0) && ((uintptr_t)path % 16 == 0);
   return launch_mas(p, stream) == hipSuccess ? MAS_OK : MAS_ERR_HIP;
 }

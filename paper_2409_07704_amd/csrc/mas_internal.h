@@ -19,10 +19,11 @@ struct KParams {
   uint8_t* path;        // nullable [B][T][S]; null: no path is written
   WsHeader* hdr;
   uint32_t* done;       // [B][NW] sweep finished (decision words published)
-  uint32_t* walked;     // [B] row_start published (tag values)
+  uint64_t* order;      // [B] items in the order their row_start tables were published: tag << 32 | item
   uint64_t* slots;      // [B][NW][NC*32]
   uint32_t* dec;        // [B][NC][TP] decision words, row-indexed
   int32_t B, T, S, NW, NC, TP, NB;
+  int32_t ntile;        // path tiles per item: ceil(T / kPathTileRows)
   int32_t path16;       // path 16-byte aligned and S % 16 == 0
 };
 

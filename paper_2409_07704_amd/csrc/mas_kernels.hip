@@ -20,14 +20,16 @@
 // The sweep wave holding row t_x-1 walks the decision words back from
 // (t_x-1, t_y-1) once every wave of the item has published them, while the
 // four loaders of its workgroup stage the decision words of upcoming chunks
-// in LDS, and publishes the item's row_start table.  Path-writer workgroups,
-// last in the grid, then write the item's dense path from that table, every
-// byte once (zeros and ones in one pass).
+// in LDS, and publishes the item's row_start table, appending the item to the
+// call's completion order.  Path-writer workgroups, last in the grid, take
+// tiles of 64 rows of one item from a shared counter in that order and write
+// them from the table, every byte once (zeros and ones in one pass): an item
+// that finishes late is written by many workgroups at once.
 //
 // Every wait is bounded, and a wave only waits on waves of its own workgroup
 // or of workgroups with lower ids, which the hardware dispatches first:
-// workgroup (band r, item b) has id r * B + b, and path writer (part k, item
-// b) has id B * NB + k * B + b.
+// workgroup (band r, item b) has id r * B + b, and the path writers have the
+// ids from B * NB on.
 //
 // Memory ordering across workgroups: data handed between workgroups (decision
 // words, boundary words, row_start, flags) is written with device-scope
@@ -125,6 +127,7 @@ struct SweepLds {
   i32x4 wready;                 // window loader k: its windows of chunks >= wready[k] are in LDS
   f32x4 sink[kWavesPerBlock][kChunk / 4 + 1];  // target of hand-offs nobody reads (a fixed LDS op count per step)
   long long wpos;               // walker position (walk_pos), or -1 once the walk is over
+  int tile;                     // path writer: the tile taken next
 };
 static_assert(sizeof(SweepLds) <= 160 * 1024, "LDS");
 
@@ -1001,13 +1004,20 @@ __device__ __forceinline__ void walk(const KParams& p, SweepLds& L, int tx, int 
       __builtin_amdgcn_s_sleep(1);
     }
   };
+  // First rows of the window slots (lane k: slot k), read once the block's
+  // windows are staged: the chunk loop reads nothing from LDS but the words.
+  int wlo_v = 0;
+  auto read_wlo = [&]() __attribute__((always_inline)) {
+    if (banded) wlo_v = lds_load(&L.wlo[min(lane, kNWin - 1)]);
+  };
   // Word of row e - lane from window slot sl (clamped into the window).
   auto row_word = [&](int sl, int e) __attribute__((always_inline)) -> uint32_t {
-    const int r = e - lane - (banded ? lds_load(&L.wlo[sl]) : 0);
+    const int r = e - lane - (banded ? __builtin_amdgcn_readlane(wlo_v, sl) : 0);
     return L.u.walk.win[sl][min(max(r, 0), kWinRows - 1)];
   };
   if (idx > 0) {
     ensure(cw);
+    read_wlo();
     uint32_t Wa = row_word(slot, idx), Wb = 0;
     uint32_t rec_pm = 0;  // lane k: steps of chunk (64-aligned base) + k
     int rec_e = 0;        // lane k: its entry row
@@ -1016,8 +1026,10 @@ __device__ __forceinline__ void walk(const KParams& p, SweepLds& L, int tx, int 
     // One chunk on the words in Wc, the next chunk's read into Wn; false once
     // the walk is over or the chunk was the last of its block.
     auto chunk = [&](uint32_t& Wc, uint32_t& Wn) __attribute__((always_inline)) -> bool {
-      const int nslot = slot == 0 ? kNWin - 1 : slot - 1;
-      if (cw > 0) Wn = row_word(nslot, idx);
+      const int nslot = uni(slot == 0 ? kNWin - 1 : slot - 1);
+      // (also read past chunk 0, unused: a conditional read would make the
+      // compiler wait for every LDS read in flight where the paths join)
+      Wn = row_word(nslot, idx);
       __builtin_amdgcn_sched_barrier(0);
       // (readfirstlane: the compiler treats asm results as per-lane values)
       const uint32_t pm = (uint32_t)uni((int)walk_chunk(Wc, Wc >> 1, uni(off), uni(q0)));
@@ -1041,6 +1053,7 @@ __device__ __forceinline__ void walk(const KParams& p, SweepLds& L, int tx, int 
     while (more) {
       lds_put64(lds_off(&L.wpos), walk_pos(cw, idx));
       ensure(max((cw & ~7) - 1, 0));
+      read_wlo();
       bool in_b = false;  // the next chunk's words are in Wb
 #pragma unroll
       for (int k = 0; k < 4; ++k) {
@@ -1064,23 +1077,15 @@ __device__ __forceinline__ void walk(const KParams& p, SweepLds& L, int tx, int 
 }
 
 // ---------------------------------------------------------------- path writer
-// The dense path of item b (Sec. 2: the alignment as a 0/1 matrix of the
-// input's size) from its published row_start table: row i holds ones at
-// columns [rs[i], rs[i+1]) and zeros elsewhere (rows t_x .. T-1 and invalid
-// items: all zeros).  kPathParts workgroups per item each write a contiguous
-// share of the rows once the item's walker has published, each wave an
-// eighth of that share.  path16: per row, zero pieces by plain 16-byte
-// stores (the pieces holding ones are skipped: offset past the resource),
-// then the few pieces holding ones; otherwise bytes.  (Bounds are clamped to
-// the row: the table is read back from memory, never trusted blindly.)
-__device__ __forceinline__ void path_writer(const KParams& p, int k, uint32_t tag, int wv, int lane, bool& timed_out) {
-  const int b = k % p.B, part = k / p.B;
-  constexpr int kWaves = kThreads / kWave;
-  const int q0 = (int)((int64_t)p.T * part / kPathParts), q1 = (int)((int64_t)p.T * (part + 1) / kPathParts);
-  const int per = (q1 - q0 + kWaves - 1) / kWaves;
-  const int r0 = min(q0 + wv * per, q1), r1 = min(r0 + per, q1);
-  if (r1 <= r0) return;
-  wait_flags(p.walked + b, 1, tag, lane, timed_out);
+// Rows [r0, r1) of the dense path of item b (Sec. 2: the alignment as a 0/1
+// matrix of the input's size) from its published row_start table: row i
+// holds ones at columns [rs[i], rs[i+1]) and zeros elsewhere (rows t_x .. T-1
+// and invalid items: all zeros).  path16: per row, zero pieces by plain
+// 16-byte stores (the pieces holding ones are skipped: offset past the
+// resource), then the few pieces holding ones; otherwise bytes.  (Bounds are
+// clamped to the row: the table is read back from memory, never trusted
+// blindly.)
+__device__ __forceinline__ void write_path_rows(const KParams& p, int b, int r0, int r1, int lane) {
   const uint32_t* const rs = reinterpret_cast<const uint32_t*>(p.row_start) + (size_t)b * ((size_t)p.T + 1);
   uint8_t* const item_path = p.path + (size_t)b * (size_t)p.T * (size_t)p.S;
   const __amdgpu_buffer_rsrc_t r = make_cursor(item_path, (uint64_t)p.T * p.S).rsrc();
@@ -1108,7 +1113,66 @@ __device__ __forceinline__ void path_writer(const KParams& p, int k, uint32_t ta
   }
 }
 
+// The item published k-th in this call (its entry in the completion order
+// carries the call's tag), or -1 once the bounded wait times out.
+__device__ __forceinline__ int wait_published(const KParams& p, int k, uint32_t tag, bool& timed_out) {
+  int spins = 0;
+  for (;;) {
+    const uint64_t e = __hip_atomic_load(p.order + k, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if ((uint32_t)(e >> 32) == tag) {
+      const int b = (int)(uint32_t)e;
+      return b < p.B ? b : -1;
+    }
+    if (timed_out || ++spins > kSpinLimit) {
+      timed_out = true;
+      return -1;
+    }
+    __builtin_amdgcn_s_sleep(2);
+  }
+}
+
+// A path-writer workgroup: takes tile t = (k, part) from the shared counter,
+// rows [64 part, 64 part + 64) of the item published k-th, waits for that
+// item, writes the tile (each wave an eighth of its rows) and goes on until
+// the tiles run out.  The next tile is taken while this one is written.
+__device__ __forceinline__ void path_writer(const KParams& p, SweepLds& L, uint32_t tag, int wv, int lane, bool& timed_out) {
+  constexpr int kWaves = kThreads / kWave;
+  const int ntiles = p.B * p.ntile;
+  if (threadIdx.x == 0)
+    L.tile = (int)__hip_atomic_fetch_add(&p.hdr->tile_next, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  __syncthreads();
+  int t = L.tile;
+  while (t < ntiles) {
+    __syncthreads();  // every wave has read L.tile
+    uint32_t next = 0;
+    if (threadIdx.x == 0)
+      next = __hip_atomic_fetch_add(&p.hdr->tile_next, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    const int k = t / p.ntile, part = t - k * p.ntile;
+    const int q0 = part * kPathTileRows, q1 = min(q0 + kPathTileRows, p.T);
+    const int per = (q1 - q0 + kWaves - 1) / kWaves;
+    const int r0 = min(q0 + wv * per, q1), r1 = min(r0 + per, q1);
+    if (r1 > r0) {
+      const int b = wait_published(p, k, tag, timed_out);
+      if (b >= 0) write_path_rows(p, b, r0, r1, lane);
+    }
+    if (threadIdx.x == 0) L.tile = (int)next;
+    __syncthreads();
+    t = L.tile;
+  }
+}
+
 // ---------------------------------------------------------------- roles
+// Item b's row_start table is complete once this wave's stores have landed:
+// append b to the call's completion order, which the path writers follow.
+__device__ __forceinline__ void publish_item(const KParams& p, int b, uint32_t tag, int lane) {
+  vm_wait<0>();
+  if (lane == 0) {
+    const uint32_t k = __hip_atomic_fetch_add(&p.hdr->walk_count, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (k < (uint32_t)p.B)
+      __hip_atomic_store(p.order + k, ((uint64_t)tag << 32) | (uint32_t)b, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  }
+}
+
 // The workgroup of the wave holding row t_x-1 walks the item: that wave walks
 // and publishes row_start, the workgroup's four loaders stage the decision
 // windows.
@@ -1139,8 +1203,7 @@ __device__ __forceinline__ void sweep_role(const KParams& p, SweepLds& L, const 
   walk(p, L, x.tx, x.ty, lane, timed_out);
   int32_t* rs_out = p.row_start + (size_t)b * ((size_t)p.T + 1);
   for (int i = lane; i <= p.T; i += kWave) st_dev(reinterpret_cast<uint32_t*>(rs_out + i), (uint32_t)L.u.walk.rs[i]);
-  vm_wait<0>();
-  if (lane == 0) st_dev(p.walked + b, tag);
+  publish_item(p, b, tag, lane);
 }
 
 template <bool ALIGNED>
@@ -1164,12 +1227,12 @@ __device__ __forceinline__ void invalid_item(const KParams& p, int b, int g, boo
     if (p.status) p.status[b] = st;
   }
   // The path writers write the all-zero slab from this table.
-  vm_wait<0>();
-  if (lane == 0) st_dev(p.walked + b, tag);
+  publish_item(p, b, tag, lane);
 }
 
-// The last workgroup of the call to finish advances the generation (one
-// counter update per workgroup: updates of one word serialise).
+// The last workgroup of the call to finish clears the call's counters and
+// advances the generation (one counter update per workgroup: updates of one
+// word serialise).
 __device__ __forceinline__ void finish_call(const KParams& p, uint32_t gen) {
   vm_wait<0>();
   __syncthreads();
@@ -1177,6 +1240,8 @@ __device__ __forceinline__ void finish_call(const KParams& p, uint32_t gen) {
     const uint32_t total = gridDim.x;
     const uint32_t prev = __hip_atomic_fetch_add(&p.hdr->exit_count, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     if (prev == total - 1) {
+      __hip_atomic_store(&p.hdr->walk_count, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      __hip_atomic_store(&p.hdr->tile_next, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       __hip_atomic_store(&p.hdr->exit_count, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       __hip_atomic_store(&p.hdr->gen, gen + 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }
@@ -1193,7 +1258,7 @@ __global__ void __launch_bounds__(kThreads, 1) mas_kernel(KParams p) {
   const int sid = blockIdx.x;
   if (sid >= p.B * p.NB) {
     // A path writer.
-    path_writer(p, sid - p.B * p.NB, tag, uni(threadIdx.x / kWave), threadIdx.x & (kWave - 1), timed_out);
+    path_writer(p, L, tag, uni(threadIdx.x / kWave), threadIdx.x & (kWave - 1), timed_out);
     if (timed_out) __hip_atomic_store(&p.hdr->error, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     finish_call(p, gen);
     return;
@@ -1279,7 +1344,8 @@ __global__ void __launch_bounds__(256) mas_zero_kernel(uint4* __restrict__ p, si
 
 // ---------------------------------------------------------------- launchers
 hipError_t launch_mas(const KParams& p, hipStream_t stream) {
-  const dim3 grid((unsigned)(p.B * p.NB + (p.path ? p.B * kPathParts : 0))), block(kThreads);
+  const int writers = p.path ? min(p.B * p.ntile, kPathWorkgroups) : 0;
+  const dim3 grid((unsigned)(p.B * p.NB + writers)), block(kThreads);
   const bool aligned = (p.S % 4 == 0) && ((uintptr_t)p.value % 16 == 0);
   if (aligned)
     hipLaunchKernelGGL(mas_kernel<true>, grid, block, 0, stream, p);

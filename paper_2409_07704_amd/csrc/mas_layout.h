@@ -33,15 +33,19 @@ __host__ __device__ constexpr int dec_bit(int j) { return 31 - (j % kChunk); }
 // Q[63g+62][j] (its last row) for every column j it computes as one 64-bit word
 // {low: fp32 bits, high: tag}.  The tag identifies the call (see WsHeader),
 // so stale words from earlier calls are never mistaken for fresh ones.
-// Path-writer workgroups per item (the dense path of an item is written by
-// this many workgroups once its row_start table is published).
-constexpr int kPathParts = 8;
+// Dense path: written in tiles of kPathTileRows rows of one item, taken in
+// the order the items' row_start tables are published, by at most
+// kPathWorkgroups path-writer workgroups (one per CU of the MI355X).
+constexpr int kPathTileRows = 64;
+constexpr int kPathWorkgroups = 256;
 
 struct WsHeader {
   uint32_t gen;         // call generation; tag of a call = 2 * gen + 1
   uint32_t exit_count;  // workgroups that finished the current call
   uint32_t error;       // sticky: non-zero once a device-side wait timed out
-  uint32_t pad[61];
+  uint32_t walk_count;  // row_start tables published in the current call
+  uint32_t tile_next;   // path tiles taken in the current call
+  uint32_t pad[59];
 };
 static_assert(sizeof(WsHeader) == kAlign, "header is one alignment unit");
 
@@ -53,7 +57,8 @@ struct Layout {
   int32_t NB;      // workgroups per item = ceil(NW / 4)
   int32_t NC;      // decision chunks per item = ceil(S / 32)
   int32_t TP;      // decision words per chunk of an item (rows + scratch, multiple of 64)
-  size_t off_done;   // uint32 [B][NW] sweep-finished flags, then [B] row_start-published flags (tag values)
+  size_t off_done;   // uint32 [B][NW] sweep-finished flags (tag values)
+  size_t off_order;  // uint64 [B] items in the order their row_start tables were published: tag << 32 | item
   size_t off_slots;  // uint64 [B][NW][NC*32] boundary hand-off words
   size_t off_dec;    // uint32 [B][NC][TP] decision words
   size_t off_rs;     // int32  [B][T+1] row_start table (mas_forward_ex)
@@ -71,13 +76,15 @@ __host__ inline bool make_layout(int32_t B, int32_t T, int32_t S, Layout* L) {
   L->NC = (S + kChunk - 1) / kChunk;
   L->TP = (int32_t)round_up((size_t)L->NW * kRowsPerWave + 1, kWave);
   // Overflow guard: every product below stays far under 2^62 when these hold.
-  if ((uint64_t)B * (uint64_t)(L->NB + kPathParts) > 0x7fffffffull) return false;  // grid size
+  if ((uint64_t)B * (uint64_t)L->NB + kPathWorkgroups > 0x7fffffffull) return false;  // grid size
   if ((uint64_t)B * (uint64_t)T * (uint64_t)S > (1ull << 46)) return false;
   // One item's value slab is addressed with signed 32-bit byte offsets.
   if ((uint64_t)T * (uint64_t)S * 4u >= (1ull << 31)) return false;
   size_t off = sizeof(WsHeader);
   L->off_done = off;
-  off = round_up(off + (size_t)B * (L->NW + 1) * sizeof(uint32_t), kAlign);
+  off = round_up(off + (size_t)B * L->NW * sizeof(uint32_t), kAlign);
+  L->off_order = off;
+  off = round_up(off + (size_t)B * sizeof(uint64_t), kAlign);
   L->off_slots = off;
   off = round_up(off + (size_t)B * L->NW * (size_t)L->NC * kChunk * sizeof(uint64_t), kAlign);
   L->off_dec = off;

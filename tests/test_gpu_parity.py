@@ -149,6 +149,33 @@ def test_full_length_batch(mas):
     assert_parity(mas, value, tx, ty, "full-length-b64-t1024-s4096")
 
 
+def test_long_items(mas):
+    """Long speech axes: a backtrack over hundreds of chunks with banded
+    decision windows (T above the window height), a path pinned to the last
+    diagonal by a ridge of high values, and lengths around 1024 chunks with
+    the walking wave last in its workgroup (t_x 190 and 252)."""
+    st = synth.Stream(91)
+    B, T, S = 3, 1500, 9000
+    value = st.normal_f32(B * T * S).reshape(B, T, S) * np.float32(4.0) - np.float32(2.0)
+    assert_parity(mas, value, np.array([1500, 1200, 700], np.int32), np.array([9000, 8500, 6000], np.int32),
+                  "long-banded")
+
+    B, T, S = 2, 300, 5000
+    tx = np.array([300, 250], np.int32)
+    ty = np.array([5000, 4990], np.int32)
+    value = st.normal_f32(B * T * S).reshape(B, T, S) * np.float32(0.1)
+    for b in range(B):
+        i = np.arange(tx[b])
+        value[b, i, i + (ty[b] - tx[b])] += np.float32(50.0)
+    assert_parity(mas, value, tx, ty, "long-ridge")
+
+    B, T, S = 6, 256, 32800
+    tx = np.array([256, 190, 2, 1, 252, 200], np.int32)
+    ty = np.array([32768, 32769, 992, 993, 1024, 32800], np.int32)
+    value = st.normal_f32(B * T * S).reshape(B, T, S) * np.float32(4.0) - np.float32(2.0)
+    assert_parity(mas, value, tx, ty, "long-1024-chunks")
+
+
 def test_unaligned_value_pointer(mas):
     value, tx, ty = synth.generate("tts-b16-t128-s512")
     B, T, S = value.shape
