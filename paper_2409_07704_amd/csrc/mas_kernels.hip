@@ -509,9 +509,9 @@ __device__ __forceinline__ f32x4 gather_last_row(const float (&q)[kChunk]) {
 // Sweeps the wave's rows over its chunks and returns the score candidate
 // (Q at (row, t_y-1) of this lane; only meaningful for the wave holding row
 // t_x-1).  IN: where the row above the wave comes from — 0 nowhere (the wave
-// holds row 0: -inf), 1 the previous wave of the workgroup (its slots, with
-// tags), 2 the global boundary words of the previous workgroup (polled by
-// this wave one chunk ahead and copied into its own slots).  OUT: 0 no
+// holds row 0: -inf), 1 the wave's slots and prod mailbox, filled by the
+// previous wave of the workgroup or, for wave 0 of a later workgroup, by its
+// loader from the previous workgroup's global boundary words.  OUT: 0 no
 // consumer, 1 the next wave of the workgroup, 2 global boundary words for the
 // next workgroup.
 //
@@ -521,7 +521,7 @@ __device__ __forceinline__ f32x4 gather_last_row(const float (&q)[kChunk]) {
 // waits when the tile or the boundary row of chunk c+1 was not there yet.
 template <int IN, int OUT>
 __device__ __forceinline__ float sweep_wave(const KParams& p, SweepLds& L, const WaveCtx& x, uint32_t tag, bool& timed_out) {
-  constexpr bool IN1 = IN == 1, IN2 = IN == 2;
+  constexpr bool IN1 = IN == 1;
   const int lane = x.lane, w = x.w;
   float t = -0.0f;  // lane 0 keeps -0 for the whole sweep (see cols8)
   char* const Lc = reinterpret_cast<char*>(&L);
@@ -551,36 +551,11 @@ __device__ __forceinline__ float sweep_wave(const KParams& p, SweepLds& L, const
       make_cursor(p.dec + (size_t)x.b * p.NC * (size_t)p.TP, (uint64_t)p.NC * p.TP * 4u).rsrc();
   const int dvo = 4 * (lane > 0 ? x.row : p.TP - 1);
   const int dstride = p.TP * 4;
-  // Global boundary words: this wave's (OUT2) and the previous wave's (IN2):
-  // word 32c + j = {Q of the wave's last row at column 32c + j, tag}.
+  // Global boundary words of this wave (OUT2): word 32c + j = {Q of the
+  // wave's last row at column 32c + j, tag}.
   const size_t slot_words = (size_t)p.NC * kChunk;
   const __amdgpu_buffer_rsrc_t sr =
       make_cursor(p.slots + ((size_t)x.b * p.NW + x.g) * slot_words, slot_words * 8u).rsrc();
-  const uint64_t* const pslots = p.slots + ((size_t)x.b * p.NW + (x.g > 0 ? x.g - 1 : 0)) * slot_words;
-
-  // IN2: the boundary words of chunk c (256 bytes: lane l < 32 loads column
-  // 32c + l; lanes 32..63 load the same words again).  A device-scope load
-  // issued one step before the words are needed; when their tags are not all
-  // this call's, the wave loads them again until they are.  Then lanes 0..31
-  // write the values into the chunk's slot.
-  uint64_t pw = 0;
-  auto poll = [&](int c) __attribute__((always_inline)) {
-    pw = __hip_atomic_load(pslots + (size_t)c * kChunk + (lane & (kChunk - 1)), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-  };
-  // (The reload waits for itself inside the assembly and writes pw in place,
-  // so the usual path keeps a single wait for the poll of the step before.)
-  auto deliver = [&](int c, int k) __attribute__((always_inline)) {
-    const uint64_t* const src = pslots + (size_t)c * kChunk + (lane & (kChunk - 1));
-    int spins = 0;
-    while (!timed_out) {
-      uint64_t stale = __builtin_amdgcn_ballot_w64((uint32_t)(pw >> 32) != tag);
-      asm volatile("" : "+s"(stale));
-      if (stale == 0) break;
-      if (++spins > kSpinLimit) timed_out = true;
-      asm volatile("global_load_dwordx2 %0, %1, off sc1\n\ts_waitcnt vmcnt(0)" : "+v"(pw) : "v"(src) : "memory");
-    }
-    if (lane < kChunk) bound_ptr(k)[lane] = __uint_as_float((uint32_t)pw);
-  };
 
   if (IN == 0) {
     // The row above row 0 is -inf in every slot.
@@ -594,12 +569,7 @@ __device__ __forceinline__ float sweep_wave(const KParams& p, SweepLds& L, const
   // last row there (its chunk c_begin-1, always computed), or -inf.  It
   // sits in slot kRing-1 (chunk c_begin-1).
   float q = neg_inf();
-  if (IN1) {
-    wait_at_least(my_box + 1, x.c_begin, timed_out);
-  } else if (IN2) {
-    poll(x.c_begin - 1);
-    deliver(x.c_begin - 1, kRing - 1);
-  }
+  if (IN1) wait_at_least(my_box + 1, x.c_begin, timed_out);
   if (IN != 0) {
     wave_lds_sync();
     const float e = bound_ptr(kRing - 1)[kChunk - 1];
@@ -612,13 +582,7 @@ __device__ __forceinline__ float sweep_wave(const KParams& p, SweepLds& L, const
   // register sets by ring position: chunk c uses set (c - c_begin) % 2.
   f32x4 va[8], vb[8];
   wait_at_least(my_box + 0, x.c_begin + 1, timed_out);
-  if (IN1 && x.c_begin < x.prev_end) {
-    wait_at_least(my_box + 1, x.c_begin + 1, timed_out);
-  } else if (IN2 && x.c_begin < x.prev_end) {
-    poll(x.c_begin);
-    deliver(x.c_begin, 0);
-    if (x.c_begin + 1 < x.prev_end) poll(x.c_begin + 1);
-  }
+  if (IN1 && x.c_begin < x.prev_end) wait_at_least(my_box + 1, x.c_begin + 1, timed_out);
   int cons_seen;  // the consumer's progress as last read (OUT1)
   {
     // (Through the same inline-assembly reads as the loop: values the
@@ -669,12 +633,6 @@ __device__ __forceinline__ float sweep_wave(const KParams& p, SweepLds& L, const
     constexpr int J1 = (J + 1) & (kRing - 1);
     const bool has_next = c + 1 < x.c_end;
     const bool need_prod = IN1 && c + 1 < x.prev_end;
-    // IN2: the boundary row of chunk c+1 into slot J1, and the poll of chunk
-    // c+2 (used at the next step).
-    if (IN2 && has_next && c + 1 < x.prev_end) {
-      deliver(c + 1, J1);
-      if (c + 2 < x.prev_end) poll(c + 2);
-    }
     // Reads of chunk c+1, in flight during the compute of chunk c: the
     // mailbox first, then the values (one LDS queue per wave: in order).
     // After the last chunk they read the next slot's stale contents, unused.
@@ -760,8 +718,18 @@ __device__ __forceinline__ int start_delay(const KParams& p, int b, int lane) {
 // (L % 8) ^ swz(row), so each load covers eight 128-byte row segments and
 // lands as eight contiguous swizzled LDS rows; up to kRing tiles in flight.
 // Otherwise 4-byte loads of the same layout, one tile in flight.
-template <bool ALIGNED>
-__device__ __forceinline__ void load_tiles(const KParams& p, SweepLds& L, const WaveCtx& x, bool& timed_out) {
+//
+// BOUND (the loader of wave 0 of every workgroup but an item's first): the
+// sweep wave's boundary rows too.  The previous workgroup's last wave
+// publishes Q of its last row as {value, tag} words in global memory; the
+// loader polls two chunks per device-scope load, and once a chunk's 32 words
+// all carry this call's tag and its ring slot is free, moves the values into
+// the slot's boundary row and raises the sweep wave's prod, as a wave of the
+// same workgroup would.  So the sweep wave waits on LDS only: none of its
+// steps waits for a global load (which would also wait for its own
+// write-through stores).
+template <bool ALIGNED, bool BOUND>
+__device__ __forceinline__ void load_tiles(const KParams& p, SweepLds& L, const WaveCtx& x, uint32_t tag, bool& timed_out) {
   const int lane = x.lane, w = x.w;
   const float* slab = p.value + (size_t)x.b * (size_t)p.T * (size_t)p.S;
   const uint64_t slab_bytes = (uint64_t)p.T * (uint64_t)p.S * 4u;
@@ -787,7 +755,14 @@ __device__ __forceinline__ void load_tiles(const KParams& p, SweepLds& L, const 
   const int* const progress = w > 0 ? reinterpret_cast<const int*>(&L.box[w - 1]) + 2 : &L.cons0;
   const uint32_t ready_addr = lds_off(&L.box[w]);
   int cons = x.c_begin - 1;
-  while (readied < x.c_end && !timed_out) {
+  // BOUND: chunks bnext .. bend-1 still to deliver (from c_begin-1, which the
+  // previous wave always computes).
+  int bnext = x.c_begin - 1;
+  const int bend = BOUND ? x.prev_end : bnext;
+  const uint64_t* const bsrc = p.slots + ((size_t)x.b * p.NW + (x.g > 0 ? x.g - 1 : 0)) * ((size_t)p.NC * kChunk);
+  const uint32_t prod_addr = lds_off(&L.box[w]) + 4u;
+  int bspins = 0;
+  while ((readied < x.c_end || bnext < bend) && !timed_out) {
     // Issue while slots are free (the slot of chunk c held chunk c-4).
     while (issued < x.c_end && issued - readied < kInflight) {
       if (issued > cons + kRing - 1) {
@@ -814,9 +789,42 @@ __device__ __forceinline__ void load_tiles(const KParams& p, SweepLds& L, const 
         while (wall_clock64() < until) __builtin_amdgcn_s_sleep(127);
       }
     }
+    if (BOUND && bnext < bend) {
+      if (bnext > cons + kRing - 1) cons = uni(lds_load(progress));
+      if (bnext <= cons + kRing - 1) {
+        // Lane l polls column l % 32 of chunk bnext + l / 32 (the last
+        // chunk again past the end); the wait covers the tiles in flight.
+        const int c0 = bnext;
+        const uint64_t wv = __hip_atomic_load(bsrc + (size_t)min(c0 + (lane >> 5), bend - 1) * kChunk + (lane & (kChunk - 1)),
+                                              __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        vm_wait<0>();
+        if (readied < issued) {
+          readied = issued;
+          lds_put(ready_addr, readied);
+        }
+        const uint64_t stale = __builtin_amdgcn_ballot_w64((uint32_t)(wv >> 32) != tag);
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+          const int c = c0 + h;
+          if (bnext != c || c >= bend || c > cons + kRing - 1 || (uint32_t)(stale >> (kChunk * h)) != 0u) break;
+          float* const brow = reinterpret_cast<float*>(reinterpret_cast<char*>(&L.u.ring[w][0]) +
+                                                       ((c - x.c_begin) & (kRing - 1)) * kSlotStride + kBoundOff);
+          if ((lane >> 5) == h) brow[lane & (kChunk - 1)] = __uint_as_float((uint32_t)wv);
+          lds_put(prod_addr, c + 1);
+          ++bnext;
+        }
+        if (bnext == c0) {
+          // Not published yet.
+          if (++bspins > kSpinLimit) timed_out = true;
+          __builtin_amdgcn_s_sleep(1);
+        }
+        continue;
+      }
+    }
     if (issued == readied) {
       // Nothing in flight and no free slot: wait for the sweep wave.
-      cons = wait_at_least(progress, issued - (kRing - 1), timed_out);
+      const int need = BOUND && bnext < bend ? min(issued, bnext) : issued;
+      cons = wait_at_least(progress, need - (kRing - 1), timed_out);
       continue;
     }
     // The oldest tile in flight has landed once at most the younger ones
@@ -1186,11 +1194,9 @@ __device__ __forceinline__ void sweep_role(const KParams& p, SweepLds& L, const 
   if (g == 0 && lane == 0 && p.status) p.status[b] = kItemOk;
   float score;
   if (g == g_last) {
-    score = g == 0 ? sweep_wave<0, 0>(p, L, x, tag, timed_out)
-                   : (w > 0 ? sweep_wave<1, 0>(p, L, x, tag, timed_out) : sweep_wave<2, 0>(p, L, x, tag, timed_out));
+    score = g == 0 ? sweep_wave<0, 0>(p, L, x, tag, timed_out) : sweep_wave<1, 0>(p, L, x, tag, timed_out);
   } else if (w < kWavesPerBlock - 1) {
-    score = g == 0 ? sweep_wave<0, 1>(p, L, x, tag, timed_out)
-                   : (w > 0 ? sweep_wave<1, 1>(p, L, x, tag, timed_out) : sweep_wave<2, 1>(p, L, x, tag, timed_out));
+    score = g == 0 ? sweep_wave<0, 1>(p, L, x, tag, timed_out) : sweep_wave<1, 1>(p, L, x, tag, timed_out);
   } else {
     score = sweep_wave<1, 2>(p, L, x, tag, timed_out);
   }
@@ -1209,7 +1215,12 @@ __device__ __forceinline__ void sweep_role(const KParams& p, SweepLds& L, const 
 template <bool ALIGNED>
 __device__ __forceinline__ void loader_role(const KParams& p, SweepLds& L, const WaveCtx& x, uint32_t tag, bool& timed_out) {
   const int lane = x.lane, b = x.b, g = x.g, g_last = x.g_last;
-  if (g <= g_last) load_tiles<ALIGNED>(p, L, x, timed_out);
+  if (g <= g_last) {
+    if (g > 0 && x.w == 0)
+      load_tiles<ALIGNED, true>(p, L, x, tag, timed_out);
+    else
+      load_tiles<ALIGNED, false>(p, L, x, tag, timed_out);
+  }
   if (!walker_workgroup(x)) return;
   // Decision windows for the walk, once every wave of the item has published
   // its words.
