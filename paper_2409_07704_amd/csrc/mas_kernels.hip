@@ -296,28 +296,16 @@ __device__ __forceinline__ void cols8(float& q, float& t, uint32_t& bits, float 
   q = o[7];
 }
 
-// One column of the same step (for the chunks that cross the masked triangle).
-__device__ __forceinline__ float col1(float q, float& t, uint32_t& bits, float v) {
-  float o, u;
-  asm volatile("s_nop 1\n\t"
-      "v_max_f32_dpp %[t], %[q], %[q] wave_shr:1 row_mask:0xf bank_mask:0xf\n\t"
-      "v_add_f32 %[o], %[t], %[v]\n\t"
-      "v_sub_f32 %[u], %[q], %[t]\n\t"
-      "v_alignbit_b32 %[b], %[b], %[u], 31"
-      : [o] "=&v"(o), [t] "+v"(t), [b] "+v"(bits), [u] "=&v"(u)
-      : [q] "v"(q), [v] "v"(v));
-  return o;
-}
-
 // One 32-column chunk for lanes 1..63 (rows row0 + lane - 1) and the carried
 // row in lane 0.  v4: this lane's 32 values (lane 0: the row above's Q);
 // qc: Q of every column (out); bits: decisions, first column in bit 31.
-// MASKED: the chunk crosses the triangle i > j, where Q is -inf (lane 0's
-// copies already are), and holds the first cell Q[0][0] = value[0][0] when
-// j0 == 0.
-template <bool MASKED>
-__device__ __forceinline__ void sweep_chunk(float& q, float& t, const f32x4 (&v4)[8], float (&qc)[kChunk], uint32_t& bits,
-                                            int lane, int row, int j0) {
+// Cells of the triangle i > j hold -inf in the tile (the loader writes it
+// there): both predecessors of such a cell lie in the triangle too (lane 0's
+// copies of the row above are -inf there already), so its Q comes out
+// -inf + -inf = -inf, whatever the input held; decision bits of those cells
+// are never read.  (The first cell Q[0][0] = value[0][0] comes from row 0's
+// Q at column -1 being -0, see sweep_wave.)
+__device__ __forceinline__ void sweep_chunk(float& q, float& t, const f32x4 (&v4)[8], float (&qc)[kChunk], uint32_t& bits) {
   float v[kChunk];
 #pragma unroll
   for (int k = 0; k < 8; ++k) {
@@ -327,25 +315,12 @@ __device__ __forceinline__ void sweep_chunk(float& q, float& t, const f32x4 (&v4
     v[4 * k + 3] = v4[k].w;
   }
   uint32_t w = 0;
-  if (!MASKED) {
 #pragma unroll
-    for (int k = 0; k < 4; ++k) {
-      float o[8];
-      cols8(q, t, w, o, v + 8 * k);
+  for (int k = 0; k < 4; ++k) {
+    float o[8];
+    cols8(q, t, w, o, v + 8 * k);
 #pragma unroll
-      for (int m = 0; m < 8; ++m) qc[8 * k + m] = o[m];
-    }
-  } else {
-    const bool own = lane > 0;
-#pragma unroll
-    for (int m = 0; m < kChunk; ++m) {
-      const int j = j0 + m;
-      float qn = col1(q, t, w, v[m]);
-      qn = (own && row > j) ? neg_inf() : qn;
-      if (j == 0) qn = (own && row == 0) ? v[m] : qn;
-      qc[m] = qn;
-      q = qn;
-    }
+    for (int m = 0; m < 8; ++m) qc[8 * k + m] = o[m];
   }
   bits = w;
 }
@@ -567,8 +542,11 @@ __device__ __forceinline__ float sweep_wave(const KParams& p, SweepLds& L, const
 
   // Lane 0's Q at the column before the first chunk: the previous wave's
   // last row there (its chunk c_begin-1, always computed), or -inf.  It
-  // sits in slot kRing-1 (chunk c_begin-1).
-  float q = neg_inf();
+  // sits in slot kRing-1 (chunk c_begin-1).  Every other row's Q at the
+  // column before its first chunk is -inf, except row 0's at column -1: -0,
+  // so that the first cell comes out as -0 + value[0][0] = value[0][0]
+  // exactly (its predecessors are -inf and -0, their max -0).
+  float q = (IN == 0 && lane == 1) ? -0.0f : neg_inf();
   if (IN1) wait_at_least(my_box + 1, x.c_begin, timed_out);
   if (IN != 0) {
     wave_lds_sync();
@@ -641,10 +619,7 @@ __device__ __forceinline__ float sweep_wave(const KParams& p, SweepLds& L, const
     __builtin_amdgcn_sched_barrier(0);
 
     uint32_t bits = 0;
-    if (c < x.mask_end)
-      sweep_chunk<true>(q, t, vc, qc, bits, lane, x.row, c * kChunk);
-    else
-      sweep_chunk<false>(q, t, vc, qc, bits, lane, x.row, c * kChunk);
+    sweep_chunk(q, t, vc, qc, bits);
     __builtin_amdgcn_sched_barrier(0);
     hand_off(c);
     __builtin_amdgcn_raw_buffer_store_b32(bits, dr, dvo, soff, kPolicyDev);
@@ -712,8 +687,32 @@ __device__ __forceinline__ int start_delay(const KParams& p, int b, int lane) {
 }
 
 // ---------------------------------------------------------------- loader wave
+// The cells of the triangle i > j in the landed tile of chunk c of wave g
+// (slot at LDS byte address slot) become -inf: lane r rewrites tile row r
+// (item row 63g + r), whose columns 32c .. 32c + nm - 1 lie in the triangle:
+// whole pieces are overwritten, a piece cut by the diagonal is read and
+// written back.  Only the first chunks of a wave cross the triangle.
+__device__ __forceinline__ void mask_tile(uint32_t slot, int g, int c, int lane) {
+  const int nm = min(max(g * kRowsPerWave + lane - c * kChunk, 0), kChunk);
+  using lds_f4 = __attribute__((address_space(3))) f32x4;
+  const float ninf = neg_inf();
+  for (int pc = 0; 4 * pc < nm; ++pc) {
+    lds_f4* const a = (lds_f4*)(uintptr_t)(slot + (uint32_t)lane * 128u + 16u * (uint32_t)(pc ^ swz(lane)));
+    f32x4 v = {ninf, ninf, ninf, ninf};
+    if (4 * pc + 4 > nm) {
+      const f32x4 old = *a;
+      v.y = 4 * pc + 1 < nm ? ninf : old.y;
+      v.z = 4 * pc + 2 < nm ? ninf : old.z;
+      v.w = old.w;
+    }
+    *a = v;
+  }
+}
+
+
 // Value tiles of sweep wave w, chunks [c_begin, c_end), each into the slot
-// its sweep wave has handed back.  ALIGNED (value 16-byte aligned, S % 4 ==
+// its sweep wave has handed back; tiles that cross the triangle i > j get
+// -inf there (mask_tile) before they are published.  ALIGNED (value 16-byte aligned, S % 4 ==
 // 0): lane L of load k (k = 0..7) fetches tile row 8k + L/8, piece
 // (L % 8) ^ swz(row), so each load covers eight 128-byte row segments and
 // lands as eight contiguous swizzled LDS rows; up to kRing tiles in flight.
@@ -722,10 +721,10 @@ __device__ __forceinline__ int start_delay(const KParams& p, int b, int lane) {
 // BOUND (the loader of wave 0 of every workgroup but an item's first): the
 // sweep wave's boundary rows too.  The previous workgroup's last wave
 // publishes Q of its last row as {value, tag} words in global memory; the
-// loader polls two chunks per device-scope load, and once a chunk's 32 words
-// all carry this call's tag and its ring slot is free, moves the values into
-// the slot's boundary row and raises the sweep wave's prod, as a wave of the
-// same workgroup would.  So the sweep wave waits on LDS only: none of its
+// loader polls four chunks per round trip (two chunks per device-scope
+// load), and once a chunk's 32 words all carry this call's tag and its ring
+// slot is free, moves the values into the slot's boundary row and raises the
+// sweep wave's prod, as a wave of the same workgroup would.  So the sweep wave waits on LDS only: none of its
 // steps waits for a global load (which would also wait for its own
 // write-through stores).
 template <bool ALIGNED, bool BOUND>
@@ -792,24 +791,31 @@ __device__ __forceinline__ void load_tiles(const KParams& p, SweepLds& L, const 
     if (BOUND && bnext < bend) {
       if (bnext > cons + kRing - 1) cons = uni(lds_load(progress));
       if (bnext <= cons + kRing - 1) {
-        // Lane l polls column l % 32 of chunk bnext + l / 32 (the last
-        // chunk again past the end); the wait covers the tiles in flight.
+        // Lane l polls column l % 32 of chunks bnext + l / 32 (load A) and
+        // bnext + 2 + l / 32 (load B), the last chunk again past the end;
+        // the wait covers the tiles in flight.
         const int c0 = bnext;
-        const uint64_t wv = __hip_atomic_load(bsrc + (size_t)min(c0 + (lane >> 5), bend - 1) * kChunk + (lane & (kChunk - 1)),
-                                              __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        const uint64_t* const ba = bsrc + (lane & (kChunk - 1));
+        const uint64_t wa = __hip_atomic_load(ba + (size_t)min(c0 + (lane >> 5), bend - 1) * kChunk, __ATOMIC_RELAXED,
+                                              __HIP_MEMORY_SCOPE_AGENT);
+        const uint64_t wb = __hip_atomic_load(ba + (size_t)min(c0 + 2 + (lane >> 5), bend - 1) * kChunk, __ATOMIC_RELAXED,
+                                              __HIP_MEMORY_SCOPE_AGENT);
         vm_wait<0>();
         if (readied < issued) {
-          readied = issued;
+          for (; readied < issued; ++readied)
+            if (readied < x.mask_end) mask_tile(ring + (uint32_t)((readied - x.c_begin) & (kRing - 1)) * kSlotStride, x.g, readied, lane);
           lds_put(ready_addr, readied);
         }
-        const uint64_t stale = __builtin_amdgcn_ballot_w64((uint32_t)(wv >> 32) != tag);
+        const uint64_t stale_a = __builtin_amdgcn_ballot_w64((uint32_t)(wa >> 32) != tag);
+        const uint64_t stale_b = __builtin_amdgcn_ballot_w64((uint32_t)(wb >> 32) != tag);
 #pragma unroll
-        for (int h = 0; h < 2; ++h) {
+        for (int h = 0; h < 4; ++h) {
           const int c = c0 + h;
-          if (bnext != c || c >= bend || c > cons + kRing - 1 || (uint32_t)(stale >> (kChunk * h)) != 0u) break;
+          const uint64_t stale = h < 2 ? stale_a : stale_b;
+          if (bnext != c || c >= bend || c > cons + kRing - 1 || (uint32_t)(stale >> (kChunk * (h & 1))) != 0u) break;
           float* const brow = reinterpret_cast<float*>(reinterpret_cast<char*>(&L.u.ring[w][0]) +
                                                        ((c - x.c_begin) & (kRing - 1)) * kSlotStride + kBoundOff);
-          if ((lane >> 5) == h) brow[lane & (kChunk - 1)] = __uint_as_float((uint32_t)wv);
+          if ((lane >> 5) == (h & 1)) brow[lane & (kChunk - 1)] = __uint_as_float((uint32_t)(h < 2 ? wa : wb));
           lds_put(prod_addr, c + 1);
           ++bnext;
         }
@@ -830,6 +836,7 @@ __device__ __forceinline__ void load_tiles(const KParams& p, SweepLds& L, const 
     // The oldest tile in flight has landed once at most the younger ones
     // are outstanding.
     vm_wait_usual<kOps * (kInflight - 1)>(kOps * (issued - readied - 1));
+    if (readied < x.mask_end) mask_tile(ring + (uint32_t)((readied - x.c_begin) & (kRing - 1)) * kSlotStride, x.g, readied, lane);
     ++readied;
     lds_put(ready_addr, readied);
   }
@@ -1146,8 +1153,16 @@ __device__ __forceinline__ int wait_published(const KParams& p, int k, uint32_t 
 __device__ __forceinline__ void path_writer(const KParams& p, SweepLds& L, uint32_t tag, int wv, int lane, bool& timed_out) {
   constexpr int kWaves = kThreads / kWave;
   const int ntiles = p.B * p.ntile;
-  if (threadIdx.x == 0)
+  if (threadIdx.x == 0) {
+    // Hold while more than kPathHoldItems items are still sweeping (bounded).
+    const uint32_t want = p.B > kPathHoldItems ? (uint32_t)(p.B - kPathHoldItems) : 0u;
+    int spins = 0;
+    while (__hip_atomic_load(&p.hdr->swept, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < want && !timed_out) {
+      if (++spins > kSpinLimit) timed_out = true;
+      __builtin_amdgcn_s_sleep(8);
+    }
     L.tile = (int)__hip_atomic_fetch_add(&p.hdr->tile_next, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  }
   __syncthreads();
   int t = L.tile;
   while (t < ntiles) {
@@ -1202,6 +1217,8 @@ __device__ __forceinline__ void sweep_role(const KParams& p, SweepLds& L, const 
   }
   // Publish this wave's decision words (its stores are complete).
   if (lane == 0) st_dev(p.done + (size_t)b * p.NW + g, tag);
+  // The wave holding row t_x-1 finishes the item's sweep last.
+  if (g == g_last && lane == 0) __hip_atomic_fetch_add(&p.hdr->swept, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   if (g != g_last) return;
 
   // The walker.
@@ -1238,6 +1255,7 @@ __device__ __forceinline__ void invalid_item(const KParams& p, int b, int g, boo
     if (p.status) p.status[b] = st;
   }
   // The path writers write the all-zero slab from this table.
+  if (lane == 0) __hip_atomic_fetch_add(&p.hdr->swept, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   publish_item(p, b, tag, lane);
 }
 
@@ -1253,6 +1271,7 @@ __device__ __forceinline__ void finish_call(const KParams& p, uint32_t gen) {
     if (prev == total - 1) {
       __hip_atomic_store(&p.hdr->walk_count, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       __hip_atomic_store(&p.hdr->tile_next, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      __hip_atomic_store(&p.hdr->swept, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       __hip_atomic_store(&p.hdr->exit_count, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       __hip_atomic_store(&p.hdr->gen, gen + 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }
