@@ -946,11 +946,14 @@ __device__ __forceinline__ void load_windows(const KParams& p, SweepLds& L, int 
   vm_wait<0>();
 }
 
-// Lane l of v becomes x (x and l wave-uniform, l in [0, 63]); the lane
-// select goes through M0 (one VALU operand may read one SGPR besides M0).
-template <typename T>
-__device__ __forceinline__ void write_lane(T& v, T x, int l) {
-  asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tv_writelane_b32 %0, %1, m0" : "+v"(v) : "s"(x), "s"(l) : "m0");
+// Lane l of a becomes x and lane l of b becomes y (x, y, l wave-uniform, l
+// in [0, 63]); the lane select goes through M0 (one VALU operand may read one
+// SGPR besides M0).
+__device__ __forceinline__ void write_lanes(uint32_t& a, uint32_t x, int& b, int y, int l) {
+  asm volatile("s_mov_b32 m0, %4\n\ts_nop 0\n\tv_writelane_b32 %0, %2, m0\n\tv_writelane_b32 %1, %3, m0"
+               : "+v"(a), "+v"(b)
+               : "s"(x), "s"(y), "s"(l)
+               : "m0");
 }
 
 // Row starts from the walk's records of up to 64 chunks: lane k holds the
@@ -986,9 +989,12 @@ __device__ __forceinline__ void flush_records(int* rsl, int base, int lo, int hi
 // 32 rows per chunk, so those 64 rows cover the next chunk too.  Each chunk's
 // step set and entry row go into lane (chunk % 64) of two registers; every 64
 // chunks the lanes turn them into row starts in parallel.
+// BANDED: T > kWinRows, windows start at their own first rows (row 0
+// otherwise).
+template <bool BANDED>
 __device__ __forceinline__ void walk(const KParams& p, SweepLds& L, int tx, int ty, int lane, bool& timed_out) {
   int* rsl = L.u.walk.rs;
-  const bool banded = p.T > kWinRows;  // windows start at row 0 otherwise
+  constexpr bool banded = BANDED;
   int idx = tx - 1;                    // row of the path at the chunk's last column
   int cw = (ty - 1) / kChunk;          // chunk being walked
   const int c_top = cw;
@@ -1025,10 +1031,15 @@ __device__ __forceinline__ void walk(const KParams& p, SweepLds& L, int tx, int 
   auto read_wlo = [&]() __attribute__((always_inline)) {
     if (banded) wlo_v = lds_load(&L.wlo[min(lane, kNWin - 1)]);
   };
-  // Word of row e - lane from window slot sl (clamped into the window).
+  // Word of row e - lane from window slot sl (clamped to the slot's first
+  // row below; the walk never reaches past a window's last row).
+  const int lane4 = 4 * lane;
+  const uint32_t win0 = lds_off(&L.u.walk.win[0][0]);
   auto row_word = [&](int sl, int e) __attribute__((always_inline)) -> uint32_t {
-    const int r = e - lane - (banded ? __builtin_amdgcn_readlane(wlo_v, sl) : 0);
-    return L.u.walk.win[sl][min(max(r, 0), kWinRows - 1)];
+    const int lo = banded ? __builtin_amdgcn_readlane(wlo_v, sl) : 0;
+    const int base = (int)win0 + sl * (kWinRows * 4);
+    const int a = max(base + 4 * (e - lo) - lane4, base);
+    return *(const __attribute__((address_space(3))) uint32_t*)(uintptr_t)(uint32_t)a;
   };
   if (idx > 0) {
     ensure(cw);
@@ -1037,48 +1048,68 @@ __device__ __forceinline__ void walk(const KParams& p, SweepLds& L, int tx, int 
     uint32_t rec_pm = 0;  // lane k: steps of chunk (64-aligned base) + k
     int rec_e = 0;        // lane k: its entry row
     int off = 0;          // lane of row idx in the current words
-    bool more = true;
-    // One chunk on the words in Wc, the next chunk's read into Wn; false once
-    // the walk is over or the chunk was the last of its block.
-    auto chunk = [&](uint32_t& Wc, uint32_t& Wn) __attribute__((always_inline)) -> bool {
-      const int nslot = uni(slot == 0 ? kNWin - 1 : slot - 1);
-      // (also read past chunk 0, unused: a conditional read would make the
-      // compiler wait for every LDS read in flight where the paths join)
+    // One chunk on the words in Wc, the next chunk's read into Wn (also past
+    // chunk 0 or the walk's end, unused: a conditional read would make the
+    // compiler wait for every LDS read in flight where the paths join).
+    auto chunk = [&](uint32_t& Wc, uint32_t& Wn, int nslot) __attribute__((always_inline)) {
       Wn = row_word(nslot, idx);
       __builtin_amdgcn_sched_barrier(0);
       // (readfirstlane: the compiler treats asm results as per-lane values)
       const uint32_t pm = (uint32_t)uni((int)walk_chunk(Wc, Wc >> 1, uni(off), uni(q0)));
       __builtin_amdgcn_sched_barrier(0);
       const int kk = __builtin_popcount(pm);
-      write_lane(rec_pm, pm, uni(cw & (kWave - 1)));
-      write_lane(rec_e, uni(idx), uni(cw & (kWave - 1)));
+      write_lanes(rec_pm, pm, rec_e, uni(idx), uni(cw & (kWave - 1)));
       idx -= kk;
-      more = idx > 0 && cw > 0;
       off = kk;
       q0 = 0;
       cw -= 1;
       slot = nslot;
-      return more && (cw & 7) != 7;
     };
     // Blocks of chunks down to a multiple of 8: the windows a block reads are
     // checked once, and the walker's position is published once per block
-    // (the loader refills slots of chunks above it).  The chunk loop holds
-    // no inner loop, so the compiler waits for each read only where its
-    // words are used, one chunk after it was issued.
-    while (more) {
+    // (the loader refills slots of chunks above it).  The first block walks
+    // chunk by chunk until the walk ends or the block does; every later block
+    // walks all eight chunks unconditionally (a path that reaches row 0 inside
+    // the block only yields records of rows <= 0, which are not rows) and
+    // checks for the end after them.  The chunk code holds no inner loop, so
+    // the compiler waits for each read only where its words are used, one
+    // chunk after it was issued.
+    bool more = true;
+    {
       lds_put64(lds_off(&L.wpos), walk_pos(cw, idx));
       ensure(max((cw & ~7) - 1, 0));
       read_wlo();
       bool in_b = false;  // the next chunk's words are in Wb
 #pragma unroll
       for (int k = 0; k < 4; ++k) {
-        if (!chunk(Wa, Wb)) {
+        chunk(Wa, Wb, uni(slot == 0 ? kNWin - 1 : slot - 1));
+        more = idx > 0 && cw >= 0;
+        if (!more || (cw & 7) == 7) {
           in_b = true;
           break;
         }
-        if (!chunk(Wb, Wa)) break;
+        chunk(Wb, Wa, uni(slot == 0 ? kNWin - 1 : slot - 1));
+        more = idx > 0 && cw >= 0;
+        if (!more || (cw & 7) == 7) break;
       }
       if (in_b) Wa = Wb;
+      if (!more || ((cw + 1) & (kWave - 1)) == 0)
+        flush_records(rsl, (cw + 1) & ~(kWave - 1), cw + 1, c_top, rec_pm, rec_e, lane);
+    }
+    static_assert(kNWin % 8 == 0, "an aligned block of chunks occupies consecutive slots");
+    while (more) {
+      lds_put64(lds_off(&L.wpos), walk_pos(cw, idx));
+      ensure(max(cw - 8, 0));
+      read_wlo();
+      // Chunks cw .. cw-7 sit in slots bs+7 .. bs, chunk cw-8 in the slot
+      // before bs.
+      const int bs = uni(slot - 7), before = uni(bs == 0 ? kNWin - 1 : bs - 1);
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        chunk(Wa, Wb, bs + 6 - 2 * k);
+        chunk(Wb, Wa, k < 3 ? bs + 5 - 2 * k : before);
+      }
+      more = idx > 0 && cw >= 0;
       // Records are complete for every 64-aligned group the walk has left.
       if (!more || ((cw + 1) & (kWave - 1)) == 0)
         flush_records(rsl, (cw + 1) & ~(kWave - 1), cw + 1, c_top, rec_pm, rec_e, lane);
@@ -1223,7 +1254,10 @@ __device__ __forceinline__ void sweep_role(const KParams& p, SweepLds& L, const 
 
   // The walker.
   if (lane == (x.tx - 1) - g_last * kRowsPerWave + 1 && p.score) p.score[b] = score;
-  walk(p, L, x.tx, x.ty, lane, timed_out);
+  if (p.T > kWinRows)
+    walk<true>(p, L, x.tx, x.ty, lane, timed_out);
+  else
+    walk<false>(p, L, x.tx, x.ty, lane, timed_out);
   int32_t* rs_out = p.row_start + (size_t)b * ((size_t)p.T + 1);
   for (int i = lane; i <= p.T; i += kWave) st_dev(reinterpret_cast<uint32_t*>(rs_out + i), (uint32_t)L.u.walk.rs[i]);
   publish_item(p, b, tag, lane);
