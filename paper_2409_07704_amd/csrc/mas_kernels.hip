@@ -1184,16 +1184,8 @@ __device__ __forceinline__ int wait_published(const KParams& p, int k, uint32_t 
 __device__ __forceinline__ void path_writer(const KParams& p, SweepLds& L, uint32_t tag, int wv, int lane, bool& timed_out) {
   constexpr int kWaves = kThreads / kWave;
   const int ntiles = p.B * p.ntile;
-  if (threadIdx.x == 0) {
-    // Hold while more than kPathHoldItems items are still sweeping (bounded).
-    const uint32_t want = p.B > kPathHoldItems ? (uint32_t)(p.B - kPathHoldItems) : 0u;
-    int spins = 0;
-    while (__hip_atomic_load(&p.hdr->swept, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < want && !timed_out) {
-      if (++spins > kSpinLimit) timed_out = true;
-      __builtin_amdgcn_s_sleep(8);
-    }
+  if (threadIdx.x == 0)
     L.tile = (int)__hip_atomic_fetch_add(&p.hdr->tile_next, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-  }
   __syncthreads();
   int t = L.tile;
   while (t < ntiles) {
@@ -1248,8 +1240,6 @@ __device__ __forceinline__ void sweep_role(const KParams& p, SweepLds& L, const 
   }
   // Publish this wave's decision words (its stores are complete).
   if (lane == 0) st_dev(p.done + (size_t)b * p.NW + g, tag);
-  // The wave holding row t_x-1 finishes the item's sweep last.
-  if (g == g_last && lane == 0) __hip_atomic_fetch_add(&p.hdr->swept, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   if (g != g_last) return;
 
   // The walker.
@@ -1289,7 +1279,6 @@ __device__ __forceinline__ void invalid_item(const KParams& p, int b, int g, boo
     if (p.status) p.status[b] = st;
   }
   // The path writers write the all-zero slab from this table.
-  if (lane == 0) __hip_atomic_fetch_add(&p.hdr->swept, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   publish_item(p, b, tag, lane);
 }
 
@@ -1305,7 +1294,6 @@ __device__ __forceinline__ void finish_call(const KParams& p, uint32_t gen) {
     if (prev == total - 1) {
       __hip_atomic_store(&p.hdr->walk_count, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       __hip_atomic_store(&p.hdr->tile_next, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      __hip_atomic_store(&p.hdr->swept, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       __hip_atomic_store(&p.hdr->exit_count, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       __hip_atomic_store(&p.hdr->gen, gen + 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }

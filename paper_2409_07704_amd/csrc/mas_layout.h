@@ -38,10 +38,6 @@ __host__ __device__ constexpr int dec_bit(int j) { return 31 - (j % kChunk); }
 // kPathWorkgroups path-writer workgroups (one per CU of the MI355X).
 constexpr int kPathTileRows = 64;
 constexpr int kPathWorkgroups = 256;
-// Path writers start once at most this many items are still sweeping: the
-// path's stores then overlap the backtracks instead of slowing the sweeps'
-// value loads.
-constexpr int kPathHoldItems = 4;
 
 struct WsHeader {
   uint32_t gen;         // call generation; tag of a call = 2 * gen + 1
@@ -49,8 +45,7 @@ struct WsHeader {
   uint32_t error;       // sticky: non-zero once a device-side wait timed out
   uint32_t walk_count;  // row_start tables published in the current call
   uint32_t tile_next;   // path tiles taken in the current call
-  uint32_t swept;       // items whose forward sweep is done in the current call
-  uint32_t pad[58];
+  uint32_t pad[59];
 };
 static_assert(sizeof(WsHeader) == kAlign, "header is one alignment unit");
 
