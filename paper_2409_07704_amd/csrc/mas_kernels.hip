@@ -659,13 +659,15 @@ __device__ __forceinline__ float sweep_wave(const KParams& p, SweepLds& L, const
 // waits, before loading more than its first tiles, for a share of the time by
 // which its estimated run is shorter than the batch's longest: long items
 // sweep first with little contention and short ones fill in behind them.
-// Estimates are in wall-clock ticks (100 MHz) of one item running alone:
-// kTicksPerChunk per 32 columns and kTicksPerGroup per 63 rows, fitted to
-// measured single-item runs.  Batches larger than kDelayMaxBatch start at
-// once (every workgroup would read every length), and no delay exceeds
+// Estimates are in wall-clock ticks (100 MHz): kTicksPerChunk per 32
+// columns (about one chunk step of a sweep wave in a full batch) and
+// kTicksPerGroup per 63 rows, chosen by timing full batches of mixed lengths
+// (a per-wave term close to a wave's own start lag, about 270 ticks, delays
+// items with few rows too long).  Batches larger than kDelayMaxBatch start
+// at once (every workgroup would read every length), and no delay exceeds
 // kDelayMaxTicks (1 ms, far below the bound of any device-side wait).
-constexpr int kTicksPerChunk = 75;
-constexpr int kTicksPerGroup = 480;
+constexpr int kTicksPerChunk = 85;
+constexpr int kTicksPerGroup = 100;
 constexpr int kDelayPercent = 80;
 constexpr int kDelayMaxBatch = 1024;
 constexpr int kDelayMaxTicks = 100000;
