@@ -75,7 +75,8 @@ __device__ __forceinline__ int uni(int v) { return __builtin_amdgcn_readfirstlan
 
 constexpr int kSpinLimit = 1 << 20;  // bound of every device-side wait
 constexpr int kLoaders = 4;          // loader waves per workgroup
-constexpr int kThreads = kThreadsPerBlock + kLoaders * kWave;
+constexpr int kStorers = 1;         // storer waves per workgroup (decision words to memory)
+constexpr int kThreads = kThreadsPerBlock + (kLoaders + kStorers) * kWave;
 constexpr int kRing = 4;             // tile and boundary slots per sweep wave
 constexpr int kPolicyDev = 16;       // cache policy sc1: device scope (write-through stores)
 
@@ -88,11 +89,14 @@ constexpr int kPolicyDev = 16;       // cache policy sc1: device scope (write-th
 //     occupy 16 distinct four-bank groups of the 64-bank LDS, so the reads of
 //     a wave (lane l reads row l-1) are conflict-free;
 //   * at kBoundOff, the chunk's boundary row: Q of the row above the wave
-//     for the chunk's 32 columns (lane 0's values).
+//     for the chunk's 32 columns (lane 0's values);
+//   * at kBitsOff, the chunk's decision words (lane l: word of row l-1, lane
+//     0: a scratch word), left there by the sweep wave for the storer wave.
 // Chunk c uses slot (c - c_begin) % kRing of its wave.
 constexpr int kTileBytes = kWave * kChunk * 4;  // 8192
 constexpr int kBoundOff = kTileBytes;
-constexpr int kSlotStride = kTileBytes + 256;
+constexpr int kBitsOff = kTileBytes + 256;
+constexpr int kSlotStride = kTileBytes + 512;
 constexpr int kWaveRegion = kRing * kSlotStride;
 __host__ __device__ constexpr int swz(int r) { return (r >> 1) & 7; }
 
@@ -119,7 +123,9 @@ struct SweepLds {
   //   .x ready: value tiles of chunks < ready are in w's slots (loader w);
   //   .y prod:  boundary rows of chunks < prod are in w's slots (wave w-1);
   //   .z cnext: progress of wave w+1: it has read every chunk < cnext, whose
-  //             slots are free again (written by wave w+1).
+  //             slots are free again (written by wave w+1);
+  //   .w taken: the storer has taken the decision words of chunks < taken
+  //             out of w's slots.
   // Wave 0's own progress goes to cons0.
   i32x4 box[kWavesPerBlock];
   int cons0;
@@ -521,11 +527,11 @@ __device__ __forceinline__ float sweep_wave(const KParams& p, SweepLds& L, const
   const uint32_t my_cons = w > 0 ? lds_off(&L.box[w - 1]) + 8u : lds_off(&L.cons0);
   const int* const my_box = reinterpret_cast<const int*>(&L.box[w]);
 
-  // Decision words: dec[b][c][row], lane 0 into the chunk's scratch word.
-  const __amdgpu_buffer_rsrc_t dr =
-      make_cursor(p.dec + (size_t)x.b * p.NC * (size_t)p.TP, (uint64_t)p.NC * p.TP * 4u).rsrc();
-  const int dvo = 4 * (lane > 0 ? x.row : p.TP - 1);
-  const int dstride = p.TP * 4;
+  // Decision words: into the chunk's slot (the storer wave writes them to
+  // memory); a lane's word of chunk c at bits_ptr(J)[lane].
+  auto bits_ptr = [&](int k) __attribute__((always_inline)) -> uint32_t* {
+    return reinterpret_cast<uint32_t*>(Lc + wbase + (uint32_t)k * kSlotStride + kBitsOff);
+  };
   // Global boundary words of this wave (OUT2): word 32c + j = {Q of the
   // wave's last row at column 32c + j, tag}.
   const size_t slot_words = (size_t)p.NC * kChunk;
@@ -572,7 +578,6 @@ __device__ __forceinline__ float sweep_wave(const KParams& p, SweepLds& L, const
   lds_put(my_cons, x.c_begin + 1);
 
   float qc[kChunk] = {};
-  int soff = x.c_begin * dstride;
   float score = neg_inf();
   const int m_last = (x.ty - 1) % kChunk;
 
@@ -622,8 +627,13 @@ __device__ __forceinline__ float sweep_wave(const KParams& p, SweepLds& L, const
     sweep_chunk(q, t, vc, qc, bits);
     __builtin_amdgcn_sched_barrier(0);
     hand_off(c);
-    __builtin_amdgcn_raw_buffer_store_b32(bits, dr, dvo, soff, kPolicyDev);
-    soff += dstride;
+    // The slot's decision words of chunk c-4 must have been taken (mailbox
+    // .w, read with this step's mailbox; rarely not yet).
+    if (uni(mb.w) < c - (kRing - 1)) {
+      wait_at_least(my_box + 3, c - (kRing - 1), timed_out);
+      lgkm_wait0();
+    }
+    bits_ptr(J)[lane] = bits;
     if (OUT == 0 && c == x.c_end - 1) {
 #pragma unroll
       for (int m = 0; m < kChunk; ++m) score = (m == m_last) ? qc[m] : score;
@@ -648,6 +658,9 @@ __device__ __forceinline__ float sweep_wave(const KParams& p, SweepLds& L, const
     if (c + 2 < x.c_end) step(std::integral_constant<int, 2>(), c + 2, va, vb);
     if (c + 3 < x.c_end) step(std::integral_constant<int, 3>(), c + 3, vb, va);
   }
+  // Every chunk's decision words are in the slots (the storer takes chunk c
+  // once this progress passes c + 1).
+  lds_put(my_cons, x.c_end + 1);
   vm_wait<0>();
   return score;
 }
@@ -1209,6 +1222,64 @@ __device__ __forceinline__ void path_writer(const KParams& p, SweepLds& L, uint3
   }
 }
 
+// ---------------------------------------------------------------- storer wave
+// Decision words of the workgroup's four sweep waves, from their slots to
+// dec[b][c][row] with device-scope write-through stores (lane 0 holds the
+// row above, whose word nobody reads: its offset lies past the resource, so
+// that store is dropped), in chunk order per wave; chunk c of a wave is
+// complete in its slot once that wave's progress passes c + 1.  Once all of a
+// wave's stores have landed, its done flag goes up.  The stores are kept out
+// of the sweep waves, whose every step would otherwise wait behind the
+// loaders' traffic to issue its store, and out of the loaders, whose waits
+// count their own loads only.
+__device__ __forceinline__ void storer_role(const KParams& p, SweepLds& L, int b, int r, int tx, int ty, int lane, uint32_t tag,
+                                            bool& timed_out) {
+  const __amdgpu_buffer_rsrc_t dr =
+      make_cursor(p.dec + (size_t)b * p.NC * (size_t)p.TP, (uint64_t)p.NC * p.TP * 4u).rsrc();
+  const int dstride = p.TP * 4;
+  int taken[kWavesPerBlock], cend[kWavesPerBlock], cbeg[kWavesPerBlock], dvo[kWavesPerBlock];
+  int left = 0;
+#pragma unroll
+  for (int w = 0; w < kWavesPerBlock; ++w) {
+    const WaveCtx xw = make_ctx(b, r * kWavesPerBlock + w, w, lane, tx, ty);
+    cbeg[w] = xw.c_begin;
+    cend[w] = xw.g <= xw.g_last ? xw.c_end : xw.c_begin;
+    taken[w] = cbeg[w];
+    dvo[w] = lane > 0 ? 4 * xw.row : -1;  // lane 0's word (the row above) is not stored
+    left += cend[w] - cbeg[w];
+    // (a wave of the item without chunks has nothing to store)
+    if (xw.g <= xw.g_last && cend[w] == cbeg[w] && lane == 0) st_dev(p.done + (size_t)b * p.NW + xw.g, tag);
+  }
+  int spins = 0;
+  while (left > 0 && !timed_out) {
+    bool moved = false;
+#pragma unroll
+    for (int w = 0; w < kWavesPerBlock; ++w) {
+      if (taken[w] >= cend[w]) continue;
+      const int* const progress = w > 0 ? reinterpret_cast<const int*>(&L.box[w - 1]) + 2 : &L.cons0;
+      const int cons = uni(lds_load(progress));
+      while (taken[w] < cend[w] && cons >= taken[w] + 2) {
+        const uint32_t* const src = reinterpret_cast<const uint32_t*>(
+            &L.u.ring[w][((taken[w] - cbeg[w]) & (kRing - 1)) * kSlotStride + kBitsOff]);
+        const uint32_t v = src[lane];
+        __builtin_amdgcn_raw_buffer_store_b32(v, dr, dvo[w], taken[w] * dstride, kPolicyDev);
+        ++taken[w];
+        --left;
+        lds_put(lds_off(&L.box[w]) + 12u, taken[w]);  // (after the read: LDS operations run in order)
+        moved = true;
+        if (taken[w] == cend[w]) {
+          vm_wait<0>();
+          if (lane == 0) st_dev(p.done + (size_t)b * p.NW + r * kWavesPerBlock + w, tag);
+        }
+      }
+    }
+    if (!moved) {
+      if (++spins > kSpinLimit) timed_out = true;
+      __builtin_amdgcn_s_sleep(1);
+    }
+  }
+}
+
 // ---------------------------------------------------------------- roles
 // Item b's row_start table is complete once this wave's stores have landed:
 // append b to the call's completion order, which the path writers follow.
@@ -1240,8 +1311,6 @@ __device__ __forceinline__ void sweep_role(const KParams& p, SweepLds& L, const 
   } else {
     score = sweep_wave<1, 2>(p, L, x, tag, timed_out);
   }
-  // Publish this wave's decision words (its stores are complete).
-  if (lane == 0) st_dev(p.done + (size_t)b * p.NW + g, tag);
   if (g != g_last) return;
 
   // The walker.
@@ -1302,7 +1371,8 @@ __device__ __forceinline__ void finish_call(const KParams& p, uint32_t gen) {
   }
 }
 
-// Eight waves per workgroup, one workgroup per CU.
+// Nine waves per workgroup (four sweep waves, four loaders, one storer), one
+// workgroup per CU.
 template <bool ALIGNED>
 __global__ void __launch_bounds__(kThreads, 1) mas_kernel(KParams p) {
   __shared__ SweepLds L;
@@ -1322,7 +1392,8 @@ __global__ void __launch_bounds__(kThreads, 1) mas_kernel(KParams p) {
   const int lane = threadIdx.x & (kWave - 1);
   const int wv = uni(threadIdx.x / kWave);
   const int w = wv & (kWavesPerBlock - 1);
-  const bool is_loader = wv >= kWavesPerBlock;
+  const bool is_storer = wv >= 2 * kWavesPerBlock;
+  const bool is_loader = wv >= kWavesPerBlock && !is_storer;
   const int g = r * kWavesPerBlock + w;
   const int tx = p.t_x[b];
   const int ty = p.t_y[b];
@@ -1333,7 +1404,7 @@ __global__ void __launch_bounds__(kThreads, 1) mas_kernel(KParams p) {
     // Nothing loaded or delivered yet; every wave's progress is just below
     // its first chunk (it first reads the boundary row of chunk c_begin-1).
     const int gg = r * kWavesPerBlock + (int)threadIdx.x;
-    L.box[threadIdx.x] = i32x4{chunk_begin(gg), chunk_begin(gg) - 1, chunk_begin(gg + 1) - 1, 0};
+    L.box[threadIdx.x] = i32x4{chunk_begin(gg), chunk_begin(gg) - 1, chunk_begin(gg + 1) - 1, chunk_begin(gg)};
   }
   if (threadIdx.x == 0) {
     L.cons0 = chunk_begin(r * kWavesPerBlock) - 1;
@@ -1344,7 +1415,9 @@ __global__ void __launch_bounds__(kThreads, 1) mas_kernel(KParams p) {
   __syncthreads();
 
   if (st != kItemOk) {
-    invalid_item(p, b, g, is_loader, lane, st, tag);
+    invalid_item(p, b, g, is_loader || is_storer, lane, st, tag);
+  } else if (is_storer) {
+    storer_role(p, L, b, r, tx, ty, lane, tag, timed_out);
   } else {
     const WaveCtx x = make_ctx(b, g, w, lane, tx, ty);
     if (is_loader)
