@@ -35,9 +35,11 @@ __host__ __device__ constexpr int dec_bit(int j) { return 31 - (j % kChunk); }
 // so stale words from earlier calls are never mistaken for fresh ones.
 // Dense path: written in tiles of kPathTileRows rows of one item, taken in
 // the order the items' row_start tables are published, by at most
-// kPathWorkgroups path-writer workgroups (one per CU of the MI355X).
+// kPathWorkgroups path-writer workgroups (three quarters of the MI355X's 256
+// CUs: enough to keep up, while the stores of all 256 slow the sweeps still
+// running more than they gain; timed on full batches of mixed lengths).
 constexpr int kPathTileRows = 64;
-constexpr int kPathWorkgroups = 256;
+constexpr int kPathWorkgroups = 192;
 
 struct WsHeader {
   uint32_t gen;         // call generation; tag of a call = 2 * gen + 1
