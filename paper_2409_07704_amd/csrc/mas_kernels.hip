@@ -22,7 +22,7 @@
 // four loaders of its workgroup stage the decision words of upcoming chunks
 // in LDS, and publishes the item's row_start table, appending the item to the
 // call's completion order.  Path-writer workgroups, last in the grid, take
-// tiles of 64 rows of one item from a shared counter in that order and write
+// tiles of 32 rows of one item from a shared counter in that order and write
 // them from the table, every byte once (zeros and ones in one pass): an item
 // that finishes late is written by many workgroups at once.
 //
@@ -1193,9 +1193,10 @@ __device__ __forceinline__ int wait_published(const KParams& p, int k, uint32_t 
 }
 
 // A path-writer workgroup: takes tile t = (k, part) from the shared counter,
-// rows [64 part, 64 part + 64) of the item published k-th, waits for that
-// item, writes the tile (each wave an eighth of its rows) and goes on until
-// the tiles run out.  The next tile is taken while this one is written.
+// rows [R part, R part + R) of the item published k-th (R = kPathTileRows),
+// waits for that item, writes the tile (each wave an equal share of its rows)
+// and goes on until the tiles run out.  The next tile is taken while this one
+// is written.
 __device__ __forceinline__ void path_writer(const KParams& p, SweepLds& L, uint32_t tag, int wv, int lane, bool& timed_out) {
   constexpr int kWaves = kThreads / kWave;
   const int ntiles = p.B * p.ntile;

@@ -38,7 +38,7 @@ __host__ __device__ constexpr int dec_bit(int j) { return 31 - (j % kChunk); }
 // kPathWorkgroups path-writer workgroups (three quarters of the MI355X's 256
 // CUs: enough to keep up, while the stores of all 256 slow the sweeps still
 // running more than they gain; timed on full batches of mixed lengths).
-constexpr int kPathTileRows = 64;
+constexpr int kPathTileRows = 32;
 constexpr int kPathWorkgroups = 192;
 
 struct WsHeader {
