@@ -184,7 +184,7 @@ def main():
         pmc_summary(args.pmc_summary, TRAFFIC_FILE)
         return
     if args.gpus != 1:
-        print(f"bench.py: this build measures one GPU; --gpus {args.gpus} is not supported "
+        print(f"bench.py: only the one-GPU path is built and measured; --gpus {args.gpus} is not supported "
               "(items are independent, so more GPUs would each run their own share of the batch)",
               file=sys.stderr)
         sys.exit(2)
