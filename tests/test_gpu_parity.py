@@ -176,6 +176,24 @@ def test_long_items(mas):
     assert_parity(mas, value, tx, ty, "long-1024-chunks")
 
 
+def test_mixed_batch_tall_items(mas):
+    """A mixed batch with T above the walk's window height (banded windows),
+    several workgroups per item (boundary rows handed on by the loaders, one
+    storer per workgroup) and many path tiles per item, plus degenerate items
+    (single row, diagonal, empty) in the same launch."""
+    st = synth.Stream(123)
+    B, T, S = 12, 2048, 3000
+    value = st.normal_f32(B * T * S).reshape(B, T, S) * np.float32(3.0) - np.float32(1.0)
+    tx = st.randint(1, T, B)
+    ty = np.array([int(st.randint(int(a), S)[0]) for a in tx], np.int32)
+    tx[0], ty[0] = T, S          # full extent
+    tx[1], ty[1] = 1500, 1500    # diagonal
+    tx[2], ty[2] = 1, 2999       # one row
+    tx[3], ty[3] = 0, 100        # empty
+    tx[4], ty[4] = 1100, 2999    # just above the window height
+    assert_parity(mas, value, tx, ty, "mixed-tall-b12-t2048-s3000")
+
+
 def test_unaligned_value_pointer(mas):
     value, tx, ty = synth.generate("tts-b16-t128-s512")
     B, T, S = value.shape
