@@ -70,18 +70,65 @@ def algorithmic_bytes(tx, ty, B, T, S):
     return cells, metric, 4 * band + B * T * S + dec
 
 
-def cpu_oracle_rate(value, tx, ty, budget_s: float):
-    """Oracle cells/s on the host (single thread), full batch repeated."""
+def host_description():
+    """CPU model and thread counts of the host the CPU baselines ran on."""
+    model = "unknown"
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    try:
+        usable = len(os.sched_getaffinity(0))
+    except AttributeError:
+        usable = os.cpu_count() or 1
+    return {"cpu_model": model, "nproc": os.cpu_count(), "usable_cpus": usable}
+
+
+def oracle_threads():
+    """Threads for the all-core oracle run: the CPUs this process may use,
+    at most 16 (the host share of one GPU on a shared GPU machine)."""
+    return max(1, min(16, host_description()["usable_cpus"]))
+
+
+def oracle_batch(value, tx, ty, threads: int):
+    """The CPU oracle over the batch, items split into `threads` contiguous
+    slices run concurrently (the oracle's C code runs without the GIL), as a
+    batch-parallel CPU implementation runs one item per core."""
     import numpy as np
 
     import oracle
+
+    B = value.shape[0]
+    if threads <= 1 or B == 1:
+        return oracle.mas(value, tx, ty)
+    from concurrent.futures import ThreadPoolExecutor
+
+    cuts = np.linspace(0, B, min(threads, B) + 1).astype(int)
+    parts = [(a, b) for a, b in zip(cuts[:-1], cuts[1:]) if b > a]
+    with ThreadPoolExecutor(len(parts)) as ex:
+        outs = list(ex.map(lambda ab: oracle.mas(value[ab[0]:ab[1]], tx[ab[0]:ab[1]], ty[ab[0]:ab[1]]), parts))
+    return tuple(np.concatenate([o[i] for o in outs]) for i in range(3))
+
+
+def cpu_oracle_rate(value, tx, ty, budget_s: float, threads: int = 1, around=None):
+    """Oracle cells/s on the host, the full batch repeated for about budget_s
+    seconds.  `around`, if given, is a pair of callables run before and after
+    each oracle pass inside the timed region (device copies)."""
+    import numpy as np
 
     cells = int((tx.astype(np.int64) * ty).sum())
     reps, t = 0, 0.0
     out = None
     while reps == 0 or t < budget_s:
         t0 = time.perf_counter()
-        out = oracle.mas(value, tx, ty)
+        v = around[0]() if around else value
+        out = oracle_batch(v, tx, ty, threads)
+        if around:
+            around[1](out[0])
         t += time.perf_counter() - t0
         reps += 1
     return cells * reps / t, reps, t, out
@@ -175,7 +222,10 @@ def main():
     ap.add_argument("--steps", type=int, default=500)
     ap.add_argument("--warmup", type=int, default=25)
     ap.add_argument("--workload", default=None)
-    ap.add_argument("--cpu-budget", type=float, default=10.0, help="seconds of oracle timing")
+    ap.add_argument("--cpu-budget", type=float, default=10.0, help="seconds of oracle timing per CPU variant")
+    ap.add_argument("--no-secondary", action="store_true",
+                    help="skip the secondary lines (path-less call, the smaller workloads)")
+    ap.add_argument("--secondary-steps", type=int, default=200)
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle timing (parity still checked)")
     ap.add_argument("--copy-probe", action="store_true", help="run copies of a known size after the timed region")
     ap.add_argument("--pmc-summary", nargs="+", default=None, metavar="CSV")
@@ -239,19 +289,49 @@ def main():
         torch.cuda.synchronize(dev)
         del src, dst
 
-    # Parity of the timed outputs against the oracle (and the CPU baseline).
+    # Parity of the timed outputs against the oracle (and the CPU baselines).
     gpu_path = path.cpu().numpy()
     gpu_score = score.cpu().numpy()
     gpu_status = status.cpu().numpy()
+    host = host_description()
+    nthr = oracle_threads()
     if args.no_cpu:
-        cpu = None
-        _, _, _, (op, os_, ost) = cpu_oracle_rate(value, tx, ty, 0.0)
+        cpu, variants = None, None
+        op, os_, ost = oracle_batch(value, tx, ty, nthr)
     else:
-        rate, reps, tcpu, (op, os_, ost) = cpu_oracle_rate(value, tx, ty, args.cpu_budget)
-        cpu = {"value": rate, "unit": "cells/s", "cores": 1, "kind": "oracle",
-               "sample": f"full {wname} batch ({cells} cells) x {reps} reps, {tcpu:.1f} s, single thread"}
+        rate, reps, tcpu, (op, os_, ost) = cpu_oracle_rate(value, tx, ty, args.cpu_budget, threads=nthr)
+        cpu = {"value": rate, "unit": "cells/s", "cores": nthr, "kind": "oracle",
+               "sample": f"full {wname} batch ({cells} cells) x {reps} reps, {tcpu:.1f} s, items split over "
+                         f"{nthr} threads", **host}
+        r1, reps1, t1, _ = cpu_oracle_rate(value, tx, ty, args.cpu_budget, threads=1)
+        # The same all-core oracle with the copies a CPU implementation called
+        # from a GPU training step makes: value device-to-host before, the
+        # path host-to-device after.
+        vdev = v
+
+        def d2h():
+            return vdev.cpu().numpy()
+
+        def h2d(p):
+            torch.from_numpy(p).to(dev)
+            torch.cuda.synchronize(dev)
+
+        rc, repsc, tc, _ = cpu_oracle_rate(value, tx, ty, args.cpu_budget, threads=nthr, around=(d2h, h2d))
+        variants = [
+            {"value": r1, "unit": "cells/s", "cores": 1, "kind": "oracle",
+             "sample": f"full batch x {reps1} reps, {t1:.1f} s, one thread"},
+            {"value": rc, "unit": "cells/s", "cores": nthr, "kind": "oracle+copies",
+             "sample": f"full batch x {repsc} reps, {tc:.1f} s, {nthr} threads, including the value "
+                       f"device-to-host copy and the path host-to-device copy"},
+        ]
     parity = bool(np.array_equal(gpu_path, op) and gpu_score.tobytes() == os_.tobytes()
                   and np.array_equal(gpu_status, ost))
+
+    secondary = None
+    if not args.no_secondary:
+        secondary = secondary_lines(mas, synth, dev, stream, wname, v, x, y, ws, op, tx, ty, cells,
+                                    args.secondary_steps, max(3, args.warmup // 5))
+        parity = parity and all(s["parity"] for s in secondary.values())
 
     achieved = bytes_metric / t_mean / 1e9
     tr = load_traffic(wname)
@@ -280,11 +360,75 @@ def main():
                      "traffic_unit": "bytes/launch",
                      "algorithmic_bytes": bytes_metric},
         "cpu_baseline": cpu,
+        "cpu_baseline_variants": variants,
+        "secondary": secondary,
         "parity": "bit-exact" if parity else "MISMATCH",
     }
     print(json.dumps(out), flush=True)
     if not parity:
         sys.exit(1)
+
+
+def time_launches(fn, stream, steps, warmup):
+    """Per-launch seconds of `fn` (one library call), HIP events on `stream`."""
+    import numpy as np
+    import torch
+
+    for _ in range(warmup):
+        fn()
+    torch.cuda.synchronize()
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(steps + 1)]
+    ev[0].record(stream)
+    for k in range(steps):
+        fn()
+        ev[k + 1].record(stream)
+    torch.cuda.synchronize()
+    return np.array([ev[k].elapsed_time(ev[k + 1]) for k in range(steps)]) * 1e-3
+
+
+def secondary_lines(mas, synth, dev, stream, wname, v, x, y, ws, op, tx, ty, cells, steps, warmup):
+    """Secondary measurements reported beside the headline: the path-less call
+    (mas_search: row_start, durations and score, no dense path) on the headline
+    workload, and one mas_forward_ex line per smaller workload.  Each checks
+    its outputs against the oracle."""
+    import numpy as np
+    import torch
+
+    import oracle
+
+    out = {}
+    B, T, S = v.shape
+    rs = torch.empty((B, T + 1), dtype=torch.int32, device=dev)
+    du = torch.empty((B, T), dtype=torch.int32, device=dev)
+    sc = torch.empty(B, dtype=torch.float32, device=dev)
+    st = torch.empty(B, dtype=torch.int32, device=dev)
+    pl = time_launches(lambda: mas.mas_search(v, x, y, rs, sc, st, workspace=ws, stream=stream, durations_out=du),
+                       stream, steps, warmup)
+    ok = bool(np.array_equal(rs.cpu().numpy(), oracle.row_start(op, tx, ty))
+              and np.array_equal(du.cpu().numpy(), oracle.durations(op)))
+    out["path_less"] = {"call": "mas_search", "workload": wname, "launch_us_mean": float(pl.mean()) * 1e6,
+                        "launch_us_median": float(np.median(pl)) * 1e6, "cells_per_s": cells / float(pl.mean()),
+                        "parity": ok}
+    for name in synth.WORKLOADS:
+        if name == wname or name.startswith("tiny"):
+            continue
+        value, a, b = synth.generate(name)
+        Bn, Tn, Sn = value.shape
+        cn, metric, _ = algorithmic_bytes(a, b, Bn, Tn, Sn)
+        vv, xx, yy = (torch.from_numpy(t).to(dev) for t in (value, a, b))
+        pth = torch.empty((Bn, Tn, Sn), dtype=torch.uint8, device=dev)
+        scn = torch.empty(Bn, dtype=torch.float32, device=dev)
+        wsn = mas.Workspace(Bn, Tn, Sn, device=dev)
+        tl = time_launches(lambda: mas.mas_forward_ex(vv, xx, yy, pth, scn, None, workspace=wsn, stream=stream),
+                           stream, steps, warmup)
+        o_path, o_score, _ = oracle.mas(value, a, b)
+        ok = bool(np.array_equal(pth.cpu().numpy(), o_path) and scn.cpu().numpy().tobytes() == o_score.tobytes())
+        t = float(tl.mean())
+        out[name] = {"call": "mas_forward_ex", "launch_us_mean": t * 1e6, "launch_us_median": float(np.median(tl)) * 1e6,
+                     "cells": cn, "cells_per_s": cn / t, "metric_bytes": metric, "gbs": metric / t / 1e9,
+                     "frac": metric / t / 1e9 / HBM_PEAK_GBS, "parity": ok}
+        del vv, pth, wsn
+    return out
 
 
 if __name__ == "__main__":

@@ -12,13 +12,20 @@
  *     depends only on the previous one and is parallel over text rows
  *     (Algorithm 2);
  *   - backtrack from (t_x-1, t_y-1): at column j in row i the path continues
- *     in row i-1 at column j-1 when Q[i][j-1] < Q[i-1][j-1] strictly or
- *     i == j, and stays in row i otherwise (ties stay);
+ *     in row i-1 at column j-1 when Q[i][j-1] is strictly below
+ *     Q[i-1][j-1] in the order defined next, or when i == j; it stays in row
+ *     i otherwise (ties stay);
  *   - output: the 0/1 alignment A* of the input's [T, S] size per item, with
  *     exactly one 1 per speech column j < t_y (Sec. 2).
- * The max is the select (stay < diag) ? diag : stay and every add is one
- * fp32 round-to-nearest-even operation in column order, so paths and scores
- * are bit-for-bit reproducible and equal to a sequential CPU evaluation.
+ * Order of the max and of the backtrack's comparison: the numeric order of
+ * IEEE 754-2019 maximum(), in which -0 is below +0.  Algorithm 1's max is a
+ * real-valued max and does not say how signed zeros compare; this order
+ * answers it.  It differs from the plain IEEE `<` only when the two
+ * candidates are zeros of opposite sign: for stay = -0, diag = +0 the
+ * forward max is +0 and the path steps to row i-1 (with `<` it would keep
+ * -0 and stay).  Every add is one fp32 round-to-nearest-even operation in
+ * column order, with subnormals kept, so paths and scores are bit-for-bit
+ * reproducible and equal to a sequential CPU evaluation in this order.
  *
  * Conventions for every entry point:
  *   - value is [B, T, S] fp32, t_x / t_y are [B] int32, path_out is
@@ -59,7 +66,7 @@
 extern "C" {
 #endif
 
-#define MAS_VERSION 1
+#define MAS_VERSION 2
 
 typedef enum mas_status {
   MAS_OK = 0,
@@ -75,6 +82,16 @@ typedef enum mas_status {
 #define MAS_ITEM_INFEASIBLE 2   /* t_y < t_x: no monotonic alignment exists */
 #define MAS_ITEM_OUT_OF_RANGE 3 /* t_x or t_y negative, t_x > T or t_y > S */
 #define MAS_ITEM_SYNC_TIMEOUT 4 /* an internal device-side wait hit its bound; the item's outputs are invalid */
+#define MAS_ITEM_BAD_WORKSPACE 5 /* the workspace was never initialised by mas_workspace_init; nothing was computed */
+
+/*
+ * Every device-side wait is bounded: a wave gives up after a number of polls
+ * without progress (about 2^20 by default, far beyond any real wait) and its
+ * item is reported as MAS_ITEM_SYNC_TIMEOUT; the kernel still ends normally.
+ * Diagnostics: the environment variable MAS_WAIT_BOUND, read at every call,
+ * replaces that bound with a positive integer of at most 2^30 (tests use a
+ * small one to exercise the timeout path).
+ */
 
 /*
  * Bytes of device workspace that mas_search / mas_forward_ex need for a
@@ -85,10 +102,12 @@ typedef enum mas_status {
 size_t mas_workspace_bytes(int32_t B, int32_t T, int32_t S);
 
 /*
- * Prepare a workspace for first use: zero-fills it on `stream`.  Required
- * once per workspace allocation before the first mas_search /
- * mas_forward_ex that uses it; every later call leaves the workspace ready
- * for the next one.  A workspace serves one call at a time: calls that share
+ * Prepare a workspace for first use: zero-fills it on `stream` and marks it
+ * initialised.  Required once per workspace allocation before the first
+ * mas_search / mas_forward_ex that uses it; every later call leaves the
+ * workspace ready for the next one.  A call on a workspace without that mark
+ * computes nothing and sets every item_status_out entry to
+ * MAS_ITEM_BAD_WORKSPACE (other outputs are left as they were).  A workspace serves one call at a time: calls that share
  * a workspace must be ordered (same stream or synchronised).
  */
 mas_status mas_workspace_init(void* workspace, size_t workspace_bytes, hipStream_t stream);
@@ -99,8 +118,12 @@ mas_status mas_workspace_init(void* workspace, size_t workspace_bytes, hipStream
  *
  * row_start_out [B, T+1] int32 (required): for a valid item, row_start[b][i]
  * is the first speech column whose alignment is text row i (i < t_x), so row
- * i covers columns [row_start[b][i], row_start[b][i+1]) and its duration is
- * the difference; entries i >= t_x equal t_y.  Invalid items get all zeros.
+ * i covers columns [row_start[b][i], row_start[b][i+1]); entries i >= t_x
+ * equal t_y.  Invalid items get all zeros.
+ * durations_out [B, T] int32 (nullable): the number of speech frames aligned
+ * to each text row (Sec. 2: the durations a duration predictor is trained
+ * on), row_start[b][i+1] - row_start[b][i]; 0 for rows i >= t_x and for
+ * invalid items.  Equal to the row sums of the dense path.
  * score_out [B] fp32 (nullable): Q[t_x-1][t_y-1], the log-likelihood of the
  * chosen alignment, -inf for invalid items.
  * item_status_out [B] int32 (nullable): MAS_ITEM_* per item.
@@ -109,7 +132,7 @@ mas_status mas_workspace_init(void* workspace, size_t workspace_bytes, hipStream
  */
 mas_status mas_search(const float* value, const int32_t* t_x, const int32_t* t_y,
                       int32_t B, int32_t T, int32_t S,
-                      int32_t* row_start_out, float* score_out, int32_t* item_status_out,
+                      int32_t* row_start_out, int32_t* durations_out, float* score_out, int32_t* item_status_out,
                       void* workspace, size_t workspace_bytes, hipStream_t stream);
 
 /*

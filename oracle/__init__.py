@@ -47,7 +47,7 @@ def _load():
         lib = ctypes.CDLL(_LIB)
         P = ctypes.c_void_p
         i32 = ctypes.c_int32
-        lib.oracle_mas_batch_neg.argtypes = [P, i32, i32, i32, P, P, ctypes.c_float, P, P, P, P]
+        lib.oracle_mas_batch_neg.argtypes = [P, i32, i32, i32, P, P, ctypes.c_float, P, P, P]
         lib.oracle_mas_batch_neg.restype = ctypes.c_int
         lib.oracle_durations.argtypes = [P, i32, i32, i32, P]
         lib.oracle_durations.restype = None
@@ -59,12 +59,11 @@ def _ptr(a: np.ndarray | None):
     return None if a is None else a.ctypes.data_as(ctypes.c_void_p)
 
 
-def mas(value: np.ndarray, t_x, t_y, *, neg: float = -np.inf, with_dec: bool = False):
+def mas(value: np.ndarray, t_x, t_y, *, neg: float = -np.inf):
     """Run the oracle on a batch.
 
     value: float32 [B, T, S] (C-contiguous); t_x, t_y: int [B].
-    Returns (path u8 [B,T,S], score f32 [B], status i32 [B]) and, when
-    ``with_dec``, the per-cell forward choice u8 [B,T,S] as a fourth item.
+    Returns (path u8 [B,T,S], score f32 [B], status i32 [B]).
     """
     value = np.ascontiguousarray(value, dtype=np.float32)
     if value.ndim != 3:
@@ -75,12 +74,11 @@ def mas(value: np.ndarray, t_x, t_y, *, neg: float = -np.inf, with_dec: bool = F
     path = np.empty((B, T, S), dtype=np.uint8)
     score = np.empty(B, dtype=np.float32)
     status = np.empty(B, dtype=np.int32)
-    dec = np.empty((B, T, S), dtype=np.uint8) if with_dec else None
     rc = _load().oracle_mas_batch_neg(_ptr(value), B, T, S, _ptr(tx), _ptr(ty), float(neg),
-                                      _ptr(path), _ptr(score), _ptr(status), _ptr(dec))
+                                      _ptr(path), _ptr(score), _ptr(status))
     if rc != 0:
         raise MemoryError("oracle allocation failed")
-    return (path, score, status, dec) if with_dec else (path, score, status)
+    return path, score, status
 
 
 def durations(path: np.ndarray) -> np.ndarray:

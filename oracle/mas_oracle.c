@@ -71,14 +71,12 @@ static int item_status(int32_t tx, int32_t ty, int32_t T, int32_t S) {
 
 /*
  * One item.  q points at the item's [T, S] slab (row stride S); path at its
- * [T, S] output slab.  Q is scratch of tx*ty floats, stored column by column.  neg is the value of
- * masked cells (-INFINITY for the method; a finite number only for the
- * legacy-sentinel test).  dec (nullable, [tx*ty]) receives, for every
- * computed cell with j >= 1, 1 if the forward max took the diagonal
- * predecessor Q[i-1][j-1], else 0: a debugging export.
+ * [T, S] output slab.  Q is scratch of tx*ty floats, stored column by
+ * column.  neg is the value of masked cells (-INFINITY for the method; a
+ * finite number only for the legacy-sentinel test).
  */
 static void mas_one(const float* q, int32_t S, int32_t tx, int32_t ty, float neg,
-                    float* Q, uint8_t* path, float* score, uint8_t* dec) {
+                    float* Q, uint8_t* path, float* score) {
 #define QC(i, j) Q[(size_t)(j) * (size_t)tx + (size_t)(i)] /* column-major: the inner loop runs over i */
 #define QV(i, j) q[(size_t)(i) * (size_t)S + (size_t)(j)]
   /* Algorithm 1: initialise the cache to -inf (R3). */
@@ -86,10 +84,7 @@ static void mas_one(const float* q, int32_t S, int32_t tx, int32_t ty, float neg
 
   /* Algorithm 1: first row, running sum over speech columns (R4, R5). */
   QC(0, 0) = QV(0, 0);
-  for (int32_t j = 1; j < ty; ++j) {
-    QC(0, j) = QC(0, j - 1) + QV(0, j);
-    if (dec) dec[(size_t)j] = 0; /* row 0 has no diagonal predecessor */
-  }
+  for (int32_t j = 1; j < ty; ++j) QC(0, j) = QC(0, j - 1) + QV(0, j);
 
   /* Algorithm 1: forward loop, speech column outer, text row inner; the
    * inner bound min(j, T) keeps the cells a monotonic path can reach. */
@@ -100,7 +95,6 @@ static void mas_one(const float* q, int32_t S, int32_t tx, int32_t ty, float neg
       float diag = QC(i - 1, j - 1);
       int take_diag = below(stay, diag); /* R2 */
       QC(i, j) = (take_diag ? diag : stay) + QV(i, j);
-      if (dec) dec[(size_t)i * (size_t)ty + (size_t)j] = (uint8_t)take_diag;
     }
   }
 
@@ -120,16 +114,14 @@ static void mas_one(const float* q, int32_t S, int32_t tx, int32_t ty, float neg
 /*
  * Batched entry: value [B, T, S] fp32 row-major, t_x / t_y [B] int32,
  * path [B, T, S] u8 (fully overwritten), score [B] fp32 (nullable),
- * status [B] int32 (nullable), dec [B, T, S] u8 (nullable: per-cell forward
- * choice for computed cells j >= 1, 0 elsewhere).  neg: masked value.
+ * status [B] int32 (nullable).  neg: masked value.
  * Returns 0, or -1 on allocation failure.
  */
 int oracle_mas_batch_neg(const float* value, int32_t B, int32_t T, int32_t S,
                          const int32_t* t_x, const int32_t* t_y, float neg,
-                         uint8_t* path, float* score, int32_t* status, uint8_t* dec) {
+                         uint8_t* path, float* score, int32_t* status) {
   size_t slab = (size_t)T * (size_t)S;
   memset(path, 0, (size_t)B * slab);
-  if (dec) memset(dec, 0, (size_t)B * slab);
   for (int32_t b = 0; b < B; ++b) {
     int32_t tx = t_x[b], ty = t_y[b];
     int st = item_status(tx, ty, T, S);
@@ -139,21 +131,11 @@ int oracle_mas_batch_neg(const float* value, int32_t B, int32_t T, int32_t S,
       continue;
     }
     float* Q = (float*)malloc((size_t)tx * (size_t)ty * sizeof(float));
-    uint8_t* d = dec ? (uint8_t*)malloc((size_t)tx * (size_t)ty) : NULL;
-    if (!Q || (dec && !d)) {
-      free(Q);
-      free(d);
-      return -1;
-    }
+    if (!Q) return -1;
     float sc;
-    mas_one(value + (size_t)b * slab, S, tx, ty, neg, Q, path + (size_t)b * slab, &sc, d);
+    mas_one(value + (size_t)b * slab, S, tx, ty, neg, Q, path + (size_t)b * slab, &sc);
     if (score) score[b] = sc;
-    if (d) {
-      for (int32_t i = 0; i < tx; ++i)
-        memcpy(dec + (size_t)b * slab + (size_t)i * (size_t)S, d + (size_t)i * (size_t)ty, (size_t)ty);
-    }
     free(Q);
-    free(d);
   }
   return 0;
 }
@@ -161,7 +143,7 @@ int oracle_mas_batch_neg(const float* value, int32_t B, int32_t T, int32_t S,
 int oracle_mas_batch(const float* value, int32_t B, int32_t T, int32_t S,
                      const int32_t* t_x, const int32_t* t_y,
                      uint8_t* path, float* score, int32_t* status) {
-  return oracle_mas_batch_neg(value, B, T, S, t_x, t_y, -INFINITY, path, score, status, NULL);
+  return oracle_mas_batch_neg(value, B, T, S, t_x, t_y, -INFINITY, path, score, status);
 }
 
 /* Durations (frames per text token) of a path slab: the row sums of A*, the

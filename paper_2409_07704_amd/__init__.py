@@ -5,6 +5,7 @@ The alignment runs in hand-written HIP kernels behind the C ABI of
 entry-point names.  It never computes an alignment in Python.
 """
 from ._native import (  # noqa: F401
+    ITEM_BAD_WORKSPACE,
     ITEM_EMPTY,
     ITEM_INFEASIBLE,
     ITEM_OK,

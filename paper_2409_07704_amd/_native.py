@@ -18,14 +18,14 @@ LIB_PATH = os.path.join(_PKG, "libmas.so")
 
 MAS_OK = 0
 STATUS_NAMES = {0: "MAS_OK", 1: "MAS_ERR_NULL_POINTER", 2: "MAS_ERR_BAD_SHAPE", 3: "MAS_ERR_WORKSPACE", 4: "MAS_ERR_HIP"}
-ITEM_OK, ITEM_EMPTY, ITEM_INFEASIBLE, ITEM_OUT_OF_RANGE, ITEM_SYNC_TIMEOUT = 0, 1, 2, 3, 4
+ITEM_OK, ITEM_EMPTY, ITEM_INFEASIBLE, ITEM_OUT_OF_RANGE, ITEM_SYNC_TIMEOUT, ITEM_BAD_WORKSPACE = 0, 1, 2, 3, 4, 5
 
 # Every function declared in include/mas.h, with its ctypes signature.
 _P, _I32, _SZ = ctypes.c_void_p, ctypes.c_int32, ctypes.c_size_t
 SIGNATURES = {
     "mas_workspace_bytes": ([_I32, _I32, _I32], _SZ),
     "mas_workspace_init": ([_P, _SZ, _P], ctypes.c_int),
-    "mas_search": ([_P, _P, _P, _I32, _I32, _I32, _P, _P, _P, _P, _SZ, _P], ctypes.c_int),
+    "mas_search": ([_P, _P, _P, _I32, _I32, _I32, _P, _P, _P, _P, _P, _SZ, _P], ctypes.c_int),
     "mas_expand_path": ([_P, _I32, _I32, _I32, _P, _P], ctypes.c_int),
     "mas_forward_ex": ([_P, _P, _P, _P, _I32, _I32, _I32, _P, _P, _P, _SZ, _P], ctypes.c_int),
     "mas_forward": ([_P, _P, _P, _P, _I32, _I32, _I32, _P], ctypes.c_int),
@@ -138,17 +138,20 @@ def _workspace(ws, B, T, S, device, stream):
     return ws
 
 
-def mas_search(value, t_x, t_y, row_start_out=None, score_out=None, item_status_out=None, workspace=None, stream=None):
-    """Forward pass + backtrack; returns row_start [B, T+1] int32 (see mas.h)."""
+def mas_search(value, t_x, t_y, row_start_out=None, score_out=None, item_status_out=None, workspace=None, stream=None,
+               durations_out=None):
+    """Forward pass + backtrack without the dense path; returns row_start
+    [B, T+1] int32 (see mas.h).  durations_out [B, T] int32 is optional."""
     B, T, S, pv, px, py = _batch(value, t_x, t_y)
     if row_start_out is None:
         row_start_out = torch.empty((B, T + 1), dtype=torch.int32, device=value.device)
     prs = _dev_ptr(row_start_out, "row_start_out", torch.int32, (B, T + 1))
+    pdu = _dev_ptr(durations_out, "durations_out", torch.int32, (B, T))
     psc = _dev_ptr(score_out, "score_out", torch.float32, (B,))
     pst = _dev_ptr(item_status_out, "item_status_out", torch.int32, (B,))
     s = _stream(stream, value.device)
     ws = _workspace(workspace, B, T, S, value.device, s)
-    _check("mas_search", lib().mas_search(pv, px, py, B, T, S, prs, psc, pst, ws.ptr, ws.nbytes, s))
+    _check("mas_search", lib().mas_search(pv, px, py, B, T, S, prs, pdu, psc, pst, ws.ptr, ws.nbytes, s))
     return row_start_out
 
 

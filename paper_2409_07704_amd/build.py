@@ -41,11 +41,15 @@ def build(verbose: bool = False) -> str:
     res = subprocess.run(cmd, capture_output=True, text=True)
     # hipcc's host pass does not know the packed-fp32 feature; that warning is harmless.
     noise = "'-packed-fp32-ops' is not a recognized feature for this target (ignoring feature)"
-    err = "\n".join(l for l in res.stderr.splitlines() if noise not in l)
+    err = "\n".join(l for l in res.stderr.splitlines() if noise not in l and "warning generated" not in l
+                    and "warnings generated" not in l)
     if res.returncode != 0:
         raise RuntimeError(f"hipcc failed ({res.returncode}):\n{err}")
-    if err.strip() and verbose:
-        print(err, file=sys.stderr)
+    if err.strip():
+        # Any other diagnostic (an inline-assembly constraint the compiler
+        # cannot honour, say) fails the build.
+        os.remove(tmp)
+        raise RuntimeError(f"hipcc reported warnings:\n{err}")
     os.replace(tmp, LIB)
     return LIB
 

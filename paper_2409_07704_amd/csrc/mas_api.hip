@@ -4,6 +4,7 @@
 // kernels on the caller's stream; nothing synchronises or copies to the host.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
+#include <stdlib.h>
 
 #include "mas.h"
 #include "mas_internal.h"
@@ -14,8 +15,21 @@ static bool ws_ok(const void* ws, size_t bytes, const Layout& L) {
   return ws != nullptr && ((uintptr_t)ws % kAlign) == 0 && bytes >= L.bytes;
 }
 
+// Bound of every device-side wait, in polls without progress.  The
+// MAS_WAIT_BOUND environment variable (a positive integer) replaces it: a
+// diagnostic that lets tests drive the timeout path with small bounds.
+static int32_t wait_bound() {
+  const char* s = getenv("MAS_WAIT_BOUND");
+  if (s && *s) {
+    char* end = nullptr;
+    const long v = strtol(s, &end, 10);
+    if (end && *end == '\0' && v > 0 && v <= (1l << 30)) return (int32_t)v;
+  }
+  return kDefaultWaitBound;
+}
+
 static mas_status run(const float* value, const int32_t* t_x, const int32_t* t_y, const Layout& L,
-                      int32_t* row_start, float* score, int32_t* status, uint8_t* path, void* ws,
+                      int32_t* row_start, int32_t* durations, float* score, int32_t* status, uint8_t* path, void* ws,
                       hipStream_t stream) {
   char* base = static_cast<char*>(ws);
   KParams p;
@@ -25,9 +39,11 @@ static mas_status run(const float* value, const int32_t* t_x, const int32_t* t_y
   p.row_start = row_start;
   p.score = score;
   p.status = status;
+  p.durations = durations;
   p.path = path;
   p.hdr = reinterpret_cast<WsHeader*>(base);
   p.done = reinterpret_cast<uint32_t*>(base + L.off_done);
+  p.tmo = reinterpret_cast<uint32_t*>(base + L.off_tmo);
   p.order = reinterpret_cast<uint64_t*>(base + L.off_order);
   p.slots = reinterpret_cast<uint64_t*>(base + L.off_slots);
   p.dec = reinterpret_cast<uint32_t*>(base + L.off_dec);
@@ -40,6 +56,7 @@ static mas_status run(const float* value, const int32_t* t_x, const int32_t* t_y
   p.NB = L.NB;
   p.ntile = (L.T + kPathTileRows - 1) / kPathTileRows;
   p.path16 = path && (L.S % 16 == 0) && ((uintptr_t)path % 16 == 0);
+  p.spin_limit = wait_bound();
   return launch_mas(p, stream) == hipSuccess ? MAS_OK : MAS_ERR_HIP;
 }
 }  // namespace mas
@@ -57,17 +74,17 @@ mas_status mas_workspace_init(void* workspace, size_t workspace_bytes, hipStream
   if (!workspace) return MAS_ERR_NULL_POINTER;
   if ((uintptr_t)workspace % kAlign != 0 || workspace_bytes < sizeof(WsHeader) || workspace_bytes % 16 != 0)
     return MAS_ERR_WORKSPACE;
-  return launch_zero(workspace, workspace_bytes, stream) == hipSuccess ? MAS_OK : MAS_ERR_HIP;
+  return launch_ws_init(workspace, workspace_bytes, stream) == hipSuccess ? MAS_OK : MAS_ERR_HIP;
 }
 
 mas_status mas_search(const float* value, const int32_t* t_x, const int32_t* t_y, int32_t B, int32_t T, int32_t S,
-                      int32_t* row_start_out, float* score_out, int32_t* item_status_out, void* workspace,
-                      size_t workspace_bytes, hipStream_t stream) {
+                      int32_t* row_start_out, int32_t* durations_out, float* score_out, int32_t* item_status_out,
+                      void* workspace, size_t workspace_bytes, hipStream_t stream) {
   if (!value || !t_x || !t_y || !row_start_out) return MAS_ERR_NULL_POINTER;
   Layout L;
   if (!make_layout(B, T, S, &L)) return MAS_ERR_BAD_SHAPE;
   if (!ws_ok(workspace, workspace_bytes, L)) return MAS_ERR_WORKSPACE;
-  return run(value, t_x, t_y, L, row_start_out, score_out, item_status_out, nullptr, workspace, stream);
+  return run(value, t_x, t_y, L, row_start_out, durations_out, score_out, item_status_out, nullptr, workspace, stream);
 }
 
 mas_status mas_expand_path(const int32_t* row_start, int32_t B, int32_t T, int32_t S, uint8_t* path_out,
@@ -86,7 +103,7 @@ mas_status mas_forward_ex(const float* value, const int32_t* t_x, const int32_t*
   if (!make_layout(B, T, S, &L)) return MAS_ERR_BAD_SHAPE;
   if (!ws_ok(workspace, workspace_bytes, L)) return MAS_ERR_WORKSPACE;
   int32_t* rs = reinterpret_cast<int32_t*>(static_cast<char*>(workspace) + L.off_rs);
-  return run(value, t_x, t_y, L, rs, score_out, item_status_out, path_out, workspace, stream);
+  return run(value, t_x, t_y, L, rs, nullptr, score_out, item_status_out, path_out, workspace, stream);
 }
 
 mas_status mas_forward(const float* value, const int32_t* t_x, const int32_t* t_y, uint8_t* path_out, int32_t B,

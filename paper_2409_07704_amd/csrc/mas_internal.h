@@ -9,6 +9,8 @@
 
 namespace mas {
 
+constexpr int32_t kDefaultWaitBound = 1 << 20;  // bound of a device-side wait, in polls without progress
+
 struct KParams {
   const float* value;
   const int32_t* t_x;
@@ -16,24 +18,29 @@ struct KParams {
   int32_t* row_start;   // [B][T+1]
   float* score;         // nullable [B]
   int32_t* status;      // nullable [B]
+  int32_t* durations;   // nullable [B][T]
   uint8_t* path;        // nullable [B][T][S]; null: no path is written
   WsHeader* hdr;
   uint32_t* done;       // [B][NW] sweep finished (decision words published)
+  uint32_t* tmo;        // [B] a wave of the item gave up a wait in this call (tag)
   uint64_t* order;      // [B] items in the order their row_start tables were published: tag << 32 | item
   uint64_t* slots;      // [B][NW][NC*32]
   uint32_t* dec;        // [B][NC][TP] decision words, row-indexed
   int32_t B, T, S, NW, NC, TP, NB;
   int32_t ntile;        // path tiles per item: ceil(T / kPathTileRows)
   int32_t path16;       // path 16-byte aligned and S % 16 == 0
+  int32_t spin_limit;   // bound of a device-side wait, in polls without progress
 };
 
 // Forward sweep, backtrack and (when p.path) the dense path, in one launch:
-// one 512-thread workgroup (four sweep waves, four loader waves) per 252 text
-// rows of every item, then (when p.path) the path-writer workgroups.
+// one 576-thread workgroup (four sweep waves, four loader waves, one storer
+// wave) per 252 text rows of every item, then (when p.path) the path-writer
+// workgroups.
 hipError_t launch_mas(const KParams& p, hipStream_t stream);
 // Dense [B, T, S] u8 path from row_start [B, T+1].
 hipError_t launch_path(const int32_t* row_start, int32_t B, int32_t T, int32_t S, uint8_t* path, hipStream_t stream);
-// Zero-fill of `bytes` (a multiple of 16) at a 16-byte aligned pointer.
-hipError_t launch_zero(void* p, size_t bytes, hipStream_t stream);
+// Workspace initialisation: zero-fill of `bytes` (a multiple of 16, at least
+// the header) at a 256-byte aligned pointer, with the header's magic set.
+hipError_t launch_ws_init(void* p, size_t bytes, hipStream_t stream);
 
 }  // namespace mas

@@ -68,12 +68,44 @@ __device__ __forceinline__ uint32_t ld_dev(const uint32_t* p) { return __hip_ato
 __device__ __forceinline__ int lds_load(const int* p) { return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP); }
 __device__ __forceinline__ void lds_store(int* p, int v) { __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP); }
 __device__ __forceinline__ long long lds_load(const long long* p) { return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP); }
+template <typename T>
+__device__ __forceinline__ uint32_t lds_off(T* p) {
+  return (uint32_t)(uintptr_t)(__attribute__((address_space(3))) T*)p;
+}
+// Polled reads of mailbox words in waves that also move data into LDS with
+// buffer loads: the compiler cannot tell a mailbox word from the tiles in
+// flight and would wait for every load of the wave before each read, so these
+// reads are issued directly, each with its own wait for LDS.
+__device__ __forceinline__ int lds_poll(const int* p) {
+  int v;
+  asm volatile("ds_read_b32 %0, %1\n\ts_waitcnt lgkmcnt(0)" : "=v"(v) : "v"(lds_off(p)) : "memory");
+  return v;
+}
+__device__ __forceinline__ long long lds_poll(const long long* p) {
+  long long v;
+  asm volatile("ds_read_b64 %0, %1\n\ts_waitcnt lgkmcnt(0)" : "=v"(v) : "v"(lds_off(p)) : "memory");
+  return v;
+}
 __device__ __forceinline__ void lds_store(long long* p, long long v) { __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP); }
 
 __device__ __forceinline__ uint32_t call_tag(uint32_t gen) { return 2u * gen + 1u; }
 __device__ __forceinline__ int uni(int v) { return __builtin_amdgcn_readfirstlane(v); }
 
-constexpr int kSpinLimit = 1 << 20;  // bound of every device-side wait
+
+// State of the bounded waits of one wave: the bound (polls without progress;
+// the host may lower it, see KParams::spin_limit) and whether a wait ran out.
+// A wave whose wait runs out stops waiting from then on.  It first stores the
+// call's tag into its flag (its item's timeout flag, or the call's path-writer
+// flag) and waits for that store to land, so that the flag is visible before
+// anything the wave does afterwards: the item's walker reads it after every
+// wave whose work reaches the item's outputs has passed its last wait.
+struct Bound {
+  int limit;
+  bool out;
+  uint32_t* flag;
+  uint32_t tag;
+  __device__ __forceinline__ void expire();
+};
 constexpr int kLoaders = 4;          // loader waves per workgroup
 constexpr int kStorers = 1;         // storer waves per workgroup (decision words to memory)
 constexpr int kThreads = kThreadsPerBlock + (kLoaders + kStorers) * kWave;
@@ -137,11 +169,6 @@ struct SweepLds {
 };
 static_assert(sizeof(SweepLds) <= 160 * 1024, "LDS");
 
-template <typename T>
-__device__ __forceinline__ uint32_t lds_off(T* p) {
-  return (uint32_t)(uintptr_t)(__attribute__((address_space(3))) T*)p;
-}
-
 // ---------------------------------------------------------------- vector memory
 // Waits until at most N vector-memory operations of this wave are outstanding.
 template <int N>
@@ -180,6 +207,15 @@ __device__ __forceinline__ void vm_wait_usual(int n) {
     vm_wait_le(n);
 }
 
+__device__ __forceinline__ void Bound::expire() {
+  if (out) return;
+  out = true;
+  if (flag) {
+    st_dev(flag, tag);
+    vm_wait<0>();
+  }
+}
+
 // A buffer resource that moves forward through a region: base and number of
 // bytes left.  Loads at per-lane offsets >= the count return 0 and such
 // stores are dropped (the per-lane offset is range-checked, the scalar offset
@@ -211,33 +247,19 @@ __device__ __forceinline__ Cursor make_cursor(const void* p, uint64_t bytes) {
 // M0 + size * lane.  A scalar write of M0 needs one wait state before the
 // load.  dma16 / dma4: read-only input (default cache policy); dma16_dev /
 // dma4_dev: data written by other workgroups (device scope).
+using lds_void = __attribute__((address_space(3))) void;
+__device__ __forceinline__ lds_void* lds_at(uint32_t off) { return (lds_void*)(uintptr_t)uni((int)off); }
 __device__ __forceinline__ void dma16(uint32_t lds, __amdgpu_buffer_rsrc_t r, int voff) {
-  lds = uni(lds);
-  asm volatile("s_mov_b32 m0, %[l]\n\ts_nop 0\n\tbuffer_load_dwordx4 %[v], %[r], 0 offen lds"
-               :
-               : [l] "s"(lds), [r] "s"(r), [v] "v"(voff)
-               : "memory", "m0");
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(r, lds_at(lds), 16, voff, 0, 0, 0);
 }
 __device__ __forceinline__ void dma16_dev(uint32_t lds, __amdgpu_buffer_rsrc_t r, int voff) {
-  lds = uni(lds);
-  asm volatile("s_mov_b32 m0, %[l]\n\ts_nop 0\n\tbuffer_load_dwordx4 %[v], %[r], 0 offen sc1 lds"
-               :
-               : [l] "s"(lds), [r] "s"(r), [v] "v"(voff)
-               : "memory", "m0");
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(r, lds_at(lds), 16, voff, 0, 0, kPolicyDev);
 }
 __device__ __forceinline__ void dma4_dev(uint32_t lds, __amdgpu_buffer_rsrc_t r, int voff) {
-  lds = uni(lds);
-  asm volatile("s_mov_b32 m0, %[l]\n\ts_nop 0\n\tbuffer_load_dword %[v], %[r], 0 offen sc1 lds"
-               :
-               : [l] "s"(lds), [r] "s"(r), [v] "v"(voff)
-               : "memory", "m0");
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(r, lds_at(lds), 4, voff, 0, 0, kPolicyDev);
 }
 __device__ __forceinline__ void dma4(uint32_t lds, __amdgpu_buffer_rsrc_t r, int voff) {
-  lds = uni(lds);
-  asm volatile("s_mov_b32 m0, %[l]\n\ts_nop 0\n\tbuffer_load_dword %[v], %[r], 0 offen lds"
-               :
-               : [l] "s"(lds), [r] "s"(r), [v] "v"(voff)
-               : "memory", "m0");
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(r, lds_at(lds), 4, voff, 0, 0, 0);
 }
 
 // ---------------------------------------------------------------- recurrence
@@ -383,39 +405,38 @@ __device__ __forceinline__ WaveCtx make_ctx(int b, int g, int w, int lane, int t
   return x;
 }
 
-// Waits (bounded) until flag[k] == tag for every k in [0, n).
-__device__ __forceinline__ void wait_flags(const uint32_t* flag, int n, uint32_t tag, int lane, bool& timed_out) {
+// Waits (bounded) until flag[k] == tag for every k in [0, n).  The bound
+// counts polls since a flag last went up.
+__device__ __forceinline__ void wait_flags(const uint32_t* flag, int n, uint32_t tag, int lane, Bound& bd) {
   for (int k0 = 0; k0 < n; k0 += kWave) {
     const int k = k0 + lane;
     int spins = 0;
-    while (!timed_out) {
+    uint64_t missing = ~0ull;
+    while (!bd.out) {
       const bool ready = k >= n || ld_dev(flag + k) == tag;
-      if (__builtin_amdgcn_ballot_w64(!ready) == 0) break;
-      if (++spins > kSpinLimit) timed_out = true;
+      const uint64_t m = __builtin_amdgcn_ballot_w64(!ready);
+      if (m == 0) break;
+      spins = m != missing ? 0 : spins + 1;
+      missing = m;
+      if (spins > bd.limit) bd.expire();
       __builtin_amdgcn_s_sleep(2);
     }
   }
 }
 
 // Spins (bounded) until the LDS word *p >= v; returns the last value read.
-__device__ __forceinline__ int wait_at_least(const int* p, int v, bool& timed_out) {
-  int seen = uni(lds_load(p));
+// The bound counts polls since the word last changed.
+__device__ __forceinline__ int wait_at_least(const int* p, int v, Bound& bd) {
+  int seen = uni(lds_poll(p));
   int spins = 0;
-  while (seen < v && !timed_out) {
-    if (++spins > kSpinLimit) timed_out = true;
+  while (seen < v && !bd.out) {
     __builtin_amdgcn_s_sleep(1);
-    seen = uni(lds_load(p));
+    const int now = uni(lds_poll(p));
+    spins = now != seen ? 0 : spins + 1;
+    seen = now;
+    if (spins > bd.limit) bd.expire();
   }
   return seen;
-}
-
-// Spins (bounded) until the LDS word *p == v.
-__device__ __forceinline__ void wait_equal(const int* p, int v, bool& timed_out) {
-  int spins = 0;
-  while (uni(lds_load(p)) != v && !timed_out) {
-    if (++spins > kSpinLimit) timed_out = true;
-    __builtin_amdgcn_s_sleep(1);
-  }
 }
 
 using lds_cchar = const __attribute__((address_space(3))) char;
@@ -501,7 +522,7 @@ __device__ __forceinline__ f32x4 gather_last_row(const float (&q)[kChunk]) {
 // chunk's last row to the consumer, and then checks the mailbox: it only
 // waits when the tile or the boundary row of chunk c+1 was not there yet.
 template <int IN, int OUT>
-__device__ __forceinline__ float sweep_wave(const KParams& p, SweepLds& L, const WaveCtx& x, uint32_t tag, bool& timed_out) {
+__device__ __forceinline__ float sweep_wave(const KParams& p, SweepLds& L, const WaveCtx& x, uint32_t tag, Bound& bd) {
   constexpr bool IN1 = IN == 1;
   const int lane = x.lane, w = x.w;
   float t = -0.0f;  // lane 0 keeps -0 for the whole sweep (see cols8)
@@ -553,7 +574,7 @@ __device__ __forceinline__ float sweep_wave(const KParams& p, SweepLds& L, const
   // so that the first cell comes out as -0 + value[0][0] = value[0][0]
   // exactly (its predecessors are -inf and -0, their max -0).
   float q = (IN == 0 && lane == 1) ? -0.0f : neg_inf();
-  if (IN1) wait_at_least(my_box + 1, x.c_begin, timed_out);
+  if (IN1) wait_at_least(my_box + 1, x.c_begin, bd);
   if (IN != 0) {
     wave_lds_sync();
     const float e = bound_ptr(kRing - 1)[kChunk - 1];
@@ -565,8 +586,8 @@ __device__ __forceinline__ float sweep_wave(const KParams& p, SweepLds& L, const
   // The first chunk's tile and boundary row.  Values alternate between two
   // register sets by ring position: chunk c uses set (c - c_begin) % 2.
   f32x4 va[8], vb[8];
-  wait_at_least(my_box + 0, x.c_begin + 1, timed_out);
-  if (IN1 && x.c_begin < x.prev_end) wait_at_least(my_box + 1, x.c_begin + 1, timed_out);
+  wait_at_least(my_box + 0, x.c_begin + 1, bd);
+  if (IN1 && x.c_begin < x.prev_end) wait_at_least(my_box + 1, x.c_begin + 1, bd);
   int cons_seen;  // the consumer's progress as last read (OUT1)
   {
     // (Through the same inline-assembly reads as the loop: values the
@@ -593,7 +614,7 @@ __device__ __forceinline__ float sweep_wave(const KParams& p, SweepLds& L, const
   auto hand_off = [&](int cp) __attribute__((always_inline)) {
     const bool real = cp >= x.next_begin - 1;
     if (OUT == 1) {
-      if (real && cons_seen < cp - (kRing - 1)) cons_seen = wait_at_least(my_box + 2, cp - (kRing - 1), timed_out);
+      if (real && cons_seen < cp - (kRing - 1)) cons_seen = wait_at_least(my_box + 2, cp - (kRing - 1), bd);
       const int kn = (cp - x.next_begin) & (kRing - 1);
       const uint32_t ns = real ? wbase + kWaveRegion + (uint32_t)kn * kSlotStride + kBoundOff : sink;
       lds_put_hi8(ns + 16u * (uint32_t)(lane - (kWave - 8)), gather_last_row(qc));
@@ -630,7 +651,7 @@ __device__ __forceinline__ float sweep_wave(const KParams& p, SweepLds& L, const
     // The slot's decision words of chunk c-4 must have been taken (mailbox
     // .w, read with this step's mailbox; rarely not yet).
     if (uni(mb.w) < c - (kRing - 1)) {
-      wait_at_least(my_box + 3, c - (kRing - 1), timed_out);
+      wait_at_least(my_box + 3, c - (kRing - 1), bd);
       lgkm_wait0();
     }
     bits_ptr(J)[lane] = bits;
@@ -644,8 +665,8 @@ __device__ __forceinline__ float sweep_wave(const KParams& p, SweepLds& L, const
       // were there when they were issued; otherwise wait and read again.
       if (OUT == 1) cons_seen = max(cons_seen, uni(mb.z));
       if (uni(mb.x) < c + 2 || (need_prod && uni(mb.y) < c + 2)) {
-        wait_at_least(my_box + 0, c + 2, timed_out);
-        if (need_prod) wait_at_least(my_box + 1, c + 2, timed_out);
+        wait_at_least(my_box + 0, c + 2, bd);
+        if (need_prod) wait_at_least(my_box + 1, c + 2, bd);
         read_ahead<J1>(Lb, box_off, ra, vn, mb);
         lgkm_wait0();
       }
@@ -715,7 +736,9 @@ __device__ __forceinline__ void mask_tile(uint32_t slot, int g, int c, int lane)
     lds_f4* const a = (lds_f4*)(uintptr_t)(slot + (uint32_t)lane * 128u + 16u * (uint32_t)(pc ^ swz(lane)));
     f32x4 v = {ninf, ninf, ninf, ninf};
     if (4 * pc + 4 > nm) {
-      const f32x4 old = *a;
+      // (the piece has landed; other tiles may still be in flight)
+      f32x4 old;
+      asm volatile("ds_read_b128 %0, %1\n\ts_waitcnt lgkmcnt(0)" : "=v"(old) : "v"((uint32_t)(uintptr_t)a) : "memory");
       v.y = 4 * pc + 1 < nm ? ninf : old.y;
       v.z = 4 * pc + 2 < nm ? ninf : old.z;
       v.w = old.w;
@@ -743,7 +766,7 @@ __device__ __forceinline__ void mask_tile(uint32_t slot, int g, int c, int lane)
 // steps waits for a global load (which would also wait for its own
 // write-through stores).
 template <bool ALIGNED, bool BOUND>
-__device__ __forceinline__ void load_tiles(const KParams& p, SweepLds& L, const WaveCtx& x, uint32_t tag, bool& timed_out) {
+__device__ __forceinline__ void load_tiles(const KParams& p, SweepLds& L, const WaveCtx& x, uint32_t tag, Bound& bd) {
   const int lane = x.lane, w = x.w;
   const float* slab = p.value + (size_t)x.b * (size_t)p.T * (size_t)p.S;
   const uint64_t slab_bytes = (uint64_t)p.T * (uint64_t)p.S * 4u;
@@ -776,11 +799,11 @@ __device__ __forceinline__ void load_tiles(const KParams& p, SweepLds& L, const 
   const uint64_t* const bsrc = p.slots + ((size_t)x.b * p.NW + (x.g > 0 ? x.g - 1 : 0)) * ((size_t)p.NC * kChunk);
   const uint32_t prod_addr = lds_off(&L.box[w]) + 4u;
   int bspins = 0;
-  while ((readied < x.c_end || bnext < bend) && !timed_out) {
+  while ((readied < x.c_end || bnext < bend) && !bd.out) {
     // Issue while slots are free (the slot of chunk c held chunk c-4).
     while (issued < x.c_end && issued - readied < kInflight) {
       if (issued > cons + kRing - 1) {
-        cons = uni(lds_load(progress));
+        cons = uni(lds_poll(progress));
         if (issued > cons + kRing - 1) break;
       }
       const __amdgpu_buffer_rsrc_t r = vr.rsrc_s();
@@ -804,7 +827,7 @@ __device__ __forceinline__ void load_tiles(const KParams& p, SweepLds& L, const 
       }
     }
     if (BOUND && bnext < bend) {
-      if (bnext > cons + kRing - 1) cons = uni(lds_load(progress));
+      if (bnext > cons + kRing - 1) cons = uni(lds_poll(progress));
       if (bnext <= cons + kRing - 1) {
         // Lane l polls column l % 32 of chunks bnext + l / 32 (load A) and
         // bnext + 2 + l / 32 (load B), the last chunk again past the end;
@@ -836,8 +859,10 @@ __device__ __forceinline__ void load_tiles(const KParams& p, SweepLds& L, const 
         }
         if (bnext == c0) {
           // Not published yet.
-          if (++bspins > kSpinLimit) timed_out = true;
+          if (++bspins > bd.limit) bd.expire();
           __builtin_amdgcn_s_sleep(1);
+        } else {
+          bspins = 0;
         }
         continue;
       }
@@ -845,7 +870,7 @@ __device__ __forceinline__ void load_tiles(const KParams& p, SweepLds& L, const 
     if (issued == readied) {
       // Nothing in flight and no free slot: wait for the sweep wave.
       const int need = BOUND && bnext < bend ? min(issued, bnext) : issued;
-      cons = wait_at_least(progress, need - (kRing - 1), timed_out);
+      cons = wait_at_least(progress, need - (kRing - 1), bd);
       continue;
     }
     // The oldest tile in flight has landed once at most the younger ones
@@ -918,7 +943,7 @@ __device__ __forceinline__ uint32_t walk_chunk(uint32_t w, uint32_t wh, int sl, 
 // ends 63 rows above the walker's row at issue time: the walk cannot descend
 // past the window before it reaches the chunk.  Stops early once the walker
 // has reached row 0.
-__device__ __forceinline__ void load_windows(const KParams& p, SweepLds& L, int b, int ty, int k, int lane, bool& timed_out) {
+__device__ __forceinline__ void load_windows(const KParams& p, SweepLds& L, int b, int ty, int k, int lane, Bound& bd) {
   const int C = (ty + kChunk - 1) / kChunk;
   const uint32_t* db = p.dec + (size_t)b * p.NC * (size_t)p.TP;
   const uint64_t chunk_bytes = (uint64_t)p.TP * 4u;
@@ -927,12 +952,12 @@ __device__ __forceinline__ void load_windows(const KParams& p, SweepLds& L, int 
   constexpr int kStep = kWinLoaders;
   // Own chunks above `issued` are issued; own chunks >= `readied` are staged.
   int issued = C - 1 - k, readied = C - 1 - k + kStep;
-  long long wpos = lds_load(&L.wpos);
+  long long wpos = lds_poll(&L.wpos);
   int spins = 0;
-  while (readied - kStep >= 0 && wpos >= 0 && !timed_out) {
+  while (readied - kStep >= 0 && wpos >= 0 && !bd.out) {
     while (issued >= 0 && readied - kStep - issued < kStep * kWinAhead) {
       if ((int)(wpos >> 32) > issued + kNWin) {
-        wpos = lds_load(&L.wpos);
+        wpos = lds_poll(&L.wpos);
         if (wpos < 0 || (int)(wpos >> 32) > issued + kNWin) break;
       }
       const int e = uni((int)(uint32_t)wpos);
@@ -945,13 +970,14 @@ __device__ __forceinline__ void load_windows(const KParams& p, SweepLds& L, int 
       for (int q = 0; q < kWinRows / 256; ++q)
         dma16_dev(win0 + (uint32_t)slot * (kWinRows * 4) + 1024u * q, r, 16 * lane + 1024 * q);
       issued -= kStep;
+      spins = 0;
     }
     const int inflight = (readied - kStep - issued) / kStep;
     if (inflight == 0) {
       // Nothing in flight: wait for the walker to free a slot.
-      if (++spins > kSpinLimit) timed_out = true;
+      if (++spins > bd.limit) bd.expire();
       __builtin_amdgcn_s_sleep(1);
-      wpos = lds_load(&L.wpos);
+      wpos = lds_poll(&L.wpos);
       continue;
     }
     vm_wait_usual<(kWinRows / 256) * (kWinAhead - 1)>((kWinRows / 256) * (inflight - 1));
@@ -961,14 +987,11 @@ __device__ __forceinline__ void load_windows(const KParams& p, SweepLds& L, int 
   vm_wait<0>();
 }
 
-// Lane l of a becomes x and lane l of b becomes y (x, y, l wave-uniform, l
-// in [0, 63]); the lane select goes through M0 (one VALU operand may read one
-// SGPR besides M0).
+// Lane l of a becomes x and lane l of b becomes y (x, y, l wave-uniform).
 __device__ __forceinline__ void write_lanes(uint32_t& a, uint32_t x, int& b, int y, int l) {
-  asm volatile("s_mov_b32 m0, %4\n\ts_nop 0\n\tv_writelane_b32 %0, %2, m0\n\tv_writelane_b32 %1, %3, m0"
-               : "+v"(a), "+v"(b)
-               : "s"(x), "s"(y), "s"(l)
-               : "m0");
+  const bool mine = (int)__lane_id() == l;
+  a = mine ? x : a;
+  b = mine ? y : b;
 }
 
 // Row starts from the walk's records of up to 64 chunks: lane k holds the
@@ -1007,7 +1030,7 @@ __device__ __forceinline__ void flush_records(int* rsl, int base, int lo, int hi
 // BANDED: T > kWinRows, windows start at their own first rows (row 0
 // otherwise).
 template <bool BANDED>
-__device__ __forceinline__ void walk(const KParams& p, SweepLds& L, int tx, int ty, int lane, bool& timed_out) {
+__device__ __forceinline__ void walk(const KParams& p, SweepLds& L, int tx, int ty, int lane, Bound& bd) {
   int* rsl = L.u.walk.rs;
   constexpr bool banded = BANDED;
   int idx = tx - 1;                    // row of the path at the chunk's last column
@@ -1029,14 +1052,14 @@ __device__ __forceinline__ void walk(const KParams& p, SweepLds& L, int tx, int 
   // Waits (bounded) until the windows of chunks >= ch are in LDS.
   auto ensure = [&](int ch) __attribute__((always_inline)) {
     int spins = 0;
-    while (!staged(ch) && !timed_out) {
+    while (!staged(ch) && !bd.out) {
       const i32x4 r = *reinterpret_cast<const volatile i32x4*>(&L.wready);
       kn0 = uni(r.x);
       kn1 = uni(r.y);
       kn2 = uni(r.z);
       kn3 = uni(r.w);
       if (staged(ch)) break;
-      if (++spins > kSpinLimit) timed_out = true;
+      if (++spins > bd.limit) bd.expire();
       __builtin_amdgcn_s_sleep(1);
     }
   };
@@ -1175,18 +1198,25 @@ __device__ __forceinline__ void write_path_rows(const KParams& p, int b, int r0,
 }
 
 // The item published k-th in this call (its entry in the completion order
-// carries the call's tag), or -1 once the bounded wait times out.
-__device__ __forceinline__ int wait_published(const KParams& p, int k, uint32_t tag, bool& timed_out) {
-  int spins = 0;
+// carries the call's tag), or -1 once the bounded wait times out.  That wait
+// spans whole sweeps and walks, so its bound grows with the longest item
+// (limit polls per 256 chunks).
+__device__ __forceinline__ int wait_published(const KParams& p, int k, uint32_t tag, int64_t limit, Bound& bd) {
+  int64_t spins = 0;
   for (;;) {
     const uint64_t e = __hip_atomic_load(p.order + k, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     if ((uint32_t)(e >> 32) == tag) {
       const int b = (int)(uint32_t)e;
       return b < p.B ? b : -1;
     }
-    if (timed_out || ++spins > kSpinLimit) {
-      timed_out = true;
-      return -1;
+    if (bd.out) return -1;
+    if (++spins > limit) {
+      // Raise the call's flag, then look once more: an item published after
+      // this point reads the flag and reports itself as timed out.
+      bd.expire();
+      const uint64_t e2 = __hip_atomic_load(p.order + k, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      const int b = (int)(uint32_t)e2;
+      return (uint32_t)(e2 >> 32) == tag && b < p.B ? b : -1;
     }
     __builtin_amdgcn_s_sleep(2);
   }
@@ -1197,9 +1227,15 @@ __device__ __forceinline__ int wait_published(const KParams& p, int k, uint32_t 
 // waits for that item, writes the tile (each wave an equal share of its rows)
 // and goes on until the tiles run out.  The next tile is taken while this one
 // is written.
-__device__ __forceinline__ void path_writer(const KParams& p, SweepLds& L, uint32_t tag, int wv, int lane, bool& timed_out) {
+__device__ __forceinline__ void path_writer(const KParams& p, SweepLds& L, uint32_t tag, int wv, int lane, Bound& bd) {
   constexpr int kWaves = kThreads / kWave;
   const int ntiles = p.B * p.ntile;
+  int max_chunks = 0;
+  for (int i = lane; i < p.B; i += kWave)
+    if (item_status(p.t_x[i], p.t_y[i], p.T, p.S) == kItemOk) max_chunks = max(max_chunks, (p.t_y[i] + kChunk - 1) / kChunk);
+#pragma unroll
+  for (int off = kWave / 2; off >= 1; off >>= 1) max_chunks = max(max_chunks, __shfl_xor(max_chunks, off));
+  const int64_t limit = (int64_t)bd.limit * (1 + uni(max_chunks) / 256);
   if (threadIdx.x == 0)
     L.tile = (int)__hip_atomic_fetch_add(&p.hdr->tile_next, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   __syncthreads();
@@ -1214,7 +1250,7 @@ __device__ __forceinline__ void path_writer(const KParams& p, SweepLds& L, uint3
     const int per = (q1 - q0 + kWaves - 1) / kWaves;
     const int r0 = min(q0 + wv * per, q1), r1 = min(r0 + per, q1);
     if (r1 > r0) {
-      const int b = wait_published(p, k, tag, timed_out);
+      const int b = wait_published(p, k, tag, limit, bd);
       if (b >= 0) write_path_rows(p, b, r0, r1, lane);
     }
     if (threadIdx.x == 0) L.tile = (int)next;
@@ -1234,7 +1270,7 @@ __device__ __forceinline__ void path_writer(const KParams& p, SweepLds& L, uint3
 // loaders' traffic to issue its store, and out of the loaders, whose waits
 // count their own loads only.
 __device__ __forceinline__ void storer_role(const KParams& p, SweepLds& L, int b, int r, int tx, int ty, int lane, uint32_t tag,
-                                            bool& timed_out) {
+                                            Bound& bd) {
   const __amdgpu_buffer_rsrc_t dr =
       make_cursor(p.dec + (size_t)b * p.NC * (size_t)p.TP, (uint64_t)p.NC * p.TP * 4u).rsrc();
   const int dstride = p.TP * 4;
@@ -1252,13 +1288,13 @@ __device__ __forceinline__ void storer_role(const KParams& p, SweepLds& L, int b
     if (xw.g <= xw.g_last && cend[w] == cbeg[w] && lane == 0) st_dev(p.done + (size_t)b * p.NW + xw.g, tag);
   }
   int spins = 0;
-  while (left > 0 && !timed_out) {
+  while (left > 0 && !bd.out) {
     bool moved = false;
 #pragma unroll
     for (int w = 0; w < kWavesPerBlock; ++w) {
       if (taken[w] >= cend[w]) continue;
       const int* const progress = w > 0 ? reinterpret_cast<const int*>(&L.box[w - 1]) + 2 : &L.cons0;
-      const int cons = uni(lds_load(progress));
+      const int cons = uni(lds_poll(progress));
       while (taken[w] < cend[w] && cons >= taken[w] + 2) {
         const uint32_t* const src = reinterpret_cast<const uint32_t*>(
             &L.u.ring[w][((taken[w] - cbeg[w]) & (kRing - 1)) * kSlotStride + kBitsOff]);
@@ -1275,8 +1311,10 @@ __device__ __forceinline__ void storer_role(const KParams& p, SweepLds& L, int b
       }
     }
     if (!moved) {
-      if (++spins > kSpinLimit) timed_out = true;
+      if (++spins > bd.limit) bd.expire();
       __builtin_amdgcn_s_sleep(1);
+    } else {
+      spins = 0;
     }
   }
 }
@@ -1300,45 +1338,57 @@ __device__ __forceinline__ bool walker_workgroup(const WaveCtx& x) {
   return x.g / kWavesPerBlock == x.g_last / kWavesPerBlock;
 }
 
-__device__ __forceinline__ void sweep_role(const KParams& p, SweepLds& L, const WaveCtx& x, uint32_t tag, bool& timed_out) {
+__device__ __forceinline__ void sweep_role(const KParams& p, SweepLds& L, const WaveCtx& x, uint32_t tag, Bound& bd) {
   const int lane = x.lane, b = x.b, g = x.g, w = x.w, g_last = x.g_last;
   if (g > g_last) return;  // no rows of the alignment here
-  if (g == 0 && lane == 0 && p.status) p.status[b] = kItemOk;
   float score;
   if (g == g_last) {
-    score = g == 0 ? sweep_wave<0, 0>(p, L, x, tag, timed_out) : sweep_wave<1, 0>(p, L, x, tag, timed_out);
+    score = g == 0 ? sweep_wave<0, 0>(p, L, x, tag, bd) : sweep_wave<1, 0>(p, L, x, tag, bd);
   } else if (w < kWavesPerBlock - 1) {
-    score = g == 0 ? sweep_wave<0, 1>(p, L, x, tag, timed_out) : sweep_wave<1, 1>(p, L, x, tag, timed_out);
+    score = g == 0 ? sweep_wave<0, 1>(p, L, x, tag, bd) : sweep_wave<1, 1>(p, L, x, tag, bd);
   } else {
-    score = sweep_wave<1, 2>(p, L, x, tag, timed_out);
+    score = sweep_wave<1, 2>(p, L, x, tag, bd);
   }
   if (g != g_last) return;
 
   // The walker.
   if (lane == (x.tx - 1) - g_last * kRowsPerWave + 1 && p.score) p.score[b] = score;
   if (p.T > kWinRows)
-    walk<true>(p, L, x.tx, x.ty, lane, timed_out);
+    walk<true>(p, L, x.tx, x.ty, lane, bd);
   else
-    walk<false>(p, L, x.tx, x.ty, lane, timed_out);
+    walk<false>(p, L, x.tx, x.ty, lane, bd);
   int32_t* rs_out = p.row_start + (size_t)b * ((size_t)p.T + 1);
-  for (int i = lane; i <= p.T; i += kWave) st_dev(reinterpret_cast<uint32_t*>(rs_out + i), (uint32_t)L.u.walk.rs[i]);
+  const int* const rsl = L.u.walk.rs;
+  for (int i = lane; i <= p.T; i += kWave) st_dev(reinterpret_cast<uint32_t*>(rs_out + i), (uint32_t)rsl[i]);
+  if (p.durations) {
+    // Frames per text row (Sec. 2: what the duration predictor learns): the
+    // row's span of columns; 0 for rows past t_x.
+    int32_t* d = p.durations + (size_t)b * (size_t)p.T;
+    for (int i = lane; i < p.T; i += kWave) d[i] = rsl[i + 1] - rsl[i];
+  }
   publish_item(p, b, tag, lane);
+  // The item's status, once every wave whose work reaches its outputs has
+  // passed its last wait: timed out if any of them (or this walker) gave up,
+  // or if a path writer gave up before the publication became visible to it.
+  vm_wait<0>();
+  const bool tmo = bd.out || ld_dev(p.tmo + b) == tag || ld_dev(&p.hdr->path_fail) == tag;
+  if (lane == 0 && p.status) p.status[b] = tmo ? kItemSyncTimeout : kItemOk;
 }
 
 template <bool ALIGNED>
-__device__ __forceinline__ void loader_role(const KParams& p, SweepLds& L, const WaveCtx& x, uint32_t tag, bool& timed_out) {
+__device__ __forceinline__ void loader_role(const KParams& p, SweepLds& L, const WaveCtx& x, uint32_t tag, Bound& bd) {
   const int lane = x.lane, b = x.b, g = x.g, g_last = x.g_last;
   if (g <= g_last) {
     if (g > 0 && x.w == 0)
-      load_tiles<ALIGNED, true>(p, L, x, tag, timed_out);
+      load_tiles<ALIGNED, true>(p, L, x, tag, bd);
     else
-      load_tiles<ALIGNED, false>(p, L, x, tag, timed_out);
+      load_tiles<ALIGNED, false>(p, L, x, tag, bd);
   }
   if (!walker_workgroup(x)) return;
   // Decision windows for the walk, once every wave of the item has published
   // its words.
-  wait_flags(p.done + (size_t)b * p.NW, g_last + 1, tag, lane, timed_out);
-  load_windows(p, L, b, x.ty, x.w, lane, timed_out);
+  wait_flags(p.done + (size_t)b * p.NW, g_last + 1, tag, lane, bd);
+  load_windows(p, L, b, x.ty, x.w, lane, bd);
 }
 
 // Items with invalid lengths: an all-zero slab, zero row_start, score -inf.
@@ -1346,6 +1396,8 @@ __device__ __forceinline__ void invalid_item(const KParams& p, int b, int g, boo
   if (is_loader || g != 0) return;
   int32_t* rs_out = p.row_start + (size_t)b * ((size_t)p.T + 1);
   for (int i = lane; i <= p.T; i += kWave) st_dev(reinterpret_cast<uint32_t*>(rs_out + i), 0u);
+  if (p.durations)
+    for (int i = lane; i < p.T; i += kWave) p.durations[(size_t)b * (size_t)p.T + i] = 0;
   if (lane == 0) {
     if (p.score) p.score[b] = neg_inf();
     if (p.status) p.status[b] = st;
@@ -1377,14 +1429,20 @@ __device__ __forceinline__ void finish_call(const KParams& p, uint32_t gen) {
 template <bool ALIGNED>
 __global__ void __launch_bounds__(kThreads, 1) mas_kernel(KParams p) {
   __shared__ SweepLds L;
+  if (__hip_atomic_load(&p.hdr->magic, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != kWsMagic) {
+    // Not an initialised workspace: report it and touch nothing else.
+    if (blockIdx.x == 0 && p.status)
+      for (int i = threadIdx.x; i < p.B; i += blockDim.x) p.status[i] = kItemBadWorkspace;
+    return;
+  }
   const uint32_t gen = __hip_atomic_load(&p.hdr->gen, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   const uint32_t tag = call_tag(gen);
-  bool timed_out = false;
   const int sid = blockIdx.x;
   if (sid >= p.B * p.NB) {
     // A path writer.
-    path_writer(p, L, tag, uni(threadIdx.x / kWave), threadIdx.x & (kWave - 1), timed_out);
-    if (timed_out) __hip_atomic_store(&p.hdr->error, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    Bound bd{p.spin_limit, false, &p.hdr->path_fail, tag};
+    path_writer(p, L, tag, uni(threadIdx.x / kWave), threadIdx.x & (kWave - 1), bd);
+    if (bd.out) __hip_atomic_store(&p.hdr->error, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     finish_call(p, gen);
     return;
   }
@@ -1399,6 +1457,7 @@ __global__ void __launch_bounds__(kThreads, 1) mas_kernel(KParams p) {
   const int tx = p.t_x[b];
   const int ty = p.t_y[b];
   const int st = item_status(tx, ty, p.T, p.S);
+  Bound bd{p.spin_limit, false, p.tmo + b, tag};
 
   // Workgroup set-up: the LDS holds whatever earlier workgroups left.
   if (threadIdx.x < kWavesPerBlock) {
@@ -1418,18 +1477,15 @@ __global__ void __launch_bounds__(kThreads, 1) mas_kernel(KParams p) {
   if (st != kItemOk) {
     invalid_item(p, b, g, is_loader || is_storer, lane, st, tag);
   } else if (is_storer) {
-    storer_role(p, L, b, r, tx, ty, lane, tag, timed_out);
+    storer_role(p, L, b, r, tx, ty, lane, tag, bd);
   } else {
     const WaveCtx x = make_ctx(b, g, w, lane, tx, ty);
     if (is_loader)
-      loader_role<ALIGNED>(p, L, x, tag, timed_out);
+      loader_role<ALIGNED>(p, L, x, tag, bd);
     else
-      sweep_role(p, L, x, tag, timed_out);
+      sweep_role(p, L, x, tag, bd);
   }
-  if (timed_out) {
-    if (p.status) p.status[b] = kItemSyncTimeout;
-    __hip_atomic_store(&p.hdr->error, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-  }
+  if (bd.out) __hip_atomic_store(&p.hdr->error, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   finish_call(p, gen);
 }
 
@@ -1465,9 +1521,11 @@ __global__ void __launch_bounds__(256) mas_path_kernel1(const int32_t* __restric
 }
 
 // ---------------------------------------------------------------- workspace fill
-__global__ void __launch_bounds__(256) mas_zero_kernel(uint4* __restrict__ p, size_t n16) {
+// Zeros, except the header's magic word (its 16-byte piece is written by one
+// thread, whole).
+__global__ void __launch_bounds__(256) mas_ws_init_kernel(uint4* __restrict__ p, size_t n16) {
   for (size_t k = (size_t)blockIdx.x * blockDim.x + threadIdx.x; k < n16; k += (size_t)gridDim.x * blockDim.x)
-    p[k] = make_uint4(0u, 0u, 0u, 0u);
+    p[k] = k == (size_t)kWsMagicPiece ? make_uint4(0u, kWsMagic, 0u, 0u) : make_uint4(0u, 0u, 0u, 0u);
 }
 
 // ---------------------------------------------------------------- launchers
@@ -1500,9 +1558,10 @@ hipError_t launch_path(const int32_t* row_start, int32_t B, int32_t T, int32_t S
   return hipGetLastError();
 }
 
-hipError_t launch_zero(void* p, size_t bytes, hipStream_t stream) {
+hipError_t launch_ws_init(void* p, size_t bytes, hipStream_t stream) {
+  static_assert(offsetof(WsHeader, magic) == 16 * kWsMagicPiece + 4, "magic is the second word of its piece");
   const size_t n16 = bytes / 16;
-  hipLaunchKernelGGL(mas_zero_kernel, dim3(stream_grid(n16, 256)), dim3(256), 0, stream, reinterpret_cast<uint4*>(p), n16);
+  hipLaunchKernelGGL(mas_ws_init_kernel, dim3(stream_grid(n16, 256)), dim3(256), 0, stream, reinterpret_cast<uint4*>(p), n16);
   return hipGetLastError();
 }
 

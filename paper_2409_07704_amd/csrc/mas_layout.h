@@ -3,8 +3,8 @@
 // Rows of an item are processed by 64-lane waves.  Lane 0 of wave g carries
 // the row above the wave (row 63g-1, a copy handed down by the previous
 // wave; for g = 0 the virtual -inf row above row 0) and lanes 1..63 own
-// rows 63g .. 63g+62, one text row per lane.  Four waves form a 256-thread
-// workgroup.  Speech columns are processed in chunks of 32, and every lane
+// rows 63g .. 63g+62, one text row per lane.  Four such waves (252 rows)
+// share a workgroup with the waves that feed them.  Speech columns are processed in chunks of 32, and every lane
 // packs its row's 32 forward decisions of a chunk into one 32-bit word.
 #pragma once
 
@@ -47,8 +47,12 @@ struct WsHeader {
   uint32_t error;       // sticky: non-zero once a device-side wait timed out
   uint32_t walk_count;  // row_start tables published in the current call
   uint32_t tile_next;   // path tiles taken in the current call
-  uint32_t pad[59];
+  uint32_t magic;       // kWsMagic once the workspace has been initialised
+  uint32_t path_fail;   // tag of the last call in which a path writer gave up a wait
+  uint32_t pad[57];
 };
+constexpr uint32_t kWsMagic = 0x3153414du;  // "MAS1"
+constexpr int kWsMagicPiece = 1;            // the header's 16-byte piece holding magic (bytes 16..31)
 static_assert(sizeof(WsHeader) == kAlign, "header is one alignment unit");
 
 __host__ __device__ inline size_t round_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
@@ -60,6 +64,7 @@ struct Layout {
   int32_t NC;      // decision chunks per item = ceil(S / 32)
   int32_t TP;      // decision words per chunk of an item (rows + scratch, multiple of 64)
   size_t off_done;   // uint32 [B][NW] sweep-finished flags (tag values)
+  size_t off_tmo;    // uint32 [B] per-item timeout flags (tag values)
   size_t off_order;  // uint64 [B] items in the order their row_start tables were published: tag << 32 | item
   size_t off_slots;  // uint64 [B][NW][NC*32] boundary hand-off words
   size_t off_dec;    // uint32 [B][NC][TP] decision words
@@ -85,6 +90,8 @@ __host__ inline bool make_layout(int32_t B, int32_t T, int32_t S, Layout* L) {
   size_t off = sizeof(WsHeader);
   L->off_done = off;
   off = round_up(off + (size_t)B * L->NW * sizeof(uint32_t), kAlign);
+  L->off_tmo = off;
+  off = round_up(off + (size_t)B * sizeof(uint32_t), kAlign);
   L->off_order = off;
   off = round_up(off + (size_t)B * sizeof(uint64_t), kAlign);
   L->off_slots = off;
@@ -98,7 +105,14 @@ __host__ inline bool make_layout(int32_t B, int32_t T, int32_t S, Layout* L) {
 }
 
 // Per-item status codes (same values as MAS_ITEM_* in the public header).
-enum ItemStatus : int32_t { kItemOk = 0, kItemEmpty = 1, kItemInfeasible = 2, kItemOutOfRange = 3, kItemSyncTimeout = 4 };
+enum ItemStatus : int32_t {
+  kItemOk = 0,
+  kItemEmpty = 1,
+  kItemInfeasible = 2,
+  kItemOutOfRange = 3,
+  kItemSyncTimeout = 4,
+  kItemBadWorkspace = 5
+};
 
 __host__ __device__ inline int32_t item_status(int32_t tx, int32_t ty, int32_t T, int32_t S) {
   if (tx < 0 || ty < 0 || tx > T || ty > S) return kItemOutOfRange;

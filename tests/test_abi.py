@@ -36,7 +36,7 @@ def test_library_exports_every_declared_symbol():
 
 
 def test_version_and_status_strings():
-    assert mas.mas_version() == 1
+    assert mas.mas_version() == 2
     assert mas.mas_status_string(0) == "MAS_OK"
     assert mas.mas_status_string(3) == "MAS_ERR_WORKSPACE"
     assert mas.mas_status_string(99) == "MAS_ERR_UNKNOWN"
@@ -66,14 +66,15 @@ FAKE = ctypes.c_void_p(0x10000)  # never dereferenced: validation fails first
 @pytest.mark.parametrize(
     "args,code",
     [
-        ((None, FAKE, FAKE, 1, 1, 1, FAKE, None, None, FAKE, 1 << 20, None), 1),
-        ((FAKE, None, FAKE, 1, 1, 1, FAKE, None, None, FAKE, 1 << 20, None), 1),
-        ((FAKE, FAKE, FAKE, 1, 1, 1, None, None, None, FAKE, 1 << 20, None), 1),
-        ((FAKE, FAKE, FAKE, 0, 1, 1, FAKE, None, None, FAKE, 1 << 20, None), 2),
-        ((FAKE, FAKE, FAKE, 1, -5, 1, FAKE, None, None, FAKE, 1 << 20, None), 2),
-        ((FAKE, FAKE, FAKE, 1, 1, 1, FAKE, None, None, None, 1 << 20, None), 3),
-        ((FAKE, FAKE, FAKE, 1, 1, 1, FAKE, None, None, ctypes.c_void_p(0x10010), 1 << 20, None), 3),
-        ((FAKE, FAKE, FAKE, 4, 64, 64, FAKE, None, None, FAKE, 256, None), 3),
+        # value, t_x, t_y, B, T, S, row_start, durations, score, status, workspace, bytes, stream
+        ((None, FAKE, FAKE, 1, 1, 1, FAKE, None, None, None, FAKE, 1 << 20, None), 1),
+        ((FAKE, None, FAKE, 1, 1, 1, FAKE, None, None, None, FAKE, 1 << 20, None), 1),
+        ((FAKE, FAKE, FAKE, 1, 1, 1, None, None, None, None, FAKE, 1 << 20, None), 1),
+        ((FAKE, FAKE, FAKE, 0, 1, 1, FAKE, None, None, None, FAKE, 1 << 20, None), 2),
+        ((FAKE, FAKE, FAKE, 1, -5, 1, FAKE, None, None, None, FAKE, 1 << 20, None), 2),
+        ((FAKE, FAKE, FAKE, 1, 1, 1, FAKE, None, None, None, None, 1 << 20, None), 3),
+        ((FAKE, FAKE, FAKE, 1, 1, 1, FAKE, None, None, None, ctypes.c_void_p(0x10010), 1 << 20, None), 3),
+        ((FAKE, FAKE, FAKE, 4, 64, 64, FAKE, None, None, None, FAKE, 256, None), 3),
     ],
 )
 def test_mas_search_host_validation(args, code):

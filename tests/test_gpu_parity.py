@@ -37,7 +37,8 @@ def _dev(a, dtype=None):
 
 
 def run_gpu(mas, value, tx, ty, workspace=None, value_dev=None):
-    """mas_forward_ex + mas_search on the device; results back on the host."""
+    """mas_forward_ex, then mas_search (no dense path) on the same workspace;
+    every output back on the host."""
     B, T, S = value.shape
     v = _dev(value) if value_dev is None else value_dev
     x = _dev(np.asarray(tx, np.int32))
@@ -47,20 +48,28 @@ def run_gpu(mas, value, tx, ty, workspace=None, value_dev=None):
     score = torch.empty(B, dtype=torch.float32, device="cuda")
     status = torch.empty(B, dtype=torch.int32, device="cuda")
     mas.mas_forward_ex(v, x, y, path, score, status, workspace=ws)
-    rs = mas.mas_search(v, x, y, workspace=ws)
+    s_score = torch.full((B,), 7.0, dtype=torch.float32, device="cuda")
+    s_status = torch.full((B,), 99, dtype=torch.int32, device="cuda")
+    s_dur = torch.full((B, T), -5, dtype=torch.int32, device="cuda")
+    rs = mas.mas_search(v, x, y, None, s_score, s_status, workspace=ws, durations_out=s_dur)
     torch.cuda.synchronize()
-    return path.cpu().numpy(), score.cpu().numpy(), status.cpu().numpy(), rs.cpu().numpy()
+    return (path.cpu().numpy(), score.cpu().numpy(), status.cpu().numpy(), rs.cpu().numpy(),
+            s_score.cpu().numpy(), s_status.cpu().numpy(), s_dur.cpu().numpy())
 
 
 def assert_parity(mas, value, tx, ty, label, **kw):
     _say(f"{label} shape={value.shape}")
-    gp, gs, gst, grs = run_gpu(mas, value, tx, ty, **kw)
+    gp, gs, gst, grs, sgs, sgst, sdur = run_gpu(mas, value, tx, ty, **kw)
     op, os_, ost = oracle.mas(value, tx, ty)
     assert np.array_equal(gst, ost), f"{label}: status {gst} vs {ost}"
     bad = np.argwhere(gp != op)
     assert bad.size == 0, f"{label}: {len(bad)} path bytes differ, first at {bad[:5].tolist()}"
     assert gs.tobytes() == os_.tobytes(), f"{label}: scores differ {gs} vs {os_}"
+    # the path-less call: row_start, durations, score and status
     assert np.array_equal(grs, oracle.row_start(op, tx, ty)), f"{label}: row_start differs"
+    assert np.array_equal(sdur, oracle.durations(op)), f"{label}: durations differ"
+    assert sgs.tobytes() == os_.tobytes(), f"{label}: mas_search scores differ"
+    assert np.array_equal(sgst, ost), f"{label}: mas_search status differs"
     return gp, gs
 
 
@@ -108,6 +117,22 @@ def test_signed_zero_inputs(mas):
     pairs = [(a, c) for a in range(1, 6) for c in range(a, 11)]
     z = np.where(st.randint(0, 1, 40 * 5 * 10).astype(bool), np.float32(-0.0), np.float32(0.0)).reshape(40, 5, 10)
     assert_parity(mas, z, np.array([a for a, _ in pairs], np.int32), np.array([c for _, c in pairs], np.int32), "zeros-40")
+
+
+def test_subnormal_values_and_partial_sums(mas):
+    """Integer multiples of 2^-140 (values and partial sums on both sides of
+    the smallest normal, many subnormal), and values around 1e-40: bit-exact
+    only if neither side flushes subnormals to zero."""
+    st = synth.Stream(321)
+    B, T, S = 12, 200, 700
+    q = np.float32(2.0 ** -140)
+    value = (st.randint(-40000, 40000, B * T * S).astype(np.float32) * q).reshape(B, T, S)
+    value[6:] = (st.normal_f32(6 * T * S).reshape(6, T, S) * np.float32(2.0 ** -133)).astype(np.float32)
+    tx = st.randint(1, T, B)
+    ty = np.array([int(st.randint(int(a), S)[0]) for a in tx], np.int32)
+    tx[0], ty[0] = T, S
+    _, gs = assert_parity(mas, value, tx, ty, "subnormals")
+    assert ((gs != 0) & (np.abs(gs) < np.float32(2.0 ** -126))).any()
 
 
 @pytest.mark.parametrize(

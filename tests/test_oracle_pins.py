@@ -52,6 +52,37 @@ def test_hand_derived_cases(case):
         assert np.float32(ls) == np.float32(case["legacy_score"])
 
 
+# ------------------------------------------------------------- row_start / durations
+def _path_from_rows(rows, T, S):
+    """The 0/1 alignment of one item built directly from A(j) (no oracle)."""
+    p = np.zeros((1, T, S), np.uint8)
+    for j, r in enumerate(rows):
+        p[0, r, j] = 1
+    return p
+
+
+@pytest.mark.parametrize("case", json.load(open(GOLDEN))["cases"], ids=lambda c: c["name"])
+def test_row_start_and_durations_hand_tables(case):
+    """oracle.row_start and oracle.durations on paths built from the hand
+    cases' rows, against tables counted by hand."""
+    T, S = len(case["value"]), len(case["value"][0])
+    p = _path_from_rows(case["rows"], T, S)
+    rs = oracle.row_start(p, [case["t_x"]], [case["t_y"]])
+    assert rs.shape == (1, T + 1) and rs[0].tolist() == case["row_start"]
+    assert oracle.durations(p)[0].tolist() == case["durations"]
+
+
+def test_row_start_invalid_items_and_padding():
+    # invalid items: all-zero tables; a valid item in a wider padded slab
+    p = np.zeros((3, 4, 9), np.uint8)
+    for j, r in enumerate([0, 0, 1, 2, 2, 2]):
+        p[2, r, j] = 1
+    rs = oracle.row_start(p, [0, 5, 3], [4, 3, 6])
+    assert rs[0].tolist() == [0] * 5 and rs[1].tolist() == [0] * 5
+    assert rs[2].tolist() == [0, 2, 3, 6, 6]
+    assert oracle.durations(p)[2].tolist() == [2, 1, 3, 0]
+
+
 # ------------------------------------------------------------- brute force
 def _all_pairs():
     return [(tx, ty) for tx in range(1, 6) for ty in range(tx, 11)]
@@ -100,6 +131,33 @@ def test_bruteforce_large_magnitudes():
     for tx, ty in _all_pairs():
         v = (st.normal_f32(50).reshape(5, 10) * np.float32(13.0) - np.float32(153.0)) * np.float32(1024.0)
         _check_bruteforce(v.astype(np.float32), tx, ty)
+
+
+def test_bruteforce_subnormal_values():
+    """Values on the subnormal scale (|v| ~ 1e-40): fp32 keeps them (no
+    flush to zero), so the DP must still equal the brute force bit for bit."""
+    st = synth.Stream(91)
+    tiny = np.float32(2.0 ** -133)  # ~9.2e-41, subnormal
+    for tx, ty in _all_pairs():
+        v = (st.normal_f32(50).reshape(5, 10) * tiny).astype(np.float32)
+        assert (np.abs(v[v != 0]) < np.float32(2.0 ** -126)).any()
+        _check_bruteforce(v, tx, ty)
+
+
+def test_bruteforce_partial_sums_cross_the_subnormal_range():
+    """Integer multiples of 2^-140 up to about 3e-38: values on both sides of
+    the smallest normal (2^-126), partial sums landing among the subnormals;
+    every sum is exact, so the brute force is exact, and a flush to zero of
+    any subnormal input or partial sum changes the result."""
+    st = synth.Stream(92)
+    q = np.float32(2.0 ** -140)
+    hit = 0
+    for tx, ty in _all_pairs():
+        v = (st.randint(-40000, 40000, 50).astype(np.float32) * q).reshape(5, 10)
+        _check_bruteforce(v, tx, ty)
+        path, score, _ = _one(v, tx, ty)
+        hit += bool(score != 0 and abs(score) < np.float32(2.0 ** -126))
+    assert hit > 3  # some scores themselves are subnormal
 
 
 # ------------------------------------------------------------- tie rule
@@ -256,6 +314,10 @@ _MUTATIONS = {
     "signed_zero_order_dropped": ("return a < b || (a == 0.0f && b == 0.0f && signbit(a) && !signbit(b));", "return a < b;"),
     "diag_wrong_row": ("float diag = QC(i - 1, j - 1);", "float diag = QC(i - 1, j);"),
     "loop_bound_off_by_one": ("int32_t imax = j < tx - 1 ? j : tx - 1;", "int32_t imax = j - 1 < tx - 1 ? j - 1 : tx - 1;"),
+    # what a flush-to-zero build (or a kernel compiled with denormals off) does
+    "subnormals_flushed": ("QC(i, j) = (take_diag ? diag : stay) + QV(i, j);",
+                           "{ float r_ = (take_diag ? diag : stay) + QV(i, j); "
+                           "QC(i, j) = fabsf(r_) < 1.17549435e-38f ? 0.0f * r_ : r_; }"),
 }
 
 
@@ -270,7 +332,7 @@ def _compile_variant(src: str, d: str) -> str:
 def _variant_mas(so):
     lib = ctypes.CDLL(so)
     P, i32 = ctypes.c_void_p, ctypes.c_int32
-    lib.oracle_mas_batch_neg.argtypes = [P, i32, i32, i32, P, P, ctypes.c_float, P, P, P, P]
+    lib.oracle_mas_batch_neg.argtypes = [P, i32, i32, i32, P, P, ctypes.c_float, P, P, P]
 
     def mas(value, t_x, t_y, neg=-np.inf):
         value = np.ascontiguousarray(value, dtype=np.float32)
@@ -281,7 +343,7 @@ def _variant_mas(so):
         score = np.empty(B, np.float32)
         status = np.empty(B, np.int32)
         p = lambda a: a.ctypes.data_as(P)
-        lib.oracle_mas_batch_neg(p(value), B, T, S, p(tx), p(ty), float(neg), p(path), p(score), p(status), None)
+        lib.oracle_mas_batch_neg(p(value), B, T, S, p(tx), p(ty), float(neg), p(path), p(score), p(status))
         return path, score, status
 
     return mas
@@ -296,9 +358,12 @@ def _pins_pass(mas) -> bool:
             assert _pins.alignment_of(path, case["t_x"], case["t_y"]) == tuple(case["rows"])
             assert np.float32(score).tobytes() == np.float32(case["score"]).tobytes()
         st = synth.Stream(31)
+        q = np.float32(2.0 ** -140)
         for tx, ty in _all_pairs():
             v = st.normal_f32(50).reshape(5, 10)
             _check_bruteforce(v, tx, ty, impl=mas)
+            vs = (st.randint(-40000, 40000, 50).astype(np.float32) * q).reshape(5, 10)
+            _check_bruteforce(vs, tx, ty, impl=mas)
             vi = st.randint(-2, 2, 50).astype(np.float32).reshape(5, 10)
             path, score, _ = _one(vi, tx, ty, impl=mas)
             best, arg = _pins.brute_force(vi, tx, ty)
