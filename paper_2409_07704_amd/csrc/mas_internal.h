@@ -24,7 +24,7 @@ struct KParams {
   uint32_t* done;       // [B][NW] sweep finished (decision words published)
   uint32_t* tmo;        // [B] a wave of the item gave up a wait in this call (tag)
   uint64_t* order;      // [B] items in the order their row_start tables were published: tag << 32 | item
-  uint64_t* slots;      // [B][NW][NC*32]
+  uint64_t* slots;      // [B][NB][NC*32] boundary words of each workgroup's last wave
   uint32_t* dec;        // [B][NC][TP] decision words, row-indexed
   int32_t B, T, S, NW, NC, TP, NB;
   int32_t ntile;        // path tiles per item: ceil(T / kPathTileRows)

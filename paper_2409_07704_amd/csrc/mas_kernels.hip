@@ -553,11 +553,11 @@ __device__ __forceinline__ float sweep_wave(const KParams& p, SweepLds& L, const
   auto bits_ptr = [&](int k) __attribute__((always_inline)) -> uint32_t* {
     return reinterpret_cast<uint32_t*>(Lc + wbase + (uint32_t)k * kSlotStride + kBitsOff);
   };
-  // Global boundary words of this wave (OUT2): word 32c + j = {Q of the
-  // wave's last row at column 32c + j, tag}.
+  // Global boundary words of this wave (OUT2: the last wave of workgroup
+  // g / 4): word 32c + j = {Q of the wave's last row at column 32c + j, tag}.
   const size_t slot_words = (size_t)p.NC * kChunk;
   const __amdgpu_buffer_rsrc_t sr =
-      make_cursor(p.slots + ((size_t)x.b * p.NW + x.g) * slot_words, slot_words * 8u).rsrc();
+      make_cursor(p.slots + ((size_t)x.b * p.NB + x.g / kWavesPerBlock) * slot_words, slot_words * 8u).rsrc();
 
   if (IN == 0) {
     // The row above row 0 is -inf in every slot.
@@ -796,7 +796,8 @@ __device__ __forceinline__ void load_tiles(const KParams& p, SweepLds& L, const 
   // previous wave always computes).
   int bnext = x.c_begin - 1;
   const int bend = BOUND ? x.prev_end : bnext;
-  const uint64_t* const bsrc = p.slots + ((size_t)x.b * p.NW + (x.g > 0 ? x.g - 1 : 0)) * ((size_t)p.NC * kChunk);
+  // (the boundary words of the previous workgroup's last wave)
+  const uint64_t* const bsrc = p.slots + ((size_t)x.b * p.NB + (x.g > 0 ? x.g / kWavesPerBlock - 1 : 0)) * ((size_t)p.NC * kChunk);
   const uint32_t prod_addr = lds_off(&L.box[w]) + 4u;
   int bspins = 0;
   while ((readied < x.c_end || bnext < bend) && !bd.out) {

@@ -29,10 +29,12 @@ constexpr int kMaxRows = 8192;               // largest T (the walker keeps row_
 // of every chunk is a scratch slot (lane 0 of every wave stores there).
 __host__ __device__ constexpr int dec_bit(int j) { return 31 - (j % kChunk); }
 
-// Boundary hand-off between consecutive waves of an item: wave g publishes
-// Q[63g+62][j] (its last row) for every column j it computes as one 64-bit word
-// {low: fp32 bits, high: tag}.  The tag identifies the call (see WsHeader),
-// so stale words from earlier calls are never mistaken for fresh ones.
+// Boundary hand-off between consecutive workgroups of an item: the last wave
+// g of a workgroup publishes Q[63g+62][j] (its last row) for every column j it
+// computes as one 64-bit word {low: fp32 bits, high: tag} (waves of one
+// workgroup hand on through LDS).  The tag identifies the call (see
+// WsHeader), so stale words from earlier calls are never mistaken for fresh
+// ones.
 // Dense path: written in tiles of kPathTileRows rows of one item, taken in
 // the order the items' row_start tables are published, by at most
 // kPathWorkgroups path-writer workgroups (three quarters of the MI355X's 256
@@ -66,7 +68,7 @@ struct Layout {
   size_t off_done;   // uint32 [B][NW] sweep-finished flags (tag values)
   size_t off_tmo;    // uint32 [B] per-item timeout flags (tag values)
   size_t off_order;  // uint64 [B] items in the order their row_start tables were published: tag << 32 | item
-  size_t off_slots;  // uint64 [B][NW][NC*32] boundary hand-off words
+  size_t off_slots;  // uint64 [B][NB][NC*32] boundary hand-off words of each workgroup's last wave
   size_t off_dec;    // uint32 [B][NC][TP] decision words
   size_t off_rs;     // int32  [B][T+1] row_start table (mas_forward_ex)
   size_t bytes;
@@ -95,7 +97,7 @@ __host__ inline bool make_layout(int32_t B, int32_t T, int32_t S, Layout* L) {
   L->off_order = off;
   off = round_up(off + (size_t)B * sizeof(uint64_t), kAlign);
   L->off_slots = off;
-  off = round_up(off + (size_t)B * L->NW * (size_t)L->NC * kChunk * sizeof(uint64_t), kAlign);
+  off = round_up(off + (size_t)B * L->NB * (size_t)L->NC * kChunk * sizeof(uint64_t), kAlign);
   L->off_dec = off;
   off = round_up(off + (size_t)B * L->NC * (size_t)L->TP * sizeof(uint32_t), kAlign);
   L->off_rs = off;
