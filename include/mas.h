@@ -73,7 +73,8 @@ typedef enum mas_status {
   MAS_ERR_NULL_POINTER = 1, /* a required pointer is NULL */
   MAS_ERR_BAD_SHAPE = 2,    /* B, T or S < 1, or past the shape limits above */
   MAS_ERR_WORKSPACE = 3,    /* workspace NULL, misaligned or too small */
-  MAS_ERR_HIP = 4           /* a HIP runtime call or kernel launch failed */
+  MAS_ERR_HIP = 4,          /* a HIP runtime call or kernel launch failed */
+  MAS_ERR_SCRATCH = 5       /* mas_forward_static: the batch needs more than MAS_STATIC_SCRATCH_BYTES */
 } mas_status;
 
 /* Per-item status codes written to item_status_out[b]. */
@@ -162,6 +163,27 @@ mas_status mas_forward_ex(const float* value, const int32_t* t_x, const int32_t*
  */
 mas_status mas_forward(const float* value, const int32_t* t_x, const int32_t* t_y,
                        uint8_t* path_out, int32_t B, int32_t T, int32_t S, hipStream_t stream);
+
+/*
+ * For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc): the same
+ * call as mas_forward_ex, with the workspace taken from a static device array
+ * of MAS_STATIC_SCRATCH_BYTES that the library holds on every device it runs
+ * on until the process ends.  No allocation, ever.
+ *   - Limit: batches with mas_workspace_bytes(B, T, S) > MAS_STATIC_SCRATCH_BYTES
+ *     return MAS_ERR_SCRATCH and enqueue nothing (64 MiB holds, e.g.,
+ *     B = 64, T = 1024, S = 4096).
+ *   - The first call on a device enqueues the array's initialisation (a fill
+ *     kernel, no memset) on `stream` ahead of the work; it must not be a call
+ *     under graph capture.
+ *   - Every call on one device shares that device's array, which keeps the
+ *     last call's state: calls on one device must not overlap (issue them on
+ *     one stream, or synchronise); overlapping calls race.
+ */
+#define MAS_STATIC_SCRATCH_BYTES ((size_t)64 << 20)
+mas_status mas_forward_static(const float* value, const int32_t* t_x, const int32_t* t_y,
+                              uint8_t* path_out, int32_t B, int32_t T, int32_t S,
+                              float* score_out, int32_t* item_status_out, hipStream_t stream);
 
 /* Human-readable name of a status code (static storage). */
 const char* mas_status_string(mas_status status);

@@ -12,12 +12,14 @@ from ._native import (  # noqa: F401
     ITEM_OUT_OF_RANGE,
     ITEM_SYNC_TIMEOUT,
     LIB_PATH,
+    STATIC_SCRATCH_BYTES,
     MasError,
     Workspace,
     lib,
     mas_expand_path,
     mas_forward,
     mas_forward_ex,
+    mas_forward_static,
     mas_search,
     mas_status_string,
     mas_version,

@@ -6,6 +6,8 @@
 #include <stdint.h>
 #include <stdlib.h>
 
+#include <mutex>
+
 #include "mas.h"
 #include "mas_internal.h"
 
@@ -58,6 +60,33 @@ static mas_status run(const float* value, const int32_t* t_x, const int32_t* t_y
   p.path16 = path && (L.S % 16 == 0) && ((uintptr_t)path % 16 == 0);
   p.spin_limit = wait_bound();
   return launch_mas(p, stream) == hipSuccess ? MAS_OK : MAS_ERR_HIP;
+}
+
+// Workspace of mas_forward_static: one array per device, held until the
+// process ends.  In host code `scratch` only names the symbol; its device
+// address comes from hipGetSymbolAddress, once per device (scratch_ptr).
+static __device__ __align__(256) uint8_t scratch[MAS_STATIC_SCRATCH_BYTES];
+
+constexpr int kMaxDevices = 64;
+static std::mutex g_scratch_mu;
+static void* g_scratch[kMaxDevices];  // device address of `scratch` per device, null until set up
+
+// The current device's scratch address.  The first call on a device looks
+// the address up and enqueues the array's initialisation (zeros and the
+// workspace mark, by a fill kernel) on `stream`.
+static mas_status scratch_ptr(hipStream_t stream, void** out) {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return MAS_ERR_HIP;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch[dev]) {
+    void* ptr = nullptr;
+    if (hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)) != hipSuccess || ptr == nullptr) return MAS_ERR_HIP;
+    if ((uintptr_t)ptr % kAlign != 0) return MAS_ERR_HIP;
+    if (launch_ws_init(ptr, MAS_STATIC_SCRATCH_BYTES, stream) != hipSuccess) return MAS_ERR_HIP;
+    g_scratch[dev] = ptr;
+  }
+  *out = g_scratch[dev];
+  return MAS_OK;
 }
 }  // namespace mas
 
@@ -119,6 +148,20 @@ mas_status mas_forward(const float* value, const int32_t* t_x, const int32_t* t_
   return s;
 }
 
+mas_status mas_forward_static(const float* value, const int32_t* t_x, const int32_t* t_y, uint8_t* path_out,
+                              int32_t B, int32_t T, int32_t S, float* score_out, int32_t* item_status_out,
+                              hipStream_t stream) {
+  if (!value || !t_x || !t_y || !path_out) return MAS_ERR_NULL_POINTER;
+  Layout L;
+  if (!make_layout(B, T, S, &L)) return MAS_ERR_BAD_SHAPE;
+  if (L.bytes > MAS_STATIC_SCRATCH_BYTES) return MAS_ERR_SCRATCH;
+  void* ws = nullptr;
+  const mas_status s = scratch_ptr(stream, &ws);
+  if (s != MAS_OK) return s;
+  int32_t* rs = reinterpret_cast<int32_t*>(static_cast<char*>(ws) + L.off_rs);
+  return run(value, t_x, t_y, L, rs, nullptr, score_out, item_status_out, path_out, ws, stream);
+}
+
 const char* mas_status_string(mas_status status) {
   switch (status) {
     case MAS_OK:
@@ -131,6 +174,8 @@ const char* mas_status_string(mas_status status) {
       return "MAS_ERR_WORKSPACE";
     case MAS_ERR_HIP:
       return "MAS_ERR_HIP";
+    case MAS_ERR_SCRATCH:
+      return "MAS_ERR_SCRATCH";
   }
   return "MAS_ERR_UNKNOWN";
 }

@@ -93,6 +93,12 @@ def test_other_entry_points_host_validation():
     assert L.mas_workspace_init(None, 256, None) == 1
     assert L.mas_workspace_init(ctypes.c_void_p(0x10008), 256, None) == 3
     assert L.mas_workspace_init(FAKE, 100, None) == 3
+    # the static-scratch entry point: checked before any device call
+    assert L.mas_forward_static(None, FAKE, FAKE, FAKE, 1, 1, 1, None, None, None) == 1
+    assert L.mas_forward_static(FAKE, FAKE, FAKE, FAKE, 1, 0, 1, None, None, None) == 2
+    assert mas.mas_workspace_bytes(64, 1024, 8192) > mas.STATIC_SCRATCH_BYTES
+    assert L.mas_forward_static(FAKE, FAKE, FAKE, FAKE, 64, 1024, 8192, None, None, None) == 5
+    assert mas.mas_status_string(5) == "MAS_ERR_SCRATCH"
 
 
 def test_binding_refuses_host_tensors():
