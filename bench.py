@@ -229,6 +229,9 @@ def main():
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle timing (parity still checked)")
     ap.add_argument("--copy-probe", action="store_true", help="run copies of a known size after the timed region")
     ap.add_argument("--pmc-summary", nargs="+", default=None, metavar="CSV")
+    ap.add_argument("--trace", default=None, metavar="OUT",
+                    help="instead of timing: record the launch timeline with the debug build libmas_trace.so "
+                         "(full batch with and without the path, and the last-finishing item alone) into OUT")
     args = ap.parse_args()
     if args.pmc_summary:
         pmc_summary(args.pmc_summary, TRAFFIC_FILE)
@@ -249,6 +252,9 @@ def main():
     value, tx, ty = synth.generate(wname)
     B, T, S = value.shape
     cells, bytes_metric, bytes_band = algorithmic_bytes(tx, ty, B, T, S)
+    if args.trace:
+        timeline(args.trace, wname, value, tx, ty)
+        return
 
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
@@ -367,6 +373,39 @@ def main():
     print(json.dumps(out), flush=True)
     if not parity:
         sys.exit(1)
+
+
+def timeline(out_path, wname, value, tx, ty):
+    """Timeline summaries from the debug build (see paper_2409_07704_amd/trace.py)."""
+    import numpy as np
+    import torch
+
+    from paper_2409_07704_amd import trace
+
+    dev = torch.device("cuda:0")
+    v, x, y = (torch.from_numpy(a).to(dev) for a in (value, tx, ty))
+    parts = [f"Timeline of one launch on {wname} from the debug build (libmas_trace.so, MAS_TRACE: 100 MHz "
+             f"wall-clock stamps; the product build has none).",
+             f"Command: python bench.py --trace {os.path.relpath(out_path, ROOT)}"
+             + (f" --workload {wname}" if wname != "tts-b64-t1024-s4096" else ""),
+             f"kernel sources sha256 {kernel_source_hash()}", ""]
+    lay, st = trace.run(v, x, y, with_path=True)
+    s_full = trace.summary(lay, st, tx, ty, with_path=True)
+    print(f"trace: full batch with path {s_full['launch_us']:.1f} us", flush=True)
+    parts += [trace.format_summary(s_full, "== full batch, mas_forward_ex (dense path)"), ""]
+    lay, st = trace.run(v, x, y, with_path=False)
+    s_np = trace.summary(lay, st, tx, ty, with_path=False)
+    print(f"trace: full batch without path {s_np['launch_us']:.1f} us", flush=True)
+    parts += [trace.format_summary(s_np, "== full batch, mas_search (no dense path)"), ""]
+    b = s_full["longest"][0]["b"]
+    va, xa, ya = (torch.from_numpy(np.ascontiguousarray(a[b:b + 1])).to(dev) for a in (value, tx, ty))
+    lay, st = trace.run(va, xa, ya, with_path=True)
+    s_one = trace.summary(lay, st, tx[b:b + 1], ty[b:b + 1], with_path=True)
+    print(f"trace: item {b} alone {s_one['launch_us']:.1f} us", flush=True)
+    parts += [trace.format_summary(s_one, f"== item {b} alone (B=1), mas_forward_ex"), ""]
+    with open(out_path, "w") as f:
+        f.write("\n".join(parts))
+    print("\n".join(parts), flush=True)
 
 
 def time_launches(fn, stream, steps, warmup):

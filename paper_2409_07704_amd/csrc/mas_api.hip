@@ -48,13 +48,13 @@ static mas_status run(const float* value, const int32_t* t_x, const int32_t* t_y
   p.tmo = reinterpret_cast<uint32_t*>(base + L.off_tmo);
   p.order = reinterpret_cast<uint64_t*>(base + L.off_order);
   p.slots = reinterpret_cast<uint64_t*>(base + L.off_slots);
-  p.dec = reinterpret_cast<uint32_t*>(base + L.off_dec);
+  p.pm = reinterpret_cast<uint32_t*>(base + L.off_pm);
   p.B = L.B;
   p.T = L.T;
   p.S = L.S;
   p.NW = L.NW;
   p.NC = L.NC;
-  p.TP = L.TP;
+  p.EP = L.EP;
   p.NB = L.NB;
   p.ntile = (L.T + kPathTileRows - 1) / kPathTileRows;
   p.path16 = path && (L.S % 16 == 0) && ((uintptr_t)path % 16 == 0);

@@ -21,21 +21,44 @@ struct KParams {
   int32_t* durations;   // nullable [B][T]
   uint8_t* path;        // nullable [B][T][S]; null: no path is written
   WsHeader* hdr;
-  uint32_t* done;       // [B][NW] sweep finished (decision words published)
+  uint32_t* done;       // [B][NW] a wave's step masks published (tag)
   uint32_t* tmo;        // [B] a wave of the item gave up a wait in this call (tag)
   uint64_t* order;      // [B] items in the order their row_start tables were published: tag << 32 | item
   uint64_t* slots;      // [B][NB][NC*32] boundary words of each workgroup's last wave
-  uint32_t* dec;        // [B][NC][TP] decision words, row-indexed
-  int32_t B, T, S, NW, NC, TP, NB;
+  uint32_t* pm;         // [B][NC][EP] step masks (see mas_layout.h)
+  int32_t B, T, S, NW, NC, EP, NB;
   int32_t ntile;        // path tiles per item: ceil(T / kPathTileRows)
   int32_t path16;       // path 16-byte aligned and S % 16 == 0
   int32_t spin_limit;   // bound of a device-side wait, in polls without progress
 };
 
+// Timeline of one launch in the debug build (MAS_TRACE): indices of 64-bit
+// 100 MHz wall-clock stamps.  wg: [grid][2] start and end of each workgroup;
+// chunk: [B][NW][64] slot k: sweep wave g done with chunk 8k+7 (or its last
+// chunk; chunks past 511 are not recorded); walk: [B][64] slot k: walker done
+// with the chunks from 8k up (slot k = its start, for the first block);
+// item: [B][8] step masks of every wave published (windows may start),
+// walk start, walk end, row_start published, ticks the walker waited for
+// windows, (unused) x3; tile: [B * ntile][2] start and
+// end of path tile t.
+struct TraceLayout {
+  size_t wg, chunk, walk, item, tile, total;
+};
+__host__ __device__ inline TraceLayout trace_layout(int B, int NW, int NC, int ntile, int grid) {
+  TraceLayout t;
+  t.wg = 0;
+  t.chunk = t.wg + 2 * (size_t)grid;
+  t.walk = t.chunk + (size_t)B * NW * 64;
+  t.item = t.walk + (size_t)B * 64;
+  t.tile = t.item + 8 * (size_t)B;
+  t.total = t.tile + 2 * (size_t)B * ntile;
+  return t;
+}
+
 // Forward sweep, backtrack and (when p.path) the dense path, in one launch:
-// one 576-thread workgroup (four sweep waves, four loader waves, one storer
-// wave) per 252 text rows of every item, then (when p.path) the path-writer
-// workgroups.
+// one 768-thread workgroup (four sweep waves, four loader waves, four
+// finisher waves) per 252 text rows of every item, then (when p.path) the
+// path-writer workgroups.
 hipError_t launch_mas(const KParams& p, hipStream_t stream);
 // Dense [B, T, S] u8 path from row_start [B, T+1].
 hipError_t launch_path(const int32_t* row_start, int32_t B, int32_t T, int32_t S, uint8_t* path, hipStream_t stream);

@@ -3,7 +3,7 @@
 // Algorithm 2) and the dense path writer.
 //
 // One launch computes everything (mas_kernel).  A workgroup owns 252 text
-// rows of one item and has eight waves:
+// rows of one item and has twelve waves:
 //   * four sweep waves (one per SIMD): wave w owns 63 rows, one text row per
 //     lane in lanes 1..63, and lane 0 carries a copy of the row above the
 //     wave.  A wave walks the speech axis in chunks of 32 columns.  The
@@ -17,11 +17,15 @@
 //     up to four chunks ahead, and publishes each tile once it has landed.
 //     The sweep waves issue no loads of values; they read their tiles from LDS
 //     while the next chunk's reads are already in flight.
-// The sweep wave holding row t_x-1 walks the decision words back from
-// (t_x-1, t_y-1) once every wave of the item has published them, while the
-// four loaders of its workgroup stage the decision words of upcoming chunks
-// in LDS, and publishes the item's row_start table, appending the item to the
-// call's completion order.  Path-writer workgroups, last in the grid, take
+//   * four finisher waves: finisher w turns each chunk's decision words of
+//     sweep wave w into step masks (for every row the wave owns, the columns
+//     at which the backtrack, entering the chunk in that row, moves up a row)
+//     and stores them.
+// The sweep wave holding row t_x-1 walks back from (t_x-1, t_y-1) once every
+// wave of the item has published its masks, one lookup per chunk, while the
+// four loaders of its workgroup stage the masks of upcoming chunks in LDS,
+// and publishes the item's row_start table, appending the item to the call's
+// completion order.  Path-writer workgroups, last in the grid, take
 // tiles of 32 rows of one item from a shared counter in that order and write
 // them from the table, every byte once (zeros and ones in one pass): an item
 // that finishes late is written by many workgroups at once.
@@ -31,8 +35,8 @@
 // workgroup (band r, item b) has id r * B + b, and the path writers have the
 // ids from B * NB on.
 //
-// Memory ordering across workgroups: data handed between workgroups (decision
-// words, boundary words, row_start, flags) is written with device-scope
+// Memory ordering across workgroups: data handed between workgroups (step
+// masks, boundary words, row_start, flags) is written with device-scope
 // (write-through) stores and read with device-scope loads, and a wave waits
 // for its stores (vmcnt(0)) before raising a flag, so no cache write-back or
 // invalidation is needed.
@@ -89,6 +93,59 @@ __device__ __forceinline__ long long lds_poll(const long long* p) {
 __device__ __forceinline__ void lds_store(long long* p, long long v) { __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP); }
 
 __device__ __forceinline__ uint32_t call_tag(uint32_t gen) { return 2u * gen + 1u; }
+
+// ---------------------------------------------------------------- timeline (debug build)
+// With MAS_TRACE defined (the libmas_trace.so build), waves record 100 MHz
+// wall-clock stamps of their milestones into the buffer set by mas_trace_set
+// (layout: TraceLayout); otherwise every stamp compiles to nothing.  Stamps
+// inside the sweep and walk loops are kept in one register (lane k: the k-th
+// stamp, one per eight chunks) and stored once the loop is over, so that the
+// traced loops issue no extra memory operations.
+#ifdef MAS_TRACE
+__device__ uint64_t* g_trace;
+__device__ __forceinline__ void stamp(size_t idx) {
+  uint64_t* const t = g_trace;
+  if (t && __lane_id() == 0) t[idx] = __builtin_amdgcn_s_memrealtime();
+}
+// Time spent in some waits, summed (stored as one value).
+struct Waited {
+  uint64_t total = 0, since = 0;
+  __device__ __forceinline__ void begin() { since = __builtin_amdgcn_s_memrealtime(); }
+  __device__ __forceinline__ void end() {
+    if (since) total += __builtin_amdgcn_s_memrealtime() - since;
+    since = 0;
+  }
+  __device__ __forceinline__ void flush(size_t idx) {
+    uint64_t* const t = g_trace;
+    if (t && __lane_id() == 0) t[idx] = total;
+  }
+};
+struct Stamps {
+  uint64_t v = 0;
+  __device__ __forceinline__ void at(int k) {
+    const uint64_t now = __builtin_amdgcn_s_memrealtime();
+    v = (int)__lane_id() == k ? now : v;
+  }
+  __device__ __forceinline__ void flush(size_t base) {
+    uint64_t* const t = g_trace;
+    if (t) t[base + __lane_id()] = v;
+  }
+};
+#else
+__device__ __forceinline__ void stamp(size_t) {}
+struct Waited {
+  __device__ __forceinline__ void begin() {}
+  __device__ __forceinline__ void end() {}
+  __device__ __forceinline__ void flush(size_t) {}
+};
+struct Stamps {
+  __device__ __forceinline__ void at(int) {}
+  __device__ __forceinline__ void flush(size_t) {}
+};
+#endif
+__device__ __forceinline__ TraceLayout trace_of(const KParams& p) {
+  return trace_layout(p.B, p.NW, p.NC, p.ntile, (int)gridDim.x);
+}
 __device__ __forceinline__ int uni(int v) { return __builtin_amdgcn_readfirstlane(v); }
 
 
@@ -107,8 +164,8 @@ struct Bound {
   __device__ __forceinline__ void expire();
 };
 constexpr int kLoaders = 4;          // loader waves per workgroup
-constexpr int kStorers = 1;         // storer waves per workgroup (decision words to memory)
-constexpr int kThreads = kThreadsPerBlock + (kLoaders + kStorers) * kWave;
+constexpr int kFinishers = 4;        // finisher waves per workgroup (step masks to memory)
+constexpr int kThreads = kThreadsPerBlock + (kLoaders + kFinishers) * kWave;
 constexpr int kRing = 4;             // tile and boundary slots per sweep wave
 constexpr int kPolicyDev = 16;       // cache policy sc1: device scope (write-through stores)
 
@@ -123,7 +180,7 @@ constexpr int kPolicyDev = 16;       // cache policy sc1: device scope (write-th
 //   * at kBoundOff, the chunk's boundary row: Q of the row above the wave
 //     for the chunk's 32 columns (lane 0's values);
 //   * at kBitsOff, the chunk's decision words (lane l: word of row l-1, lane
-//     0: a scratch word), left there by the sweep wave for the storer wave.
+//     0: a scratch word), left there by the sweep wave for its finisher.
 // Chunk c uses slot (c - c_begin) % kRing of its wave.
 constexpr int kTileBytes = kWave * kChunk * 4;  // 8192
 constexpr int kBoundOff = kTileBytes;
@@ -132,14 +189,19 @@ constexpr int kSlotStride = kTileBytes + 512;
 constexpr int kWaveRegion = kRing * kSlotStride;
 __host__ __device__ constexpr int swz(int r) { return (r >> 1) & 7; }
 
-// The walk reuses the slot area: decision-word windows of kWinRows rows for
-// kNWin chunks, and the row_start table under construction.
-constexpr int kWinRows = 1024;
-constexpr int kNWin = 24;
+// The walk reuses the slot area: windows of kWinEnt step-mask entries for
+// kNWin chunks, and the row_start table under construction.  A window is
+// staged for chunk c while the walker is at most kNWin chunks above it, so the
+// path can have climbed at most 32 * kNWin rows by then; the window starts at
+// the mid entries of the wave below the lowest such row.
+constexpr int kWinEnt = 1280;
+constexpr int kNWin = 20;
 constexpr int kWinLoaders = 4;  // loader waves staging windows: loader k takes chunks C-1-k, C-1-k-4, ...
-constexpr int kWinAhead = 6;    // windows in flight per loader (4 loads each)
+constexpr int kWinAhead = 5;    // windows in flight per loader (kWinEnt / 256 loads each)
 static_assert(kWinLoaders * kWinAhead <= kNWin, "windows in flight fit the slots");
-static_assert(kWinRows >= 32 * (kNWin - 1) + kWave + 96, "a window covers the rows the walk can reach");
+static_assert(kWinEnt % 256 == 0, "a window is whole 1 KiB loads");
+static_assert(kEntPerWave * ((kChunk * kNWin + 1) / kRowsPerWave + 2) <= kWinEnt,
+              "a window covers the entries the walk can reach");
 // Walker position: (chunk << 32) | row, or -1 once the walk is over.
 __device__ __forceinline__ long long walk_pos(int chunk, int row) { return ((long long)chunk << 32) | (uint32_t)row; }
 
@@ -147,7 +209,7 @@ struct SweepLds {
   union {
     uint8_t ring[kWavesPerBlock][kWaveRegion];
     struct {
-      uint32_t win[kNWin][kWinRows];
+      uint32_t win[kNWin][kWinEnt];
       int rs[kMaxRows + 1 + kWave];
     } walk;
   } u;
@@ -156,12 +218,12 @@ struct SweepLds {
   //   .y prod:  boundary rows of chunks < prod are in w's slots (wave w-1);
   //   .z cnext: progress of wave w+1: it has read every chunk < cnext, whose
   //             slots are free again (written by wave w+1);
-  //   .w taken: the storer has taken the decision words of chunks < taken
+  //   .w taken: the finisher has read the decision words of chunks < taken
   //             out of w's slots.
   // Wave 0's own progress goes to cons0.
   i32x4 box[kWavesPerBlock];
   int cons0;
-  int wlo[kNWin];               // first row of each walk window (T > kWinRows)
+  int wlo[kNWin];               // first entry of each walk window (EP > kWinEnt)
   i32x4 wready;                 // window loader k: its windows of chunks >= wready[k] are in LDS
   f32x4 sink[kWavesPerBlock][kChunk / 4 + 1];  // target of hand-offs nobody reads (a fixed LDS op count per step)
   long long wpos;               // walker position (walk_pos), or -1 once the walk is over
@@ -548,8 +610,8 @@ __device__ __forceinline__ float sweep_wave(const KParams& p, SweepLds& L, const
   const uint32_t my_cons = w > 0 ? lds_off(&L.box[w - 1]) + 8u : lds_off(&L.cons0);
   const int* const my_box = reinterpret_cast<const int*>(&L.box[w]);
 
-  // Decision words: into the chunk's slot (the storer wave writes them to
-  // memory); a lane's word of chunk c at bits_ptr(J)[lane].
+  // Decision words: into the chunk's slot (the finisher wave turns them into
+  // step masks); a lane's word of chunk c at bits_ptr(J)[lane].
   auto bits_ptr = [&](int k) __attribute__((always_inline)) -> uint32_t* {
     return reinterpret_cast<uint32_t*>(Lc + wbase + (uint32_t)k * kSlotStride + kBitsOff);
   };
@@ -600,6 +662,7 @@ __device__ __forceinline__ float sweep_wave(const KParams& p, SweepLds& L, const
 
   float qc[kChunk] = {};
   float score = neg_inf();
+  Stamps stamps;  // (debug build) lane k: chunk 8k+7 (or the last chunk) done
   const int m_last = (x.ty - 1) % kChunk;
 
   // The last row of chunk cp (in lane 63's qc) for the next wave, right
@@ -672,6 +735,7 @@ __device__ __forceinline__ float sweep_wave(const KParams& p, SweepLds& L, const
       }
       lds_put(my_cons, c + 2);
     }
+    if ((c & 7) == 7 || c == x.c_end - 1) stamps.at(c >> 3);
   };
   for (int c = x.c_begin; c < x.c_end; c += kRing) {
     step(std::integral_constant<int, 0>(), c, va, vb);
@@ -679,9 +743,10 @@ __device__ __forceinline__ float sweep_wave(const KParams& p, SweepLds& L, const
     if (c + 2 < x.c_end) step(std::integral_constant<int, 2>(), c + 2, va, vb);
     if (c + 3 < x.c_end) step(std::integral_constant<int, 3>(), c + 3, vb, va);
   }
-  // Every chunk's decision words are in the slots (the storer takes chunk c
-  // once this progress passes c + 1).
+  // Every chunk's decision words are in the slots (the finisher takes chunk
+  // c once this progress passes c + 1).
   lds_put(my_cons, x.c_end + 1);
+  stamps.flush(trace_of(p).chunk + ((size_t)x.b * p.NW + x.g) * kWave);
   vm_wait<0>();
   return score;
 }
@@ -884,92 +949,140 @@ __device__ __forceinline__ void load_tiles(const KParams& p, SweepLds& L, const 
   vm_wait<0>();
 }
 
-// ---------------------------------------------------------------- backtrack
-// One step of the walk inside a chunk, for row k >= 1 below the chunk's
-// first row (its word, shifted right by one, in CUR), with the word of row
-// k+1 read into NXT meanwhile.  q is the position of the previous row's
-// step: the row's own step is the lowest set bit of its word above q, at
-// q + 1 + ff1(word >> (q + 1)); none (shifted word zero, also for q = 31)
-// ends the chunk.  s_lshr sets SCC to (result != 0), s_ff1 leaves it, so the
-// s_addc adds the 1.
-#define MAS_WALK_STEP(CUR, NXT)                  \
-  "v_readlane_b32 %[" NXT "], %[wh], %[sl]\n\t" \
-  "s_add_u32 %[sl], %[sl], 1\n\t"               \
-  "s_lshr_b32 %[t], %[" CUR "], %[q]\n\t"       \
-  "s_cbranch_scc0 .Lmas_walk_end%=\n\t"         \
-  "s_ff1_i32_b32 %[t], %[t]\n\t"                \
-  "s_addc_u32 %[q], %[q], %[t]\n\t"             \
-  "s_bitset1_b32 %[pm], %[q]\n\t"
-#define MAS_WALK_STEP2 MAS_WALK_STEP("y", "x") MAS_WALK_STEP("x", "y")
-#define MAS_WALK_STEP8 MAS_WALK_STEP2 MAS_WALK_STEP2 MAS_WALK_STEP2 MAS_WALK_STEP2
-
-// The steps of one chunk.  Row k of the chunk (k = 0 at the row the path
-// enters the chunk in) is lane sl + k of w (and of wh = w >> 1).  The first
-// row's step is its lowest set bit at or above position q0 (the column the
-// path enters at); every later row's is its lowest set bit above the
-// previous row's.  Returns the set of step positions: bit p set means one
-// row starts at column 32c + 31 - p, the k-th lowest set bit for row k.  At
-// most 32 rows step (one per column), so the 33rd row is never looked at.
-__device__ __forceinline__ uint32_t walk_chunk(uint32_t w, uint32_t wh, int sl, int q0) {
-  uint32_t pm, t, x, y;
-  int q = q0;
-  asm volatile(
-      "s_mov_b32 %[pm], 0\n\t"
-      "v_readlane_b32 %[x], %[w], %[sl]\n\t"
-      "s_add_u32 %[sl], %[sl], 1\n\t"
-      "v_readlane_b32 %[y], %[wh], %[sl]\n\t"
-      "s_add_u32 %[sl], %[sl], 1\n\t"
-      "s_lshr_b32 %[t], %[x], %[q]\n\t"
-      "s_cbranch_scc0 .Lmas_walk_end%=\n\t"
-      "s_ff1_i32_b32 %[t], %[t]\n\t"
-      "s_add_u32 %[q], %[q], %[t]\n\t"
-      "s_bitset1_b32 %[pm], %[q]\n\t"
-      MAS_WALK_STEP8 MAS_WALK_STEP8 MAS_WALK_STEP8 MAS_WALK_STEP2 MAS_WALK_STEP2 MAS_WALK_STEP2
-      MAS_WALK_STEP("y", "x")
-      ".Lmas_walk_end%=:"
-      : [pm] "=&s"(pm), [t] "=&s"(t), [x] "=&s"(x), [y] "=&s"(y), [q] "+s"(q), [sl] "+s"(sl)
-      : [w] "v"(w), [wh] "v"(wh)
-      : "scc");
-  return pm;
+// ---------------------------------------------------------------- step masks
+// Eight columns of the step-mask recurrence (Algorithm 1's argmax loop read
+// forward): the mask of (row r, column j) is d(r, j) ? mask(r-1, j-1) :
+// mask(r, j-1), shifted left by one with d(r, j) as its new lowest bit, so
+// that after the chunk's last column a step at column 32c + k sits at
+// position 31 - k.  Everything is complemented, which lets one carry chain do
+// the work:
+//   v_add_co  wc += wc     VCC = the lane's complemented decision for this
+//                          column (the top bit of wc), wc moves on one bit;
+//   v_cndmask_dpp  xc = VCC ? pc : pc of the lane below (wave_shr:1);
+//   v_addc    pc = xc + xc + VCC   (shift in the complemented decision).
+// Lane 0 (the row above the wave) has no lane below: DPP leaves its xc
+// unwritten, all ones (mask 0), so a path that climbs into it contributes
+// nothing more.  A DPP read of a VGPR needs two wait states after the VALU
+// write of it: the v_add_co and one s_nop.
+__device__ __forceinline__ void mask_cols8(uint32_t& wc, uint32_t& xc, uint32_t pc, uint32_t (&o)[8]) {
+#define MAS_MASK_COL(P, O)                                                            \
+  "v_add_co_u32 %[w], vcc, %[w], %[w]\n\t"                                            \
+  "s_nop 0\n\t"                                                                       \
+  "v_cndmask_b32_dpp %[x], %[" P "], %[" P "], vcc wave_shr:1 row_mask:0xf bank_mask:0xf\n\t" \
+  "v_addc_co_u32 %[" O "], vcc, %[x], %[x], vcc\n\t"
+  asm volatile(MAS_MASK_COL("p", "o0") MAS_MASK_COL("o0", "o1") MAS_MASK_COL("o1", "o2") MAS_MASK_COL("o2", "o3")
+               MAS_MASK_COL("o3", "o4") MAS_MASK_COL("o4", "o5") MAS_MASK_COL("o5", "o6") MAS_MASK_COL("o6", "o7")
+               : [o0] "=&v"(o[0]), [o1] "=&v"(o[1]), [o2] "=&v"(o[2]), [o3] "=&v"(o[3]), [o4] "=&v"(o[4]),
+                 [o5] "=&v"(o[5]), [o6] "=&v"(o[6]), [o7] "=&v"(o[7]), [w] "+v"(wc), [x] "+v"(xc)
+               : [p] "v"(pc)
+               : "vcc");
+#undef MAS_MASK_COL
 }
-#undef MAS_WALK_STEP8
-#undef MAS_WALK_STEP2
-#undef MAS_WALK_STEP
 
-// Loader side of the walk: loader k (of kWinLoaders) stages the decision
-// words of chunks C-1-k, C-1-k-4, ... down to 0, a window of kWinRows rows per
+// A finisher wave: for every chunk of its sweep wave, once that wave's
+// decision words of the chunk are in the ring slot (its progress passes c+1),
+// reads them, frees the slot, computes the step masks of the wave's rows and
+// of its last row entered at every position, and stores them to
+// pm[b][c][kEntPerWave * g + ...] with device-scope write-through stores.
+// Decisions at columns >= t_y (the last chunk's tail) count as "stay", so
+// that the last row's mask describes the path from (t_x-1, t_y-1).  Once all
+// of its stores have landed, the wave's done flag goes up.  The work is kept
+// out of the sweep waves, whose column chain sets the pace, and out of the
+// loaders, whose waits count their own loads only.
+__device__ __forceinline__ void finisher_role(const KParams& p, SweepLds& L, const WaveCtx& x, uint32_t tag, Bound& bd) {
+  const int lane = x.lane, w = x.w;
+  if (x.g > x.g_last) return;
+  const int C = (x.ty + kChunk - 1) / kChunk;
+  const uint32_t top_keep = ~0u << (kChunk - 1 - (x.ty - 1) % kChunk);
+  const __amdgpu_buffer_rsrc_t dr = make_cursor(p.pm + (size_t)x.b * p.NC * (size_t)p.EP, (uint64_t)p.NC * p.EP * 4u).rsrc();
+  const int base = kEntPerWave * x.g;
+  const int row_off = lane > 0 ? 4 * (base + lane - 1) : -1;  // lane 0's mask (the row above) is not stored
+  const int mid_off = lane >= kWave - 8 ? 4 * (base + kMidOff + 4 * (lane - (kWave - 8))) : -1;
+  const int q0 = 4 * (lane - (kWave - 8));  // the first mid entry a lane in 56..63 stores
+  const int* const progress = w > 0 ? reinterpret_cast<const int*>(&L.box[w - 1]) + 2 : &L.cons0;
+  const uint32_t taken_addr = lds_off(&L.box[w]) + 12u;
+  const uint32_t* const bits0 = reinterpret_cast<const uint32_t*>(&L.u.ring[w][kBitsOff]);
+  for (int c = x.c_begin; c < x.c_end && !bd.out; ++c) {
+    wait_at_least(progress, c + 2, bd);
+    const uint32_t bits = bits0[((c - x.c_begin) & (kRing - 1)) * (kSlotStride / 4) + lane];
+    lgkm_wait0();
+    lds_put(taken_addr, c + 1);  // the slot is free again
+    uint32_t wd = lane > 0 ? bits : 0u;
+    if (c == C - 1) wd &= top_keep;
+    uint32_t wc = ~wd, xc = ~0u;
+    uint32_t h[kChunk];  // complemented masks after each column of the chunk
+    {
+      uint32_t o[8];
+      mask_cols8(wc, xc, ~0u, o);
+#pragma unroll
+      for (int m = 0; m < 8; ++m) h[m] = o[m];
+      mask_cols8(wc, xc, h[7], o);
+#pragma unroll
+      for (int m = 0; m < 8; ++m) h[8 + m] = o[m];
+      mask_cols8(wc, xc, h[15], o);
+#pragma unroll
+      for (int m = 0; m < 8; ++m) h[16 + m] = o[m];
+      mask_cols8(wc, xc, h[23], o);
+#pragma unroll
+      for (int m = 0; m < 8; ++m) h[24 + m] = o[m];
+    }
+    const int soff = c * p.EP * 4;
+    __builtin_amdgcn_raw_buffer_store_b32(~h[kChunk - 1], dr, row_off, soff, kPolicyDev);
+    // Mid entry q: the last row's mask after column 31 - q, its positions
+    // raised by q; lane 63's values gathered into lanes 56..63, four each.
+    float hq[kChunk];
+#pragma unroll
+    for (int q = 0; q < kChunk; ++q) hq[q] = __uint_as_float(h[kChunk - 1 - q]);
+    const f32x4 f = gather_last_row(hq);
+    const u32x4 mv = {~__float_as_uint(f.x) << q0, ~__float_as_uint(f.y) << (q0 + 1), ~__float_as_uint(f.z) << (q0 + 2),
+                      ~__float_as_uint(f.w) << (q0 + 3)};
+    __builtin_amdgcn_raw_buffer_store_b128(mv, dr, mid_off, soff, kPolicyDev);
+  }
+  vm_wait<0>();
+  if (lane == 0) st_dev(p.done + (size_t)x.b * p.NW + x.g, tag);
+}
+
+// ---------------------------------------------------------------- backtrack
+// Loader side of the walk: loader k (of kWinLoaders) stages the step masks
+// of chunks C-1-k, C-1-k-4, ... down to 0, a window of kWinEnt entries per
 // chunk, kWinAhead windows in flight, into slot ch % kNWin once the walker
-// has moved past the chunk that slot held, and publishes the lowest chunk of
-// its sequence staged so far in wready[k].  When T exceeds kWinRows a window
-// ends 63 rows above the walker's row at issue time: the walk cannot descend
-// past the window before it reaches the chunk.  Stops early once the walker
-// has reached row 0.
+// has walked the chunk that slot held, and publishes the lowest chunk of
+// its sequence staged so far in wready[k].  When an item has more than
+// kWinEnt entries per chunk, a window starts at the mid entries of the wave
+// below the lowest row the walk can reach before it leaves the chunk (32
+// rows per chunk below the walker's row at issue time).  Stops early once the
+// walker has reached row 0.
 __device__ __forceinline__ void load_windows(const KParams& p, SweepLds& L, int b, int ty, int k, int lane, Bound& bd) {
   const int C = (ty + kChunk - 1) / kChunk;
-  const uint32_t* db = p.dec + (size_t)b * p.NC * (size_t)p.TP;
-  const uint64_t chunk_bytes = (uint64_t)p.TP * 4u;
+  const uint32_t* db = p.pm + (size_t)b * p.NC * (size_t)p.EP;
+  const uint64_t chunk_bytes = (uint64_t)p.EP * 4u;
+  const bool banded = p.EP > kWinEnt;
   const uint32_t win0 = lds_off(&L.u.walk.win[0][0]);
   const uint32_t ready_addr = lds_off(&L.wready) + 4u * (uint32_t)k;
   constexpr int kStep = kWinLoaders;
+  constexpr int kLoads = kWinEnt / 256;  // 1 KiB per load
   // Own chunks above `issued` are issued; own chunks >= `readied` are staged.
   int issued = C - 1 - k, readied = C - 1 - k + kStep;
   long long wpos = lds_poll(&L.wpos);
   int spins = 0;
   while (readied - kStep >= 0 && wpos >= 0 && !bd.out) {
     while (issued >= 0 && readied - kStep - issued < kStep * kWinAhead) {
-      if ((int)(wpos >> 32) > issued + kNWin) {
+      // The slot holds chunk issued + kNWin until the walker has walked it:
+      // the published position is the chunk the walker walks next.
+      if ((int)(wpos >> 32) >= issued + kNWin) {
         wpos = lds_poll(&L.wpos);
-        if (wpos < 0 || (int)(wpos >> 32) > issued + kNWin) break;
+        if (wpos < 0 || (int)(wpos >> 32) >= issued + kNWin) break;
       }
       const int e = uni((int)(uint32_t)wpos);
-      const int lo = p.T <= kWinRows ? 0 : (max(e - (kWinRows - 64), 0) & ~3);
+      const int row_lo = max(e - kChunk * kNWin - 1, 0);
+      const int lo = banded ? max(kEntPerWave * (row_lo / kRowsPerWave) - (kEntPerWave - kMidOff), 0) : 0;
       const int slot = issued % kNWin;
-      if (p.T > kWinRows) lds_put(lds_off(&L.wlo[slot]), lo);
-      const Cursor cr = make_cursor(db + (size_t)issued * p.TP + lo, chunk_bytes - (uint64_t)lo * 4u);
+      if (banded) lds_put(lds_off(&L.wlo[slot]), lo);
+      const Cursor cr = make_cursor(db + (size_t)issued * p.EP + lo, chunk_bytes - (uint64_t)lo * 4u);
       const __amdgpu_buffer_rsrc_t r = cr.rsrc_s();
 #pragma unroll
-      for (int q = 0; q < kWinRows / 256; ++q)
-        dma16_dev(win0 + (uint32_t)slot * (kWinRows * 4) + 1024u * q, r, 16 * lane + 1024 * q);
+      for (int q = 0; q < kLoads; ++q)
+        dma16_dev(win0 + (uint32_t)slot * (kWinEnt * 4) + 1024u * q, r, 16 * lane + 1024 * q);
       issued -= kStep;
       spins = 0;
     }
@@ -981,7 +1094,7 @@ __device__ __forceinline__ void load_windows(const KParams& p, SweepLds& L, int 
       wpos = lds_poll(&L.wpos);
       continue;
     }
-    vm_wait_usual<(kWinRows / 256) * (kWinAhead - 1)>((kWinRows / 256) * (inflight - 1));
+    vm_wait_usual<kLoads * (kWinAhead - 1)>(kLoads * (inflight - 1));
     readied -= kStep;
     lds_put(ready_addr, readied);
   }
@@ -996,10 +1109,10 @@ __device__ __forceinline__ void write_lanes(uint32_t& a, uint32_t x, int& b, int
 }
 
 // Row starts from the walk's records of up to 64 chunks: lane k holds the
-// record of chunk base + k (valid when lo <= chunk <= hi): the set pm of its
-// step positions and the row e the path entered it in.  The k-th lowest set
-// bit p of pm is where row e - k begins: column 32 * chunk + 31 - p.  Steps
-// from row 0 or below (possible only as the walk stops) are not rows.
+// record of chunk base + k (valid when lo <= chunk <= hi): the step mask pm
+// of its path and the row e the path entered it in.  The k-th lowest set bit
+// p of pm is where row e - k begins: column 32 * chunk + 31 - p.  Steps from
+// row 0 or below (possible only as the walk stops) are not rows.
 __device__ __forceinline__ void flush_records(int* rsl, int base, int lo, int hi, uint32_t pm, int e, int lane) {
   const int c = base + lane;
   uint32_t m = (c >= lo && c <= hi) ? pm : 0u;
@@ -1015,29 +1128,28 @@ __device__ __forceinline__ void flush_records(int* rsl, int base, int lo, int hi
 }
 
 // The walk of one item from (t_x-1, t_y-1) back to (0, 0) (Algorithm 1's
-// argmax loop, read off the decision words): in chunk c the path in row i
-// stays there until the nearest column to the left whose decision bit is
-// set, then continues one row up at the column before.  Builds row_start in
-// L.u.walk.rs: the first column of every row, with rs[0] = 0 and
-// rs[t_x .. T] = t_y.  Runs on the sweep wave that holds row t_x-1; its
-// loader stages the windows.
-//
-// Per chunk the wave runs the scalar step chain (walk_chunk) on the words of
-// rows idx, idx-1, ... (lane k: row idx - k) while the LDS read of the next
-// chunk's words, at the same rows, is in flight: the path descends at most
-// 32 rows per chunk, so those 64 rows cover the next chunk too.  Each chunk's
-// step set and entry row go into lane (chunk % 64) of two registers; every 64
-// chunks the lanes turn them into row starts in parallel.
-// BANDED: T > kWinRows, windows start at their own first rows (row 0
-// otherwise).
+// argmax loop, read off the step masks): per chunk, from the top, one LDS
+// lookup of the mask of the row the path enters the chunk in gives every
+// step the path takes inside the chunk, and the row it leaves the chunk in.
+// A path that climbs into the row above its wave ends its mask with that
+// step at position p; the mid entry p + 1 of the wave above completes it.
+// Each chunk's mask and entry row go into lane (chunk % 64) of two
+// registers; every 64 chunks the lanes turn them into row starts in parallel
+// (flush_records).  Builds row_start in L.u.walk.rs: the first column of
+// every row, with rs[0] = 0 and rs[t_x .. T] = t_y.  Runs on the sweep wave
+// that holds row t_x-1; the loaders of its workgroup stage the windows.
+// BANDED: entries per chunk exceed kWinEnt, so windows start at their own
+// first entries (entry 0 otherwise).
 template <bool BANDED>
-__device__ __forceinline__ void walk(const KParams& p, SweepLds& L, int tx, int ty, int lane, Bound& bd) {
+__device__ __forceinline__ void walk(const KParams& p, SweepLds& L, int b, int tx, int ty, int lane, Bound& bd) {
+  stamp(trace_of(p).item + 8 * (size_t)b + 1);
   int* rsl = L.u.walk.rs;
-  constexpr bool banded = BANDED;
-  int idx = tx - 1;                    // row of the path at the chunk's last column
+  Stamps wstamps;
+  int e = tx - 1;                      // row of the path at the current chunk's last column
+  int g = e / kRowsPerWave;            // its wave
+  int rr = e - g * kRowsPerWave;       // and its row within the wave
   int cw = (ty - 1) / kChunk;          // chunk being walked
   const int c_top = cw;
-  int q0 = 31 - (ty - 1) % kChunk;     // position of the path's column in chunk cw
   int slot = cw % kNWin;               // window slot of chunk cw
   // The staging progress of the window loaders as last read; chunk c's
   // window comes from loader (c_top - c) % kWinLoaders.
@@ -1051,8 +1163,10 @@ __device__ __forceinline__ void walk(const KParams& p, SweepLds& L, int tx, int 
            (c3 > c_top || kn3 <= c3);
   };
   // Waits (bounded) until the windows of chunks >= ch are in LDS.
+  Waited waited;  // (debug build) ticks spent waiting for windows
   auto ensure = [&](int ch) __attribute__((always_inline)) {
     int spins = 0;
+    if (!staged(ch)) waited.begin();
     while (!staged(ch) && !bd.out) {
       const i32x4 r = *reinterpret_cast<const volatile i32x4*>(&L.wready);
       kn0 = uni(r.x);
@@ -1063,97 +1177,80 @@ __device__ __forceinline__ void walk(const KParams& p, SweepLds& L, int tx, int 
       if (++spins > bd.limit) bd.expire();
       __builtin_amdgcn_s_sleep(1);
     }
+    waited.end();
   };
-  // First rows of the window slots (lane k: slot k), read once the block's
-  // windows are staged: the chunk loop reads nothing from LDS but the words.
+  // First entries of the window slots (lane k: slot k), read once a block's
+  // windows are staged.
   int wlo_v = 0;
-  auto read_wlo = [&]() __attribute__((always_inline)) {
-    if (banded) wlo_v = lds_load(&L.wlo[min(lane, kNWin - 1)]);
-  };
-  // Word of row e - lane from window slot sl (clamped to the slot's first
-  // row below; the walk never reaches past a window's last row).
-  const int lane4 = 4 * lane;
   const uint32_t win0 = lds_off(&L.u.walk.win[0][0]);
-  auto row_word = [&](int sl, int e) __attribute__((always_inline)) -> uint32_t {
-    const int lo = banded ? __builtin_amdgcn_readlane(wlo_v, sl) : 0;
-    const int base = (int)win0 + sl * (kWinRows * 4);
-    const int a = max(base + 4 * (e - lo) - lane4, base);
-    return *(const __attribute__((address_space(3))) uint32_t*)(uintptr_t)(uint32_t)a;
-  };
-  if (idx > 0) {
-    ensure(cw);
-    read_wlo();
-    uint32_t Wa = row_word(slot, idx), Wb = 0;
-    uint32_t rec_pm = 0;  // lane k: steps of chunk (64-aligned base) + k
-    int rec_e = 0;        // lane k: its entry row
-    int off = 0;          // lane of row idx in the current words
-    // One chunk on the words in Wc, the next chunk's read into Wn (also past
-    // chunk 0 or the walk's end, unused: a conditional read would make the
-    // compiler wait for every LDS read in flight where the paths join).
-    auto chunk = [&](uint32_t& Wc, uint32_t& Wn, int nslot) __attribute__((always_inline)) {
-      Wn = row_word(nslot, idx);
-      __builtin_amdgcn_sched_barrier(0);
-      // (readfirstlane: the compiler treats asm results as per-lane values)
-      const uint32_t pm = (uint32_t)uni((int)walk_chunk(Wc, Wc >> 1, uni(off), uni(q0)));
-      __builtin_amdgcn_sched_barrier(0);
-      const int kk = __builtin_popcount(pm);
-      write_lanes(rec_pm, pm, rec_e, uni(idx), uni(cw & (kWave - 1)));
-      idx -= kk;
-      off = kk;
-      q0 = 0;
-      cw -= 1;
-      slot = nslot;
-    };
-    // Blocks of chunks down to a multiple of 8: the windows a block reads are
-    // checked once, and the walker's position is published once per block
-    // (the loader refills slots of chunks above it).  The first block walks
-    // chunk by chunk until the walk ends or the block does; every later block
-    // walks all eight chunks unconditionally (a path that reaches row 0 inside
-    // the block only yields records of rows <= 0, which are not rows) and
-    // checks for the end after them.  The chunk code holds no inner loop, so
-    // the compiler waits for each read only where its words are used, one
-    // chunk after it was issued.
-    bool more = true;
-    {
-      lds_put64(lds_off(&L.wpos), walk_pos(cw, idx));
-      ensure(max((cw & ~7) - 1, 0));
-      read_wlo();
-      bool in_b = false;  // the next chunk's words are in Wb
-#pragma unroll
-      for (int k = 0; k < 4; ++k) {
-        chunk(Wa, Wb, uni(slot == 0 ? kNWin - 1 : slot - 1));
-        more = idx > 0 && cw >= 0;
-        if (!more || (cw & 7) == 7) {
-          in_b = true;
-          break;
+  constexpr uint32_t kWinBytes = kWinEnt * 4;
+  uint32_t rec_pm = 0;  // lane k: step mask of chunk (64-aligned base) + k
+  int rec_e = 0;        // lane k: its entry row
+  if (e > 0) {
+    wstamps.at(min((cw >> 3) + 1, kWave - 1));  // (debug build) lane k: chunks >= 8k walked; lane C/8+1: start
+    int ent = kEntPerWave * g + rr;             // the entry of row e in its chunk
+    uint32_t wb = win0 + (uint32_t)slot * kWinBytes;  // window of chunk cw
+    using lds_u32 = __attribute__((address_space(3))) uint32_t;
+    using lds_i64 = __attribute__((address_space(3))) long long;
+    lds_i64* const wpos_p = (lds_i64*)(uintptr_t)lds_off(&L.wpos);
+    // Chunk by chunk from the top: the walker's position is published with
+    // each chunk (the loaders may then refill the slot of the chunk kNWin
+    // below it once it is walked), and the staging of the next eight chunks
+    // is checked every eighth chunk.  The chain per chunk is one LDS read at
+    // a wave-uniform address plus scalar arithmetic.
+    for (; cw >= 0 && e > 0; --cw) {
+      if (cw == c_top || (cw & 7) == 7) {
+        ensure(max(cw - 7, 0));
+        if (BANDED) {
+          wlo_v = lds_load(&L.wlo[min(lane, kNWin - 1)]);
+          lgkm_wait0();  // (so that no wait for it is left inside the chunk loop)
         }
-        chunk(Wb, Wa, uni(slot == 0 ? kNWin - 1 : slot - 1));
-        more = idx > 0 && cw >= 0;
-        if (!more || (cw & 7) == 7) break;
+        wstamps.at((cw + 1) >> 3);
       }
-      if (in_b) Wa = Wb;
-      if (!more || ((cw + 1) & (kWave - 1)) == 0)
-        flush_records(rsl, (cw + 1) & ~(kWave - 1), cw + 1, c_top, rec_pm, rec_e, lane);
-    }
-    static_assert(kNWin % 8 == 0, "an aligned block of chunks occupies consecutive slots");
-    while (more) {
-      lds_put64(lds_off(&L.wpos), walk_pos(cw, idx));
-      ensure(max(cw - 8, 0));
-      read_wlo();
-      // Chunks cw .. cw-7 sit in slots bs+7 .. bs, chunk cw-8 in the slot
-      // before bs.
-      const int bs = uni(slot - 7), before = uni(bs == 0 ? kNWin - 1 : bs - 1);
-#pragma unroll
-      for (int k = 0; k < 4; ++k) {
-        chunk(Wa, Wb, bs + 6 - 2 * k);
-        chunk(Wb, Wa, k < 3 ? bs + 5 - 2 * k : before);
+      const int lo = BANDED ? uni(__builtin_amdgcn_readlane(wlo_v, slot)) : 0;
+      // Entry en of the window (a correct walk never leaves it; with data of
+      // a timed-out call an address outside the LDS reads 0).
+      auto at = [&](int en) __attribute__((always_inline)) -> uint32_t {
+        const uint32_t a = wb + 4u * (uint32_t)(en - lo);
+        return (uint32_t)uni((int)*(const lds_u32*)(uintptr_t)a);
+      };
+      uint32_t pm = at(ent);
+      // (issued after the read: LDS operations of a wave complete in order)
+      if (lane == 0) *wpos_p = walk_pos(cw, e);
+      int s = __builtin_popcount(pm);
+      if (rr < s) {
+        // The path climbed into the row above the wave at position pos.
+        const int pos = 31 - __builtin_clz(pm);
+        if (pos < kChunk - 1) pm |= at(ent - rr - (kEntPerWave - kMidOff) + pos + 1);
+        s = __builtin_popcount(pm);
       }
-      more = idx > 0 && cw >= 0;
-      // Records are complete for every 64-aligned group the walk has left.
-      if (!more || ((cw + 1) & (kWave - 1)) == 0)
-        flush_records(rsl, (cw + 1) & ~(kWave - 1), cw + 1, c_top, rec_pm, rec_e, lane);
+      write_lanes(rec_pm, pm, rec_e, e, cw & (kWave - 1));
+      e -= s;
+      rr -= s;
+      ent -= s;
+      if (rr < 0) {
+        // into the wave above: its row 63 + rr, entry kEntPerWave * (g - 1) + 63 + rr
+        rr += kRowsPerWave;
+        ent -= kEntPerWave - kRowsPerWave;
+      }
+      if (slot == 0) {
+        slot = kNWin - 1;
+        wb = win0 + (uint32_t)(kNWin - 1) * kWinBytes;
+      } else {
+        slot -= 1;
+        wb -= kWinBytes;
+      }
+      slot = uni(slot);
+      wb = (uint32_t)uni((int)wb);
+      // Records are complete for a 64-aligned group once its lowest chunk is walked.
+      if ((cw & (kWave - 1)) == 0) flush_records(rsl, cw, cw, c_top, rec_pm, rec_e, lane);
     }
+    wstamps.at(max(cw + 1, 0) >> 3);
+    // The partial group the walk ended in (chunk cw + 1 was walked last).
+    if (((cw + 1) & (kWave - 1)) != 0) flush_records(rsl, (cw + 1) & ~(kWave - 1), cw + 1, c_top, rec_pm, rec_e, lane);
   }
+  wstamps.flush(trace_of(p).walk + (size_t)b * kWave);
+  waited.flush(trace_of(p).item + 8 * (size_t)b + 4);
   wave_lds_sync();
   lds_put64(lds_off(&L.wpos), -1ll);
   if (lane == 0) rsl[0] = 0;
@@ -1252,71 +1349,13 @@ __device__ __forceinline__ void path_writer(const KParams& p, SweepLds& L, uint3
     const int r0 = min(q0 + wv * per, q1), r1 = min(r0 + per, q1);
     if (r1 > r0) {
       const int b = wait_published(p, k, tag, limit, bd);
+      if (wv == 0) stamp(trace_of(p).tile + 2 * (size_t)t + 0);
       if (b >= 0) write_path_rows(p, b, r0, r1, lane);
+      if (wv == 0) stamp(trace_of(p).tile + 2 * (size_t)t + 1);
     }
     if (threadIdx.x == 0) L.tile = (int)next;
     __syncthreads();
     t = L.tile;
-  }
-}
-
-// ---------------------------------------------------------------- storer wave
-// Decision words of the workgroup's four sweep waves, from their slots to
-// dec[b][c][row] with device-scope write-through stores (lane 0 holds the
-// row above, whose word nobody reads: its offset lies past the resource, so
-// that store is dropped), in chunk order per wave; chunk c of a wave is
-// complete in its slot once that wave's progress passes c + 1.  Once all of a
-// wave's stores have landed, its done flag goes up.  The stores are kept out
-// of the sweep waves, whose every step would otherwise wait behind the
-// loaders' traffic to issue its store, and out of the loaders, whose waits
-// count their own loads only.
-__device__ __forceinline__ void storer_role(const KParams& p, SweepLds& L, int b, int r, int tx, int ty, int lane, uint32_t tag,
-                                            Bound& bd) {
-  const __amdgpu_buffer_rsrc_t dr =
-      make_cursor(p.dec + (size_t)b * p.NC * (size_t)p.TP, (uint64_t)p.NC * p.TP * 4u).rsrc();
-  const int dstride = p.TP * 4;
-  int taken[kWavesPerBlock], cend[kWavesPerBlock], cbeg[kWavesPerBlock], dvo[kWavesPerBlock];
-  int left = 0;
-#pragma unroll
-  for (int w = 0; w < kWavesPerBlock; ++w) {
-    const WaveCtx xw = make_ctx(b, r * kWavesPerBlock + w, w, lane, tx, ty);
-    cbeg[w] = xw.c_begin;
-    cend[w] = xw.g <= xw.g_last ? xw.c_end : xw.c_begin;
-    taken[w] = cbeg[w];
-    dvo[w] = lane > 0 ? 4 * xw.row : -1;  // lane 0's word (the row above) is not stored
-    left += cend[w] - cbeg[w];
-    // (a wave of the item without chunks has nothing to store)
-    if (xw.g <= xw.g_last && cend[w] == cbeg[w] && lane == 0) st_dev(p.done + (size_t)b * p.NW + xw.g, tag);
-  }
-  int spins = 0;
-  while (left > 0 && !bd.out) {
-    bool moved = false;
-#pragma unroll
-    for (int w = 0; w < kWavesPerBlock; ++w) {
-      if (taken[w] >= cend[w]) continue;
-      const int* const progress = w > 0 ? reinterpret_cast<const int*>(&L.box[w - 1]) + 2 : &L.cons0;
-      const int cons = uni(lds_poll(progress));
-      while (taken[w] < cend[w] && cons >= taken[w] + 2) {
-        const uint32_t* const src = reinterpret_cast<const uint32_t*>(
-            &L.u.ring[w][((taken[w] - cbeg[w]) & (kRing - 1)) * kSlotStride + kBitsOff]);
-        const uint32_t v = src[lane];
-        __builtin_amdgcn_raw_buffer_store_b32(v, dr, dvo[w], taken[w] * dstride, kPolicyDev);
-        ++taken[w];
-        --left;
-        lds_put(lds_off(&L.box[w]) + 12u, taken[w]);  // (after the read: LDS operations run in order)
-        moved = true;
-        if (taken[w] == cend[w]) {
-          vm_wait<0>();
-          if (lane == 0) st_dev(p.done + (size_t)b * p.NW + r * kWavesPerBlock + w, tag);
-        }
-      }
-    }
-    if (!moved) {
-      if (++spins > bd.limit) bd.expire();
-      __builtin_amdgcn_s_sleep(1);
-    } else {
-      spins = 0;
-    }
   }
 }
 
@@ -1354,10 +1393,11 @@ __device__ __forceinline__ void sweep_role(const KParams& p, SweepLds& L, const 
 
   // The walker.
   if (lane == (x.tx - 1) - g_last * kRowsPerWave + 1 && p.score) p.score[b] = score;
-  if (p.T > kWinRows)
-    walk<true>(p, L, x.tx, x.ty, lane, bd);
+  if (p.EP > kWinEnt)
+    walk<true>(p, L, b, x.tx, x.ty, lane, bd);
   else
-    walk<false>(p, L, x.tx, x.ty, lane, bd);
+    walk<false>(p, L, b, x.tx, x.ty, lane, bd);
+  stamp(trace_of(p).item + 8 * (size_t)b + 2);
   int32_t* rs_out = p.row_start + (size_t)b * ((size_t)p.T + 1);
   const int* const rsl = L.u.walk.rs;
   for (int i = lane; i <= p.T; i += kWave) st_dev(reinterpret_cast<uint32_t*>(rs_out + i), (uint32_t)rsl[i]);
@@ -1368,6 +1408,7 @@ __device__ __forceinline__ void sweep_role(const KParams& p, SweepLds& L, const 
     for (int i = lane; i < p.T; i += kWave) d[i] = rsl[i + 1] - rsl[i];
   }
   publish_item(p, b, tag, lane);
+  stamp(trace_of(p).item + 8 * (size_t)b + 3);
   // The item's status, once every wave whose work reaches its outputs has
   // passed its last wait: timed out if any of them (or this walker) gave up,
   // or if a path writer gave up before the publication became visible to it.
@@ -1389,6 +1430,7 @@ __device__ __forceinline__ void loader_role(const KParams& p, SweepLds& L, const
   // Decision windows for the walk, once every wave of the item has published
   // its words.
   wait_flags(p.done + (size_t)b * p.NW, g_last + 1, tag, lane, bd);
+  if (x.w == 0) stamp(trace_of(p).item + 8 * (size_t)b + 0);
   load_windows(p, L, b, x.ty, x.w, lane, bd);
 }
 
@@ -1425,11 +1467,12 @@ __device__ __forceinline__ void finish_call(const KParams& p, uint32_t gen) {
   }
 }
 
-// Nine waves per workgroup (four sweep waves, four loaders, one storer), one
-// workgroup per CU.
+// Twelve waves per workgroup (four sweep waves, four loaders, four
+// finishers), one workgroup per CU.
 template <bool ALIGNED>
 __global__ void __launch_bounds__(kThreads, 1) mas_kernel(KParams p) {
   __shared__ SweepLds L;
+  if (threadIdx.x == 0) stamp(trace_of(p).wg + 2 * (size_t)blockIdx.x);
   if (__hip_atomic_load(&p.hdr->magic, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != kWsMagic) {
     // Not an initialised workspace: report it and touch nothing else.
     if (blockIdx.x == 0 && p.status)
@@ -1444,6 +1487,7 @@ __global__ void __launch_bounds__(kThreads, 1) mas_kernel(KParams p) {
     Bound bd{p.spin_limit, false, &p.hdr->path_fail, tag};
     path_writer(p, L, tag, uni(threadIdx.x / kWave), threadIdx.x & (kWave - 1), bd);
     if (bd.out) __hip_atomic_store(&p.hdr->error, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (threadIdx.x == 0) stamp(trace_of(p).wg + 2 * (size_t)blockIdx.x + 1);
     finish_call(p, gen);
     return;
   }
@@ -1452,8 +1496,8 @@ __global__ void __launch_bounds__(kThreads, 1) mas_kernel(KParams p) {
   const int lane = threadIdx.x & (kWave - 1);
   const int wv = uni(threadIdx.x / kWave);
   const int w = wv & (kWavesPerBlock - 1);
-  const bool is_storer = wv >= 2 * kWavesPerBlock;
-  const bool is_loader = wv >= kWavesPerBlock && !is_storer;
+  const bool is_finisher = wv >= 2 * kWavesPerBlock;
+  const bool is_loader = wv >= kWavesPerBlock && !is_finisher;
   const int g = r * kWavesPerBlock + w;
   const int tx = p.t_x[b];
   const int ty = p.t_y[b];
@@ -1476,17 +1520,18 @@ __global__ void __launch_bounds__(kThreads, 1) mas_kernel(KParams p) {
   __syncthreads();
 
   if (st != kItemOk) {
-    invalid_item(p, b, g, is_loader || is_storer, lane, st, tag);
-  } else if (is_storer) {
-    storer_role(p, L, b, r, tx, ty, lane, tag, bd);
+    invalid_item(p, b, g, is_loader || is_finisher, lane, st, tag);
   } else {
     const WaveCtx x = make_ctx(b, g, w, lane, tx, ty);
-    if (is_loader)
+    if (is_finisher)
+      finisher_role(p, L, x, tag, bd);
+    else if (is_loader)
       loader_role<ALIGNED>(p, L, x, tag, bd);
     else
       sweep_role(p, L, x, tag, bd);
   }
   if (bd.out) __hip_atomic_store(&p.hdr->error, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  stamp(trace_of(p).wg + 2 * (size_t)blockIdx.x + 1);  // (one wave's stamp: the last to get here wins)
   finish_call(p, gen);
 }
 
@@ -1567,3 +1612,10 @@ hipError_t launch_ws_init(void* p, size_t bytes, hipStream_t stream) {
 }
 
 }  // namespace mas
+
+#ifdef MAS_TRACE
+// Debug build only: where the kernels record their timeline (nullptr: off).
+extern "C" int mas_trace_set(void* buffer) {
+  return (int)hipMemcpyToSymbol(HIP_SYMBOL(mas::g_trace), &buffer, sizeof(buffer));
+}
+#endif

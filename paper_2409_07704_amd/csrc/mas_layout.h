@@ -23,11 +23,27 @@ constexpr int kMaxRows = 8192;               // largest T (the walker keeps row_
 
 // Decision bit of text row i at speech column j (j >= 1): 1 when the forward
 // max took the diagonal predecessor Q[i-1][j-1] (the backtrack then moves to
-// row i-1), 0 when it kept Q[i][j-1].  Stored as
-//   dec[b][c][i]  (uint32, c = j / 32, bit 31 - (j % 32)),
-// i.e. the first column of a chunk is the most significant bit.  Word TP-1
-// of every chunk is a scratch slot (lane 0 of every wave stores there).
-__host__ __device__ constexpr int dec_bit(int j) { return 31 - (j % kChunk); }
+// row i-1), 0 when it kept Q[i][j-1].  A sweep wave packs a row's decisions
+// of one chunk into one 32-bit word, the chunk's first column in bit 31.
+// Those words never leave the CU: they are turned into step masks.
+//
+// Step mask of row i in chunk c: the set of positions p (column 32c + 31 - p)
+// at which the backtrack, entering the chunk in row i at its last column,
+// moves up one row while walking back to the chunk's first column; row i - k
+// begins at the column of the k-th lowest position.  A wave stores, per chunk,
+// kEntPerWave entries at pm[b][c][kEntPerWave * g + ...]:
+//   entry r (r < 63):           the mask of its row 63g + r, for the path
+//                               while it stays in the wave's rows; a path that
+//                               climbs into the row above the wave ends there,
+//                               with that step as its highest position p;
+//   entry kMidOff + q (q < 32): the mask of the wave's last row entered at
+//                               position q (column 32c + 31 - q), positions
+//                               >= q, which completes such a path of the next
+//                               wave at q = p + 1.
+// A path climbs at most 32 rows per chunk, so it crosses at most one wave
+// boundary in a chunk.
+constexpr int kEntPerWave = 96;
+constexpr int kMidOff = 64;
 
 // Boundary hand-off between consecutive workgroups of an item: the last wave
 // g of a workgroup publishes Q[63g+62][j] (its last row) for every column j it
@@ -63,13 +79,13 @@ struct Layout {
   int32_t B, T, S;
   int32_t NW;      // waves per item = ceil(T / 63)
   int32_t NB;      // workgroups per item = ceil(NW / 4)
-  int32_t NC;      // decision chunks per item = ceil(S / 32)
-  int32_t TP;      // decision words per chunk of an item (rows + scratch, multiple of 64)
+  int32_t NC;      // chunks per item = ceil(S / 32)
+  int32_t EP;      // step-mask entries per chunk of an item = kEntPerWave * NW
   size_t off_done;   // uint32 [B][NW] sweep-finished flags (tag values)
   size_t off_tmo;    // uint32 [B] per-item timeout flags (tag values)
   size_t off_order;  // uint64 [B] items in the order their row_start tables were published: tag << 32 | item
   size_t off_slots;  // uint64 [B][NB][NC*32] boundary hand-off words of each workgroup's last wave
-  size_t off_dec;    // uint32 [B][NC][TP] decision words
+  size_t off_pm;     // uint32 [B][NC][EP] step masks
   size_t off_rs;     // int32  [B][T+1] row_start table (mas_forward_ex)
   size_t bytes;
 };
@@ -83,7 +99,7 @@ __host__ inline bool make_layout(int32_t B, int32_t T, int32_t S, Layout* L) {
   L->NW = (T + kRowsPerWave - 1) / kRowsPerWave;
   L->NB = (L->NW + kWavesPerBlock - 1) / kWavesPerBlock;
   L->NC = (S + kChunk - 1) / kChunk;
-  L->TP = (int32_t)round_up((size_t)L->NW * kRowsPerWave + 1, kWave);
+  L->EP = kEntPerWave * L->NW;
   // Overflow guard: every product below stays far under 2^62 when these hold.
   if ((uint64_t)B * (uint64_t)L->NB + kPathWorkgroups > 0x7fffffffull) return false;  // grid size
   if ((uint64_t)B * (uint64_t)T * (uint64_t)S > (1ull << 46)) return false;
@@ -98,8 +114,8 @@ __host__ inline bool make_layout(int32_t B, int32_t T, int32_t S, Layout* L) {
   off = round_up(off + (size_t)B * sizeof(uint64_t), kAlign);
   L->off_slots = off;
   off = round_up(off + (size_t)B * L->NB * (size_t)L->NC * kChunk * sizeof(uint64_t), kAlign);
-  L->off_dec = off;
-  off = round_up(off + (size_t)B * L->NC * (size_t)L->TP * sizeof(uint32_t), kAlign);
+  L->off_pm = off;
+  off = round_up(off + (size_t)B * L->NC * (size_t)L->EP * sizeof(uint32_t), kAlign);
   L->off_rs = off;
   off = round_up(off + (size_t)B * ((size_t)T + 1) * sizeof(int32_t), kAlign);
   L->bytes = off;
