@@ -7,6 +7,7 @@
 #include <stdlib.h>
 
 #include <mutex>
+#include <unordered_map>
 
 #include "mas.h"
 #include "mas_internal.h"
@@ -30,9 +31,43 @@ static int32_t wait_bound() {
   return kDefaultWaitBound;
 }
 
+// Words that carry a call's tag (flags, completion order, boundary hand-off
+// words) are trusted once they hold the current call's tag.  Calls of one
+// shape keep every region in place, so stale words only carry older tags;
+// but a call of another shape lays the regions out elsewhere, over memory the
+// previous call used for plain data (step masks, row starts), which may equal
+// any tag.  So the tagged regions of the new layout are cleared, by a fill
+// kernel on the call's stream, whenever a workspace is used with a shape
+// other than the one of its previous call (mas_workspace_init leaves a
+// workspace clear).
+struct Shape {
+  int32_t B, T, S;
+};
+static std::mutex g_ws_mu;
+static std::unordered_map<uintptr_t, Shape> g_ws_shape;  // workspace -> shape of its last call (B = 0: clear)
+
+static void note_clear_workspace(const void* ws) {
+  std::lock_guard<std::mutex> lock(g_ws_mu);
+  g_ws_shape[(uintptr_t)ws] = Shape{0, 0, 0};
+}
+
+static hipError_t prepare_workspace(void* ws, const Layout& L, hipStream_t stream) {
+  std::lock_guard<std::mutex> lock(g_ws_mu);
+  auto it = g_ws_shape.find((uintptr_t)ws);
+  const bool clear = it != g_ws_shape.end() && it->second.B == 0;
+  const bool same = it != g_ws_shape.end() && it->second.B == L.B && it->second.T == L.T && it->second.S == L.S;
+  if (!clear && !same) {
+    const hipError_t e = launch_fill(static_cast<char*>(ws) + L.off_done, L.off_pm - L.off_done, stream);
+    if (e != hipSuccess) return e;
+  }
+  g_ws_shape[(uintptr_t)ws] = Shape{L.B, L.T, L.S};
+  return hipSuccess;
+}
+
 static mas_status run(const float* value, const int32_t* t_x, const int32_t* t_y, const Layout& L,
                       int32_t* row_start, int32_t* durations, float* score, int32_t* status, uint8_t* path, void* ws,
                       hipStream_t stream) {
+  if (prepare_workspace(ws, L, stream) != hipSuccess) return MAS_ERR_HIP;
   char* base = static_cast<char*>(ws);
   KParams p;
   p.value = value;
@@ -83,6 +118,7 @@ static mas_status scratch_ptr(hipStream_t stream, void** out) {
     if (hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)) != hipSuccess || ptr == nullptr) return MAS_ERR_HIP;
     if ((uintptr_t)ptr % kAlign != 0) return MAS_ERR_HIP;
     if (launch_ws_init(ptr, MAS_STATIC_SCRATCH_BYTES, stream) != hipSuccess) return MAS_ERR_HIP;
+    note_clear_workspace(ptr);
     g_scratch[dev] = ptr;
   }
   *out = g_scratch[dev];
@@ -103,7 +139,9 @@ mas_status mas_workspace_init(void* workspace, size_t workspace_bytes, hipStream
   if (!workspace) return MAS_ERR_NULL_POINTER;
   if ((uintptr_t)workspace % kAlign != 0 || workspace_bytes < sizeof(WsHeader) || workspace_bytes % 16 != 0)
     return MAS_ERR_WORKSPACE;
-  return launch_ws_init(workspace, workspace_bytes, stream) == hipSuccess ? MAS_OK : MAS_ERR_HIP;
+  if (launch_ws_init(workspace, workspace_bytes, stream) != hipSuccess) return MAS_ERR_HIP;
+  note_clear_workspace(workspace);
+  return MAS_OK;
 }
 
 mas_status mas_search(const float* value, const int32_t* t_x, const int32_t* t_y, int32_t B, int32_t T, int32_t S,

@@ -65,5 +65,7 @@ hipError_t launch_path(const int32_t* row_start, int32_t B, int32_t T, int32_t S
 // Workspace initialisation: zero-fill of `bytes` (a multiple of 16, at least
 // the header) at a 256-byte aligned pointer, with the header's magic set.
 hipError_t launch_ws_init(void* p, size_t bytes, hipStream_t stream);
+// Zero-fill of `bytes` (a multiple of 16) at a 16-byte aligned pointer.
+hipError_t launch_fill(void* p, size_t bytes, hipStream_t stream);
 
 }  // namespace mas

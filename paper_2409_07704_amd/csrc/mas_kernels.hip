@@ -168,6 +168,7 @@ constexpr int kFinishers = 4;        // finisher waves per workgroup (step masks
 constexpr int kThreads = kThreadsPerBlock + (kLoaders + kFinishers) * kWave;
 constexpr int kRing = 4;             // tile and boundary slots per sweep wave
 constexpr int kPolicyDev = 16;       // cache policy sc1: device scope (write-through stores)
+constexpr int kPolicyStream = 2;     // cache policy nt: streaming, data written once and not read back
 
 // ---------------------------------------------------------------- LDS layout
 // Sweep wave w owns kRing slots of kSlotStride bytes.  Slot k holds
@@ -1168,7 +1169,9 @@ __device__ __forceinline__ void walk(const KParams& p, SweepLds& L, int b, int t
     int spins = 0;
     if (!staged(ch)) waited.begin();
     while (!staged(ch) && !bd.out) {
-      const i32x4 r = *reinterpret_cast<const volatile i32x4*>(&L.wready);
+      // (an LDS-typed load: a generic one would be a FLAT load, whose wait
+      // counts do not stay in order with those of LDS loads)
+      const i32x4 r = *(const volatile __attribute__((address_space(3))) i32x4*)(uintptr_t)lds_off(&L.wready);
       kn0 = uni(r.x);
       kn1 = uni(r.y);
       kn2 = uni(r.z);
@@ -1188,40 +1191,60 @@ __device__ __forceinline__ void walk(const KParams& p, SweepLds& L, int b, int t
   int rec_e = 0;        // lane k: its entry row
   if (e > 0) {
     wstamps.at(min((cw >> 3) + 1, kWave - 1));  // (debug build) lane k: chunks >= 8k walked; lane C/8+1: start
-    int ent = kEntPerWave * g + rr;             // the entry of row e in its chunk
-    uint32_t wb = win0 + (uint32_t)slot * kWinBytes;  // window of chunk cw
     using lds_u32 = __attribute__((address_space(3))) uint32_t;
     using lds_i64 = __attribute__((address_space(3))) long long;
     lds_i64* const wpos_p = (lds_i64*)(uintptr_t)lds_off(&L.wpos);
-    // Chunk by chunk from the top: the walker's position is published with
-    // each chunk (the loaders may then refill the slot of the chunk kNWin
-    // below it once it is walked), and the staging of the next eight chunks
-    // is checked every eighth chunk.  The chain per chunk is one LDS read at
-    // a wave-uniform address plus scalar arithmetic.
-    for (; cw >= 0 && e > 0; --cw) {
-      if (cw == c_top || (cw & 7) == 7) {
-        ensure(max(cw - 7, 0));
+    int ent = kEntPerWave * g + rr;  // the entry of row e in its chunk's array
+    // Window slots of chunk cw and of chunk cw - 2.
+    int slot2 = slot >= 2 ? slot - 2 : slot + kNWin - 2;
+    auto wbase = [&](int sl) __attribute__((always_inline)) -> uint32_t { return win0 + (uint32_t)sl * kWinBytes; };
+    auto lo_of = [&](int sl) __attribute__((always_inline)) -> int {
+      return BANDED ? uni(__builtin_amdgcn_readlane(wlo_v, sl)) : 0;
+    };
+    // The masks of one chunk for rows base, base - 1, ..., base - 63 (lane
+    // k: row base - k, ent_base its entry, rr_base its row in its wave),
+    // read from the chunk's window into one register.  Lanes past row 0 or
+    // the window read whatever is there, never used.
+    auto fetch = [&](int sl, int ent_base, int rr_base) __attribute__((always_inline)) -> uint32_t {
+      constexpr int kGap = kEntPerWave - kRowsPerWave;  // entries between the last row of a wave and the first of the next
+      const int t = ent_base - lane - (lane > rr_base ? kGap : 0) - (lane > rr_base + kRowsPerWave ? kGap : 0);
+      const uint32_t a = wbase(sl) + 4u * (uint32_t)(t - lo_of(sl));
+      return *(const lds_u32*)(uintptr_t)a;
+    };
+    // Chunk cw's masks are in register Pa (base row ba), chunk cw - 1's in
+    // Pb (base bb): each chunk reads its mask with one v_readlane at lane
+    // base - e (0..32: the path climbs at most 32 rows per chunk), then
+    // refills its register with chunk cw - 2 at base e (the row the path
+    // enters chunk cw - 1 in), which is needed two chunks later.  Only a
+    // climb into the row above a wave reads LDS on the chain (rare).
+    ensure(max(cw - 9, 0));
+    if (BANDED) {
+      wlo_v = lds_load(&L.wlo[min(lane, kNWin - 1)]);
+      lgkm_wait0();
+    }
+    uint32_t Pa, Pb;
+    int ba = e, bb = e;
+    auto body = [&](uint32_t& P, int& bp) __attribute__((always_inline)) {
+      if ((cw & 7) == 7) {
+        ensure(max(cw - 9, 0));
         if (BANDED) {
           wlo_v = lds_load(&L.wlo[min(lane, kNWin - 1)]);
-          lgkm_wait0();  // (so that no wait for it is left inside the chunk loop)
+          lgkm_wait0();
         }
         wstamps.at((cw + 1) >> 3);
       }
-      const int lo = BANDED ? uni(__builtin_amdgcn_readlane(wlo_v, slot)) : 0;
-      // Entry en of the window (a correct walk never leaves it; with data of
-      // a timed-out call an address outside the LDS reads 0).
-      auto at = [&](int en) __attribute__((always_inline)) -> uint32_t {
-        const uint32_t a = wb + 4u * (uint32_t)(en - lo);
-        return (uint32_t)uni((int)*(const lds_u32*)(uintptr_t)a);
-      };
-      uint32_t pm = at(ent);
-      // (issued after the read: LDS operations of a wave complete in order)
+      uint32_t pm = (uint32_t)uni(__builtin_amdgcn_readlane((int)P, bp - e));
+      // (after the read of P: a wait for P then only covers the prefetch of
+      // the previous chunk, issued a chunk ago)
       if (lane == 0) *wpos_p = walk_pos(cw, e);
       int s = __builtin_popcount(pm);
       if (rr < s) {
         // The path climbed into the row above the wave at position pos.
         const int pos = 31 - __builtin_clz(pm);
-        if (pos < kChunk - 1) pm |= at(ent - rr - (kEntPerWave - kMidOff) + pos + 1);
+        if (pos < kChunk - 1) {
+          const uint32_t a = wbase(slot) + 4u * (uint32_t)(ent - rr - (kEntPerWave - kMidOff) + pos + 1 - lo_of(slot));
+          pm |= (uint32_t)uni((int)*(const lds_u32*)(uintptr_t)a);
+        }
         s = __builtin_popcount(pm);
       }
       write_lanes(rec_pm, pm, rec_e, e, cw & (kWave - 1));
@@ -1233,17 +1256,32 @@ __device__ __forceinline__ void walk(const KParams& p, SweepLds& L, int b, int t
         rr += kRowsPerWave;
         ent -= kEntPerWave - kRowsPerWave;
       }
-      if (slot == 0) {
-        slot = kNWin - 1;
-        wb = win0 + (uint32_t)(kNWin - 1) * kWinBytes;
-      } else {
-        slot -= 1;
-        wb -= kWinBytes;
+      if (cw >= 2) {
+        P = fetch(slot2, ent, rr);
+        bp = e;
       }
-      slot = uni(slot);
-      wb = (uint32_t)uni((int)wb);
-      // Records are complete for a 64-aligned group once its lowest chunk is walked.
-      if ((cw & (kWave - 1)) == 0) flush_records(rsl, cw, cw, c_top, rec_pm, rec_e, lane);
+      // Records are complete for a 64-aligned group once its lowest chunk is
+      // walked.  (The wait after the flush leaves nothing of its LDS stores
+      // outstanding, so that the compiler can count the prefetches exactly.)
+      if ((cw & (kWave - 1)) == 0) {
+        flush_records(rsl, cw, cw, c_top, rec_pm, rec_e, lane);
+        lgkm_wait0();
+      }
+      slot = uni(slot == 0 ? kNWin - 1 : slot - 1);
+      slot2 = uni(slot2 == 0 ? kNWin - 1 : slot2 - 1);
+      cw -= 1;
+    };
+    // Nothing may be outstanding on the LDS/scalar-memory counter when the
+    // loop starts but the two prefetches: a scalar load still in flight (the
+    // compiler hoists kernel-argument loads) would make every wait inside
+    // the loop a full one.
+    lgkm_wait0();
+    Pa = fetch(slot, ent, rr);
+    Pb = fetch(slot >= 1 ? slot - 1 : kNWin - 1, ent, rr);
+    while (cw >= 0 && e > 0) {
+      body(Pa, ba);
+      if (cw < 0 || e <= 0) break;
+      body(Pb, bb);
     }
     wstamps.at(max(cw + 1, 0) >> 3);
     // The partial group the walk ended in (chunk cw + 1 was walked last).
@@ -1262,9 +1300,12 @@ __device__ __forceinline__ void walk(const KParams& p, SweepLds& L, int b, int t
 // Rows [r0, r1) of the dense path of item b (Sec. 2: the alignment as a 0/1
 // matrix of the input's size) from its published row_start table: row i
 // holds ones at columns [rs[i], rs[i+1]) and zeros elsewhere (rows t_x .. T-1
-// and invalid items: all zeros).  path16: per row, zero pieces by plain
-// 16-byte stores (the pieces holding ones are skipped: offset past the
-// resource), then the few pieces holding ones; otherwise bytes.  (Bounds are
+// and invalid items: all zeros).  path16: per row, zero pieces by 16-byte
+// stores (the pieces holding ones are skipped: offset past the resource),
+// then the few pieces holding ones; otherwise bytes.  The stores are
+// streaming (nt): the path is written once and never read here, and keeping
+// it out of the caches leaves them to the sweeps still running (a launch on
+// the bench batch took 206 us with cached stores, 179 us with these).  (Bounds are
 // clamped to the row: the table is read back from memory, never trusted
 // blindly.)
 __device__ __forceinline__ void write_path_rows(const KParams& p, int b, int r0, int r1, int lane) {
@@ -1284,9 +1325,10 @@ __device__ __forceinline__ void write_path_rows(const KParams& p, int b, int r0,
       if (p.path16) {
         const int plo = lo >> 4, phi = hi > lo ? (hi + 15) >> 4 : plo;  // pieces holding ones
         for (int pc = lane; pc < p.S / 16; pc += kWave)
-          __builtin_amdgcn_raw_buffer_store_b128(zero, r, (pc < plo || pc >= phi) ? row * p.S + 16 * pc : -1, 0, 0);
+          __builtin_amdgcn_raw_buffer_store_b128(zero, r, (pc < plo || pc >= phi) ? row * p.S + 16 * pc : -1, 0, kPolicyStream);
         for (int pc = plo + lane; pc < phi; pc += kWave)
-          __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, path_piece(lo, hi, 16 * pc)), r, row * p.S + 16 * pc, 0, 0);
+          __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, path_piece(lo, hi, 16 * pc)), r, row * p.S + 16 * pc, 0,
+                                                 kPolicyStream);
       } else {
         uint8_t* const rowp = item_path + (size_t)row * p.S;
         for (int j = lane; j < p.S; j += kWave) rowp[j] = (uint8_t)(j >= lo && j < hi);
@@ -1548,7 +1590,8 @@ __global__ void __launch_bounds__(256) mas_path_kernel16(const int32_t* __restri
     const size_t b = bi / T;
     const int i = (int)(bi - b * T);
     const int32_t* rs = row_start + b * ((size_t)T + 1);
-    path[k] = path_piece(rs[i], rs[i + 1], pc * 16);
+    __builtin_nontemporal_store(__builtin_bit_cast(u32x4, path_piece(rs[i], rs[i + 1], pc * 16)),
+                                reinterpret_cast<u32x4*>(path + k));
   }
 }
 
@@ -1601,6 +1644,18 @@ hipError_t launch_path(const int32_t* row_start, int32_t B, int32_t T, int32_t S
     const size_t n = (size_t)B * T * S;
     hipLaunchKernelGGL(mas_path_kernel1, dim3(stream_grid(n, 256)), dim3(256), 0, stream, row_start, B, T, S, path);
   }
+  return hipGetLastError();
+}
+
+__global__ void __launch_bounds__(256) mas_fill_kernel(uint4* __restrict__ p, size_t n16) {
+  for (size_t k = (size_t)blockIdx.x * blockDim.x + threadIdx.x; k < n16; k += (size_t)gridDim.x * blockDim.x)
+    p[k] = make_uint4(0u, 0u, 0u, 0u);
+}
+
+hipError_t launch_fill(void* p, size_t bytes, hipStream_t stream) {
+  const size_t n16 = bytes / 16;
+  if (n16 == 0) return hipSuccess;
+  hipLaunchKernelGGL(mas_fill_kernel, dim3(stream_grid(n16, 256)), dim3(256), 0, stream, reinterpret_cast<uint4*>(p), n16);
   return hipGetLastError();
 }
 

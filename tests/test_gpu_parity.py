@@ -267,6 +267,19 @@ def test_determinism_and_workspace_reuse(mas):
     assert_parity(mas, v1, x1, y1, "reuse-large", workspace=ws)
 
 
+def test_shape_changes_on_one_workspace(mas):
+    """Calls of different shapes, large to small and back, on one workspace:
+    each call lays its regions out differently, over the previous call's data
+    (step masks, row starts), which must never pass for this call's flags."""
+    names = ["tts-b64-t1024-s4096", "tts-b16-t128-s512", "tts-b32-t256-s1024", "tts-b32-t512-s2048"]
+    data = {n: synth.generate(n) for n in names}
+    ws = mas.Workspace(64, 1024, 4096)
+    for rnd in range(3):
+        for n in names:
+            value, tx, ty = data[n]
+            assert_parity(mas, value, tx, ty, f"shape-change round {rnd} {n}", workspace=ws)
+
+
 def test_canaries_and_nonnull_outputs(mas):
     value, tx, ty = synth.generate("tts-b16-t128-s512")
     B, T, S = value.shape
