@@ -171,7 +171,7 @@ mas_status mas_forward(const float* value, const int32_t* t_x, const int32_t* t_
  * of MAS_STATIC_SCRATCH_BYTES that the library holds on every device it runs
  * on until the process ends.  No allocation, ever.
  *   - Limit: batches with mas_workspace_bytes(B, T, S) > MAS_STATIC_SCRATCH_BYTES
- *     return MAS_ERR_SCRATCH and enqueue nothing (64 MiB holds, e.g.,
+ *     return MAS_ERR_SCRATCH and enqueue nothing (80 MiB holds, e.g.,
  *     B = 64, T = 1024, S = 4096).
  *   - The first call on a device enqueues the array's initialisation (a fill
  *     kernel, no memset) on `stream` ahead of the work; it must not be a call
@@ -180,7 +180,7 @@ mas_status mas_forward(const float* value, const int32_t* t_x, const int32_t* t_
  *     last call's state: calls on one device must not overlap (issue them on
  *     one stream, or synchronise); overlapping calls race.
  */
-#define MAS_STATIC_SCRATCH_BYTES ((size_t)64 << 20)
+#define MAS_STATIC_SCRATCH_BYTES ((size_t)80 << 20)
 mas_status mas_forward_static(const float* value, const int32_t* t_x, const int32_t* t_y,
                               uint8_t* path_out, int32_t B, int32_t T, int32_t S,
                               float* score_out, int32_t* item_status_out, hipStream_t stream);

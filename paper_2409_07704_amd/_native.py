@@ -19,7 +19,7 @@ LIB_PATH = os.path.join(_PKG, "libmas.so")
 MAS_OK = 0
 STATUS_NAMES = {0: "MAS_OK", 1: "MAS_ERR_NULL_POINTER", 2: "MAS_ERR_BAD_SHAPE", 3: "MAS_ERR_WORKSPACE", 4: "MAS_ERR_HIP",
                 5: "MAS_ERR_SCRATCH"}
-STATIC_SCRATCH_BYTES = 64 << 20  # MAS_STATIC_SCRATCH_BYTES
+STATIC_SCRATCH_BYTES = 80 << 20  # MAS_STATIC_SCRATCH_BYTES
 ITEM_OK, ITEM_EMPTY, ITEM_INFEASIBLE, ITEM_OUT_OF_RANGE, ITEM_SYNC_TIMEOUT, ITEM_BAD_WORKSPACE = 0, 1, 2, 3, 4, 5
 
 # Every function declared in include/mas.h, with its ctypes signature.

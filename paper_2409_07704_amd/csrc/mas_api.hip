@@ -84,6 +84,7 @@ static mas_status run(const float* value, const int32_t* t_x, const int32_t* t_y
   p.order = reinterpret_cast<uint64_t*>(base + L.off_order);
   p.slots = reinterpret_cast<uint64_t*>(base + L.off_slots);
   p.pm = reinterpret_cast<uint32_t*>(base + L.off_pm);
+  p.pd = reinterpret_cast<uint8_t*>(base + L.off_pd);
   p.B = L.B;
   p.T = L.T;
   p.S = L.S;

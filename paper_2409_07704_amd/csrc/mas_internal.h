@@ -26,6 +26,7 @@ struct KParams {
   uint64_t* order;      // [B] items in the order their row_start tables were published: tag << 32 | item
   uint64_t* slots;      // [B][NB][NC*32] boundary words of each workgroup's last wave
   uint32_t* pm;         // [B][NC][EP] step masks (see mas_layout.h)
+  uint8_t* pd;          // [B][NC][EP] descent bytes (see mas_layout.h)
   int32_t B, T, S, NW, NC, EP, NB;
   int32_t ntile;        // path tiles per item: ceil(T / kPathTileRows)
   int32_t path16;       // path 16-byte aligned and S % 16 == 0
@@ -40,9 +41,10 @@ struct KParams {
 // item: [B][8] step masks of every wave published (windows may start),
 // walk start, walk end, row_start published, ticks the walker waited for
 // windows, (unused) x3; tile: [B * ntile][2] start and
-// end of path tile t.
+// end of path tile t; win: [B][4][2][64] window loader k's n-th window (its
+// chunk C-1-k-4n, n < 8): issue, staged.
 struct TraceLayout {
-  size_t wg, chunk, walk, item, tile, total;
+  size_t wg, chunk, walk, item, tile, win, total;
 };
 __host__ __device__ inline TraceLayout trace_layout(int B, int NW, int NC, int ntile, int grid) {
   TraceLayout t;
@@ -51,7 +53,8 @@ __host__ __device__ inline TraceLayout trace_layout(int B, int NW, int NC, int n
   t.walk = t.chunk + (size_t)B * NW * 64;
   t.item = t.walk + (size_t)B * 64;
   t.tile = t.item + 8 * (size_t)B;
-  t.total = t.tile + 2 * (size_t)B * ntile;
+  t.win = t.tile + 2 * (size_t)B * ntile;
+  t.total = t.win + (size_t)B * 4 * 2 * 64;
   return t;
 }
 

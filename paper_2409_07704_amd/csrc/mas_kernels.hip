@@ -71,7 +71,6 @@ __device__ __forceinline__ uint32_t ld_dev(const uint32_t* p) { return __hip_ato
 
 __device__ __forceinline__ int lds_load(const int* p) { return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP); }
 __device__ __forceinline__ void lds_store(int* p, int v) { __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP); }
-__device__ __forceinline__ long long lds_load(const long long* p) { return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP); }
 template <typename T>
 __device__ __forceinline__ uint32_t lds_off(T* p) {
   return (uint32_t)(uintptr_t)(__attribute__((address_space(3))) T*)p;
@@ -85,12 +84,6 @@ __device__ __forceinline__ int lds_poll(const int* p) {
   asm volatile("ds_read_b32 %0, %1\n\ts_waitcnt lgkmcnt(0)" : "=v"(v) : "v"(lds_off(p)) : "memory");
   return v;
 }
-__device__ __forceinline__ long long lds_poll(const long long* p) {
-  long long v;
-  asm volatile("ds_read_b64 %0, %1\n\ts_waitcnt lgkmcnt(0)" : "=v"(v) : "v"(lds_off(p)) : "memory");
-  return v;
-}
-__device__ __forceinline__ void lds_store(long long* p, long long v) { __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP); }
 
 __device__ __forceinline__ uint32_t call_tag(uint32_t gen) { return 2u * gen + 1u; }
 
@@ -190,28 +183,65 @@ constexpr int kSlotStride = kTileBytes + 512;
 constexpr int kWaveRegion = kRing * kSlotStride;
 __host__ __device__ constexpr int swz(int r) { return (r >> 1) & 7; }
 
-// The walk reuses the slot area: windows of kWinEnt step-mask entries for
-// kNWin chunks, and the row_start table under construction.  A window is
-// staged for chunk c while the walker is at most kNWin chunks above it, so the
-// path can have climbed at most 32 * kNWin rows by then; the window starts at
-// the mid entries of the wave below the lowest such row.
-constexpr int kWinEnt = 1280;
-constexpr int kNWin = 20;
+// The walk reuses the slot area (kWalkArea bytes): the row_start table under
+// construction at its end (rs_bytes(T)), windows of descent bytes before it,
+// one chunk per window, in nslot slots.  An item whose bytes for its rows
+// < t_x fit kMinSlots windows gets windows of all of them (in as many slots
+// as fit, at most kMaxSlots).  Otherwise windows are banded: the most slots
+// S (at least kMinSlots) whose windows of band_ent(S) bytes fit.  A window
+// is staged for chunk c while the walker is at most S chunks above it, so
+// the path can have climbed at most 32 * S rows by then; a banded window
+// starts at the mid entries of the wave below the lowest such row.
+constexpr int kWalkArea = kWavesPerBlock * kWaveRegion;
+constexpr int kMinSlots = 20;
+constexpr int kMaxSlots = 48;   // (below 64 - 10: the window addresses are kept per chunk % 64)
 constexpr int kWinLoaders = 4;  // loader waves staging windows: loader k takes chunks C-1-k, C-1-k-4, ...
-constexpr int kWinAhead = 5;    // windows in flight per loader (kWinEnt / 256 loads each)
-static_assert(kWinLoaders * kWinAhead <= kNWin, "windows in flight fit the slots");
-static_assert(kWinEnt % 256 == 0, "a window is whole 1 KiB loads");
-static_assert(kEntPerWave * ((kChunk * kNWin + 1) / kRowsPerWave + 2) <= kWinEnt,
-              "a window covers the entries the walk can reach");
-// Walker position: (chunk << 32) | row, or -1 once the walk is over.
-__device__ __forceinline__ long long walk_pos(int chunk, int row) { return ((long long)chunk << 32) | (uint32_t)row; }
+constexpr int kMaxAhead = 8;    // windows in flight per loader, at most
+__host__ __device__ constexpr int rs_bytes(int T) { return ((T + 1 + kWave) * 4 + 255) & ~255; }
+__host__ __device__ constexpr int band_ent(int S) {
+  return (kEntPerWave * ((kChunk * S + 1) / kRowsPerWave + 2) + 1023) & ~1023;
+}
+static_assert(kMinSlots * band_ent(kMinSlots) <= kWalkArea - rs_bytes(kMaxRows), "banded windows fit");
+// Window geometry of an item: bytes (entries) per window, a multiple of 1024
+// (whole 1 KiB loads: the LDS loads' rate goes by instructions more than by bytes);
+// slots; whether banded; windows in flight per loader; 1 KiB and 256-byte
+// loads per window.
+struct WinGeom {
+  int ent, nslot, banded, ahead, n16, n4;
+};
+__device__ __forceinline__ WinGeom win_geom(int tx, int T) {
+  const int area = kWalkArea - rs_bytes(T);
+  const int ep = kEntPerWave * ((tx - 1) / kRowsPerWave + 1);
+  const int full = (ep + 1023) & ~1023;
+  WinGeom w;
+  if (full * kMinSlots <= area) {
+    w.ent = full;
+    w.nslot = min(area / full, kMaxSlots);
+    w.banded = 0;
+  } else {
+    int S = kMinSlots;
+    while (S < kMaxSlots && (S + 1) * band_ent(S + 1) <= area) ++S;
+    w.ent = band_ent(S);
+    w.nslot = S;
+    w.banded = 1;
+  }
+  w.n16 = w.ent / 1024;
+  w.n4 = (w.ent % 1024) / 256;
+  // (loads in flight stay below 64, the range of vmcnt)
+  w.ahead = min(min(kMaxAhead, w.nslot / kWinLoaders), 63 / (w.n16 + w.n4));
+  return w;
+}
+// Walker position: (chunk << 16) | row (chunk < 2048, row < 8192), or -1
+// once the walk is over.
+__device__ __forceinline__ int walk_pos(int chunk, int row) { return (chunk << 16) | row; }
+__device__ __forceinline__ int pos_chunk(int wp) { return wp >> 16; }
+__device__ __forceinline__ int pos_row(int wp) { return wp & 0xFFFF; }
 
 struct SweepLds {
   union {
     uint8_t ring[kWavesPerBlock][kWaveRegion];
     struct {
-      uint32_t win[kNWin][kWinEnt];
-      int rs[kMaxRows + 1 + kWave];
+      uint8_t area[kWalkArea];  // windows from the start, row_start table at the end
     } walk;
   } u;
   // Mailbox of sweep wave w, read with one 16-byte load per chunk:
@@ -224,13 +254,26 @@ struct SweepLds {
   // Wave 0's own progress goes to cons0.
   i32x4 box[kWavesPerBlock];
   int cons0;
-  int wlo[kNWin];               // first entry of each walk window (EP > kWinEnt)
+  int wbase[kWave];             // walk window of chunk c (lane c % 64): LDS byte address of its entry 0
   i32x4 wready;                 // window loader k: its windows of chunks >= wready[k] are in LDS
   f32x4 sink[kWavesPerBlock][kChunk / 4 + 1];  // target of hand-offs nobody reads (a fixed LDS op count per step)
-  long long wpos;               // walker position (walk_pos), or -1 once the walk is over
+  int wpos;                     // walker position (walk_pos), or -1 once the walk is over
   int tile;                     // path writer: the tile taken next
+  uint32_t fdone[kWavesPerBlock];  // finisher w's step masks have all landed (the call's tag)
+  // Row-start requests from the walker to its helper: records of up to 64
+  // chunks (two buffers, request n in buffer n % 2), the chunk range they
+  // cover, and the counts of requests posted and done.
+  uint32_t req_d[2][kWave];
+  int req_e[2][kWave];
+  i32x4 req_arg[2];             // base chunk, lowest and highest chunk, last request (1) or not (0)
+  int req_posted, req_done;
 };
 static_assert(sizeof(SweepLds) <= 160 * 1024, "LDS");
+// The walk's row_start table (T + 1 entries, and up to 64 more that
+// flush_records may touch) at the end of the walk area.
+__device__ __forceinline__ int* walk_rs(SweepLds& L, int T) {
+  return reinterpret_cast<int*>(L.u.walk.area + kWalkArea - rs_bytes(T));
+}
 
 // ---------------------------------------------------------------- vector memory
 // Waits until at most N vector-memory operations of this wave are outstanding.
@@ -259,6 +302,20 @@ __device__ __forceinline__ void vm_wait_le(int n) {
     else if (n >= 2) vm_wait<2>();
     else if (n >= 1) vm_wait<1>();
     else vm_wait<0>();
+  }
+}
+// Waits until at most n operations are outstanding, n in [LO, HI] known only
+// at run time (a tree of compile-time branches).
+template <int LO, int HI>
+__device__ __forceinline__ void vm_wait_exact(int n) {
+  if constexpr (LO == HI) {
+    vm_wait<LO>();
+  } else {
+    constexpr int MID = (LO + HI) / 2;
+    if (n <= MID)
+      vm_wait_exact<LO, MID>(n);
+    else
+      vm_wait_exact<MID + 1, HI>(n);
   }
 }
 // vm_wait_le with the call site's usual count first.
@@ -487,6 +544,17 @@ __device__ __forceinline__ void wait_flags(const uint32_t* flag, int n, uint32_t
   }
 }
 
+// Waits (bounded) until the LDS words f[0 .. n) all hold tag.
+__device__ __forceinline__ void wait_tags(const uint32_t* f, int n, uint32_t tag, Bound& bd) {
+  for (int k = 0; k < n; ++k) {
+    int spins = 0;
+    while (!bd.out && (uint32_t)uni(lds_poll(reinterpret_cast<const int*>(f + k))) != tag) {
+      if (++spins > bd.limit) bd.expire();
+      __builtin_amdgcn_s_sleep(1);
+    }
+  }
+}
+
 // Spins (bounded) until the LDS word *p >= v; returns the last value read.
 // The bound counts polls since the word last changed.
 __device__ __forceinline__ int wait_at_least(const int* p, int v, Bound& bd) {
@@ -532,13 +600,6 @@ __device__ __forceinline__ void lgkm_wait0() { __builtin_amdgcn_s_waitcnt(0xC07F
 __device__ __forceinline__ void lds_put(uint32_t addr, int v) {
   uint64_t sv;
   asm volatile("s_mov_b64 %[sv], exec\n\ts_mov_b64 exec, 1\n\tds_write_b32 %[a], %[v]\n\ts_mov_b64 exec, %[sv]"
-               : [sv] "=&s"(sv)
-               : [a] "v"(addr), [v] "v"(v)
-               : "memory");
-}
-__device__ __forceinline__ void lds_put64(uint32_t addr, long long v) {
-  uint64_t sv;
-  asm volatile("s_mov_b64 %[sv], exec\n\ts_mov_b64 exec, 1\n\tds_write_b64 %[a], %[v]\n\ts_mov_b64 exec, %[sv]"
                : [sv] "=&s"(sv)
                : [a] "v"(addr), [v] "v"(v)
                : "memory");
@@ -996,9 +1057,12 @@ __device__ __forceinline__ void finisher_role(const KParams& p, SweepLds& L, con
   const int C = (x.ty + kChunk - 1) / kChunk;
   const uint32_t top_keep = ~0u << (kChunk - 1 - (x.ty - 1) % kChunk);
   const __amdgpu_buffer_rsrc_t dr = make_cursor(p.pm + (size_t)x.b * p.NC * (size_t)p.EP, (uint64_t)p.NC * p.EP * 4u).rsrc();
+  const __amdgpu_buffer_rsrc_t ddr = make_cursor(p.pd + (size_t)x.b * p.NC * (size_t)p.EP, (uint64_t)p.NC * p.EP).rsrc();
   const int base = kEntPerWave * x.g;
   const int row_off = lane > 0 ? 4 * (base + lane - 1) : -1;  // lane 0's mask (the row above) is not stored
   const int mid_off = lane >= kWave - 8 ? 4 * (base + kMidOff + 4 * (lane - (kWave - 8))) : -1;
+  const int row_doff = lane < 16 ? base + 4 * lane : -1;  // lanes 0..15: the row bytes, four per dword
+  const int mid_doff = lane >= kWave - 8 ? base + kMidOff + 4 * (lane - (kWave - 8)) : -1;
   const int q0 = 4 * (lane - (kWave - 8));  // the first mid entry a lane in 56..63 stores
   const int* const progress = w > 0 ? reinterpret_cast<const int*>(&L.box[w - 1]) + 2 : &L.cons0;
   const uint32_t taken_addr = lds_off(&L.box[w]) + 12u;
@@ -1028,7 +1092,24 @@ __device__ __forceinline__ void finisher_role(const KParams& p, SweepLds& L, con
       for (int m = 0; m < 8; ++m) h[24 + m] = o[m];
     }
     const int soff = c * p.EP * 4;
-    __builtin_amdgcn_raw_buffer_store_b32(~h[kChunk - 1], dr, row_off, soff, kPolicyDev);
+    const uint32_t pm_row = ~h[kChunk - 1];
+    __builtin_amdgcn_raw_buffer_store_b32(pm_row, dr, row_off, soff, kPolicyDev);
+    {
+      // The row's descent byte (lane l: row l - 1 of the wave), stored as
+      // whole dwords: lane k < 16 gathers the bytes of rows 4k .. 4k+3
+      // (lanes 4k+1 .. 4k+4; the last, past row 62, is a pad byte).
+      const int s_row = __builtin_popcount(pm_row);
+      const uint32_t d = s_row > lane - 1 ? kEscape + (31u - (uint32_t)__builtin_clz(pm_row | 1u)) : (uint32_t)s_row;
+      const int src = 4 * (4 * lane + 1);
+      const uint32_t b0 = (uint32_t)__builtin_amdgcn_ds_bpermute(src, (int)d);
+      const uint32_t b1 = (uint32_t)__builtin_amdgcn_ds_bpermute(src + 4, (int)d);
+      const uint32_t b2 = (uint32_t)__builtin_amdgcn_ds_bpermute(src + 8, (int)d);
+      // (every lane takes part in each permute: a lane left out of one
+      // would not supply its own byte to the others)
+      uint32_t b3 = (uint32_t)__builtin_amdgcn_ds_bpermute(min(src + 12, 4 * (kWave - 1)), (int)d);
+      b3 = lane < 15 ? b3 : 0u;
+      __builtin_amdgcn_raw_buffer_store_b32(b0 | b1 << 8 | b2 << 16 | b3 << 24, ddr, row_doff, c * p.EP, kPolicyDev);
+    }
     // Mid entry q: the last row's mask after column 31 - q, its positions
     // raised by q; lane 63's values gathered into lanes 56..63, four each.
     float hq[kChunk];
@@ -1038,53 +1119,75 @@ __device__ __forceinline__ void finisher_role(const KParams& p, SweepLds& L, con
     const u32x4 mv = {~__float_as_uint(f.x) << q0, ~__float_as_uint(f.y) << (q0 + 1), ~__float_as_uint(f.z) << (q0 + 2),
                       ~__float_as_uint(f.w) << (q0 + 3)};
     __builtin_amdgcn_raw_buffer_store_b128(mv, dr, mid_off, soff, kPolicyDev);
+    const uint32_t md = (uint32_t)__builtin_popcount(mv.x) | (uint32_t)__builtin_popcount(mv.y) << 8 |
+                        (uint32_t)__builtin_popcount(mv.z) << 16 | (uint32_t)__builtin_popcount(mv.w) << 24;
+    __builtin_amdgcn_raw_buffer_store_b32(md, ddr, mid_doff, c * p.EP, kPolicyDev);
   }
   vm_wait<0>();
   if (lane == 0) st_dev(p.done + (size_t)x.b * p.NW + x.g, tag);
+  lds_put(lds_off(&L.fdone[w]), (int)tag);
 }
 
 // ---------------------------------------------------------------- backtrack
 // Loader side of the walk: loader k (of kWinLoaders) stages the step masks
-// of chunks C-1-k, C-1-k-4, ... down to 0, a window of kWinEnt entries per
-// chunk, kWinAhead windows in flight, into slot ch % kNWin once the walker
-// has walked the chunk that slot held, and publishes the lowest chunk of
-// its sequence staged so far in wready[k].  When an item has more than
-// kWinEnt entries per chunk, a window starts at the mid entries of the wave
-// below the lowest row the walk can reach before it leaves the chunk (32
-// rows per chunk below the walker's row at issue time).  Stops early once the
-// walker has reached row 0.
-__device__ __forceinline__ void load_windows(const KParams& p, SweepLds& L, int b, int ty, int k, int lane, Bound& bd) {
+// of chunks C-1-k, C-1-k-4, ... down to 0, one window per chunk (WinGeom:
+// its size, the slot count, up to `ahead` windows in flight), into slot
+// ch % nslot once the walker has walked the chunk that slot held.  It
+// publishes its progress in wready[k] as its lowest chunk staged so far
+// minus 3 (its next chunk is 4 below): every chunk of its sequence at or
+// above that value is staged, so that the windows of all chunks >= ch are
+// in LDS once every loader's value is <= ch (-2^30 for a loader with no
+// chunks).  A banded window starts at the mid entries of the wave below the
+// lowest row the walk can reach before it leaves the chunk (32 rows per
+// chunk below the walker's row at issue time).  The LDS address of entry 0
+// of chunk ch's window goes to wbase[ch % 64] before the window is issued.
+// Stops early once the walk is over.
+__device__ __forceinline__ void load_windows(const KParams& p, SweepLds& L, int b, int tx, int ty, int k, int lane, Bound& bd) {
   const int C = (ty + kChunk - 1) / kChunk;
-  const uint32_t* db = p.pm + (size_t)b * p.NC * (size_t)p.EP;
-  const uint64_t chunk_bytes = (uint64_t)p.EP * 4u;
-  const bool banded = p.EP > kWinEnt;
-  const uint32_t win0 = lds_off(&L.u.walk.win[0][0]);
+  const uint8_t* db = p.pd + (size_t)b * p.NC * (size_t)p.EP;
+  const uint64_t chunk_bytes = (uint64_t)p.EP;
+  const WinGeom wg = win_geom(tx, p.T);
+  const bool banded = wg.banded;
+  const int nslot = wg.nslot;
+  const int loads = wg.n16 + wg.n4;
+  const uint32_t slot_bytes = (uint32_t)wg.ent;
+  const uint32_t win0 = lds_off(&L.u.walk.area[0]);
   const uint32_t ready_addr = lds_off(&L.wready) + 4u * (uint32_t)k;
+  const uint32_t base_addr = lds_off(&L.wbase[0]);
   constexpr int kStep = kWinLoaders;
-  constexpr int kLoads = kWinEnt / 256;  // 1 KiB per load
   // Own chunks above `issued` are issued; own chunks >= `readied` are staged.
   int issued = C - 1 - k, readied = C - 1 - k + kStep;
-  long long wpos = lds_poll(&L.wpos);
+  int slot = issued >= 0 ? issued % nslot : 0;  // slot of chunk `issued`
+  if (issued < 0) lds_put(ready_addr, -(1 << 30));
+  // Above the walker, which shares a SIMD with one of the loaders and issues
+  // without pause: a loader's few instructions then go first.
+  __builtin_amdgcn_s_setprio(3);
+  // (debug build) lane n: the n-th window issued, staged; the first eight
+  // only: a stamp costs the loader about as long as staging a window
+  Stamps t_iss, t_rdy;
+  int wpos = uni(lds_poll(&L.wpos));
   int spins = 0;
   while (readied - kStep >= 0 && wpos >= 0 && !bd.out) {
-    while (issued >= 0 && readied - kStep - issued < kStep * kWinAhead) {
-      // The slot holds chunk issued + kNWin until the walker has walked it:
-      // the published position is the chunk the walker walks next.
-      if ((int)(wpos >> 32) >= issued + kNWin) {
-        wpos = lds_poll(&L.wpos);
-        if (wpos < 0 || (int)(wpos >> 32) >= issued + kNWin) break;
+    while (issued >= 0 && readied - kStep - issued < kStep * wg.ahead) {
+      // The slot holds chunk issued + nslot until the walker has walked it:
+      // the published position is a chunk the walker has not walked yet.
+      if (pos_chunk(wpos) >= issued + nslot) {
+        wpos = uni(lds_poll(&L.wpos));
+        if (wpos < 0 || pos_chunk(wpos) >= issued + nslot) break;
       }
-      const int e = uni((int)(uint32_t)wpos);
-      const int row_lo = max(e - kChunk * kNWin - 1, 0);
+      const int e = uni(pos_row(wpos));
+      const int row_lo = max(e - kChunk * nslot - 1, 0);
       const int lo = banded ? max(kEntPerWave * (row_lo / kRowsPerWave) - (kEntPerWave - kMidOff), 0) : 0;
-      const int slot = issued % kNWin;
-      if (banded) lds_put(lds_off(&L.wlo[slot]), lo);
-      const Cursor cr = make_cursor(db + (size_t)issued * p.EP + lo, chunk_bytes - (uint64_t)lo * 4u);
+      const uint32_t win = win0 + (uint32_t)slot * slot_bytes;
+      lds_put(base_addr + 4u * (uint32_t)(issued & (kWave - 1)), (int)(win - (uint32_t)lo));
+      const Cursor cr = make_cursor(db + (size_t)issued * p.EP + lo, chunk_bytes - (uint64_t)lo);
       const __amdgpu_buffer_rsrc_t r = cr.rsrc_s();
-#pragma unroll
-      for (int q = 0; q < kLoads; ++q)
-        dma16_dev(win0 + (uint32_t)slot * (kWinEnt * 4) + 1024u * q, r, 16 * lane + 1024 * q);
+      for (int q = 0; q < wg.n16; ++q) dma16_dev(win + 1024u * q, r, 16 * lane + 1024 * q);
+      for (int q = 0; q < wg.n4; ++q) dma4_dev(win + 1024u * wg.n16 + 256u * q, r, 4 * lane + 1024 * wg.n16 + 256 * q);
+      if ((C - 1 - k - issued) / kStep < 8) t_iss.at((C - 1 - k - issued) / kStep);
       issued -= kStep;
+      slot -= kStep;
+      if (slot < 0) slot += nslot;
       spins = 0;
     }
     const int inflight = (readied - kStep - issued) / kStep;
@@ -1092,22 +1195,22 @@ __device__ __forceinline__ void load_windows(const KParams& p, SweepLds& L, int 
       // Nothing in flight: wait for the walker to free a slot.
       if (++spins > bd.limit) bd.expire();
       __builtin_amdgcn_s_sleep(1);
-      wpos = lds_poll(&L.wpos);
+      wpos = uni(lds_poll(&L.wpos));
       continue;
     }
-    vm_wait_usual<kLoads * (kWinAhead - 1)>(kLoads * (inflight - 1));
+    vm_wait_exact<0, 63>(loads * (inflight - 1));
     readied -= kStep;
-    lds_put(ready_addr, readied);
+    lds_put(ready_addr, readied - (kStep - 1));
+    if ((C - 1 - k - readied) / kStep < 8) t_rdy.at((C - 1 - k - readied) / kStep);
   }
   vm_wait<0>();
+  t_iss.flush(trace_of(p).win + ((size_t)b * kWinLoaders + k) * 2 * kWave);
+  t_rdy.flush(trace_of(p).win + ((size_t)b * kWinLoaders + k) * 2 * kWave + kWave);
 }
 
-// Lane l of a becomes x and lane l of b becomes y (x, y, l wave-uniform).
-__device__ __forceinline__ void write_lanes(uint32_t& a, uint32_t x, int& b, int y, int l) {
-  const bool mine = (int)__lane_id() == l;
-  a = mine ? x : a;
-  b = mine ? y : b;
-}
+// llvm.amdgcn.writelane (v_writelane_b32): lane l of `old` becomes v (v and l
+// wave-uniform), the other lanes keep theirs.
+extern "C" __device__ int mas_writelane(int v, int l, int old) __asm("llvm.amdgcn.writelane.i32");
 
 // Row starts from the walk's records of up to 64 chunks: lane k holds the
 // record of chunk base + k (valid when lo <= chunk <= hi): the step mask pm
@@ -1128,169 +1231,243 @@ __device__ __forceinline__ void flush_records(int* rsl, int base, int lo, int hi
   }
 }
 
+// The walker's helper, a finisher wave on another SIMD than the walker's:
+// turns the walker's records into row starts as the walker hands them over,
+// every 64 chunks, so that the walk does not stop for it.  A record is the
+// row the path entered a chunk in and its descent byte there; the helper
+// reads that row's step mask from memory (with the mid entry of the wave
+// above that completes it when the path climbed out of its wave) and
+// expands the masks (flush_records).  Ends after the request marked last.
+__device__ __forceinline__ void walk_helper(const KParams& p, SweepLds& L, int b, int lane, Bound& bd) {
+  const uint32_t* const pm_item = p.pm + (size_t)b * p.NC * (size_t)p.EP;
+  for (int n = 0;; ++n) {
+    // (polls spaced out: the wave may wait here through the sweep, beside
+    // a sweep wave on its SIMD)
+    int spins = 0;
+    while (!bd.out && uni(lds_poll(&L.req_posted)) < n + 1) {
+      if (++spins > bd.limit) bd.expire();
+      __builtin_amdgcn_s_sleep(4);
+    }
+    if (bd.out) break;
+    const int k = n & 1;
+    const int base = uni(((volatile int*)&L.req_arg[k])[0]), lo = uni(((volatile int*)&L.req_arg[k])[1]);
+    const int hi = uni(((volatile int*)&L.req_arg[k])[2]), last = uni(((volatile int*)&L.req_arg[k])[3]);
+    const uint32_t d = *(volatile uint32_t*)&L.req_d[k][lane];
+    const int e = *(volatile int*)&L.req_e[k][lane];
+    const int c = base + lane;
+    uint32_t pm = 0;
+    if (c >= lo && c <= hi && e >= 0) {
+      const int g = e / kRowsPerWave, rr = e - g * kRowsPerWave;
+      const uint32_t* const chunk = pm_item + (size_t)c * p.EP;
+      pm = ld_dev(chunk + kEntPerWave * g + rr);
+      const uint32_t pos = d - kEscape;
+      if (d >= kEscape && pos < kChunk - 1) pm |= ld_dev(chunk + kEntPerWave * (g - 1) + kMidOff + pos + 1);
+    }
+    flush_records(walk_rs(L, p.T), base, lo, hi, pm, e, lane);
+    lgkm_wait0();
+    lds_put(lds_off(&L.req_done), n + 1);
+    if (last) break;
+  }
+}
+
 // The walk of one item from (t_x-1, t_y-1) back to (0, 0) (Algorithm 1's
-// argmax loop, read off the step masks): per chunk, from the top, one LDS
-// lookup of the mask of the row the path enters the chunk in gives every
-// step the path takes inside the chunk, and the row it leaves the chunk in.
-// A path that climbs into the row above its wave ends its mask with that
-// step at position p; the mid entry p + 1 of the wave above completes it.
-// Each chunk's mask and entry row go into lane (chunk % 64) of two
-// registers; every 64 chunks the lanes turn them into row starts in parallel
-// (flush_records).  Builds row_start in L.u.walk.rs: the first column of
-// every row, with rs[0] = 0 and rs[t_x .. T] = t_y.  Runs on the sweep wave
-// that holds row t_x-1; the loaders of its workgroup stage the windows.
-// BANDED: entries per chunk exceed kWinEnt, so windows start at their own
-// first entries (entry 0 otherwise).
-template <bool BANDED>
+// argmax loop, read off the descent bytes): per chunk, from the top, the
+// byte of the row the path enters the chunk in gives the row it leaves the
+// chunk in: that many rows up, or, for a path that climbs into the row above
+// its wave at position p, to the wave's row above and then as many rows as
+// the mid entry p + 1 of the wave above says.  Each chunk's entry row and
+// byte go into lane (chunk % 64) of two registers; every 64 chunks the
+// helper turns them into row starts (walk_helper).  Builds row_start in
+// walk_rs: the first column of every row, with rs[0] = 0 and
+// rs[t_x .. T] = t_y.  Runs on the sweep wave that holds row t_x-1; the
+// loaders of its workgroup stage the windows.
+//
+// A chunk's byte is one v_readlane of a register that holds the bytes of 64
+// consecutive rows of the chunk, read from its window two chunks earlier,
+// from the row the path enters the chunk above in (the path climbs at most
+// 32 rows per chunk).  Only a climb into the row above a wave reads LDS on
+// the chain (rare).  Chunks go in groups of four, 4q+3 down to 4q (the
+// first group is partial): a group starts once the windows of its chunks and
+// of the two below it are staged, checked against the staging progress read
+// in the middle of the group before (read again, and waited for, only when
+// that falls short); the window addresses come with the same read.  The
+// walker publishes its position, by which the loaders free slots, every
+// other chunk.  Once the path is in row 0 the rest of its group is walked
+// all the same: row 0's bytes are zero.
 __device__ __forceinline__ void walk(const KParams& p, SweepLds& L, int b, int tx, int ty, int lane, Bound& bd) {
   stamp(trace_of(p).item + 8 * (size_t)b + 1);
-  int* rsl = L.u.walk.rs;
+  int* rsl = walk_rs(L, p.T);
   Stamps wstamps;
+  Waited waited;  // (debug build) ticks spent waiting for windows
   int e = tx - 1;                      // row of the path at the current chunk's last column
-  int g = e / kRowsPerWave;            // its wave
-  int rr = e - g * kRowsPerWave;       // and its row within the wave
+  const int g0 = e / kRowsPerWave;
+  int rr = e - g0 * kRowsPerWave;      // its row within its wave
+  int ent = kEntPerWave * g0 + rr;     // its entry in its chunk's mask array
   int cw = (ty - 1) / kChunk;          // chunk being walked
   const int c_top = cw;
-  int slot = cw % kNWin;               // window slot of chunk cw
-  // The staging progress of the window loaders as last read; chunk c's
-  // window comes from loader (c_top - c) % kWinLoaders.
-  int kn0 = 1 << 30, kn1 = 1 << 30, kn2 = 1 << 30, kn3 = 1 << 30;
-  // Windows of every chunk >= ch are staged: each loader's chunk among ch ..
-  // ch+3 (if it has one) is.
-  auto staged = [&](int ch) __attribute__((always_inline)) -> bool {
-    const int c0 = ch + ((c_top - ch) & 3), c1 = ch + ((c_top - 1 - ch) & 3);
-    const int c2 = ch + ((c_top - 2 - ch) & 3), c3 = ch + ((c_top - 3 - ch) & 3);
-    return (c0 > c_top || kn0 <= c0) && (c1 > c_top || kn1 <= c1) && (c2 > c_top || kn2 <= c2) &&
-           (c3 > c_top || kn3 <= c3);
-  };
-  // Waits (bounded) until the windows of chunks >= ch are in LDS.
-  Waited waited;  // (debug build) ticks spent waiting for windows
-  auto ensure = [&](int ch) __attribute__((always_inline)) {
-    int spins = 0;
-    if (!staged(ch)) waited.begin();
-    while (!staged(ch) && !bd.out) {
-      // (an LDS-typed load: a generic one would be a FLAT load, whose wait
-      // counts do not stay in order with those of LDS loads)
-      const i32x4 r = *(const volatile __attribute__((address_space(3))) i32x4*)(uintptr_t)lds_off(&L.wready);
-      kn0 = uni(r.x);
-      kn1 = uni(r.y);
-      kn2 = uni(r.z);
-      kn3 = uni(r.w);
-      if (staged(ch)) break;
-      if (++spins > bd.limit) bd.expire();
-      __builtin_amdgcn_s_sleep(1);
-    }
-    waited.end();
-  };
-  // First entries of the window slots (lane k: slot k), read once a block's
-  // windows are staged.
-  int wlo_v = 0;
-  const uint32_t win0 = lds_off(&L.u.walk.win[0][0]);
-  constexpr uint32_t kWinBytes = kWinEnt * 4;
-  uint32_t rec_pm = 0;  // lane k: step mask of chunk (64-aligned base) + k
+  uint32_t rec_d = 0;   // lane k: descent byte of chunk (64-aligned base) + k
   int rec_e = 0;        // lane k: its entry row
+  // Hands the records of chunks lo .. hi (lane k: chunk base + k) to the
+  // helper, in request buffer posted % 2 once the request two back is done.
+  int posted = 0;
+  auto post = [&](int base, int lo, int hi, int last) __attribute__((always_inline)) {
+    wait_at_least(&L.req_done, posted - 1, bd);
+    const int k = posted & 1;
+    *(volatile uint32_t*)&L.req_d[k][lane] = rec_d;
+    *(volatile int*)&L.req_e[k][lane] = rec_e;
+    if (lane < 4) ((volatile int*)&L.req_arg[k])[lane] = lane == 0 ? base : lane == 1 ? lo : lane == 2 ? hi : last;
+    ++posted;
+    lds_put(lds_off(&L.req_posted), posted);
+  };
   if (e > 0) {
     wstamps.at(min((cw >> 3) + 1, kWave - 1));  // (debug build) lane k: chunks >= 8k walked; lane C/8+1: start
     using lds_u32 = __attribute__((address_space(3))) uint32_t;
-    using lds_i64 = __attribute__((address_space(3))) long long;
-    lds_i64* const wpos_p = (lds_i64*)(uintptr_t)lds_off(&L.wpos);
-    int ent = kEntPerWave * g + rr;  // the entry of row e in its chunk's array
-    // Window slots of chunk cw and of chunk cw - 2.
-    int slot2 = slot >= 2 ? slot - 2 : slot + kNWin - 2;
-    auto wbase = [&](int sl) __attribute__((always_inline)) -> uint32_t { return win0 + (uint32_t)sl * kWinBytes; };
-    auto lo_of = [&](int sl) __attribute__((always_inline)) -> int {
-      return BANDED ? uni(__builtin_amdgcn_readlane(wlo_v, sl)) : 0;
+    using lds_u8 = __attribute__((address_space(3))) uint8_t;
+    using lds_i32x4 = __attribute__((address_space(3))) i32x4;
+    const uint32_t wpos_addr = lds_off(&L.wpos);
+    const lds_i32x4* const ready_p = (const lds_i32x4*)(uintptr_t)lds_off(&L.wready);
+    const lds_u32* const base_p = (const lds_u32*)(uintptr_t)(lds_off(&L.wbase[0]) + 4u * (uint32_t)lane);
+    // Staging progress and window addresses as last read (the addresses
+    // read after the progress: valid for every chunk it shows staged).
+    // Chunks >= max_k ready[k] are staged; chunk ch's window is at lane
+    // ch % 64 of `bases`.
+    auto staged_to = [&](const i32x4& r) __attribute__((always_inline)) -> int {
+      return max(max(uni(r.x), uni(r.y)), max(uni(r.z), uni(r.w)));
     };
-    // The masks of one chunk for rows base, base - 1, ..., base - 63 (lane
-    // k: row base - k, ent_base its entry, rr_base its row in its wave),
-    // read from the chunk's window into one register.  Lanes past row 0 or
-    // the window read whatever is there, never used.
-    auto fetch = [&](int sl, int ent_base, int rr_base) __attribute__((always_inline)) -> uint32_t {
-      constexpr int kGap = kEntPerWave - kRowsPerWave;  // entries between the last row of a wave and the first of the next
-      const int t = ent_base - lane - (lane > rr_base ? kGap : 0) - (lane > rr_base + kRowsPerWave ? kGap : 0);
-      const uint32_t a = wbase(sl) + 4u * (uint32_t)(t - lo_of(sl));
-      return *(const lds_u32*)(uintptr_t)a;
-    };
-    // Chunk cw's masks are in register Pa (base row ba), chunk cw - 1's in
-    // Pb (base bb): each chunk reads its mask with one v_readlane at lane
-    // base - e (0..32: the path climbs at most 32 rows per chunk), then
-    // refills its register with chunk cw - 2 at base e (the row the path
-    // enters chunk cw - 1 in), which is needed two chunks later.  Only a
-    // climb into the row above a wave reads LDS on the chain (rare).
-    ensure(max(cw - 9, 0));
-    if (BANDED) {
-      wlo_v = lds_load(&L.wlo[min(lane, kNWin - 1)]);
+    i32x4 ready_v;
+    uint32_t bases = 0, bases_n;
+    // Waits (bounded) until the windows of chunks >= ch are staged, reading
+    // `bases` along.
+    auto ensure = [&](int ch) __attribute__((always_inline)) {
+      waited.begin();
+      int spins = 0;
+      for (;;) {
+        const i32x4 r = *(const volatile lds_i32x4*)ready_p;
+        bases = *(const volatile lds_u32*)base_p;
+        if (staged_to(r) <= ch || bd.out) break;
+        if (++spins > bd.limit) bd.expire();
+        __builtin_amdgcn_s_sleep(1);
+      }
+      // (nothing left in flight: the group's waits count the prefetches alone)
       lgkm_wait0();
-    }
-    uint32_t Pa, Pb;
-    int ba = e, bb = e;
-    auto body = [&](uint32_t& P, int& bp) __attribute__((always_inline)) {
-      if ((cw & 7) == 7) {
-        ensure(max(cw - 9, 0));
-        if (BANDED) {
-          wlo_v = lds_load(&L.wlo[min(lane, kNWin - 1)]);
-          lgkm_wait0();
-        }
-        wstamps.at((cw + 1) >> 3);
-      }
-      uint32_t pm = (uint32_t)uni(__builtin_amdgcn_readlane((int)P, bp - e));
-      // (after the read of P: a wait for P then only covers the prefetch of
-      // the previous chunk, issued a chunk ago)
-      if (lane == 0) *wpos_p = walk_pos(cw, e);
-      int s = __builtin_popcount(pm);
-      if (rr < s) {
-        // The path climbed into the row above the wave at position pos.
-        const int pos = 31 - __builtin_clz(pm);
+      waited.end();
+    };
+    // The bytes of chunk ch for rows e_b, e_b - 1, ..., e_b - 63 (lane k:
+    // row e_b - k; ent_b and rr_b: e_b's entry and row within its wave),
+    // read from ch's window into one register.  Lanes past row 0 or the
+    // window read whatever is there, never used.
+    const uint32_t lane_off = (uint32_t)(-lane);
+    auto fetch = [&](int ch, int ent_b, int rr_b) __attribute__((always_inline)) -> uint32_t {
+      constexpr uint32_t kGap = kEntPerWave - kRowsPerWave;  // from a wave's row 0 to the last row of the wave above
+      const uint32_t base = (uint32_t)__builtin_amdgcn_readlane((int)bases, ch & (kWave - 1));
+      const uint32_t a = base + (uint32_t)ent_b + lane_off - (lane > rr_b ? kGap : 0u);
+      return *(const lds_u8*)(uintptr_t)a;
+    };
+    // One chunk: its byte from lane bp - e of P (P holds the chunk's bytes
+    // from row bp down), then P refilled with chunk cw - 2 from row e, the
+    // row the path enters chunk cw - 1 in.
+    auto body = [&](uint32_t& P, int& bp, bool publish) __attribute__((always_inline)) {
+      const uint32_t d = (uint32_t)__builtin_amdgcn_readlane((int)P, bp - e);
+      if (publish) lds_put(wpos_addr, walk_pos(cw, e));
+      int s = (int)d;
+      if (d >= kEscape) {
+        // The path climbed into the row above the wave at position pos: rr + 1
+        // rows, then what the mid entry pos + 1 of the wave above adds.
+        const uint32_t pos = d - kEscape;
+        s = rr + 1;
         if (pos < kChunk - 1) {
-          const uint32_t a = wbase(slot) + 4u * (uint32_t)(ent - rr - (kEntPerWave - kMidOff) + pos + 1 - lo_of(slot));
-          pm |= (uint32_t)uni((int)*(const lds_u32*)(uintptr_t)a);
+          const uint32_t base = (uint32_t)__builtin_amdgcn_readlane((int)bases, cw & (kWave - 1));
+          const uint32_t a = base + (uint32_t)(ent - rr - (kEntPerWave - kMidOff) + 1) + pos;
+          s += uni((int)*(const lds_u8*)(uintptr_t)a);
         }
-        s = __builtin_popcount(pm);
       }
-      write_lanes(rec_pm, pm, rec_e, e, cw & (kWave - 1));
+      rec_d = (uint32_t)mas_writelane((int)d, cw & (kWave - 1), (int)rec_d);
+      rec_e = mas_writelane(e, cw & (kWave - 1), rec_e);
       e -= s;
       rr -= s;
       ent -= s;
       if (rr < 0) {
-        // into the wave above: its row 63 + rr, entry kEntPerWave * (g - 1) + 63 + rr
+        // into the wave above: its row 63 + rr
         rr += kRowsPerWave;
         ent -= kEntPerWave - kRowsPerWave;
       }
-      if (cw >= 2) {
-        P = fetch(slot2, ent, rr);
-        bp = e;
-      }
-      // Records are complete for a 64-aligned group once its lowest chunk is
-      // walked.  (The wait after the flush leaves nothing of its LDS stores
-      // outstanding, so that the compiler can count the prefetches exactly.)
-      if ((cw & (kWave - 1)) == 0) {
-        flush_records(rsl, cw, cw, c_top, rec_pm, rec_e, lane);
+      P = fetch(max(cw - 2, 0), ent, rr);  // (chunk 0 again near the end: never used)
+      bp = e;
+      cw -= 1;
+      // The next chunk's v_readlane stays after this prefetch: hoisted above
+      // it, it would wait for the prefetch it reads to be the last LDS load
+      // in flight rather than the last but one.
+      __builtin_amdgcn_sched_barrier(0);
+    };
+    // Records are complete for a 64-aligned group once its lowest chunk is
+    // walked: the helper turns them into row starts.  (The wait after the
+    // hand-off leaves nothing of its LDS stores outstanding, so that the
+    // compiler can count the prefetches exactly.)
+    auto flush_at = [&](int walked) __attribute__((always_inline)) {
+      if ((walked & (kWave - 1)) == 0) {
+        post(walked, walked, c_top, 0);
         lgkm_wait0();
       }
-      slot = uni(slot == 0 ? kNWin - 1 : slot - 1);
-      slot2 = uni(slot2 == 0 ? kNWin - 1 : slot2 - 1);
-      cw -= 1;
     };
+
+    // The first group: windows down to two chunks below it, then the
+    // first two registers.
+    const int q_top = cw >> 2;
+    ensure(max(4 * q_top - 2, 0));
+    uint32_t Pa = fetch(cw, ent, rr), Pb = fetch(max(cw - 1, 0), ent, rr);
+    int ba = e, bb = e;
     // Nothing may be outstanding on the LDS/scalar-memory counter when the
-    // loop starts but the two prefetches: a scalar load still in flight (the
-    // compiler hoists kernel-argument loads) would make every wait inside
-    // the loop a full one.
+    // loops start: a scalar load still in flight (the compiler hoists
+    // kernel-argument loads) would make every wait inside them a full one,
+    // and the waits of the group loop count on the two prefetches alone.
     lgkm_wait0();
-    Pa = fetch(slot, ent, rr);
-    Pb = fetch(slot >= 1 ? slot - 1 : kNWin - 1, ent, rr);
+    while (cw >= 4 * q_top) {
+      // Pa holds the chunk walked next: swap after each body.
+      body(Pa, ba, true);
+      flush_at(cw + 1);
+      const uint32_t t = Pa;
+      Pa = Pb;
+      Pb = t;
+      const int tb = ba;
+      ba = bb;
+      bb = tb;
+    }
+    // Whole groups of four: chunk 4q+3 uses Pa, 4q+2 Pb, and so on.  The
+    // staging progress is read after the second chunk of a group, for the
+    // check at the next group's start.
+    bool have_read = false;
     while (cw >= 0 && e > 0) {
-      body(Pa, ba);
-      if (cw < 0 || e <= 0) break;
-      body(Pb, bb);
+      const int need = max(cw - 5, 0);
+      if (((cw + 1) & 7) == 0) wstamps.at((cw + 1) >> 3);
+      if (have_read && staged_to(ready_v) <= need)
+        bases = bases_n;
+      else
+        ensure(need);
+      body(Pa, ba, true);
+      body(Pb, bb, false);
+      ready_v = *(const volatile lds_i32x4*)ready_p;
+      bases_n = *(const volatile lds_u32*)base_p;
+      have_read = true;
+      body(Pa, ba, true);
+      body(Pb, bb, false);
+      flush_at(cw + 1);
     }
     wstamps.at(max(cw + 1, 0) >> 3);
-    // The partial group the walk ended in (chunk cw + 1 was walked last).
-    if (((cw + 1) & (kWave - 1)) != 0) flush_records(rsl, (cw + 1) & ~(kWave - 1), cw + 1, c_top, rec_pm, rec_e, lane);
   }
+  // The partial group of records the walk ended in (chunk cw + 1 was walked
+  // last; none if that group was handed over already or nothing was
+  // walked), marked last; then every request is done.
+  if (tx > 1) {
+    const int lo = cw + 1;
+    post(lo & ~(kWave - 1), lo, (lo & (kWave - 1)) != 0 ? c_top : lo - 1, 1);
+  } else {
+    post(0, 0, -1, 1);
+  }
+  wait_at_least(&L.req_done, posted, bd);
   wstamps.flush(trace_of(p).walk + (size_t)b * kWave);
   waited.flush(trace_of(p).item + 8 * (size_t)b + 4);
   wave_lds_sync();
-  lds_put64(lds_off(&L.wpos), -1ll);
+  lds_put(lds_off(&L.wpos), -1);
   if (lane == 0) rsl[0] = 0;
   for (int i = tx + lane; i <= p.T; i += kWave) rsl[i] = ty;
   wave_lds_sync();
@@ -1435,13 +1612,10 @@ __device__ __forceinline__ void sweep_role(const KParams& p, SweepLds& L, const 
 
   // The walker.
   if (lane == (x.tx - 1) - g_last * kRowsPerWave + 1 && p.score) p.score[b] = score;
-  if (p.EP > kWinEnt)
-    walk<true>(p, L, b, x.tx, x.ty, lane, bd);
-  else
-    walk<false>(p, L, b, x.tx, x.ty, lane, bd);
+  walk(p, L, b, x.tx, x.ty, lane, bd);
   stamp(trace_of(p).item + 8 * (size_t)b + 2);
   int32_t* rs_out = p.row_start + (size_t)b * ((size_t)p.T + 1);
-  const int* const rsl = L.u.walk.rs;
+  const int* const rsl = walk_rs(L, p.T);
   for (int i = lane; i <= p.T; i += kWave) st_dev(reinterpret_cast<uint32_t*>(rs_out + i), (uint32_t)rsl[i]);
   if (p.durations) {
     // Frames per text row (Sec. 2: what the duration predictor learns): the
@@ -1470,10 +1644,13 @@ __device__ __forceinline__ void loader_role(const KParams& p, SweepLds& L, const
   }
   if (!walker_workgroup(x)) return;
   // Decision windows for the walk, once every wave of the item has published
-  // its words.
-  wait_flags(p.done + (size_t)b * p.NW, g_last + 1, tag, lane, bd);
+  // its step masks: the waves of earlier workgroups through their done
+  // flags in memory, this workgroup's through LDS (no memory round trip).
+  const int g_own = (g_last / kWavesPerBlock) * kWavesPerBlock;
+  wait_flags(p.done + (size_t)b * p.NW, g_own, tag, lane, bd);
+  wait_tags(L.fdone, g_last - g_own + 1, tag, bd);
   if (x.w == 0) stamp(trace_of(p).item + 8 * (size_t)b + 0);
-  load_windows(p, L, b, x.ty, x.w, lane, bd);
+  load_windows(p, L, b, x.tx, x.ty, x.w, lane, bd);
 }
 
 // Items with invalid lengths: an all-zero slab, zero row_start, score -inf.
@@ -1559,14 +1736,24 @@ __global__ void __launch_bounds__(kThreads, 1) mas_kernel(KParams p) {
     // Walker not started: at chunk C (every window slot free), row t_x-1.
     lds_store(&L.wpos, walk_pos((ty + kChunk - 1) / kChunk, max(tx - 1, 0)));
   }
+  if (threadIdx.x < kWave) L.wbase[threadIdx.x] = (int)lds_off(&L.u.walk.area[0]);
+  if (threadIdx.x < kWavesPerBlock) L.fdone[threadIdx.x] = 0u;  // never a tag (tags are odd)
+  if (threadIdx.x == 0) {
+    L.req_posted = 0;
+    L.req_done = 0;
+  }
   __syncthreads();
 
   if (st != kItemOk) {
     invalid_item(p, b, g, is_loader || is_finisher, lane, st, tag);
   } else {
     const WaveCtx x = make_ctx(b, g, w, lane, tx, ty);
-    if (is_finisher)
+    if (is_finisher) {
       finisher_role(p, L, x, tag, bd);
+      // (the finisher two SIMDs away from the walker helps it)
+      if (walker_workgroup(x) && w == (((x.g_last & (kWavesPerBlock - 1)) + 2) & (kWavesPerBlock - 1)))
+        walk_helper(p, L, x.b, lane, bd);
+    }
     else if (is_loader)
       loader_role<ALIGNED>(p, L, x, tag, bd);
     else

@@ -44,6 +44,15 @@ constexpr int kMaxRows = 8192;               // largest T (the walker keeps row_
 // boundary in a chunk.
 constexpr int kEntPerWave = 96;
 constexpr int kMidOff = 64;
+// Descent bytes, the walk's own copy of the step masks at a quarter of
+// their size: per chunk, one byte per entry of the same layout,
+//   entry r (row 63g + r): the number of rows the path climbs in the chunk
+//                          while it stays in the wave's rows (the mask's
+//                          popcount), or 64 + p when it climbs into the row
+//                          above the wave at position p (the highest
+//                          position of the mask);
+//   entry kMidOff + q:     the popcount of mid entry q's mask.
+constexpr uint32_t kEscape = 64;
 
 // Boundary hand-off between consecutive workgroups of an item: the last wave
 // g of a workgroup publishes Q[63g+62][j] (its last row) for every column j it
@@ -87,6 +96,7 @@ struct Layout {
   size_t off_slots;  // uint64 [B][NB][NC*32] boundary hand-off words of each workgroup's last wave
   size_t off_pm;     // uint32 [B][NC][EP] step masks
   size_t off_rs;     // int32  [B][T+1] row_start table (mas_forward_ex)
+  size_t off_pd;     // uint8  [B][NC][EP] descent bytes
   size_t bytes;
 };
 
@@ -118,6 +128,8 @@ __host__ inline bool make_layout(int32_t B, int32_t T, int32_t S, Layout* L) {
   off = round_up(off + (size_t)B * L->NC * (size_t)L->EP * sizeof(uint32_t), kAlign);
   L->off_rs = off;
   off = round_up(off + (size_t)B * ((size_t)T + 1) * sizeof(int32_t), kAlign);
+  L->off_pd = off;
+  off = round_up(off + (size_t)B * L->NC * (size_t)L->EP, kAlign);
   L->bytes = off;
   return true;
 }

@@ -57,7 +57,8 @@ def layout(B, T, S, with_path: bool):
     t["walk"] = t["chunk"] + B * NW * 64
     t["item"] = t["walk"] + B * 64
     t["tile"] = t["item"] + 8 * B
-    t["total"] = t["tile"] + 2 * B * ntile
+    t["win"] = t["tile"] + 2 * B * ntile
+    t["total"] = t["win"] + B * 4 * 2 * 64
     return dict(NW=NW, NB=NB, NC=NC, ntile=ntile, grid=grid, **t)
 
 
@@ -109,7 +110,8 @@ def summary(lay, st, t_x, t_y, with_path: bool = True, top: int = 3):
     chunk = st[lay["chunk"]:lay["walk"]].reshape(B, NW, 64)  # slot k: chunk 8k+7 (or the wave's last) done
     walk = st[lay["walk"]:lay["item"]].reshape(B, 64)         # slot k: chunks >= 8k walked
     item = st[lay["item"]:lay["tile"]].reshape(B, 8)
-    tile = st[lay["tile"]:lay["total"]].reshape(B * ntile, 2)
+    tile = st[lay["tile"]:lay["win"]].reshape(B * ntile, 2)
+    win = st[lay["win"]:lay["total"]].reshape(B, 4, 2, 64)  # loader k, issue/staged, n-th window
     out = {"launch_us": float(_rel(wg[:, 1].max(), t0))}
     items = []
     for b in range(B):
@@ -147,6 +149,14 @@ def summary(lay, st, t_x, t_y, with_path: bool = True, top: int = 3):
                "hand_lag_us_median": float(np.median(lags)) if lags else 0.0,
                "step_us_median": float(np.median(steps)), "step_us_p90": float(np.percentile(steps, 90)),
                "walk_us_per_chunk": wk_chunk, "walk_waited_us": float(item[b, 4]) * TICK_US}
+        # window staging: latency of each window (issue to staged) and how
+        # long before the walk start the first ones were staged
+        w_iss, w_rdy = win[b, :, 0, :].astype(np.int64), win[b, :, 1, :].astype(np.int64)
+        ok = (w_iss > 0) & (w_rdy > 0)
+        lat = (w_rdy[ok] - w_iss[ok]) * TICK_US
+        rec["win_lat_us_median"] = float(np.median(lat)) if lat.size else 0.0
+        rec["win_lat_us_p90"] = float(np.percentile(lat, 90)) if lat.size else 0.0
+        rec["windows"] = int(ok.sum())
         rec["walk_us"] = rec["walk_end_us"] - rec["walk_start_us"]
         items.append(rec)
     items.sort(key=lambda r: -r["published_us"])
@@ -170,12 +180,16 @@ def format_summary(s, title: str) -> str:
                      f"path tail {s['path_tail_us']:.1f} us")
     lines.append("items finishing last (times from the first workgroup's start, us):")
     lines.append("   b   t_x   t_y waves chunks  sweep_end  win_ready walk_start  walk_end  published  walk_us "
-                 "walk/chunk  step_med  step_p90  hand_lag  win_wait")
+                 "walk/chunk  step_med  step_p90  hand_lag  win_wait win_lat win_lat90")
     for r in s["longest"]:
         lines.append(f"{r['b']:4d} {r['t_x']:5d} {r['t_y']:5d} {r['waves']:5d} {r['chunks']:6d} {r['sweep_end_us']:10.1f} "
                      f"{r['windows_ready_us']:10.1f} {r['walk_start_us']:10.1f} {r['walk_end_us']:9.1f} "
                      f"{r['published_us']:10.1f} {r['walk_us']:8.1f} {r['walk_us_per_chunk']:10.3f} "
-                     f"{r['step_us_median']:9.3f} {r['step_us_p90']:9.3f} {r['hand_lag_us_median']:9.2f} {r['walk_waited_us']:9.1f}")
+                     f"{r['step_us_median']:9.3f} {r['step_us_p90']:9.3f} {r['hand_lag_us_median']:9.2f} {r['walk_waited_us']:9.1f}"
+                     f" {r['win_lat_us_median']:7.2f} {r['win_lat_us_p90']:9.2f}")
+    lats = [r["win_lat_us_median"] for r in s["items"] if r["windows"]]
+    if lats:
+        lines.append(f"walk windows (issue to staged): median over items of the per-item median {np.median(lats):.2f} us")
     allsteps = np.array([r["step_us_median"] for r in s["items"]])
     lines.append(f"median per-chunk sweep step over all items: {np.median(allsteps):.3f} us; "
                  f"median walk per chunk: {np.median([r['walk_us_per_chunk'] for r in s['items']]):.3f} us")

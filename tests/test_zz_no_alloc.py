@@ -41,7 +41,7 @@ def test_static_scratch_matches_mas_forward_ex():
 
     mas.lib()
     for _ in range(2):
-        _run(mas, "tts-b64-t1024-s4096")  # the largest workload: 61 MiB of the 64 MiB scratch
+        _run(mas, "tts-b64-t1024-s4096")  # the largest workload: 72 MiB of the 80 MiB scratch
         _run(mas, "tts-b16-t128-s512")    # then smaller batches on the same scratch
         _run(mas, "tts-b32-t256-s1024")
         _run(mas, "tts-b32-t512-s2048")
