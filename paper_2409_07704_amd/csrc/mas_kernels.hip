@@ -1016,26 +1016,30 @@ __device__ __forceinline__ void load_tiles(const KParams& p, SweepLds& L, const 
 // forward): the mask of (row r, column j) is d(r, j) ? mask(r-1, j-1) :
 // mask(r, j-1), shifted left by one with d(r, j) as its new lowest bit, so
 // that after the chunk's last column a step at column 32c + k sits at
-// position 31 - k.  Everything is complemented, which lets one carry chain do
-// the work:
-//   v_add_co  wc += wc     VCC = the lane's complemented decision for this
-//                          column (the top bit of wc), wc moves on one bit;
+// position 31 - k.  Everything is complemented:
+//   v_lshrrev  b = wc >> 31        the lane's complemented decision;
+//   v_add_co   wc += wc            the same bit into VCC, wc moves on one bit;
 //   v_cndmask_dpp  xc = VCC ? pc : pc of the lane below (wave_shr:1);
-//   v_addc    pc = xc + xc + VCC   (shift in the complemented decision).
-// Lane 0 (the row above the wave) has no lane below: DPP leaves its xc
-// unwritten, all ones (mask 0), so a path that climbs into it contributes
-// nothing more.  A DPP read of a VGPR needs two wait states after the VALU
-// write of it: the v_add_co and one s_nop.
+//   v_lshl_or  pc = xc << 1 | b.
+// Only the last two depend on the previous column (the first two fill the
+// two wait states a DPP read needs after the VALU write of its source), and
+// neither writes VCC, so consecutive columns do not wait on each other's
+// carry.  Lane 0 (the row above the wave) has no lane below: DPP leaves its
+// xc unwritten, all ones (mask 0), so a path that climbs into it contributes
+// nothing more.
 __device__ __forceinline__ void mask_cols8(uint32_t& wc, uint32_t& xc, uint32_t pc, uint32_t (&o)[8]) {
-#define MAS_MASK_COL(P, O)                                                            \
+  uint32_t b0, b1;
+#define MAS_MASK_COL(P, O, B)                                                         \
+  "v_lshrrev_b32 %[" B "], 31, %[w]\n\t"                                              \
   "v_add_co_u32 %[w], vcc, %[w], %[w]\n\t"                                            \
-  "s_nop 0\n\t"                                                                       \
   "v_cndmask_b32_dpp %[x], %[" P "], %[" P "], vcc wave_shr:1 row_mask:0xf bank_mask:0xf\n\t" \
-  "v_addc_co_u32 %[" O "], vcc, %[x], %[x], vcc\n\t"
-  asm volatile(MAS_MASK_COL("p", "o0") MAS_MASK_COL("o0", "o1") MAS_MASK_COL("o1", "o2") MAS_MASK_COL("o2", "o3")
-               MAS_MASK_COL("o3", "o4") MAS_MASK_COL("o4", "o5") MAS_MASK_COL("o5", "o6") MAS_MASK_COL("o6", "o7")
+  "v_lshl_or_b32 %[" O "], %[x], 1, %[" B "]\n\t"
+  asm volatile(MAS_MASK_COL("p", "o0", "b0") MAS_MASK_COL("o0", "o1", "b1") MAS_MASK_COL("o1", "o2", "b0")
+               MAS_MASK_COL("o2", "o3", "b1") MAS_MASK_COL("o3", "o4", "b0") MAS_MASK_COL("o4", "o5", "b1")
+               MAS_MASK_COL("o5", "o6", "b0") MAS_MASK_COL("o6", "o7", "b1")
                : [o0] "=&v"(o[0]), [o1] "=&v"(o[1]), [o2] "=&v"(o[2]), [o3] "=&v"(o[3]), [o4] "=&v"(o[4]),
-                 [o5] "=&v"(o[5]), [o6] "=&v"(o[6]), [o7] "=&v"(o[7]), [w] "+v"(wc), [x] "+v"(xc)
+                 [o5] "=&v"(o[5]), [o6] "=&v"(o[6]), [o7] "=&v"(o[7]), [w] "+v"(wc), [x] "+v"(xc), [b0] "=&v"(b0),
+                 [b1] "=&v"(b1)
                : [p] "v"(pc)
                : "vcc");
 #undef MAS_MASK_COL
@@ -1061,7 +1065,7 @@ __device__ __forceinline__ void finisher_role(const KParams& p, SweepLds& L, con
   const int base = kEntPerWave * x.g;
   const int row_off = lane > 0 ? 4 * (base + lane - 1) : -1;  // lane 0's mask (the row above) is not stored
   const int mid_off = lane >= kWave - 8 ? 4 * (base + kMidOff + 4 * (lane - (kWave - 8))) : -1;
-  const int row_doff = lane < 16 ? base + 4 * lane : -1;  // lanes 0..15: the row bytes, four per dword
+  const int row_doff = lane > 0 ? base + lane - 1 : -1;
   const int mid_doff = lane >= kWave - 8 ? base + kMidOff + 4 * (lane - (kWave - 8)) : -1;
   const int q0 = 4 * (lane - (kWave - 8));  // the first mid entry a lane in 56..63 stores
   const int* const progress = w > 0 ? reinterpret_cast<const int*>(&L.box[w - 1]) + 2 : &L.cons0;
@@ -1095,20 +1099,10 @@ __device__ __forceinline__ void finisher_role(const KParams& p, SweepLds& L, con
     const uint32_t pm_row = ~h[kChunk - 1];
     __builtin_amdgcn_raw_buffer_store_b32(pm_row, dr, row_off, soff, kPolicyDev);
     {
-      // The row's descent byte (lane l: row l - 1 of the wave), stored as
-      // whole dwords: lane k < 16 gathers the bytes of rows 4k .. 4k+3
-      // (lanes 4k+1 .. 4k+4; the last, past row 62, is a pad byte).
+      // The row's descent byte (lane l: row l - 1 of the wave).
       const int s_row = __builtin_popcount(pm_row);
       const uint32_t d = s_row > lane - 1 ? kEscape + (31u - (uint32_t)__builtin_clz(pm_row | 1u)) : (uint32_t)s_row;
-      const int src = 4 * (4 * lane + 1);
-      const uint32_t b0 = (uint32_t)__builtin_amdgcn_ds_bpermute(src, (int)d);
-      const uint32_t b1 = (uint32_t)__builtin_amdgcn_ds_bpermute(src + 4, (int)d);
-      const uint32_t b2 = (uint32_t)__builtin_amdgcn_ds_bpermute(src + 8, (int)d);
-      // (every lane takes part in each permute: a lane left out of one
-      // would not supply its own byte to the others)
-      uint32_t b3 = (uint32_t)__builtin_amdgcn_ds_bpermute(min(src + 12, 4 * (kWave - 1)), (int)d);
-      b3 = lane < 15 ? b3 : 0u;
-      __builtin_amdgcn_raw_buffer_store_b32(b0 | b1 << 8 | b2 << 16 | b3 << 24, ddr, row_doff, c * p.EP, kPolicyDev);
+      __builtin_amdgcn_raw_buffer_store_b8((uint8_t)d, ddr, row_doff, c * p.EP, kPolicyDev);
     }
     // Mid entry q: the last row's mask after column 31 - q, its positions
     // raised by q; lane 63's values gathered into lanes 56..63, four each.
