@@ -74,7 +74,8 @@ typedef enum mas_status {
   MAS_ERR_BAD_SHAPE = 2,    /* B, T or S < 1, or past the shape limits above */
   MAS_ERR_WORKSPACE = 3,    /* workspace NULL, misaligned or too small */
   MAS_ERR_HIP = 4,          /* a HIP runtime call or kernel launch failed */
-  MAS_ERR_SCRATCH = 5       /* mas_forward_static: the batch needs more than MAS_STATIC_SCRATCH_BYTES */
+  MAS_ERR_SCRATCH = 5,      /* mas_forward_static: the batch needs more than MAS_STATIC_SCRATCH_BYTES */
+  MAS_ERR_BAD_VALUE = 6     /* mas_forward_sentinel: the sentinel is not a finite negative number */
 } mas_status;
 
 /* Per-item status codes written to item_status_out[b]. */
@@ -155,6 +156,27 @@ mas_status mas_forward_ex(const float* value, const int32_t* t_x, const int32_t*
                           uint8_t* path_out, int32_t B, int32_t T, int32_t S,
                           float* score_out, int32_t* item_status_out,
                           void* workspace, size_t workspace_bytes, hipStream_t stream);
+
+/*
+ * Legacy-sentinel mode (Sec. 2, issue 4 of the list of problems with the
+ * original MAS, and the max_neg_val paragraph): the same call as
+ * mas_forward_ex, except that every cell Algorithm 1 sets to -inf (the cache's
+ * initial value: the cells i > j no path reaches by column j) holds the
+ * finite `sentinel` instead, as in implementations that use max_neg_val
+ * (-1e9 in the original, -1e32 in the paper's).  The forward max and the
+ * backtrack are otherwise unchanged: the first text row is still the running
+ * sum of its values, and the backtrack still steps up where i == j.  Results
+ * equal Algorithm 1 run with that sentinel, including the alignments such a
+ * sentinel spoils once cumulative log-likelihoods fall below it (Sec. 2: -1e9
+ * is not small enough); for inputs whose partial sums stay far above it they
+ * equal mas_forward_ex's.
+ * sentinel: finite and negative, else MAS_ERR_BAD_VALUE (nothing enqueued).
+ * Other arguments as for mas_forward_ex (same workspace).
+ */
+mas_status mas_forward_sentinel(const float* value, const int32_t* t_x, const int32_t* t_y,
+                                uint8_t* path_out, int32_t B, int32_t T, int32_t S, float sentinel,
+                                float* score_out, int32_t* item_status_out,
+                                void* workspace, size_t workspace_bytes, hipStream_t stream);
 
 /*
  * Full alignment with a stream-ordered workspace: allocates it with

@@ -19,6 +19,7 @@ from ._native import (  # noqa: F401
     mas_expand_path,
     mas_forward,
     mas_forward_ex,
+    mas_forward_sentinel,
     mas_forward_static,
     mas_search,
     mas_status_string,

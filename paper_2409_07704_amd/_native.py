@@ -18,7 +18,7 @@ LIB_PATH = os.path.join(_PKG, "libmas.so")
 
 MAS_OK = 0
 STATUS_NAMES = {0: "MAS_OK", 1: "MAS_ERR_NULL_POINTER", 2: "MAS_ERR_BAD_SHAPE", 3: "MAS_ERR_WORKSPACE", 4: "MAS_ERR_HIP",
-                5: "MAS_ERR_SCRATCH"}
+                5: "MAS_ERR_SCRATCH", 6: "MAS_ERR_BAD_VALUE"}
 STATIC_SCRATCH_BYTES = 80 << 20  # MAS_STATIC_SCRATCH_BYTES
 ITEM_OK, ITEM_EMPTY, ITEM_INFEASIBLE, ITEM_OUT_OF_RANGE, ITEM_SYNC_TIMEOUT, ITEM_BAD_WORKSPACE = 0, 1, 2, 3, 4, 5
 
@@ -30,6 +30,7 @@ SIGNATURES = {
     "mas_search": ([_P, _P, _P, _I32, _I32, _I32, _P, _P, _P, _P, _P, _SZ, _P], ctypes.c_int),
     "mas_expand_path": ([_P, _I32, _I32, _I32, _P, _P], ctypes.c_int),
     "mas_forward_ex": ([_P, _P, _P, _P, _I32, _I32, _I32, _P, _P, _P, _SZ, _P], ctypes.c_int),
+    "mas_forward_sentinel": ([_P, _P, _P, _P, _I32, _I32, _I32, ctypes.c_float, _P, _P, _P, _SZ, _P], ctypes.c_int),
     "mas_forward": ([_P, _P, _P, _P, _I32, _I32, _I32, _P], ctypes.c_int),
     "mas_forward_static": ([_P, _P, _P, _P, _I32, _I32, _I32, _P, _P, _P], ctypes.c_int),
     "mas_status_string": ([ctypes.c_int], ctypes.c_char_p),
@@ -183,6 +184,23 @@ def mas_forward_ex(value, t_x, t_y, path_out=None, score_out=None, item_status_o
     s = _stream(stream, value.device)
     ws = _workspace(workspace, B, T, S, value.device, s)
     _check("mas_forward_ex", lib().mas_forward_ex(pv, px, py, pp, B, T, S, psc, pst, ws.ptr, ws.nbytes, s))
+    return path_out
+
+
+def mas_forward_sentinel(value, t_x, t_y, sentinel, path_out=None, score_out=None, item_status_out=None,
+                         workspace=None, stream=None):
+    """Full alignment in the legacy-sentinel mode: the cells Algorithm 1
+    masks hold the finite negative `sentinel` (e.g. -1e9) instead of -inf."""
+    B, T, S, pv, px, py = _batch(value, t_x, t_y)
+    if path_out is None:
+        path_out = torch.empty((B, T, S), dtype=torch.uint8, device=value.device)
+    pp = _dev_ptr(path_out, "path_out", torch.uint8, (B, T, S))
+    psc = _dev_ptr(score_out, "score_out", torch.float32, (B,))
+    pst = _dev_ptr(item_status_out, "item_status_out", torch.int32, (B,))
+    s = _stream(stream, value.device)
+    ws = _workspace(workspace, B, T, S, value.device, s)
+    _check("mas_forward_sentinel",
+           lib().mas_forward_sentinel(pv, px, py, pp, B, T, S, float(sentinel), psc, pst, ws.ptr, ws.nbytes, s))
     return path_out
 
 

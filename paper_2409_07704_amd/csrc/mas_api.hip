@@ -6,6 +6,8 @@
 #include <stdint.h>
 #include <stdlib.h>
 
+#include <cmath>
+
 #include <mutex>
 #include <unordered_map>
 
@@ -66,7 +68,7 @@ static hipError_t prepare_workspace(void* ws, const Layout& L, hipStream_t strea
 
 static mas_status run(const float* value, const int32_t* t_x, const int32_t* t_y, const Layout& L,
                       int32_t* row_start, int32_t* durations, float* score, int32_t* status, uint8_t* path, void* ws,
-                      hipStream_t stream) {
+                      hipStream_t stream, float sentinel = -INFINITY) {
   if (prepare_workspace(ws, L, stream) != hipSuccess) return MAS_ERR_HIP;
   char* base = static_cast<char*>(ws);
   KParams p;
@@ -95,6 +97,8 @@ static mas_status run(const float* value, const int32_t* t_x, const int32_t* t_y
   p.ntile = (L.T + kPathTileRows - 1) / kPathTileRows;
   p.path16 = path && (L.S % 16 == 0) && ((uintptr_t)path % 16 == 0);
   p.spin_limit = wait_bound();
+  p.neg = sentinel;
+  p.legacy = std::isfinite(sentinel) ? 1 : 0;
   return launch_mas(p, stream) == hipSuccess ? MAS_OK : MAS_ERR_HIP;
 }
 
@@ -174,6 +178,18 @@ mas_status mas_forward_ex(const float* value, const int32_t* t_x, const int32_t*
   return run(value, t_x, t_y, L, rs, nullptr, score_out, item_status_out, path_out, workspace, stream);
 }
 
+mas_status mas_forward_sentinel(const float* value, const int32_t* t_x, const int32_t* t_y, uint8_t* path_out,
+                                int32_t B, int32_t T, int32_t S, float sentinel, float* score_out,
+                                int32_t* item_status_out, void* workspace, size_t workspace_bytes, hipStream_t stream) {
+  if (!value || !t_x || !t_y || !path_out) return MAS_ERR_NULL_POINTER;
+  if (!(sentinel < 0.0f) || !std::isfinite(sentinel)) return MAS_ERR_BAD_VALUE;
+  Layout L;
+  if (!make_layout(B, T, S, &L)) return MAS_ERR_BAD_SHAPE;
+  if (!ws_ok(workspace, workspace_bytes, L)) return MAS_ERR_WORKSPACE;
+  int32_t* rs = reinterpret_cast<int32_t*>(static_cast<char*>(workspace) + L.off_rs);
+  return run(value, t_x, t_y, L, rs, nullptr, score_out, item_status_out, path_out, workspace, stream, sentinel);
+}
+
 mas_status mas_forward(const float* value, const int32_t* t_x, const int32_t* t_y, uint8_t* path_out, int32_t B,
                        int32_t T, int32_t S, hipStream_t stream) {
   if (!value || !t_x || !t_y || !path_out) return MAS_ERR_NULL_POINTER;
@@ -215,6 +231,8 @@ const char* mas_status_string(mas_status status) {
       return "MAS_ERR_HIP";
     case MAS_ERR_SCRATCH:
       return "MAS_ERR_SCRATCH";
+    case MAS_ERR_BAD_VALUE:
+      return "MAS_ERR_BAD_VALUE";
   }
   return "MAS_ERR_UNKNOWN";
 }

@@ -31,6 +31,8 @@ struct KParams {
   int32_t ntile;        // path tiles per item: ceil(T / kPathTileRows)
   int32_t path16;       // path 16-byte aligned and S % 16 == 0
   int32_t spin_limit;   // bound of a device-side wait, in polls without progress
+  float neg;            // value of the cells no path reaches: -inf, or the finite sentinel of the legacy mode
+  int32_t legacy;       // finite sentinel (mas_forward_sentinel): triangle cells hold neg exactly
 };
 
 // Timeline of one launch in the debug build (MAS_TRACE): indices of 64-bit

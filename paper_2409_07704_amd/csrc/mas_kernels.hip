@@ -694,10 +694,11 @@ __device__ __forceinline__ float sweep_wave(const KParams& p, SweepLds& L, const
   // Lane 0's Q at the column before the first chunk: the previous wave's
   // last row there (its chunk c_begin-1, always computed), or -inf.  It
   // sits in slot kRing-1 (chunk c_begin-1).  Every other row's Q at the
-  // column before its first chunk is -inf, except row 0's at column -1: -0,
-  // so that the first cell comes out as -0 + value[0][0] = value[0][0]
-  // exactly (its predecessors are -inf and -0, their max -0).
-  float q = (IN == 0 && lane == 1) ? -0.0f : neg_inf();
+  // column before its first chunk is -inf (the legacy mode's sentinel neg),
+  // except row 0's at column -1: -0, so that the first cell comes out as
+  // -0 + value[0][0] = value[0][0] exactly (its predecessors are -0 and the
+  // row above row 0, -inf in both modes: row 0 is the running sum).
+  float q = (IN == 0 && lane == 1) ? -0.0f : (IN == 0 && lane == 0) ? neg_inf() : p.neg;
   if (IN1) wait_at_least(my_box + 1, x.c_begin, bd);
   if (IN != 0) {
     wave_lds_sync();
@@ -724,6 +725,8 @@ __device__ __forceinline__ float sweep_wave(const KParams& p, SweepLds& L, const
 
   float qc[kChunk] = {};
   float score = neg_inf();
+  const int row = x.g * kRowsPerWave + lane - 1;                 // this lane's text row (lanes 1..63)
+  const int diag_last = (x.g * kRowsPerWave + kRowsPerWave - 1) / kChunk;  // the last chunk holding one of its diagonal cells
   Stamps stamps;  // (debug build) lane k: chunk 8k+7 (or the last chunk) done
   const int m_last = (x.ty - 1) % kChunk;
 
@@ -772,6 +775,13 @@ __device__ __forceinline__ float sweep_wave(const KParams& p, SweepLds& L, const
     uint32_t bits = 0;
     sweep_chunk(q, t, vc, qc, bits);
     __builtin_amdgcn_sched_barrier(0);
+    if (p.legacy && c <= diag_last) {
+      // Legacy mode: the backtrack steps up at i == j whatever Q says (the
+      // stay candidate is a masked cell); with a finite sentinel the
+      // decision there can come out 0, so its bit is set.
+      const int rel = row - c * kChunk;
+      bits |= (lane > 0 && rel >= 0 && rel < kChunk) ? 1u << (kChunk - 1 - rel) : 0u;
+    }
     hand_off(c);
     // The slot's decision words of chunk c-4 must have been taken (mailbox
     // .w, read with this step's mailbox; rarely not yet).
@@ -850,26 +860,38 @@ __device__ __forceinline__ int start_delay(const KParams& p, int b, int lane) {
 }
 
 // ---------------------------------------------------------------- loader wave
+// The value given to the tile cells of the triangle i > j.  Every cell there
+// has only triangle cells as predecessors, so its Q is the max of theirs plus
+// this value: -inf with -inf keeps them -inf (the method); in the legacy mode
+// (a finite sentinel neg, as the paper's max_neg_val) +0 keeps them at neg
+// exactly, the value Algorithm 1 initialises the cache to.  Row 0 starts from
+// -0 at column -1 (so that Q[0][0] = value[0][0]), which cell (1, 0) also
+// sees: in the legacy mode that cell gets neg as its value (-0 + neg = neg).
+__device__ __forceinline__ float triangle_value(const KParams& p) { return p.legacy ? 0.0f : neg_inf(); }
+
 // The cells of the triangle i > j in the landed tile of chunk c of wave g
 // (slot at LDS byte address slot) become -inf: lane r rewrites tile row r
 // (item row 63g + r), whose columns 32c .. 32c + nm - 1 lie in the triangle:
 // whole pieces are overwritten, a piece cut by the diagonal is read and
 // written back.  Only the first chunks of a wave cross the triangle.
-__device__ __forceinline__ void mask_tile(uint32_t slot, int g, int c, int lane) {
+__device__ __forceinline__ void mask_tile(const KParams& p, uint32_t slot, int g, int c, int lane) {
   const int nm = min(max(g * kRowsPerWave + lane - c * kChunk, 0), kChunk);
   using lds_f4 = __attribute__((address_space(3))) f32x4;
-  const float ninf = neg_inf();
+  const float tri = triangle_value(p);
   for (int pc = 0; 4 * pc < nm; ++pc) {
     lds_f4* const a = (lds_f4*)(uintptr_t)(slot + (uint32_t)lane * 128u + 16u * (uint32_t)(pc ^ swz(lane)));
-    f32x4 v = {ninf, ninf, ninf, ninf};
+    f32x4 v = {tri, tri, tri, tri};
     if (4 * pc + 4 > nm) {
       // (the piece has landed; other tiles may still be in flight)
       f32x4 old;
       asm volatile("ds_read_b128 %0, %1\n\ts_waitcnt lgkmcnt(0)" : "=v"(old) : "v"((uint32_t)(uintptr_t)a) : "memory");
-      v.y = 4 * pc + 1 < nm ? ninf : old.y;
-      v.z = 4 * pc + 2 < nm ? ninf : old.z;
+      v.y = 4 * pc + 1 < nm ? tri : old.y;
+      v.z = 4 * pc + 2 < nm ? tri : old.z;
       v.w = old.w;
     }
+    // Legacy mode: cell (1, 0) follows row 0's -0 at column -1 (see
+    // triangle_value), so its value is the sentinel itself.
+    if (p.legacy && g == 0 && c == 0 && lane == 1 && pc == 0) v.x = p.neg;
     *a = v;
   }
 }
@@ -969,7 +991,7 @@ __device__ __forceinline__ void load_tiles(const KParams& p, SweepLds& L, const 
         vm_wait<0>();
         if (readied < issued) {
           for (; readied < issued; ++readied)
-            if (readied < x.mask_end) mask_tile(ring + (uint32_t)((readied - x.c_begin) & (kRing - 1)) * kSlotStride, x.g, readied, lane);
+            if (readied < x.mask_end) mask_tile(p, ring + (uint32_t)((readied - x.c_begin) & (kRing - 1)) * kSlotStride, x.g, readied, lane);
           lds_put(ready_addr, readied);
         }
         const uint64_t stale_a = __builtin_amdgcn_ballot_w64((uint32_t)(wa >> 32) != tag);
@@ -1004,7 +1026,7 @@ __device__ __forceinline__ void load_tiles(const KParams& p, SweepLds& L, const 
     // The oldest tile in flight has landed once at most the younger ones
     // are outstanding.
     vm_wait_usual<kOps * (kInflight - 1)>(kOps * (issued - readied - 1));
-    if (readied < x.mask_end) mask_tile(ring + (uint32_t)((readied - x.c_begin) & (kRing - 1)) * kSlotStride, x.g, readied, lane);
+    if (readied < x.mask_end) mask_tile(p, ring + (uint32_t)((readied - x.c_begin) & (kRing - 1)) * kSlotStride, x.g, readied, lane);
     ++readied;
     lds_put(ready_addr, readied);
   }

@@ -99,6 +99,12 @@ def test_other_entry_points_host_validation():
     assert mas.mas_workspace_bytes(64, 1024, 8192) > mas.STATIC_SCRATCH_BYTES
     assert L.mas_forward_static(FAKE, FAKE, FAKE, FAKE, 64, 1024, 8192, None, None, None) == 5
     assert mas.mas_status_string(5) == "MAS_ERR_SCRATCH"
+    # the legacy-sentinel mode: a finite negative sentinel only
+    for bad in (float("nan"), float("inf"), float("-inf"), 0.0, 1e9):
+        assert L.mas_forward_sentinel(FAKE, FAKE, FAKE, FAKE, 1, 1, 1, bad, None, None, FAKE, 1 << 20, None) == 6
+    assert L.mas_forward_sentinel(FAKE, FAKE, FAKE, FAKE, 1, 0, 1, -1e9, None, None, FAKE, 1 << 20, None) == 2
+    assert L.mas_forward_sentinel(FAKE, None, FAKE, FAKE, 1, 1, 1, -1e9, None, None, FAKE, 1 << 20, None) == 1
+    assert mas.mas_status_string(6) == "MAS_ERR_BAD_VALUE"
 
 
 def test_binding_refuses_host_tensors():
