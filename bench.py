@@ -336,7 +336,7 @@ def main():
     secondary = None
     if not args.no_secondary:
         secondary = secondary_lines(mas, synth, dev, stream, wname, v, x, y, ws, op, tx, ty, cells,
-                                    args.secondary_steps, max(3, args.warmup // 5))
+                                    args.secondary_steps, max(3, args.warmup // 5), t_mean)
         parity = parity and all(s["parity"] for s in secondary.values())
 
     achieved = bytes_metric / t_mean / 1e9
@@ -425,7 +425,7 @@ def time_launches(fn, stream, steps, warmup):
     return np.array([ev[k].elapsed_time(ev[k + 1]) for k in range(steps)]) * 1e-3
 
 
-def secondary_lines(mas, synth, dev, stream, wname, v, x, y, ws, op, tx, ty, cells, steps, warmup):
+def secondary_lines(mas, synth, dev, stream, wname, v, x, y, ws, op, tx, ty, cells, steps, warmup, forward_s):
     """Secondary measurements reported beside the headline: the path-less call
     (mas_search: row_start, durations and score, no dense path) on the headline
     workload, and one mas_forward_ex line per smaller workload.  Each checks
@@ -448,6 +448,8 @@ def secondary_lines(mas, synth, dev, stream, wname, v, x, y, ws, op, tx, ty, cel
     out["path_less"] = {"call": "mas_search", "workload": wname, "launch_us_mean": float(pl.mean()) * 1e6,
                         "launch_us_median": float(np.median(pl)) * 1e6, "cells_per_s": cells / float(pl.mean()),
                         "parity": ok}
+    out["text_grid"] = text_grid_line(mas, synth, dev, stream, rs, op, tx, ty, float(pl.mean()), forward_s,
+                                       steps, warmup)
     for name in synth.WORKLOADS:
         if name == wname or name.startswith("tiny"):
             continue
@@ -468,6 +470,40 @@ def secondary_lines(mas, synth, dev, stream, wname, v, x, y, ws, op, tx, ty, cel
                      "frac": metric / t / 1e9 / HBM_PEAK_GBS, "parity": ok}
         del vv, pth, wsn
     return out
+
+
+def text_grid_line(mas, synth, dev, stream, rs, op, tx, ty, search_s, forward_s, steps, warmup):
+    """The aligned text grid on the headline workload: mas_expand_text from
+    mas_search's row_start, 192 fp32 channels.  Beside it, for context, the
+    dense product it replaces (torch.bmm of the 0/1 path, transposed, with the
+    text features) and the two pipelines end to end."""
+    import numpy as np
+    import torch
+
+    import oracle
+
+    B, T1 = rs.shape
+    T, S, C = T1 - 1, op.shape[2], synth.TEXT_CHANNELS
+    h = synth.text_batch(B, T, C, seed=0)
+    hd = torch.from_numpy(h).to(dev)
+    grid = torch.empty((B, S, C), dtype=torch.float32, device=dev)
+    tg = time_launches(lambda: mas.mas_expand_text(hd, rs, S, grid, stream=stream), stream, steps, warmup)
+    ok = bool(np.array_equal(grid.cpu().numpy().view(np.uint32), oracle.expand_text(op, h).view(np.uint32)))
+    t = float(tg.mean())
+    valid = (tx >= 1) & (tx <= ty) & (tx <= T) & (ty <= S)
+    moved = B * S * C * 4 + int(tx[valid].astype(np.int64).sum()) * C * 4 + B * (T + 1) * 4
+    # The dense product, timed on a few launches (it is slow and only context).
+    pt = torch.from_numpy(op).to(dev).transpose(1, 2).to(torch.float32).contiguous()
+    dense = torch.empty_like(grid)
+    td = time_launches(lambda: torch.bmm(pt, hd, out=dense), stream, 5, 2)
+    dense_equal = bool(torch.equal(dense, grid))
+    del pt, dense
+    return {"call": "mas_expand_text", "channels": C, "dtype": "f32", "launch_us_mean": t * 1e6,
+            "launch_us_median": float(np.median(tg)) * 1e6, "algorithmic_bytes": moved,
+            "gbs": moved / t / 1e9, "frac": moved / t / 1e9 / HBM_PEAK_GBS,
+            "dense_bmm_us_mean": float(td.mean()) * 1e6, "dense_bmm_equal": dense_equal,
+            "search_plus_grid_us": (search_s + t) * 1e6,
+            "forward_ex_plus_dense_us": (forward_s + float(td.mean())) * 1e6, "parity": ok}
 
 
 if __name__ == "__main__":

@@ -148,6 +148,28 @@ mas_status mas_expand_path(const int32_t* row_start, int32_t B, int32_t T, int32
                            uint8_t* path_out, hipStream_t stream);
 
 /*
+ * Aligned text grid (Sec. 5, Conclusion: the MAS path multiplied with the
+ * text to give the text features at the speech frame rate).  For every item,
+ * out[b][j] = sum over i of path[b][i][j] * text[b][i], with the path that
+ * mas_expand_path would write from row_start: frame j < t_y takes the text
+ * row whose segment [row_start[b][i], row_start[b][i+1]) holds it, copied as
+ * it is (bit for bit, any element type, -0 / inf / NaN included); frames no
+ * segment holds (j >= t_y, every frame of an invalid item) are all zero
+ * bytes.  Computed as a gather; no path is formed.
+ *   text [B, T, C] and out [B, S, C]: elements of elem_bytes (1, 2, 4 or 8)
+ *   bytes, contiguous row-major, device pointers; out is fully overwritten.
+ *   row_start [B, T+1] int32 as mas_search writes it (monotone, within
+ *   [0, S]).  A table that is not monotone cannot make the kernel access
+ *   memory outside these tensors, but its frames are then unspecified.
+ *   Shape limits: B, T, S, C >= 1, T <= 2^30, C * elem_bytes <= 2^24, each
+ *   tensor at most 2^48 bytes; else MAS_ERR_BAD_SHAPE (also for another
+ *   elem_bytes).  16-byte words when text, out and the row size allow, else
+ *   the widest that does.
+ */
+mas_status mas_expand_text(const void* text, const int32_t* row_start, int32_t B, int32_t T, int32_t S, int32_t C,
+                           int32_t elem_bytes, void* out, hipStream_t stream);
+
+/*
  * Full alignment: mas_search into the workspace's row_start table followed by
  * mas_expand_path.  score_out and item_status_out are nullable as above.
  * No allocation; workspace as for mas_search.

@@ -51,6 +51,8 @@ def _load():
         lib.oracle_mas_batch_neg.restype = ctypes.c_int
         lib.oracle_durations.argtypes = [P, i32, i32, i32, P]
         lib.oracle_durations.restype = None
+        lib.oracle_expand_text.argtypes = [P, P, i32, i32, i32, i32, i32, P]
+        lib.oracle_expand_text.restype = ctypes.c_int
         _lib = lib
     return _lib
 
@@ -106,4 +108,20 @@ def row_start(path: np.ndarray, t_x, t_y) -> np.ndarray:
         first = rows.argmax(axis=1)
         out[b, :tx] = first
         out[b, tx:] = ty
+    return out
+
+
+def expand_text(path: np.ndarray, h: np.ndarray) -> np.ndarray:
+    """Aligned text grid: out[b, j] = the row of h[b] that column j of the
+    path selects (zeros where no row does).  path u8 [B, T, S]; h [B, T, C]
+    of any fixed-width element type.  Returns [B, S, C] of h's dtype."""
+    path = np.ascontiguousarray(path, dtype=np.uint8)
+    h = np.ascontiguousarray(h)
+    B, T, S = path.shape
+    if h.ndim != 3 or h.shape[:2] != (B, T):
+        raise ValueError("h must be [B, T, C] with the path's B and T")
+    C = h.shape[2]
+    out = np.empty((B, S, C), dtype=h.dtype)
+    if _load().oracle_expand_text(_ptr(path), _ptr(h), B, T, S, C, h.dtype.itemsize, _ptr(out)) != 0:
+        raise ValueError("a path column holds more than one 1")
     return out

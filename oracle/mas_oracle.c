@@ -158,4 +158,37 @@ void oracle_durations(const uint8_t* path, int32_t B, int32_t T, int32_t S, int3
     }
 }
 
+/* Aligned text grid (Sec. 5, Conclusion: the MAS path multiplied with the
+ * text representation).  For every item, out[b][j] = sum over i of
+ * path[b][i][j] * h[b][i]: the frame-rate copy of the text features, of shape
+ * [S, C] per item, with h of shape [T, C].  A MAS path has at most one 1 per
+ * speech column, so that sum is the row of h the column is aligned to (taken
+ * as it is, element bytes copied) or all zeros for a column no row covers
+ * (the padding j >= t_y, and invalid items).  Elements are elem_bytes wide,
+ * whatever their type.  Returns -1, leaving the item's output unspecified,
+ * when a column holds more than one 1 (not a MAS path), else 0. */
+int oracle_expand_text(const uint8_t* path, const uint8_t* h, int32_t B, int32_t T, int32_t S, int32_t C,
+                       int32_t elem_bytes, uint8_t* out) {
+  const size_t row = (size_t)C * (size_t)elem_bytes;
+  int rc = 0;
+  for (int32_t b = 0; b < B; ++b) {
+    const uint8_t* pb = path + (size_t)b * (size_t)T * (size_t)S;
+    for (int32_t j = 0; j < S; ++j) {
+      uint8_t* dst = out + ((size_t)b * (size_t)S + (size_t)j) * row;
+      int32_t src = -1, ones = 0;
+      for (int32_t i = 0; i < T; ++i)
+        if (pb[(size_t)i * (size_t)S + (size_t)j]) {
+          src = i;
+          ++ones;
+        }
+      if (ones > 1) rc = -1;
+      if (src < 0)
+        memset(dst, 0, row);
+      else
+        memcpy(dst, h + ((size_t)b * (size_t)T + (size_t)src) * row, row);
+    }
+  }
+  return rc;
+}
+
 int oracle_version(void) { return 2; }

@@ -17,6 +17,7 @@ from ._native import (  # noqa: F401
     Workspace,
     lib,
     mas_expand_path,
+    mas_expand_text,
     mas_forward,
     mas_forward_ex,
     mas_forward_sentinel,

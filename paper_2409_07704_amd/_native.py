@@ -29,6 +29,7 @@ SIGNATURES = {
     "mas_workspace_init": ([_P, _SZ, _P], ctypes.c_int),
     "mas_search": ([_P, _P, _P, _I32, _I32, _I32, _P, _P, _P, _P, _P, _SZ, _P], ctypes.c_int),
     "mas_expand_path": ([_P, _I32, _I32, _I32, _P, _P], ctypes.c_int),
+    "mas_expand_text": ([_P, _P, _I32, _I32, _I32, _I32, _I32, _P, _P], ctypes.c_int),
     "mas_forward_ex": ([_P, _P, _P, _P, _I32, _I32, _I32, _P, _P, _P, _SZ, _P], ctypes.c_int),
     "mas_forward_sentinel": ([_P, _P, _P, _P, _I32, _I32, _I32, ctypes.c_float, _P, _P, _P, _SZ, _P], ctypes.c_int),
     "mas_forward": ([_P, _P, _P, _P, _I32, _I32, _I32, _P], ctypes.c_int),
@@ -171,6 +172,23 @@ def mas_expand_path(row_start, S: int, path_out=None, stream=None):
     pp = _dev_ptr(path_out, "path_out", torch.uint8, (B, T, S))
     _check("mas_expand_path", lib().mas_expand_path(prs, B, T, S, pp, _stream(stream, row_start.device)))
     return path_out
+
+
+def mas_expand_text(text, row_start, S: int, out=None, stream=None):
+    """Aligned text grid [B, S, C] from text [B, T, C] (any 1, 2, 4 or 8-byte
+    dtype) and row_start [B, T+1]: frame j copies the text row whose segment
+    holds it, zeros where none does."""
+    if text.dim() != 3 or row_start.dim() != 2:
+        raise ValueError("text must be [B, T, C] and row_start [B, T+1]")
+    B, T, C = text.shape
+    prs = _dev_ptr(row_start, "row_start", torch.int32, (B, T + 1))
+    pt = _dev_ptr(text, "text", text.dtype)
+    if out is None:
+        out = torch.empty((B, S, C), dtype=text.dtype, device=text.device)
+    po = _dev_ptr(out, "out", text.dtype, (B, S, C))
+    _check("mas_expand_text", lib().mas_expand_text(pt, prs, B, T, S, C, text.element_size(), po,
+                                                    _stream(stream, text.device)))
+    return out
 
 
 def mas_forward_ex(value, t_x, t_y, path_out=None, score_out=None, item_status_out=None, workspace=None, stream=None):

@@ -167,6 +167,19 @@ mas_status mas_expand_path(const int32_t* row_start, int32_t B, int32_t T, int32
   return launch_path(row_start, B, T, S, path_out, stream) == hipSuccess ? MAS_OK : MAS_ERR_HIP;
 }
 
+mas_status mas_expand_text(const void* text, const int32_t* row_start, int32_t B, int32_t T, int32_t S, int32_t C,
+                           int32_t elem_bytes, void* out, hipStream_t stream) {
+  if (!text || !row_start || !out) return MAS_ERR_NULL_POINTER;
+  if (B < 1 || T < 1 || S < 1 || C < 1 || T > (1 << 30)) return MAS_ERR_BAD_SHAPE;
+  if (elem_bytes != 1 && elem_bytes != 2 && elem_bytes != 4 && elem_bytes != 8) return MAS_ERR_BAD_SHAPE;
+  const size_t row_bytes = (size_t)C * (size_t)elem_bytes;
+  if (row_bytes > ((size_t)1 << 24)) return MAS_ERR_BAD_SHAPE;
+  const double limit = 281474976710656.0;  // 2^48 bytes per tensor
+  if ((double)B * (double)S * (double)row_bytes > limit || (double)B * (double)T * (double)row_bytes > limit)
+    return MAS_ERR_BAD_SHAPE;
+  return launch_text(text, row_start, B, T, S, row_bytes, out, stream) == hipSuccess ? MAS_OK : MAS_ERR_HIP;
+}
+
 mas_status mas_forward_ex(const float* value, const int32_t* t_x, const int32_t* t_y, uint8_t* path_out, int32_t B,
                           int32_t T, int32_t S, float* score_out, int32_t* item_status_out, void* workspace,
                           size_t workspace_bytes, hipStream_t stream) {

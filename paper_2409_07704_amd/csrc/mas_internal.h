@@ -67,6 +67,10 @@ __host__ __device__ inline TraceLayout trace_layout(int B, int NW, int NC, int n
 hipError_t launch_mas(const KParams& p, hipStream_t stream);
 // Dense [B, T, S] u8 path from row_start [B, T+1].
 hipError_t launch_path(const int32_t* row_start, int32_t B, int32_t T, int32_t S, uint8_t* path, hipStream_t stream);
+// Aligned text grid out [B, S, row_bytes] from text [B, T, row_bytes] and
+// row_start [B, T+1] (a gather; see mas_text.hip).
+hipError_t launch_text(const void* h, const int32_t* row_start, int32_t B, int32_t T, int32_t S, size_t row_bytes,
+                       void* out, hipStream_t stream);
 // Workspace initialisation: zero-fill of `bytes` (a multiple of 16, at least
 // the header) at a 256-byte aligned pointer, with the header's magic set.
 hipError_t launch_ws_init(void* p, size_t bytes, hipStream_t stream);

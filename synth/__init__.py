@@ -207,6 +207,20 @@ def normal_batch(B: int, T: int, S: int, tx, ty, seed: int):
     return value, np.asarray(tx, dtype=np.int32).reshape(B), np.asarray(ty, dtype=np.int32).reshape(B)
 
 
+# Text features per token for the aligned text grid: 192 channels, the hidden
+# size of the text encoders whose outputs MAS aligns in TTS training.
+TEXT_CHANNELS = 192
+
+
+def text_batch(B: int, T: int, C: int = TEXT_CHANNELS, seed: int = 0) -> np.ndarray:
+    """Seeded text features h f32 [B, T, C], i.i.d. N(0,1) (no exact zeros, so
+    that a zero frame in a grid can only come from an uncovered column)."""
+    st = Stream(seed + 7919)
+    h = st.normal_f32(B * T * C).reshape(B, T, C)
+    h[h == 0] = np.float32(1.0)
+    return h
+
+
 def sha256(*arrays) -> str:
     h = hashlib.sha256()
     for a in arrays:

@@ -90,6 +90,13 @@ def test_other_entry_points_host_validation():
     assert L.mas_forward(FAKE, FAKE, FAKE, FAKE, 1, 0, 1, None) == 2
     assert L.mas_expand_path(None, 1, 1, 1, FAKE, None) == 1
     assert L.mas_expand_path(FAKE, -1, 1, 1, FAKE, None) == 2
+    # the text grid: pointers, shape limits and element widths
+    assert L.mas_expand_text(None, FAKE, 1, 1, 1, 1, 4, FAKE, None) == 1
+    assert L.mas_expand_text(FAKE, None, 1, 1, 1, 1, 4, FAKE, None) == 1
+    assert L.mas_expand_text(FAKE, FAKE, 1, 1, 1, 1, 4, None, None) == 1
+    for bad in ((0, 1, 1, 1, 4), (1, 0, 1, 1, 4), (1, 1, 0, 1, 4), (1, 1, 1, 0, 4), (1, 1, 1, 1, 3), (1, 1, 1, 1, 16),
+                (1, 1, 1, 1 << 22, 8), (1 << 20, 8, 1 << 20, 1 << 10, 4)):
+        assert L.mas_expand_text(FAKE, FAKE, *bad[:4], bad[4], FAKE, None) == 2, bad
     assert L.mas_workspace_init(None, 256, None) == 1
     assert L.mas_workspace_init(ctypes.c_void_p(0x10008), 256, None) == 3
     assert L.mas_workspace_init(FAKE, 100, None) == 3
