@@ -53,6 +53,8 @@ def _load():
         lib.oracle_durations.restype = None
         lib.oracle_expand_text.argtypes = [P, P, i32, i32, i32, i32, i32, P]
         lib.oracle_expand_text.restype = ctypes.c_int
+        lib.oracle_gauss_loglik_cells.argtypes = [P, P, P, i32, i32, i32, i32, P, ctypes.c_int64, P]
+        lib.oracle_gauss_loglik_cells.restype = ctypes.c_int
         _lib = lib
     return _lib
 
@@ -125,3 +127,29 @@ def expand_text(path: np.ndarray, h: np.ndarray) -> np.ndarray:
     if _load().oracle_expand_text(_ptr(path), _ptr(h), B, T, S, C, h.dtype.itemsize, _ptr(out)) != 0:
         raise ValueError("a path column holds more than one 1")
     return out
+
+
+def gauss_loglik(mu: np.ndarray, log_sigma: np.ndarray | None, z: np.ndarray, cells: np.ndarray | None = None):
+    """log N(z_j; mu_i, sigma_i) summed over channels, in float64.
+
+    mu, log_sigma: f32 [B, T, D] (log_sigma None: unit variance); z: f32
+    [B, S, D].  With cells None returns every cell, float64 [B, T, S];
+    otherwise cells is int [n, 3] of (b, i, j) and the result is float64 [n].
+    """
+    mu = np.ascontiguousarray(mu, dtype=np.float32)
+    z = np.ascontiguousarray(z, dtype=np.float32)
+    ls = None if log_sigma is None else np.ascontiguousarray(log_sigma, dtype=np.float32)
+    B, T, D = mu.shape
+    S = z.shape[1]
+    if z.shape != (B, S, D) or (ls is not None and ls.shape != mu.shape):
+        raise ValueError("mu, log_sigma [B, T, D] and z [B, S, D] must agree")
+    full = cells is None
+    if full:
+        b, i, j = np.meshgrid(np.arange(B), np.arange(T), np.arange(S), indexing="ij")
+        cells = np.stack([b.ravel(), i.ravel(), j.ravel()], axis=1)
+    cells = np.ascontiguousarray(cells, dtype=np.int32).reshape(-1, 3)
+    out = np.empty(len(cells), dtype=np.float64)
+    if _load().oracle_gauss_loglik_cells(_ptr(mu), _ptr(ls), _ptr(z), B, T, S, D, _ptr(cells), len(cells),
+                                         _ptr(out)) != 0:
+        raise ValueError("a cell lies outside [B, T, S]")
+    return out.reshape(B, T, S) if full else out

@@ -191,4 +191,34 @@ int oracle_expand_text(const uint8_t* path, const uint8_t* h, int32_t B, int32_t
   return rc;
 }
 
+/* Gaussian log-likelihood of speech frames under text-token Gaussians, the
+ * input MAS maximises (Sec. 2: q[i][j] is log N(z_j; mu_i, sigma_i), here
+ * with a diagonal covariance over D channels):
+ *   q[i][j] = sum over d of ( -ln(2 pi)/2 - log_sigma[i][d]
+ *                             - (z[j][d] - mu[i][d])^2 / (2 sigma[i][d]^2) ),
+ * sigma = exp(log_sigma).  Evaluated in double, d ascending, for n cells
+ * (cells[3k], cells[3k+1], cells[3k+2]) = (b, i, j); mu and log_sigma are
+ * [B][T][D] fp32, z is [B][S][D] fp32, log_sigma NULL means sigma = 1.
+ * Returns -1 for a cell outside [B, T, S] (out left unspecified), else 0. */
+int oracle_gauss_loglik_cells(const float* mu, const float* log_sigma, const float* z, int32_t B, int32_t T,
+                              int32_t S, int32_t D, const int32_t* cells, int64_t n, double* out) {
+  const double half_log_two_pi = 0.91893853320467274178032973640562; /* ln(2 pi) / 2 */
+  for (int64_t k = 0; k < n; ++k) {
+    const int32_t b = cells[3 * k], i = cells[3 * k + 1], j = cells[3 * k + 2];
+    if (b < 0 || b >= B || i < 0 || i >= T || j < 0 || j >= S) return -1;
+    const float* m = mu + ((size_t)b * (size_t)T + (size_t)i) * (size_t)D;
+    const float* ls = log_sigma ? log_sigma + ((size_t)b * (size_t)T + (size_t)i) * (size_t)D : NULL;
+    const float* x = z + ((size_t)b * (size_t)S + (size_t)j) * (size_t)D;
+    double q = 0.0;
+    for (int32_t d = 0; d < D; ++d) {
+      const double lsd = ls ? (double)ls[d] : 0.0;
+      const double sigma = exp(lsd);
+      const double t = (double)x[d] - (double)m[d];
+      q += -half_log_two_pi - lsd - t * t / (2.0 * sigma * sigma);
+    }
+    out[k] = q;
+  }
+  return 0;
+}
+
 int oracle_version(void) { return 2; }

@@ -207,6 +207,31 @@ def normal_batch(B: int, T: int, S: int, tx, ty, seed: int):
     return value, np.asarray(tx, dtype=np.int32).reshape(B), np.asarray(ty, dtype=np.int32).reshape(B)
 
 
+def gauss_inputs(w: Workload | str, seed: int = 0, log_sigma_scale: float | None = None):
+    """The Gaussian parameters behind a "loglik" workload, as fp32 tensors:
+    (mu [B,T,D], log_sigma [B,T,D] or None, z [B,S,D], t_x [B], t_y [B]).
+
+    mu and z are the draws generate() makes for the same workload and seed
+    (in the same order), rounded to fp32.  With log_sigma_scale, log_sigma
+    is log_sigma_scale * N(0,1) from a stream of its own; without it the
+    variance is 1, as in generate()."""
+    if isinstance(w, str):
+        w = WORKLOADS[w]
+    if w.values != "loglik":
+        raise ValueError(f"{w.name} is not a log-likelihood workload")
+    st = Stream(seed)
+    tx, ty = draw_lengths(w, st)
+    mu = np.empty((w.B, w.T, w.D), dtype=np.float32)
+    z = np.empty((w.B, w.S, w.D), dtype=np.float32)
+    for b in range(w.B):
+        mu[b] = st.normal(w.T * w.D).reshape(w.T, w.D)
+        z[b] = st.normal(w.S * w.D).reshape(w.S, w.D)
+    ls = None
+    if log_sigma_scale is not None:
+        ls = (np.float32(log_sigma_scale) * Stream(seed + 104729).normal_f32(w.B * w.T * w.D)).reshape(w.B, w.T, w.D)
+    return mu, ls, z, tx, ty
+
+
 # Text features per token for the aligned text grid: 192 channels, the hidden
 # size of the text encoders whose outputs MAS aligns in TTS training.
 TEXT_CHANNELS = 192
