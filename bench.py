@@ -34,6 +34,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0  # MI355X HBM3E, public spec
+MFMA_F16_PEAK_TFLOPS = 2500.0  # MI355X dense fp16 matrix peak, public spec
 KERNEL = "mas_kernel"  # the fused kernel one mas_forward_ex call launches
 COPY_BYTES = 1 << 30  # copy-probe size (read once, written once)
 COPY_REPS = 4
@@ -450,6 +451,7 @@ def secondary_lines(mas, synth, dev, stream, wname, v, x, y, ws, op, tx, ty, cel
                         "parity": ok}
     out["text_grid"] = text_grid_line(mas, synth, dev, stream, rs, op, tx, ty, float(pl.mean()), forward_s,
                                        steps, warmup)
+    out["loglik"] = loglik_line(mas, synth, dev, stream, wname, ws, forward_s, steps, warmup)
     for name in synth.WORKLOADS:
         if name == wname or name.startswith("tiny"):
             continue
@@ -504,6 +506,84 @@ def text_grid_line(mas, synth, dev, stream, rs, op, tx, ty, search_s, forward_s,
             "dense_bmm_us_mean": float(td.mean()) * 1e6, "dense_bmm_equal": dense_equal,
             "search_plus_grid_us": (search_s + t) * 1e6,
             "forward_ex_plus_dense_us": (forward_s + float(td.mean())) * 1e6, "parity": ok}
+
+
+def loglik_line(mas, synth, dev, stream, wname, ws, forward_s, steps, warmup):
+    """The Gaussian log-likelihood producer on the headline workload's
+    Gaussians (D = 80, log-sigmas 0.2 N(0,1)): mas_loglik alone, then the
+    producer and the alignment back to back, beside the same values formed
+    with torch (the row constants plus two batched fp32 products over the
+    whole padded [B, T, S] grid, the usual way of writing it)."""
+    import numpy as np
+    import torch
+
+    import oracle
+
+    mu, ls, z, tx, ty = synth.gauss_inputs(wname, log_sigma_scale=0.2)
+    B, T, D = mu.shape
+    S = z.shape[1]
+    dm, dl, dz = (torch.from_numpy(a).to(dev) for a in (mu, ls, z))
+    dx, dy = (torch.from_numpy(a).to(dev) for a in (tx, ty))
+    val = torch.full((B, T, S), float("nan"), dtype=torch.float32, device=dev)
+    tl = time_launches(lambda: mas.mas_loglik(dm, dl, dz, dx, dy, val, stream=stream), stream, steps, warmup)
+    path = torch.empty((B, T, S), dtype=torch.uint8, device=dev)
+    sc = torch.empty(B, dtype=torch.float32, device=dev)
+
+    def both():
+        mas.mas_loglik(dm, dl, dz, dx, dy, val, stream=stream)
+        mas.mas_forward_ex(val, dx, dy, path, sc, None, workspace=ws, stream=stream)
+
+    tb = time_launches(both, stream, steps, warmup)
+    # Parity: sampled band cells against the oracle (fp32-level bounds as in
+    # the tests), the alignment against the oracle's on the same values.
+    value = val.cpu().numpy()
+    valid = (tx >= 1) & (tx <= ty)
+    cells = []
+    rng = np.random.default_rng(1)
+    for b in np.flatnonzero(valid):
+        i = rng.integers(0, tx[b], 2000)
+        j = i + rng.integers(0, ty[b] - tx[b] + 1, 2000)
+        cells.append(np.stack([np.full(2000, b), i, j], 1))
+    cells = np.concatenate(cells)
+    want = oracle.gauss_loglik(mu, ls, z, cells)
+    m = mu[cells[:, 0], cells[:, 1]].astype(np.float64)
+    r = np.exp(-2.0 * ls[cells[:, 0], cells[:, 1]].astype(np.float64))
+    x = z[cells[:, 0], cells[:, 2]].astype(np.float64)
+    M = (0.5 * np.log(2 * np.pi) + np.abs(ls[cells[:, 0], cells[:, 1]]) + 0.5 * m * m * r).sum(-1) \
+        + (np.abs(m * r * x) + 0.5 * r * x * x).sum(-1)
+    rel = np.abs(value[cells[:, 0], cells[:, 1], cells[:, 2]] - want) / (2.0 ** -24 * M)
+    Kp = (2 * D + 31) // 32 * 32
+    bound = 3 * Kp + D + 20 + 4.0 * float(np.abs(ls).max())
+    ok_values = bool(rel.max() <= bound and np.sqrt(np.mean(rel ** 2)) <= 4 * np.sqrt(3 * Kp))
+    op, os_, _ = oracle.mas(value, tx, ty)
+    ok_path = bool(np.array_equal(path.cpu().numpy(), op) and sc.cpu().numpy().tobytes() == os_.tobytes())
+    # The torch formulation (context only; fp32 batched products, contiguous operands).
+    r_t = torch.exp(-2.0 * dl)
+    c_t = (-0.5 * np.log(2 * np.pi) - dl - 0.5 * dm * dm * r_t).sum(-1, keepdim=True)
+    f1, f2 = (dm * r_t).contiguous(), (-0.5 * r_t).contiguous()
+    g1, g2 = dz.transpose(1, 2).contiguous(), (dz * dz).transpose(1, 2).contiguous()
+    ref = torch.empty((B, T, S), dtype=torch.float32, device=dev)
+
+    def torch_values():
+        torch.bmm(f1, g1, out=ref)
+        ref.baddbmm_(f2, g2)
+        ref.add_(c_t)
+
+    tt = time_launches(torch_values, stream, 5, 2)
+    del ref, f1, f2, g1, g2
+    band_cells = int(sum(int(a) * (int(b2) - int(a) + 1) for a, b2 in zip(tx[valid], ty[valid])))
+    moved = band_cells * 4 + int(tx[valid].astype(np.int64).sum()) * D * 8 + B * S * D * 4
+    t = float(tl.mean())
+    flops = 2.0 * (2 * D) * band_cells
+    return {"call": "mas_loglik", "D": D, "log_sigma": "0.2 N(0,1)", "band_cells": band_cells,
+            "launch_us_mean": t * 1e6, "launch_us_median": float(np.median(tl)) * 1e6,
+            "algorithmic_bytes": moved, "gbs": moved / t / 1e9, "frac_hbm": moved / t / 1e9 / HBM_PEAK_GBS,
+            "product_tflops": flops / t / 1e12,
+            "mfma_frac": 3 * flops / t / 1e12 / MFMA_F16_PEAK_TFLOPS,
+            "value_err_max_uM": float(rel.max()), "value_err_rms_uM": float(np.sqrt(np.mean(rel ** 2))),
+            "loglik_plus_forward_ex_us": float(tb.mean()) * 1e6, "forward_ex_us": forward_s * 1e6,
+            "torch_values_us_mean": float(tt.mean()) * 1e6,
+            "parity": ok_values and ok_path}
 
 
 if __name__ == "__main__":

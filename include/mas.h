@@ -170,6 +170,30 @@ mas_status mas_expand_text(const void* text, const int32_t* row_start, int32_t B
                            int32_t elem_bytes, void* out, hipStream_t stream);
 
 /*
+ * Gaussian log-likelihood, the quantity MAS maximises (Sec. 2: q[i][j] =
+ * log N(z_j; mu_i, sigma_i), here with a diagonal covariance over D channels;
+ * Sec. 5, Conclusion, names its calculation as the step to fuse with MAS):
+ *   value[b][i][j] = sum over d of ( -ln(2 pi)/2 - log_sigma[b][i][d]
+ *                    - (z[b][j][d] - mu[b][i][d])^2 / (2 exp(2 log_sigma[b][i][d])) )
+ * for exactly the cells MAS reads: 0 <= i < t_x[b], i <= j < t_y[b],
+ * j - i <= t_y[b] - t_x[b] (the feasible band).  Every other cell of
+ * value_out, and every cell of an item with invalid lengths, is left as it
+ * was; mas_search / mas_forward_ex on value_out never read those.
+ *   mu, log_sigma [B, T, D] and z [B, S, D] fp32, contiguous row-major,
+ *   device pointers; log_sigma may be NULL (sigma = 1).  t_x, t_y [B] int32.
+ *   Precision: fp32-level, not bit-reproducible against a CPU: the sum is
+ *   formed as a matrix product on fp16 matrix cores with each operand split
+ *   into two fp16 parts after an exact power-of-2 scaling (about 22
+ *   significant bits per product) and fp32 accumulation.  The error of a
+ *   cell is within a few units of 2^-24 times the sum of the absolute values
+ *   of its terms; repeated calls give identical bits.
+ *   Shape limits: those of mas_forward_ex, and 1 <= D <= 192; else
+ *   MAS_ERR_BAD_SHAPE.
+ */
+mas_status mas_loglik(const float* mu, const float* log_sigma, const float* z, const int32_t* t_x, const int32_t* t_y,
+                      int32_t B, int32_t T, int32_t S, int32_t D, float* value_out, hipStream_t stream);
+
+/*
  * Full alignment: mas_search into the workspace's row_start table followed by
  * mas_expand_path.  score_out and item_status_out are nullable as above.
  * No allocation; workspace as for mas_search.

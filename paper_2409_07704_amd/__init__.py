@@ -22,6 +22,7 @@ from ._native import (  # noqa: F401
     mas_forward_ex,
     mas_forward_sentinel,
     mas_forward_static,
+    mas_loglik,
     mas_search,
     mas_status_string,
     mas_version,

@@ -30,6 +30,7 @@ SIGNATURES = {
     "mas_search": ([_P, _P, _P, _I32, _I32, _I32, _P, _P, _P, _P, _P, _SZ, _P], ctypes.c_int),
     "mas_expand_path": ([_P, _I32, _I32, _I32, _P, _P], ctypes.c_int),
     "mas_expand_text": ([_P, _P, _I32, _I32, _I32, _I32, _I32, _P, _P], ctypes.c_int),
+    "mas_loglik": ([_P, _P, _P, _P, _P, _I32, _I32, _I32, _I32, _P, _P], ctypes.c_int),
     "mas_forward_ex": ([_P, _P, _P, _P, _I32, _I32, _I32, _P, _P, _P, _SZ, _P], ctypes.c_int),
     "mas_forward_sentinel": ([_P, _P, _P, _P, _I32, _I32, _I32, ctypes.c_float, _P, _P, _P, _SZ, _P], ctypes.c_int),
     "mas_forward": ([_P, _P, _P, _P, _I32, _I32, _I32, _P], ctypes.c_int),
@@ -189,6 +190,27 @@ def mas_expand_text(text, row_start, S: int, out=None, stream=None):
     _check("mas_expand_text", lib().mas_expand_text(pt, prs, B, T, S, C, text.element_size(), po,
                                                     _stream(stream, text.device)))
     return out
+
+
+def mas_loglik(mu, log_sigma, z, t_x, t_y, value_out=None, stream=None):
+    """Gaussian log-likelihood value [B, T, S] fp32 of frames z [B, S, D]
+    under text-token Gaussians mu, log_sigma [B, T, D] (log_sigma None: unit
+    variance), written for the cells of each item's feasible band only (the
+    cells MAS reads); other cells of value_out are left as they are."""
+    if mu.dim() != 3 or z.dim() != 3:
+        raise ValueError("mu must be [B, T, D] and z [B, S, D]")
+    B, T, D = mu.shape
+    S = z.shape[1]
+    pm = _dev_ptr(mu, "mu", torch.float32)
+    pl = _dev_ptr(log_sigma, "log_sigma", torch.float32, (B, T, D))
+    pz = _dev_ptr(z, "z", torch.float32, (B, S, D))
+    px = _dev_ptr(t_x, "t_x", torch.int32, (B,))
+    py = _dev_ptr(t_y, "t_y", torch.int32, (B,))
+    if value_out is None:
+        value_out = torch.empty((B, T, S), dtype=torch.float32, device=mu.device)
+    pv = _dev_ptr(value_out, "value_out", torch.float32, (B, T, S))
+    _check("mas_loglik", lib().mas_loglik(pm, pl, pz, px, py, B, T, S, D, pv, _stream(stream, mu.device)))
+    return value_out
 
 
 def mas_forward_ex(value, t_x, t_y, path_out=None, score_out=None, item_status_out=None, workspace=None, stream=None):

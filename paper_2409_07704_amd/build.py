@@ -15,7 +15,7 @@ CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "libmas.so")
 TRACE_LIB = os.path.join(PKG, "libmas_trace.so")
-SOURCES = ["mas_kernels.hip", "mas_text.hip", "mas_api.hip"]
+SOURCES = ["mas_kernels.hip", "mas_text.hip", "mas_loglik.hip", "mas_api.hip"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = [

@@ -180,6 +180,15 @@ mas_status mas_expand_text(const void* text, const int32_t* row_start, int32_t B
   return launch_text(text, row_start, B, T, S, row_bytes, out, stream) == hipSuccess ? MAS_OK : MAS_ERR_HIP;
 }
 
+mas_status mas_loglik(const float* mu, const float* log_sigma, const float* z, const int32_t* t_x, const int32_t* t_y,
+                      int32_t B, int32_t T, int32_t S, int32_t D, float* value_out, hipStream_t stream) {
+  if (!mu || !z || !t_x || !t_y || !value_out) return MAS_ERR_NULL_POINTER;
+  Layout L;
+  if (!make_layout(B, T, S, &L) || D < 1 || D > kLoglikMaxD) return MAS_ERR_BAD_SHAPE;
+  return launch_loglik(mu, log_sigma, z, t_x, t_y, value_out, B, T, S, D, stream) == hipSuccess ? MAS_OK
+                                                                                               : MAS_ERR_HIP;
+}
+
 mas_status mas_forward_ex(const float* value, const int32_t* t_x, const int32_t* t_y, uint8_t* path_out, int32_t B,
                           int32_t T, int32_t S, float* score_out, int32_t* item_status_out, void* workspace,
                           size_t workspace_bytes, hipStream_t stream) {

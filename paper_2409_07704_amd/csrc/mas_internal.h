@@ -71,6 +71,14 @@ hipError_t launch_path(const int32_t* row_start, int32_t B, int32_t T, int32_t S
 // row_start [B, T+1] (a gather; see mas_text.hip).
 hipError_t launch_text(const void* h, const int32_t* row_start, int32_t B, int32_t T, int32_t S, size_t row_bytes,
                        void* out, hipStream_t stream);
+// Gaussian log-likelihood of the band cells of value [B, T, S] from mu,
+// log_sigma (nullable) [B, T, D] and z [B, S, D]; D <= kLoglikMaxD (see
+// mas_loglik.hip).
+constexpr int32_t kLoglikMaxD = 192;
+constexpr int kLoglikMaxKs = (2 * kLoglikMaxD + 31) / 32;
+hipError_t launch_loglik(const float* mu, const float* log_sigma, const float* z, const int32_t* t_x,
+                         const int32_t* t_y, float* value, int32_t B, int32_t T, int32_t S, int32_t D,
+                         hipStream_t stream);
 // Workspace initialisation: zero-fill of `bytes` (a multiple of 16, at least
 // the header) at a 256-byte aligned pointer, with the header's magic set.
 hipError_t launch_ws_init(void* p, size_t bytes, hipStream_t stream);

@@ -100,6 +100,12 @@ def test_other_entry_points_host_validation():
     assert L.mas_workspace_init(None, 256, None) == 1
     assert L.mas_workspace_init(ctypes.c_void_p(0x10008), 256, None) == 3
     assert L.mas_workspace_init(FAKE, 100, None) == 3
+    # the log-likelihood producer
+    assert L.mas_loglik(None, None, FAKE, FAKE, FAKE, 1, 1, 1, 8, FAKE, None) == 1
+    assert L.mas_loglik(FAKE, None, FAKE, FAKE, FAKE, 1, 1, 1, 8, None, None) == 1
+    assert L.mas_loglik(FAKE, None, FAKE, FAKE, FAKE, 1, 1, 1, 0, FAKE, None) == 2
+    assert L.mas_loglik(FAKE, None, FAKE, FAKE, FAKE, 1, 1, 1, 193, FAKE, None) == 2
+    assert L.mas_loglik(FAKE, None, FAKE, FAKE, FAKE, 1, 8193, 1, 8, FAKE, None) == 2
     # the static-scratch entry point: checked before any device call
     assert L.mas_forward_static(None, FAKE, FAKE, FAKE, 1, 1, 1, None, None, None) == 1
     assert L.mas_forward_static(FAKE, FAKE, FAKE, FAKE, 1, 0, 1, None, None, None) == 2
