@@ -37,11 +37,11 @@ namespace {
 constexpr int kLlWaves = 8;                       // MFMA waves: 16 text rows each
 constexpr int kLlRows = kLlWaves * 16;            // text rows per work unit
 constexpr int kLlCols = 32;                       // speech columns per tile
-constexpr int kLlPiece = 1024;                    // speech columns per work unit, at most
 constexpr int kScaleExp = 14;                     // scaled operands lie in [2^13, 2^14)
 constexpr int kMinExp = -113;                     // scale exponents stay in range of a normal float
 constexpr int kXcds = 8;                          // MI355X: workgroups go to its 8 XCDs round-robin
 constexpr int kUnitStartCost = 3;                 // a unit's start-up, in tiles, for the schedule
+constexpr int kMaxWaves = 16;
 
 typedef _Float16 half8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
@@ -52,9 +52,8 @@ struct LlLds {
   // slot = gb_slot(lane, k-step) for the lane that reads it.
   half8 gb[2][KS][2][2][64];
   int col_e[2][kLlCols];  // exponent of the columns' scale, per tile buffer
-  int64_t sum;            // schedule: total cost, then the running prefix of a chunk
-  int first, last;        // schedule: this workgroup's first and last work unit
-  int scan[1024];         // schedule: per-thread costs of a chunk of items
+  int64_t wsum[kMaxWaves];        // schedule: per-wave sums of a block reduction or scan
+  long long first, last;          // schedule: this workgroup's first and last tile, unit << 32 | tile
 };
 
 // Where the fragment that lane `slot` of k-step ks reads is stored: the low
@@ -75,6 +74,27 @@ __device__ __forceinline__ void lds_barrier() {
 
 __device__ __forceinline__ float wave_xor_max(float v, int mask) {
   return fmaxf(v, __shfl_xor(v, mask, 64));
+}
+
+template <int CTRL>
+__device__ __forceinline__ float dpp_mov(float x) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, x), CTRL, 0xf, 0xf, false));
+}
+
+// Maximum over groups of N (2, 4, 8 or 16) consecutive lanes, every lane of a
+// group getting it, with DPP moves inside 16-lane rows (no LDS round trips):
+// swaps within pairs and quads, then rotations of the row by 4 and 8.
+template <int N>
+__device__ __forceinline__ float group_max(float v) {
+  static_assert(N == 2 || N == 4 || N == 8 || N == 16, "group size");
+  v = fmaxf(v, dpp_mov<0xB1>(v));                 // quad_perm [1, 0, 3, 2]
+  if (N >= 4) v = fmaxf(v, dpp_mov<0x4E>(v));     // quad_perm [2, 3, 0, 1]
+  if (N == 8) v = fmaxf(v, __shfl_xor(v, 4, 64));
+  if (N == 16) {
+    v = fmaxf(v, dpp_mov<0x124>(v));              // row_ror 4
+    v = fmaxf(v, dpp_mov<0x128>(v));              // row_ror 8
+  }
+  return v;
 }
 
 // hi + lo split of x * 2^(kScaleExp - e): hi is the scaled value rounded to
@@ -150,29 +170,61 @@ __device__ __forceinline__ void f_group(const float* mu_row, const float* ls_row
   }
 }
 
-// One work unit: rows [i0, i0 + 128) of item b and speech columns from piece
-// cp, cut to the item's feasible band.  ntiles = 0: nothing to do.
+// One work unit: rows [i0, i0 + 128) of item b, over the speech columns of
+// their feasible band from jlo (a multiple of 32) in tiles of 32.
+// ntiles = 0: nothing to do.
 struct LlUnit {
-  int b, rb, i0, ilast, slack, ty, jlo, ntiles;
+  int i0, ilast, slack, ty, jlo, ntiles;
 };
 
-__device__ __forceinline__ LlUnit ll_unit(int b, int rb, int cp, int tx, int ty, int T, int S) {
+__device__ __forceinline__ LlUnit ll_unit(int rb, int tx, int ty, int T, int S) {
   LlUnit u;
-  u.b = b;
-  u.rb = rb;
   u.i0 = rb * kLlRows;
   u.ty = ty;
   u.ntiles = 0;
   if (!(tx >= 1 && tx <= ty && tx <= T && ty <= S) || u.i0 >= tx) return u;
   u.ilast = min(u.i0 + kLlRows, tx) - 1;
   u.slack = ty - tx;
-  u.jlo = max(cp * kLlPiece, u.i0 & ~(kLlCols - 1));
-  const int jhi = min(min(cp * kLlPiece + kLlPiece, ty), u.ilast + u.slack + 1);
-  if (u.jlo < jhi) u.ntiles = (jhi - u.jlo + kLlCols - 1) / kLlCols;
+  u.jlo = u.i0 & ~(kLlCols - 1);
+  const int jhi = min(ty, u.ilast + u.slack + 1);
+  u.ntiles = (jhi - u.jlo + kLlCols - 1) / kLlCols;
   return u;
 }
 
-__device__ __forceinline__ int ll_cost(const LlUnit& u) { return u.ntiles ? u.ntiles + kUnitStartCost : 0; }
+// Schedule cost of a unit (its tiles plus a start-up charge) and of an item.
+__device__ __forceinline__ int64_t ll_cost(const LlUnit& u) { return u.ntiles ? u.ntiles + kUnitStartCost : 0; }
+__device__ __forceinline__ int64_t ll_item_cost(int tx, int ty, int T, int S, int nrb) {
+  int64_t c = 0;
+  for (int rb = 0; rb < nrb; ++rb) {
+    const LlUnit u = ll_unit(rb, tx, ty, T, S);
+    if (!u.ntiles) break;
+    c += ll_cost(u);
+  }
+  return c;
+}
+
+// Block-wide inclusive scan of one int64 per thread (all threads call it).
+template <int kWaves, class Lds>
+__device__ __forceinline__ int64_t block_scan(int64_t x, Lds& L, int64_t* total) {
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+#pragma unroll
+  for (int d = 1; d < 64; d <<= 1) {
+    const int64_t y = __shfl_up(x, d, 64);
+    if (lane >= d) x += y;
+  }
+  if (lane == 63) L.wsum[wave] = x;
+  __syncthreads();
+  int64_t before = 0, all = 0;
+#pragma unroll
+  for (int w = 0; w < kWaves; ++w) {
+    const int64_t t = L.wsum[w];
+    before += w < wave ? t : 0;
+    all += t;
+  }
+  __syncthreads();
+  *total = all;
+  return before + x;
+}
 
 // KS = k-steps of 32 (the padded 2 * Dp channels); VEC: D % 8 == 0 and mu,
 // log_sigma and z 16-byte aligned (16-byte loads of 8 channels); NB =
@@ -191,21 +243,22 @@ template <int KS, bool VEC, int NB>
 __global__ void __launch_bounds__((kLlWaves + NB) * 64)
     mas_loglik_kernel(const float* __restrict__ mu, const float* __restrict__ log_sigma, const float* __restrict__ z,
                       const int32_t* __restrict__ t_x, const int32_t* __restrict__ t_y, float* __restrict__ value,
-                      int32_t B, int32_t T, int32_t S, int32_t D, int32_t Dp, int32_t nrb, int32_t ncp) {
+                      int32_t B, int32_t T, int32_t S, int32_t D, int32_t Dp, int32_t nrb) {
   __shared__ LlLds<KS> L;
   constexpr int kThreads = (kLlWaves + NB) * 64;
   constexpr int FPW = kLlCols / NB;              // frames per builder wave
   constexpr int LPF = 64 / FPW;                  // lanes per frame
   constexpr int P = (2 * KS + LPF - 1) / LPF;    // channel groups per lane: Dp / 8 <= 2 KS <= LPF P
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  const int per_item = nrb * ncp;
 
-  // ---- Schedule (identical in every workgroup).
+  // ---- Schedule (identical in every workgroup).  Units (item, row block)
+  // in order; a unit's cost positions are its start-up charge, then one per
+  // tile.  This workgroup takes the tiles whose positions fall in its share
+  // [v C / G, (v + 1) C / G) of the total cost C.
   const int G = gridDim.x;
-  const int v = (blockIdx.x % kXcds) * (G / kXcds) + blockIdx.x / kXcds;  // share index; XCD x: [x G/8, (x+1) G/8)
+  const int v = (blockIdx.x % kXcds) * (G / kXcds) + blockIdx.x / kXcds;  // XCD x: shares [x G/8, (x+1) G/8)
   if (threadIdx.x == 0) {
-    L.sum = 0;
-    L.first = 0x7fffffff;
+    L.first = 0x7fffffffffffffffLL;
     L.last = -1;
   }
   // Zero every B-fragment once: the padding channels stay zero.
@@ -214,100 +267,99 @@ __global__ void __launch_bounds__((kLlWaves + NB) * 64)
     constexpr int n16 = (int)(sizeof(L.gb) / 16);
     for (int k = threadIdx.x; k < n16; k += kThreads) g[k] = make_uint4(0u, 0u, 0u, 0u);
   }
-  __syncthreads();
-  auto item_cost = [&](int b, int tx, int ty) {
-    int c = 0;
-    for (int l = 0; l < per_item; ++l) c += ll_cost(ll_unit(b, l / ncp, l % ncp, tx, ty, T, S));
-    return c;
-  };
-  for (int b = threadIdx.x; b < B; b += kThreads) atomicAdd((unsigned long long*)&L.sum, (unsigned long long)item_cost(b, t_x[b], t_y[b]));
-  __syncthreads();
-  const int64_t total = L.sum;
-  const int64_t lo = total * v / G, hi = total * (v + 1) / G;
-  __syncthreads();
-  if (threadIdx.x == 0) L.sum = 0;
-  __syncthreads();
-  // Chunks of kThreads items: an inclusive scan of their costs gives each
-  // item's starting cost; items overlapping [lo, hi) mark their units.
+  // Items in chunks of one per thread: an inclusive scan of their costs
+  // gives each item's first position.  With more items than threads, a
+  // first pass finds the total.
+  int64_t total = 0;
+  if (B > kThreads) {
+    int64_t mine = 0;
+    for (int b = threadIdx.x; b < B; b += kThreads) mine += ll_item_cost(t_x[b], t_y[b], T, S, nrb);
+    block_scan<kLlWaves + NB>(mine, L, &total);
+  }
+  int64_t run = 0;  // cost before the current chunk of items
   for (int c0 = 0; c0 < B; c0 += kThreads) {
     const int b = c0 + threadIdx.x;
     const int tx = b < B ? t_x[b] : 0, ty = b < B ? t_y[b] : 0;
-    const int mine = b < B ? item_cost(b, tx, ty) : 0;
-    L.scan[threadIdx.x] = mine;
-    __syncthreads();
-    for (int off = 1; off < kThreads; off <<= 1) {
-      const int add = threadIdx.x >= off ? L.scan[threadIdx.x - off] : 0;
-      __syncthreads();
-      L.scan[threadIdx.x] += add;
-      __syncthreads();
-    }
-    const int64_t base = L.sum;
-    int64_t at = base + L.scan[threadIdx.x] - mine;  // this item's first unit starts here
-    if (b < B && mine > 0 && at < hi && at + mine > lo) {
-      for (int l = 0; l < per_item; ++l) {
-        const int cu = ll_cost(ll_unit(b, l / ncp, l % ncp, tx, ty, T, S));
-        if (cu > 0 && at >= lo && at < hi) {
-          atomicMin(&L.first, b * per_item + l);
-          atomicMax(&L.last, b * per_item + l);
+    const int64_t mine = b < B ? ll_item_cost(tx, ty, T, S, nrb) : 0;
+    int64_t chunk = 0;
+    int64_t at = run + block_scan<kLlWaves + NB>(mine, L, &chunk) - mine;  // this item's first position
+    if (B <= kThreads) total = chunk;
+    const int64_t lo = total * v / G, hi = total * (v + 1) / G;
+    if (mine > 0 && at < hi && at + mine > lo) {
+      for (int rb = 0; rb < nrb; ++rb) {
+        const LlUnit u = ll_unit(rb, tx, ty, T, S);
+        if (!u.ntiles) break;
+        const int64_t t0 = at + kUnitStartCost;  // position of tile 0
+        const int64_t ta = max(lo - t0, (int64_t)0), tb = min(hi - t0, (int64_t)u.ntiles);
+        if (ta < tb) {
+          const long long key = (long long)(b * nrb + rb) << 32;
+          atomicMin(&L.first, key | ta);
+          atomicMax(&L.last, key | (tb - 1));
         }
-        at += cu;
+        at += ll_cost(u);
       }
     }
-    __syncthreads();
-    if (threadIdx.x == kThreads - 1) L.sum = base + L.scan[kThreads - 1];
-    __syncthreads();
+    run += chunk;
   }
-  const int u_first = L.first, u_last = L.last;
+  __syncthreads();
+  const long long s_first = L.first, s_last = L.last;
+  const int u_first = (int)(s_first >> 32), u_last = (int)(s_last >> 32);
+  const int t_first = (int)(s_first & 0xffffffff), t_last = (int)(s_last & 0xffffffff);
 
   if (wave >= kLlWaves) {
     // ---------------------------------------------------------- builders
     // Lane (n, g0): frame n of a tile, channel groups g = g0 + LPF p.
     const int n = (wave - kLlWaves) * FPW + lane / LPF, g0 = lane % LPF;
     for (int u = u_first; u <= u_last; ++u) {
-      const int b = u / per_item, l = u % per_item;
-      const LlUnit U = ll_unit(b, l / ncp, l % ncp, t_x[b], t_y[b], T, S);
-      if (!U.ntiles) continue;
-      const int ntiles = U.ntiles;
-      auto load_tile = [&](int t, float (&zr)[P][8], int (&zv)[P]) {
-        const int j = U.jlo + t * kLlCols + n;
-        const bool ok = t < ntiles && j < S;
-        const float* src = z + ((size_t)b * S + (ok ? j : 0)) * D;
+      const int b = u / nrb, rb = u % nrb;
+      const LlUnit U = ll_unit(rb, t_x[b], t_y[b], T, S);
+      // Tiles ta .. ta + ntiles - 1 of the unit are this workgroup's.
+      const int ta = u == u_first ? t_first : 0;
+      const int ntiles = (u == u_last ? t_last + 1 : U.ntiles) - ta;
+      if (ntiles <= 0) continue;
+      // Frame loads.  Frames past the unit's tiles or the tensor re-read
+      // the item's first frame, and channels past D (only without VEC)
+      // repeat the group's first one: such values only ever meet zero rows
+      // of F or land in columns that are never stored, so they need no
+      // masking (inputs are finite).
+      const float* zitem = z + (size_t)b * S * D;
+      const int jfirst = U.jlo + ta * kLlCols + n;
+      auto load_tile = [&](int t, float (&zr)[P][8]) {
+        const int j = jfirst + t * kLlCols;
+        const float* src = zitem + (size_t)(t < ntiles && j < S ? j : 0) * D;
 #pragma unroll
         for (int p = 0; p < P; ++p) {
           const int d0 = 8 * (g0 + LPF * p);
-          zv[p] = ok && d0 < D ? min(8, D - d0) : 0;
-          load8<VEC>(src + (zv[p] ? d0 : 0), zv[p], zr[p]);
+          const int valid = d0 < D ? min(8, D - d0) : 0;
+          load8<VEC>(src + (valid ? d0 : 0), valid, zr[p]);
         }
       };
       // Channel group g of frame n is k-group g of the z part and Dp / 8 + g
-      // of the z^2 part.
-      auto build_tile = [&](int buf, float (&zr)[P][8], const int (&zv)[P]) {
-        float sq[P][8];
-        float cm = 0.f;
-#pragma unroll
-        for (int p = 0; p < P; ++p) mask8(zv[p], zr[p]);
+      // of the z^2 part; the frame's scale comes from max |z| (max z^2 is
+      // its square).
+      auto build_tile = [&](int buf, const float (&zr)[P][8]) {
+        float m = 0.f;
 #pragma unroll
         for (int p = 0; p < P; ++p)
 #pragma unroll
-          for (int e = 0; e < 8; ++e) {
-            sq[p][e] = zr[p][e] * zr[p][e];
-            cm = fmaxf(cm, fmaxf(fabsf(zr[p][e]), sq[p][e]));
-          }
-#pragma unroll
-        for (int m = 1; m < LPF; m <<= 1) cm = wave_xor_max(cm, m);
-        const int ec = max(__builtin_amdgcn_frexp_expf(cm), kMinExp);
+          for (int e = 0; e < 8; ++e) m = fmaxf(m, fabsf(zr[p][e]));
+        m = group_max<LPF>(m);
+        const int ec = max(__builtin_amdgcn_frexp_expf(fmaxf(m, m * m)), kMinExp);
         const int nb = n >> 4;
 #pragma unroll
         for (int p = 0; p < P; ++p) {
           const int g = g0 + LPF * p;
           if (8 * g < Dp) {
+            float sq[8];
+#pragma unroll
+            for (int e = 0; e < 8; ++e) sq[e] = zr[p][e] * zr[p][e];
             half8 hi, lo;
             split8(zr[p], ec, hi, lo);
             int kg = g;
             int slot = gb_slot((n & 15) + 16 * (kg & 3), kg >> 2);
             L.gb[buf][kg >> 2][nb][0][slot] = hi;
             L.gb[buf][kg >> 2][nb][1][slot] = lo;
-            split8(sq[p], ec, hi, lo);
+            split8(sq, ec, hi, lo);
             kg = Dp / 8 + g;
             slot = gb_slot((n & 15) + 16 * (kg & 3), kg >> 2);
             L.gb[buf][kg >> 2][nb][0][slot] = hi;
@@ -316,46 +368,56 @@ __global__ void __launch_bounds__((kLlWaves + NB) * 64)
         }
         if (g0 == 0) L.col_e[buf][n] = ec;
       };
-      float za[P][8], zb[P][8];
-      int va[P], vb[P];
-      load_tile(0, za, va);
-      load_tile(1, zb, vb);
-      build_tile(0, za, va);
-      load_tile(2, za, va);
+      // Frames of the next kDepth tiles in registers: at MFMA step m the
+      // builders turn tile m + 1 (register set (m + 1) % kDepth) into
+      // B-fragments and refill that set with tile m + 1 + kDepth.  Full
+      // rounds of kDepth steps issue their loads on every path (past the
+      // last tile they re-read the item's first frame), so the compiler's
+      // wait before each build counts exactly the newer loads; the last
+      // partial round issues none.
+      constexpr int kDepth = 4;
+      float zr[kDepth][P][8];
+#pragma unroll
+      for (int k = 0; k < kDepth; ++k) load_tile(k, zr[k]);
+      build_tile(0, zr[0]);
+      load_tile(kDepth, zr[0]);
       lds_barrier();
-      // Tile t + 1 is built while the MFMA waves work on tile t; loads run
-      // two tiles ahead.  Both halves of an iteration issue their loads on
-      // every path (past the last tile they re-read the item's first frame),
-      // so the compiler's wait before each build counts exactly the newer
-      // loads.
-      int t = 0;
-      for (; t + 1 < ntiles; t += 2) {
-        build_tile(1, zb, vb);  // tile t + 1
-        load_tile(t + 3, zb, vb);
-        lds_barrier();
-        if (t + 2 < ntiles) build_tile(0, za, va);  // tile t + 2
-        load_tile(t + 4, za, va);
-        lds_barrier();
+      int m0 = 0;
+      for (; m0 + kDepth <= ntiles; m0 += kDepth) {
+#pragma unroll
+        for (int j = 0; j < kDepth; ++j) {
+          const int m = m0 + j;
+          if (m + 1 < ntiles) build_tile((m + 1) & 1, zr[(j + 1) % kDepth]);
+          load_tile(m + 1 + kDepth, zr[(j + 1) % kDepth]);
+          lds_barrier();
+        }
       }
-      if (t < ntiles) lds_barrier();  // the last tile: nothing left to build
+#pragma unroll
+      for (int j = 0; j < kDepth; ++j) {
+        const int m = m0 + j;
+        if (m < ntiles) {
+          if (m + 1 < ntiles) build_tile((m + 1) & 1, zr[(j + 1) % kDepth]);
+          lds_barrier();
+        }
+      }
     }
     return;
   }
 
   // ------------------------------------------------------------ MFMA waves
   const int m = lane & 15, q = lane >> 4;
-  half8 ahi[KS], alo[KS];
-  float ra[4];
-  int re[4];
-  int cur = -1;  // item * nrb + row block of the A-fragments held
   for (int u = u_first; u <= u_last; ++u) {
-    const int b = u / per_item, l = u % per_item;
-    const LlUnit U = ll_unit(b, l / ncp, l % ncp, t_x[b], t_y[b], T, S);
-    if (!U.ntiles) continue;
+    const int b = u / nrb, rb = u % nrb;
+    const LlUnit U = ll_unit(rb, t_x[b], t_y[b], T, S);
+    const int ta = u == u_first ? t_first : 0;
+    const int ntiles = (u == u_last ? t_last + 1 : U.ntiles) - ta;
+    if (ntiles <= 0) continue;
     const int r0 = U.i0 + wave * 16;
     const int ilast = U.ilast, slack = U.slack, ty = U.ty;
-    if (b * nrb + U.rb != cur) {
-      cur = b * nrb + U.rb;
+    half8 ahi[KS], alo[KS];
+    float ra[4];
+    int re[4];
+    {
       // A-fragments of this wave's 16 rows: lane (m, q) holds row m and
       // channels k = 32 ks + 8 q + e of F.  Small contractions keep F in
       // registers between the row maximum and the split; large ones read mu
@@ -415,9 +477,9 @@ __global__ void __launch_bounds__((kLlWaves + NB) * 64)
       roffb[r] = ii <= ilast ? ii * S * 4 : 0;
     }
     lds_barrier();  // tile 0 is built
-    for (int t = 0; t < U.ntiles; ++t) {
+    for (int t = 0; t < ntiles; ++t) {
       const int buf = t & 1;
-      const int c = U.jlo + t * kLlCols;
+      const int c = U.jlo + (ta + t) * kLlCols;
       // Does this wave's 16 x 32 block hold a band cell?
       if (ilo_w <= ihi_w && c + kLlCols - 1 >= ilo_w && c <= ihi_w + slack && c < ty) {
         f32x4 h0 = {0.f, 0.f, 0.f, 0.f}, h1 = h0, x0 = h0, x1 = h0;
@@ -451,18 +513,30 @@ __global__ void __launch_bounds__((kLlWaves + NB) * 64)
           __builtin_amdgcn_sched_barrier(0);
         }
         // Lane l holds column l % 16 of each n-block, rows 4 (l / 16) + r.
-        // A cell is in the band when 0 <= j - i <= slack and j < t_y.
+        // A cell is in the band when 0 <= j - i <= slack and j < t_y; a
+        // block wholly inside the band stores without per-cell checks.
         const int j0 = c + (lane & 15), j1 = j0 + 16;
         const int ce0 = L.col_e[buf][lane & 15] - 2 * kScaleExp, ce1 = L.col_e[buf][16 + (lane & 15)] - 2 * kScaleExp;
-        const bool c0 = j0 < ty, c1 = j1 < ty;
+        const bool inside = r0 + 15 <= ilast && c >= r0 + 15 && c + kLlCols - 1 - r0 <= slack && c + kLlCols <= ty;
+        if (inside) {
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const float v0 = ra[r] + ldexpf(h0[r] + x0[r], re[r] + ce0);
-          const float v1 = ra[r] + ldexpf(h1[r] + x1[r], re[r] + ce1);
-          const bool in0 = c0 && (unsigned)(j0 - rr[r]) <= (unsigned)slack;
-          const bool in1 = c1 && (unsigned)(j1 - rr[r]) <= (unsigned)slack;
-          __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(v0), vr, in0 ? roffb[r] + j0 * 4 : -1, 0, 0);
-          __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(v1), vr, in1 ? roffb[r] + j1 * 4 : -1, 0, 0);
+          for (int r = 0; r < 4; ++r) {
+            const float v0 = ra[r] + ldexpf(h0[r] + x0[r], re[r] + ce0);
+            const float v1 = ra[r] + ldexpf(h1[r] + x1[r], re[r] + ce1);
+            __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(v0), vr, roffb[r] + j0 * 4, 0, 0);
+            __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(v1), vr, roffb[r] + j1 * 4, 0, 0);
+          }
+        } else {
+          const bool c0 = j0 < ty, c1 = j1 < ty;
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const float v0 = ra[r] + ldexpf(h0[r] + x0[r], re[r] + ce0);
+            const float v1 = ra[r] + ldexpf(h1[r] + x1[r], re[r] + ce1);
+            const bool in0 = c0 && (unsigned)(j0 - rr[r]) <= (unsigned)slack;
+            const bool in1 = c1 && (unsigned)(j1 - rr[r]) <= (unsigned)slack;
+            __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(v0), vr, in0 ? roffb[r] + j0 * 4 : -1, 0, 0);
+            __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(v1), vr, in1 ? roffb[r] + j1 * 4 : -1, 0, 0);
+          }
         }
       }
       lds_barrier();  // tile t + 1 is built; buffer t % 2 may be rebuilt
@@ -474,15 +548,15 @@ template <int KS>
 hipError_t launch_ll_ks(const float* mu, const float* log_sigma, const float* z, const int32_t* t_x,
                         const int32_t* t_y, float* value, int32_t B, int32_t T, int32_t S, int32_t D, int32_t Dp,
                         bool vec, int grid, hipStream_t stream) {
-  const int32_t nrb = (T + kLlRows - 1) / kLlRows, ncp = (S + kLlPiece - 1) / kLlPiece;
+  const int32_t nrb = (T + kLlRows - 1) / kLlRows;
   constexpr int NB = KS <= 5 ? 8 : 4;
   constexpr int kThreads = (kLlWaves + NB) * 64;
   if (vec)
     hipLaunchKernelGGL((mas_loglik_kernel<KS, true, NB>), dim3(grid), dim3(kThreads), 0, stream, mu, log_sigma, z,
-                       t_x, t_y, value, B, T, S, D, Dp, nrb, ncp);
+                       t_x, t_y, value, B, T, S, D, Dp, nrb);
   else
     hipLaunchKernelGGL((mas_loglik_kernel<KS, false, NB>), dim3(grid), dim3(kThreads), 0, stream, mu, log_sigma, z,
-                       t_x, t_y, value, B, T, S, D, Dp, nrb, ncp);
+                       t_x, t_y, value, B, T, S, D, Dp, nrb);
   return hipGetLastError();
 }
 
