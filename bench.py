@@ -451,7 +451,8 @@ def secondary_lines(mas, synth, dev, stream, wname, v, x, y, ws, op, tx, ty, cel
                         "parity": ok}
     out["text_grid"] = text_grid_line(mas, synth, dev, stream, rs, op, tx, ty, float(pl.mean()), forward_s,
                                        steps, warmup)
-    out["loglik"] = loglik_line(mas, synth, dev, stream, wname, ws, forward_s, steps, warmup)
+    out["loglik"] = loglik_line(mas, synth, dev, stream, wname, ws, forward_s, steps, warmup, 0.2)
+    out["loglik_unit_variance"] = loglik_line(mas, synth, dev, stream, wname, ws, forward_s, steps, warmup, None)
     for name in synth.WORKLOADS:
         if name == wname or name.startswith("tiny"):
             continue
@@ -508,21 +509,24 @@ def text_grid_line(mas, synth, dev, stream, rs, op, tx, ty, search_s, forward_s,
             "forward_ex_plus_dense_us": (forward_s + float(td.mean())) * 1e6, "parity": ok}
 
 
-def loglik_line(mas, synth, dev, stream, wname, ws, forward_s, steps, warmup):
+def loglik_line(mas, synth, dev, stream, wname, ws, forward_s, steps, warmup, ls_scale):
     """The Gaussian log-likelihood producer on the headline workload's
-    Gaussians (D = 80, log-sigmas 0.2 N(0,1)): mas_loglik alone, then the
-    producer and the alignment back to back, beside the same values formed
-    with torch (the row constants plus two batched fp32 products over the
-    whole padded [B, T, S] grid, the usual way of writing it)."""
+    Gaussians (D = 80; log-sigmas ls_scale N(0,1), or unit variance as the
+    headline values have): mas_loglik alone, then the producer and the
+    alignment back to back, beside the same values formed with torch (the
+    row constants plus batched fp32 products over the whole padded
+    [B, T, S] grid, the usual way of writing it)."""
     import numpy as np
     import torch
 
     import oracle
 
-    mu, ls, z, tx, ty = synth.gauss_inputs(wname, log_sigma_scale=0.2)
+    mu, ls, z, tx, ty = synth.gauss_inputs(wname, log_sigma_scale=ls_scale)
     B, T, D = mu.shape
     S = z.shape[1]
-    dm, dl, dz = (torch.from_numpy(a).to(dev) for a in (mu, ls, z))
+    dm, dz = (torch.from_numpy(a).to(dev) for a in (mu, z))
+    dl = None if ls is None else torch.from_numpy(ls).to(dev)
+    lsz = np.zeros_like(mu) if ls is None else ls
     dx, dy = (torch.from_numpy(a).to(dev) for a in (tx, ty))
     val = torch.full((B, T, S), float("nan"), dtype=torch.float32, device=dev)
     tl = time_launches(lambda: mas.mas_loglik(dm, dl, dz, dx, dy, val, stream=stream), stream, steps, warmup)
@@ -547,19 +551,20 @@ def loglik_line(mas, synth, dev, stream, wname, ws, forward_s, steps, warmup):
     cells = np.concatenate(cells)
     want = oracle.gauss_loglik(mu, ls, z, cells)
     m = mu[cells[:, 0], cells[:, 1]].astype(np.float64)
-    r = np.exp(-2.0 * ls[cells[:, 0], cells[:, 1]].astype(np.float64))
+    r = np.exp(-2.0 * lsz[cells[:, 0], cells[:, 1]].astype(np.float64))
     x = z[cells[:, 0], cells[:, 2]].astype(np.float64)
-    M = (0.5 * np.log(2 * np.pi) + np.abs(ls[cells[:, 0], cells[:, 1]]) + 0.5 * m * m * r).sum(-1) \
+    M = (0.5 * np.log(2 * np.pi) + np.abs(lsz[cells[:, 0], cells[:, 1]]) + 0.5 * m * m * r).sum(-1) \
         + (np.abs(m * r * x) + 0.5 * r * x * x).sum(-1)
     rel = np.abs(value[cells[:, 0], cells[:, 1], cells[:, 2]] - want) / (2.0 ** -24 * M)
     Kp = (2 * D + 31) // 32 * 32
-    bound = 3 * Kp + D + 20 + 4.0 * float(np.abs(ls).max())
+    bound = 3 * Kp + D + 20 + 4.0 * float(np.abs(lsz).max())
     ok_values = bool(rel.max() <= bound and np.sqrt(np.mean(rel ** 2)) <= 4 * np.sqrt(3 * Kp))
     op, os_, _ = oracle.mas(value, tx, ty)
     ok_path = bool(np.array_equal(path.cpu().numpy(), op) and sc.cpu().numpy().tobytes() == os_.tobytes())
     # The torch formulation (context only; fp32 batched products, contiguous operands).
-    r_t = torch.exp(-2.0 * dl)
-    c_t = (-0.5 * np.log(2 * np.pi) - dl - 0.5 * dm * dm * r_t).sum(-1, keepdim=True)
+    dlz = torch.zeros_like(dm) if dl is None else dl
+    r_t = torch.exp(-2.0 * dlz)
+    c_t = (-0.5 * np.log(2 * np.pi) - dlz - 0.5 * dm * dm * r_t).sum(-1, keepdim=True)
     f1, f2 = (dm * r_t).contiguous(), (-0.5 * r_t).contiguous()
     g1, g2 = dz.transpose(1, 2).contiguous(), (dz * dz).transpose(1, 2).contiguous()
     ref = torch.empty((B, T, S), dtype=torch.float32, device=dev)
@@ -572,10 +577,11 @@ def loglik_line(mas, synth, dev, stream, wname, ws, forward_s, steps, warmup):
     tt = time_launches(torch_values, stream, 5, 2)
     del ref, f1, f2, g1, g2
     band_cells = int(sum(int(a) * (int(b2) - int(a) + 1) for a, b2 in zip(tx[valid], ty[valid])))
-    moved = band_cells * 4 + int(tx[valid].astype(np.int64).sum()) * D * 8 + B * S * D * 4
+    moved = band_cells * 4 + int(tx[valid].astype(np.int64).sum()) * D * (4 if ls is None else 8) + B * S * D * 4
     t = float(tl.mean())
-    flops = 2.0 * (2 * D) * band_cells
-    return {"call": "mas_loglik", "D": D, "log_sigma": "0.2 N(0,1)", "band_cells": band_cells,
+    flops = 2.0 * (D if ls is None else 2 * D) * band_cells
+    return {"call": "mas_loglik", "D": D, "log_sigma": "none (unit variance)" if ls is None else f"{ls_scale} N(0,1)",
+            "band_cells": band_cells,
             "launch_us_mean": t * 1e6, "launch_us_median": float(np.median(tl)) * 1e6,
             "algorithmic_bytes": moved, "gbs": moved / t / 1e9, "frac_hbm": moved / t / 1e9 / HBM_PEAK_GBS,
             "product_tflops": flops / t / 1e12,

@@ -9,7 +9,10 @@
 //   a_i     = sum_d ( -ln(2 pi)/2 - log_sigma[i][d] - mu[i][d]^2 r[i][d] / 2 ),
 //   F[i]    = [ mu[i][d] r[i][d] (d < D),  -r[i][d] / 2 (d < D) ],
 //   G[j]    = [ z[j][d],                   z[j][d]^2          ],
-// so the cells form a [T, 2D] x [2D, S] product: MFMA work.  To keep fp32
+// so the cells form a [T, 2D] x [2D, S] product: MFMA work.  Without
+// log_sigma (sigma = 1) the z^2 part is a per-frame constant c_j =
+// -sum_d z[j][d]^2 / 2 and the product shrinks to [T, D] x [D, S] with
+// F[i] = mu[i], G[j] = z[j].  To keep fp32
 // accuracy on fp16 matrix cores, every operand row is scaled by a power of 2
 // to magnitudes in [2^13, 2^14) and split into fp16 hi + lo (x = hi + lo up to
 // 2^-22 relative); the product takes hi*hi + hi*lo + lo*hi (three MFMAs per
@@ -52,6 +55,7 @@ struct LlLds {
   // slot = gb_slot(lane, k-step) for the lane that reads it.
   half8 gb[2][KS][2][2][64];
   int col_e[2][kLlCols];  // exponent of the columns' scale, per tile buffer
+  float col_c[2][kLlCols];  // unit variance: -|z_j|^2 / 2 of the columns, per tile buffer
   int64_t wsum[kMaxWaves];        // schedule: per-wave sums of a block reduction or scan
   long long first, last;          // schedule: this workgroup's first and last tile, unit << 32 | tile
 };
@@ -93,6 +97,20 @@ __device__ __forceinline__ float group_max(float v) {
   if (N == 16) {
     v = fmaxf(v, dpp_mov<0x124>(v));              // row_ror 4
     v = fmaxf(v, dpp_mov<0x128>(v));              // row_ror 8
+  }
+  return v;
+}
+
+// Sum over groups of N consecutive lanes (as group_max).
+template <int N>
+__device__ __forceinline__ float group_sum(float v) {
+  static_assert(N == 2 || N == 4 || N == 8 || N == 16, "group size");
+  v += dpp_mov<0xB1>(v);
+  if (N >= 4) v += dpp_mov<0x4E>(v);
+  if (N == 8) v += __shfl_xor(v, 4, 64);
+  if (N == 16) {
+    v += dpp_mov<0x124>(v);
+    v += dpp_mov<0x128>(v);
   }
   return v;
 }
@@ -139,12 +157,12 @@ __device__ __forceinline__ void mask8(int valid, float (&x)[8]) {
 // the -r / 2 part from Dp), and that row's share of a_i.  r = exp(-2 ls) is
 // formed as 2^(ls * (-2 / ln 2)) with the hardware exp2 (about 1 ulp, plus
 // the rounding of the product, relative |ls| 2^-23).
-template <bool VEC>
+template <bool VEC, bool UNIT>
 __device__ __forceinline__ void f_group(const float* mu_row, const float* ls_row, int k0, int D, int Dp, bool row_ok,
                                         float (&f)[8], float& asum) {
   const bool zpart = k0 < Dp;
   const int d0 = zpart ? k0 : k0 - Dp;
-  const int valid = row_ok && k0 < 2 * Dp && d0 < D ? min(8, D - d0) : 0;
+  const int valid = row_ok && (UNIT ? zpart : k0 < 2 * Dp) && d0 < D ? min(8, D - d0) : 0;
   float mv[8], lv[8];
   load8<VEC>(mu_row + (valid ? d0 : 0), zpart ? valid : 0, mv);
   mask8(zpart ? valid : 0, mv);
@@ -239,7 +257,7 @@ __device__ __forceinline__ int64_t block_scan(int64_t x, Lds& L, int64_t* total)
 // waves 8.. load the frames and build the B-fragments.  Each kind of wave
 // issues only one kind of global memory operation (stores, or loads), so
 // no wave ever waits on the other kind.
-template <int KS, bool VEC, int NB>
+template <int KS, bool VEC, int NB, bool UNIT>
 __global__ void __launch_bounds__((kLlWaves + NB) * 64)
     mas_loglik_kernel(const float* __restrict__ mu, const float* __restrict__ log_sigma, const float* __restrict__ z,
                       const int32_t* __restrict__ t_x, const int32_t* __restrict__ t_y, float* __restrict__ value,
@@ -248,7 +266,7 @@ __global__ void __launch_bounds__((kLlWaves + NB) * 64)
   constexpr int kThreads = (kLlWaves + NB) * 64;
   constexpr int FPW = kLlCols / NB;              // frames per builder wave
   constexpr int LPF = 64 / FPW;                  // lanes per frame
-  constexpr int P = (2 * KS + LPF - 1) / LPF;    // channel groups per lane: Dp / 8 <= 2 KS <= LPF P
+  constexpr int P = ((UNIT ? 4 : 2) * KS + LPF - 1) / LPF;  // z channel groups per lane: Dp / 8 <= LPF P
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
 
   // ---- Schedule (identical in every workgroup).  Units (item, row block)
@@ -338,35 +356,44 @@ __global__ void __launch_bounds__((kLlWaves + NB) * 64)
       // of the z^2 part; the frame's scale comes from max |z| (max z^2 is
       // its square).
       auto build_tile = [&](int buf, const float (&zr)[P][8]) {
-        float m = 0.f;
+        float m = 0.f, ss = 0.f;
 #pragma unroll
         for (int p = 0; p < P; ++p)
 #pragma unroll
-          for (int e = 0; e < 8; ++e) m = fmaxf(m, fabsf(zr[p][e]));
+          for (int e = 0; e < 8; ++e) {
+            m = fmaxf(m, fabsf(zr[p][e]));
+            if (UNIT && 8 * (g0 + LPF * p) + e < D) ss += zr[p][e] * zr[p][e];
+          }
         m = group_max<LPF>(m);
-        const int ec = max(__builtin_amdgcn_frexp_expf(fmaxf(m, m * m)), kMinExp);
+        const int ec = max(__builtin_amdgcn_frexp_expf(UNIT ? m : fmaxf(m, m * m)), kMinExp);
         const int nb = n >> 4;
 #pragma unroll
         for (int p = 0; p < P; ++p) {
           const int g = g0 + LPF * p;
           if (8 * g < Dp) {
-            float sq[8];
-#pragma unroll
-            for (int e = 0; e < 8; ++e) sq[e] = zr[p][e] * zr[p][e];
             half8 hi, lo;
             split8(zr[p], ec, hi, lo);
             int kg = g;
             int slot = gb_slot((n & 15) + 16 * (kg & 3), kg >> 2);
             L.gb[buf][kg >> 2][nb][0][slot] = hi;
             L.gb[buf][kg >> 2][nb][1][slot] = lo;
-            split8(sq, ec, hi, lo);
-            kg = Dp / 8 + g;
-            slot = gb_slot((n & 15) + 16 * (kg & 3), kg >> 2);
-            L.gb[buf][kg >> 2][nb][0][slot] = hi;
-            L.gb[buf][kg >> 2][nb][1][slot] = lo;
+            if (!UNIT) {
+              float sq[8];
+#pragma unroll
+              for (int e = 0; e < 8; ++e) sq[e] = zr[p][e] * zr[p][e];
+              split8(sq, ec, hi, lo);
+              kg = Dp / 8 + g;
+              slot = gb_slot((n & 15) + 16 * (kg & 3), kg >> 2);
+              L.gb[buf][kg >> 2][nb][0][slot] = hi;
+              L.gb[buf][kg >> 2][nb][1][slot] = lo;
+            }
           }
         }
-        if (g0 == 0) L.col_e[buf][n] = ec;
+        if (UNIT) ss = group_sum<LPF>(ss);
+        if (g0 == 0) {
+          L.col_e[buf][n] = ec;
+          if (UNIT) L.col_c[buf][n] = -0.5f * ss;
+        }
       };
       // Frames of the next kDepth tiles in registers: at MFMA step m the
       // builders turn tile m + 1 (register set (m + 1) % kDepth) into
@@ -433,7 +460,7 @@ __global__ void __launch_bounds__((kLlWaves + NB) * 64)
 #pragma unroll
       for (int ks = 0; ks < KS; ++ks) {
         float f[8];
-        f_group<VEC>(mu_row, ls_row, 32 * ks + 8 * q, D, Dp, row_ok, f, asum);
+        f_group<VEC, UNIT>(mu_row, ls_row, 32 * ks + 8 * q, D, Dp, row_ok, f, asum);
 #pragma unroll
         for (int e = 0; e < 8; ++e) {
           amax = fmaxf(amax, fabsf(f[e]));
@@ -450,7 +477,7 @@ __global__ void __launch_bounds__((kLlWaves + NB) * 64)
           split8(fv[ks], er, ahi[ks], alo[ks]);
         } else {
           float f[8], unused = 0.f;
-          f_group<VEC>(mu_row, ls_row, 32 * ks + 8 * q, D, Dp, row_ok, f, unused);
+          f_group<VEC, UNIT>(mu_row, ls_row, 32 * ks + 8 * q, D, Dp, row_ok, f, unused);
           split8(f, er, ahi[ks], alo[ks]);
         }
       }
@@ -517,12 +544,13 @@ __global__ void __launch_bounds__((kLlWaves + NB) * 64)
         // block wholly inside the band stores without per-cell checks.
         const int j0 = c + (lane & 15), j1 = j0 + 16;
         const int ce0 = L.col_e[buf][lane & 15] - 2 * kScaleExp, ce1 = L.col_e[buf][16 + (lane & 15)] - 2 * kScaleExp;
+        const float cc0 = UNIT ? L.col_c[buf][lane & 15] : 0.f, cc1 = UNIT ? L.col_c[buf][16 + (lane & 15)] : 0.f;
         const bool inside = r0 + 15 <= ilast && c >= r0 + 15 && c + kLlCols - 1 - r0 <= slack && c + kLlCols <= ty;
         if (inside) {
 #pragma unroll
           for (int r = 0; r < 4; ++r) {
-            const float v0 = ra[r] + ldexpf(h0[r] + x0[r], re[r] + ce0);
-            const float v1 = ra[r] + ldexpf(h1[r] + x1[r], re[r] + ce1);
+            const float v0 = (ra[r] + cc0) + ldexpf(h0[r] + x0[r], re[r] + ce0);
+            const float v1 = (ra[r] + cc1) + ldexpf(h1[r] + x1[r], re[r] + ce1);
             __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(v0), vr, roffb[r] + j0 * 4, 0, 0);
             __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(v1), vr, roffb[r] + j1 * 4, 0, 0);
           }
@@ -530,8 +558,8 @@ __global__ void __launch_bounds__((kLlWaves + NB) * 64)
           const bool c0 = j0 < ty, c1 = j1 < ty;
 #pragma unroll
           for (int r = 0; r < 4; ++r) {
-            const float v0 = ra[r] + ldexpf(h0[r] + x0[r], re[r] + ce0);
-            const float v1 = ra[r] + ldexpf(h1[r] + x1[r], re[r] + ce1);
+            const float v0 = (ra[r] + cc0) + ldexpf(h0[r] + x0[r], re[r] + ce0);
+            const float v1 = (ra[r] + cc1) + ldexpf(h1[r] + x1[r], re[r] + ce1);
             const bool in0 = c0 && (unsigned)(j0 - rr[r]) <= (unsigned)slack;
             const bool in1 = c1 && (unsigned)(j1 - rr[r]) <= (unsigned)slack;
             __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(v0), vr, in0 ? roffb[r] + j0 * 4 : -1, 0, 0);
@@ -544,7 +572,7 @@ __global__ void __launch_bounds__((kLlWaves + NB) * 64)
   }
 }
 
-template <int KS>
+template <int KS, bool UNIT>
 hipError_t launch_ll_ks(const float* mu, const float* log_sigma, const float* z, const int32_t* t_x,
                         const int32_t* t_y, float* value, int32_t B, int32_t T, int32_t S, int32_t D, int32_t Dp,
                         bool vec, int grid, hipStream_t stream) {
@@ -552,10 +580,10 @@ hipError_t launch_ll_ks(const float* mu, const float* log_sigma, const float* z,
   constexpr int NB = KS <= 5 ? 8 : 4;
   constexpr int kThreads = (kLlWaves + NB) * 64;
   if (vec)
-    hipLaunchKernelGGL((mas_loglik_kernel<KS, true, NB>), dim3(grid), dim3(kThreads), 0, stream, mu, log_sigma, z,
+    hipLaunchKernelGGL((mas_loglik_kernel<KS, true, NB, UNIT>), dim3(grid), dim3(kThreads), 0, stream, mu, log_sigma, z,
                        t_x, t_y, value, B, T, S, D, Dp, nrb);
   else
-    hipLaunchKernelGGL((mas_loglik_kernel<KS, false, NB>), dim3(grid), dim3(kThreads), 0, stream, mu, log_sigma, z,
+    hipLaunchKernelGGL((mas_loglik_kernel<KS, false, NB, UNIT>), dim3(grid), dim3(kThreads), 0, stream, mu, log_sigma, z,
                        t_x, t_y, value, B, T, S, D, Dp, nrb);
   return hipGetLastError();
 }
@@ -564,7 +592,9 @@ template <int KS>
 hipError_t dispatch_ll(int ks, const float* mu, const float* log_sigma, const float* z, const int32_t* t_x,
                        const int32_t* t_y, float* value, int32_t B, int32_t T, int32_t S, int32_t D, int32_t Dp,
                        bool vec, int grid, hipStream_t stream) {
-  if (ks == KS) return launch_ll_ks<KS>(mu, log_sigma, z, t_x, t_y, value, B, T, S, D, Dp, vec, grid, stream);
+  if (ks == KS)
+    return log_sigma ? launch_ll_ks<KS, false>(mu, log_sigma, z, t_x, t_y, value, B, T, S, D, Dp, vec, grid, stream)
+                     : launch_ll_ks<KS, true>(mu, log_sigma, z, t_x, t_y, value, B, T, S, D, Dp, vec, grid, stream);
   if constexpr (KS > 1)
     return dispatch_ll<KS - 1>(ks, mu, log_sigma, z, t_x, t_y, value, B, T, S, D, Dp, vec, grid, stream);
   return hipErrorInvalidValue;
@@ -576,7 +606,7 @@ hipError_t launch_loglik(const float* mu, const float* log_sigma, const float* z
                          const int32_t* t_y, float* value, int32_t B, int32_t T, int32_t S, int32_t D,
                          hipStream_t stream) {
   const int32_t Dp = (D + 7) & ~7;
-  const int ks = (2 * Dp + 31) / 32;
+  const int ks = ((log_sigma ? 2 : 1) * Dp + 31) / 32;
   const bool vec = D % 8 == 0 && ((uintptr_t)z | (uintptr_t)mu | (uintptr_t)log_sigma) % 16 == 0;
   // One persistent workgroup per CU, in whole rounds of the eight XCDs.
   int dev = 0, cus = 0;

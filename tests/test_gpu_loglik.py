@@ -123,12 +123,14 @@ def test_workloads(mas, name, ls_scale):
     check_alignment(mas, v, dx, dy, tx, ty, name)
 
 
+@pytest.mark.parametrize("unit", [False, True])
 @pytest.mark.parametrize("D", [1, 7, 80, 100, 192])
-def test_channel_counts(mas, D):
+def test_channel_counts(mas, D, unit):
     """Contractions of one k-step up to the largest (D = 192, as in VITS),
     channel counts that are no multiple of 8 (the 4-byte frame loads), and
     shapes that are no multiple of the tile sizes; large log-sigmas push
-    the operands across many binades."""
+    the operands across many binades.  unit: no log_sigma (the contraction
+    over D channels with a per-frame constant)."""
     rng = np.random.default_rng(D)
     B, T, S = 5, 150, 333
     tx = np.array([150, 1, 97, 33, 140], np.int32)
@@ -136,10 +138,12 @@ def test_channel_counts(mas, D):
     mu = (3.0 * rng.standard_normal((B, T, D))).astype(np.float32)
     ls = (1.5 * rng.standard_normal((B, T, D))).astype(np.float32)
     z = (3.0 * rng.standard_normal((B, S, D))).astype(np.float32)
-    _say(f"D={D} B={B} T={T} S={S}")
+    if unit:
+        ls = None
+    _say(f"D={D} B={B} T={T} S={S} unit={unit}")
     v, dx, dy = run_loglik(mas, mu, ls, z, tx, ty, S)
-    check_values(mu, ls, z, v.cpu().numpy(), tx, ty, label=f"D={D}")
-    check_alignment(mas, v, dx, dy, tx, ty, f"D={D}")
+    check_values(mu, ls, z, v.cpu().numpy(), tx, ty, label=f"D={D} unit={unit}")
+    check_alignment(mas, v, dx, dy, tx, ty, f"D={D} unit={unit}")
 
 
 def test_unaligned_frames_and_invalid_items(mas):
@@ -163,14 +167,15 @@ def test_unaligned_frames_and_invalid_items(mas):
     check_values(mu, ls, z, a, tx, ty, label="invalid-items")
 
 
-def test_benchmark_size(mas):
-    """B=64, T=1024, S=4096, D=80 with log-sigmas: 200k sampled band cells
-    against the oracle, every alignment against the oracle's on the same
-    values, and every cell outside the band untouched."""
-    mu, ls, z, tx, ty = synth.gauss_inputs(synth.BENCH_WORKLOAD, log_sigma_scale=0.2)
+@pytest.mark.parametrize("ls_scale", [None, 0.2])
+def test_benchmark_size(mas, ls_scale):
+    """B=64, T=1024, S=4096, D=80, unit variance and with log-sigmas: 200k
+    sampled band cells against the oracle, every alignment against the
+    oracle's on the same values, and every cell outside the band untouched."""
+    mu, ls, z, tx, ty = synth.gauss_inputs(synth.BENCH_WORKLOAD, log_sigma_scale=ls_scale)
     B, T, D = mu.shape
     S = z.shape[1]
-    _say(f"{synth.BENCH_WORKLOAD} D={D} log_sigma_scale=0.2")
+    _say(f"{synth.BENCH_WORKLOAD} D={D} log_sigma_scale={ls_scale}")
     v, dx, dy = run_loglik(mas, mu, ls, z, tx, ty, S)
     value = v.cpu().numpy()
     band = band_mask(tx, ty, T, S)
