@@ -259,6 +259,7 @@ struct SweepLds {
   f32x4 sink[kWavesPerBlock][kChunk / 4 + 1];  // target of hand-offs nobody reads (a fixed LDS op count per step)
   int wpos;                     // walker position (walk_pos), or -1 once the walk is over
   int tile;                     // path writer: the tile taken next
+  int pub;                      // path writer: the item of the tile taken (wave 0's poll), or -1
   uint32_t fdone[kWavesPerBlock];  // finisher w's step masks have all landed (the call's tag)
   // Row-start requests from the walker to its helper: records of up to 64
   // chunks (two buffers, request n in buffer n % 2), the chunk range they
@@ -1307,8 +1308,8 @@ __device__ __forceinline__ void walk_helper(const KParams& p, SweepLds& L, int b
 // of the two below it are staged, checked against the staging progress read
 // in the middle of the group before (read again, and waited for, only when
 // that falls short); the window addresses come with the same read.  The
-// walker publishes its position, by which the loaders free slots, every
-// other chunk.  Once the path is in row 0 the rest of its group is walked
+// walker publishes its position, by which the loaders free slots, once per
+// group.  Once the path is in row 0 the rest of its group is walked
 // all the same: row 0's bytes are zero.
 __device__ __forceinline__ void walk(const KParams& p, SweepLds& L, int b, int tx, int ty, int lane, Bound& bd) {
   stamp(trace_of(p).item + 8 * (size_t)b + 1);
@@ -1386,7 +1387,7 @@ __device__ __forceinline__ void walk(const KParams& p, SweepLds& L, int b, int t
       const uint32_t d = (uint32_t)__builtin_amdgcn_readlane((int)P, bp - e);
       if (publish) lds_put(wpos_addr, walk_pos(cw, e));
       int s = (int)d;
-      if (d >= kEscape) {
+      if (__builtin_expect(d >= kEscape, 0)) {
         // The path climbed into the row above the wave at position pos: rr + 1
         // rows, then what the mid entry pos + 1 of the wave above adds.
         const uint32_t pos = d - kEscape;
@@ -1464,7 +1465,7 @@ __device__ __forceinline__ void walk(const KParams& p, SweepLds& L, int b, int t
       ready_v = *(const volatile lds_i32x4*)ready_p;
       bases_n = *(const volatile lds_u32*)base_p;
       have_read = true;
-      body(Pa, ba, true);
+      body(Pa, ba, false);
       body(Pb, bb, false);
       flush_at(cw + 1);
     }
@@ -1558,8 +1559,12 @@ __device__ __forceinline__ int wait_published(const KParams& p, int k, uint32_t 
 // A path-writer workgroup: takes tile t = (k, part) from the shared counter,
 // rows [R part, R part + R) of the item published k-th (R = kPathTileRows),
 // waits for that item, writes the tile (each wave an equal share of its rows)
-// and goes on until the tiles run out.  The next tile is taken while this one
-// is written.
+// and goes on until the tiles run out.  The next tile is taken while the
+// workgroup waits for this one's item.  Wave 0 alone polls the completion
+// order (device-scope loads, which go past the caches) and hands the item to
+// the other waves through LDS; they wait at the barrier meanwhile, so a
+// waiting workgroup puts one poll rather than twelve on the memory system
+// at a time, beside the sweeps still running.
 __device__ __forceinline__ void path_writer(const KParams& p, SweepLds& L, uint32_t tag, int wv, int lane, Bound& bd) {
   constexpr int kWaves = kThreads / kWave;
   const int ntiles = p.B * p.ntile;
@@ -1574,23 +1579,26 @@ __device__ __forceinline__ void path_writer(const KParams& p, SweepLds& L, uint3
   __syncthreads();
   int t = L.tile;
   while (t < ntiles) {
-    __syncthreads();  // every wave has read L.tile
-    uint32_t next = 0;
-    if (threadIdx.x == 0)
-      next = __hip_atomic_fetch_add(&p.hdr->tile_next, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     const int k = t / p.ntile, part = t - k * p.ntile;
+    if (wv == 0) {
+      uint32_t next = 0;
+      if (lane == 0) next = __hip_atomic_fetch_add(&p.hdr->tile_next, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      const int b0 = wait_published(p, k, tag, limit, bd);
+      if (lane == 0) {
+        L.pub = b0;
+        L.tile = (int)next;
+      }
+    }
+    __syncthreads();
+    const int b = L.pub, tn = L.tile;
     const int q0 = part * kPathTileRows, q1 = min(q0 + kPathTileRows, p.T);
     const int per = (q1 - q0 + kWaves - 1) / kWaves;
     const int r0 = min(q0 + wv * per, q1), r1 = min(r0 + per, q1);
-    if (r1 > r0) {
-      const int b = wait_published(p, k, tag, limit, bd);
-      if (wv == 0) stamp(trace_of(p).tile + 2 * (size_t)t + 0);
-      if (b >= 0) write_path_rows(p, b, r0, r1, lane);
-      if (wv == 0) stamp(trace_of(p).tile + 2 * (size_t)t + 1);
-    }
-    if (threadIdx.x == 0) L.tile = (int)next;
-    __syncthreads();
-    t = L.tile;
+    if (wv == 0) stamp(trace_of(p).tile + 2 * (size_t)t + 0);
+    if (r1 > r0 && b >= 0) write_path_rows(p, b, r0, r1, lane);
+    if (wv == 0) stamp(trace_of(p).tile + 2 * (size_t)t + 1);
+    __syncthreads();  // every wave has read L.pub and L.tile
+    t = tn;
   }
 }
 
