@@ -188,47 +188,60 @@ __host__ __device__ constexpr int swz(int r) { return (r >> 1) & 7; }
 // one chunk per window, in nslot slots.  An item whose bytes for its rows
 // < t_x fit kMinSlots windows gets windows of all of them (in as many slots
 // as fit, at most kMaxSlots).  Otherwise windows are banded: the most slots
-// S (at least kMinSlots) whose windows of band_ent(S) bytes fit.  A window
+// S (at least kMinSlots) whose windows of band_bytes(S) bytes fit.  A window
 // is staged for chunk c while the walker is at most S chunks above it, so
 // the path can have climbed at most 32 * S rows by then; a banded window
-// starts at the mid entries of the wave below the lowest such row.
+// holds the rows from the lowest such row up to the walker's, and the mid
+// entries of their waves and of the wave above them.
 constexpr int kWalkArea = kWavesPerBlock * kWaveRegion;
 constexpr int kMinSlots = 20;
 constexpr int kMaxSlots = 48;   // (below 64 - 10: the window addresses are kept per chunk % 64)
 constexpr int kWinLoaders = 4;  // loader waves staging windows: loader k takes chunks C-1-k, C-1-k-4, ...
 constexpr int kMaxAhead = 8;    // windows in flight per loader, at most
 __host__ __device__ constexpr int rs_bytes(int T) { return ((T + 1 + kWave) * 4 + 255) & ~255; }
-__host__ __device__ constexpr int band_ent(int S) {
-  return (kEntPerWave * ((kChunk * S + 1) / kRowsPerWave + 2) + 1023) & ~1023;
-}
-static_assert(kMinSlots * band_ent(kMinSlots) <= kWalkArea - rs_bytes(kMaxRows), "banded windows fit");
-// Window geometry of an item: bytes (entries) per window, a multiple of 1024
-// (whole 1 KiB loads: the LDS loads' rate goes by instructions more than by bytes);
-// slots; whether banded; windows in flight per loader; 1 KiB and 256-byte
-// loads per window.
+__host__ __device__ constexpr int round_to(int x, int a) { return (x + a - 1) / a * a; }
+// A banded window of an item with S slots: the rows the walk can still reach
+// from the walker's row at issue time (32 per chunk over S chunks, and one
+// more), then the mid entries of the waves those rows belong to and of the
+// wave above them; 256-byte multiples.
+__host__ __device__ constexpr int band_rows(int S) { return round_to(kChunk * S + 2, 256); }
+__host__ __device__ constexpr int band_mids(int S) { return round_to(kChunk * ((kChunk * S + 1) / kRowsPerWave + 3), 256); }
+__host__ __device__ constexpr int band_bytes(int S) { return band_rows(S) + band_mids(S); }
+static_assert(kMinSlots * band_bytes(kMinSlots) <= kWalkArea - rs_bytes(kMaxRows), "banded windows fit");
+// LDS-DMA loads of `bytes` (a multiple of 256): whole 1 KiB loads, then
+// 256-byte ones (the LDS loads' rate goes by instructions more than by bytes).
+__host__ __device__ constexpr int dma_loads(int bytes) { return bytes / 1024 + (bytes % 1024) / 256; }
+// Window geometry of an item: bytes per window; slots; whether banded
+// (otherwise a window is a chunk's descent bytes from the start: every mid
+// entry and rows 0 .. t_x-1, rounded up to 1 KiB); windows in flight per
+// loader; loads per window; and, when banded, the bytes of its row band and
+// of its mid-entry band (which comes first in the window).
 struct WinGeom {
-  int ent, nslot, banded, ahead, n16, n4;
+  int ent, nslot, banded, ahead, loads, rows, mids;
 };
-__device__ __forceinline__ WinGeom win_geom(int tx, int T) {
+__device__ __forceinline__ WinGeom win_geom(int tx, int NW, int T) {
   const int area = kWalkArea - rs_bytes(T);
-  const int ep = kEntPerWave * ((tx - 1) / kRowsPerWave + 1);
-  const int full = (ep + 1023) & ~1023;
+  const int full = round_to(pd_row0(NW) + tx, 1024);
   WinGeom w;
   if (full * kMinSlots <= area) {
     w.ent = full;
     w.nslot = min(area / full, kMaxSlots);
     w.banded = 0;
+    w.rows = 0;
+    w.mids = 0;
+    w.loads = dma_loads(full);
   } else {
     int S = kMinSlots;
-    while (S < kMaxSlots && (S + 1) * band_ent(S + 1) <= area) ++S;
-    w.ent = band_ent(S);
+    while (S < kMaxSlots && (S + 1) * band_bytes(S + 1) <= area) ++S;
+    w.rows = band_rows(S);
+    w.mids = band_mids(S);
+    w.ent = w.rows + w.mids;
     w.nslot = S;
     w.banded = 1;
+    w.loads = dma_loads(w.rows) + dma_loads(w.mids);
   }
-  w.n16 = w.ent / 1024;
-  w.n4 = (w.ent % 1024) / 256;
   // (loads in flight stay below 64, the range of vmcnt)
-  w.ahead = min(min(kMaxAhead, w.nslot / kWinLoaders), 63 / (w.n16 + w.n4));
+  w.ahead = min(min(kMaxAhead, w.nslot / kWinLoaders), 63 / w.loads);
   return w;
 }
 // Walker position: (chunk << 16) | row (chunk < 2048, row < 8192), or -1
@@ -254,7 +267,8 @@ struct SweepLds {
   // Wave 0's own progress goes to cons0.
   i32x4 box[kWavesPerBlock];
   int cons0;
-  int wbase[kWave];             // walk window of chunk c (lane c % 64): LDS byte address of its entry 0
+  int wbase[kWave];             // walk window of chunk c (lane c % 64): LDS address of row 0's descent byte
+  int wmid[kWave];              // ... and of wave 0's mid entry 0 (the addresses of bytes a banded window lacks are unused)
   i32x4 wready;                 // window loader k: its windows of chunks >= wready[k] are in LDS
   f32x4 sink[kWavesPerBlock][kChunk / 4 + 1];  // target of hand-offs nobody reads (a fixed LDS op count per step)
   int wpos;                     // walker position (walk_pos), or -1 once the walk is over
@@ -1088,8 +1102,9 @@ __device__ __forceinline__ void finisher_role(const KParams& p, SweepLds& L, con
   const int base = kEntPerWave * x.g;
   const int row_off = lane > 0 ? 4 * (base + lane - 1) : -1;  // lane 0's mask (the row above) is not stored
   const int mid_off = lane >= kWave - 8 ? 4 * (base + kMidOff + 4 * (lane - (kWave - 8))) : -1;
-  const int row_doff = lane > 0 ? base + lane - 1 : -1;
-  const int mid_doff = lane >= kWave - 8 ? base + kMidOff + 4 * (lane - (kWave - 8)) : -1;
+  // Descent bytes: rows after every wave's mid entries (see mas_layout.h).
+  const int row_doff = lane > 0 ? pd_row0(p.NW) + kRowsPerWave * x.g + lane - 1 : -1;
+  const int mid_doff = lane >= kWave - 8 ? kChunk * x.g + 4 * (lane - (kWave - 8)) : -1;
   const int q0 = 4 * (lane - (kWave - 8));  // the first mid entry a lane in 56..63 stores
   const int* const progress = w > 0 ? reinterpret_cast<const int*>(&L.box[w - 1]) + 2 : &L.cons0;
   const uint32_t taken_addr = lds_off(&L.box[w]) + 12u;
@@ -1146,7 +1161,7 @@ __device__ __forceinline__ void finisher_role(const KParams& p, SweepLds& L, con
 }
 
 // ---------------------------------------------------------------- backtrack
-// Loader side of the walk: loader k (of kWinLoaders) stages the step masks
+// Loader side of the walk: loader k (of kWinLoaders) stages the descent bytes
 // of chunks C-1-k, C-1-k-4, ... down to 0, one window per chunk (WinGeom:
 // its size, the slot count, up to `ahead` windows in flight), into slot
 // ch % nslot once the walker has walked the chunk that slot held.  It
@@ -1154,23 +1169,35 @@ __device__ __forceinline__ void finisher_role(const KParams& p, SweepLds& L, con
 // minus 3 (its next chunk is 4 below): every chunk of its sequence at or
 // above that value is staged, so that the windows of all chunks >= ch are
 // in LDS once every loader's value is <= ch (-2^30 for a loader with no
-// chunks).  A banded window starts at the mid entries of the wave below the
-// lowest row the walk can reach before it leaves the chunk (32 rows per
-// chunk below the walker's row at issue time).  The LDS address of entry 0
-// of chunk ch's window goes to wbase[ch % 64] before the window is issued.
+// chunks).  A banded window holds the rows from the lowest one the walk can
+// reach before it leaves the chunk (32 rows per chunk below the walker's row
+// at issue time) up to the walker's row, after the mid entries of their waves
+// and of the wave above them.  The LDS addresses that row 0's byte and wave
+// 0's mid entry 0 would have in chunk ch's window go to wbase[ch % 64] and
+// wmid[ch % 64] before the window is issued.
 // Stops early once the walk is over.
 __device__ __forceinline__ void load_windows(const KParams& p, SweepLds& L, int b, int tx, int ty, int k, int lane, Bound& bd) {
   const int C = (ty + kChunk - 1) / kChunk;
   const uint8_t* db = p.pd + (size_t)b * p.NC * (size_t)p.EP;
-  const uint64_t chunk_bytes = (uint64_t)p.EP;
-  const WinGeom wg = win_geom(tx, p.T);
+  const WinGeom wg = win_geom(tx, p.NW, p.T);
   const bool banded = wg.banded;
   const int nslot = wg.nslot;
-  const int loads = wg.n16 + wg.n4;
+  const int loads = wg.loads;
+  const int row0 = pd_row0(p.NW);
   const uint32_t slot_bytes = (uint32_t)wg.ent;
   const uint32_t win0 = lds_off(&L.u.walk.area[0]);
   const uint32_t ready_addr = lds_off(&L.wready) + 4u * (uint32_t)k;
   const uint32_t base_addr = lds_off(&L.wbase[0]);
+  const uint32_t mid_addr = lds_off(&L.wmid[0]);
+  // `bytes` (a multiple of 256) of chunk ch's descent bytes from byte `off`
+  // into LDS at dst; reads past the chunk's bytes are dropped.
+  auto stage = [&](uint32_t dst, int ch, int off, int bytes) __attribute__((always_inline)) {
+    const Cursor cr = make_cursor(db + (size_t)ch * p.EP + off, (uint64_t)(p.EP - off));
+    const __amdgpu_buffer_rsrc_t r = cr.rsrc_s();
+    const int n16 = bytes / 1024, n4 = (bytes % 1024) / 256;
+    for (int q = 0; q < n16; ++q) dma16_dev(dst + 1024u * q, r, 16 * lane + 1024 * q);
+    for (int q = 0; q < n4; ++q) dma4_dev(dst + 1024u * n16 + 256u * q, r, 4 * lane + 1024 * n16 + 256 * q);
+  };
   constexpr int kStep = kWinLoaders;
   // Own chunks above `issued` are issued; own chunks >= `readied` are staged.
   int issued = C - 1 - k, readied = C - 1 - k + kStep;
@@ -1192,15 +1219,24 @@ __device__ __forceinline__ void load_windows(const KParams& p, SweepLds& L, int 
         wpos = uni(lds_poll(&L.wpos));
         if (wpos < 0 || pos_chunk(wpos) >= issued + nslot) break;
       }
-      const int e = uni(pos_row(wpos));
-      const int row_lo = max(e - kChunk * nslot - 1, 0);
-      const int lo = banded ? max(kEntPerWave * (row_lo / kRowsPerWave) - (kEntPerWave - kMidOff), 0) : 0;
       const uint32_t win = win0 + (uint32_t)slot * slot_bytes;
-      lds_put(base_addr + 4u * (uint32_t)(issued & (kWave - 1)), (int)(win - (uint32_t)lo));
-      const Cursor cr = make_cursor(db + (size_t)issued * p.EP + lo, chunk_bytes - (uint64_t)lo);
-      const __amdgpu_buffer_rsrc_t r = cr.rsrc_s();
-      for (int q = 0; q < wg.n16; ++q) dma16_dev(win + 1024u * q, r, 16 * lane + 1024 * q);
-      for (int q = 0; q < wg.n4; ++q) dma4_dev(win + 1024u * wg.n16 + 256u * q, r, 4 * lane + 1024 * wg.n16 + 256 * q);
+      const uint32_t at = 4u * (uint32_t)(issued & (kWave - 1));
+      if (banded) {
+        // Rows row_lo .. e (e: the walker's row at issue time) and the mid
+        // entries of waves g_lo - 1 .. e / 63: the mid band first, then the
+        // row band.
+        const int e = uni(pos_row(wpos));
+        const int row_lo = max(e - kChunk * nslot - 1, 0);
+        const int g_mid = max(row_lo / kRowsPerWave - 1, 0);
+        lds_put(base_addr + at, (int)(win + (uint32_t)wg.mids - (uint32_t)row_lo));
+        lds_put(mid_addr + at, (int)(win - (uint32_t)(kChunk * g_mid)));
+        stage(win, issued, kChunk * g_mid, wg.mids);
+        stage(win + (uint32_t)wg.mids, issued, row0 + row_lo, wg.rows);
+      } else {
+        lds_put(base_addr + at, (int)(win + (uint32_t)row0));
+        lds_put(mid_addr + at, (int)win);
+        stage(win, issued, 0, wg.ent);
+      }
       if ((C - 1 - k - issued) / kStep < 8) t_iss.at((C - 1 - k - issued) / kStep);
       issued -= kStep;
       slot -= kStep;
@@ -1317,9 +1353,7 @@ __device__ __forceinline__ void walk(const KParams& p, SweepLds& L, int b, int t
   Stamps wstamps;
   Waited waited;  // (debug build) ticks spent waiting for windows
   int e = tx - 1;                      // row of the path at the current chunk's last column
-  const int g0 = e / kRowsPerWave;
-  int rr = e - g0 * kRowsPerWave;      // its row within its wave
-  int ent = kEntPerWave * g0 + rr;     // its entry in its chunk's mask array
+  int g = e / kRowsPerWave;            // its wave (changes only where the path climbs out of one)
   int cw = (ty - 1) / kChunk;          // chunk being walked
   const int c_top = cw;
   uint32_t rec_d = 0;   // lane k: descent byte of chunk (64-aligned base) + k
@@ -1344,23 +1378,26 @@ __device__ __forceinline__ void walk(const KParams& p, SweepLds& L, int b, int t
     const uint32_t wpos_addr = lds_off(&L.wpos);
     const lds_i32x4* const ready_p = (const lds_i32x4*)(uintptr_t)lds_off(&L.wready);
     const lds_u32* const base_p = (const lds_u32*)(uintptr_t)(lds_off(&L.wbase[0]) + 4u * (uint32_t)lane);
+    const lds_u32* const mid_p = (const lds_u32*)(uintptr_t)(lds_off(&L.wmid[0]) + 4u * (uint32_t)lane);
     // Staging progress and window addresses as last read (the addresses
     // read after the progress: valid for every chunk it shows staged).
-    // Chunks >= max_k ready[k] are staged; chunk ch's window is at lane
-    // ch % 64 of `bases`.
+    // Chunks >= max_k ready[k] are staged; chunk ch's window addresses (of
+    // row 0's byte and of wave 0's mid entry 0) are at lane ch % 64 of
+    // `bases` and `mids`.
     auto staged_to = [&](const i32x4& r) __attribute__((always_inline)) -> int {
       return max(max(uni(r.x), uni(r.y)), max(uni(r.z), uni(r.w)));
     };
     i32x4 ready_v;
-    uint32_t bases = 0, bases_n;
+    uint32_t bases = 0, bases_n, mids = 0, mids_n;
     // Waits (bounded) until the windows of chunks >= ch are staged, reading
-    // `bases` along.
+    // `bases` and `mids` along.
     auto ensure = [&](int ch) __attribute__((always_inline)) {
       waited.begin();
       int spins = 0;
       for (;;) {
         const i32x4 r = *(const volatile lds_i32x4*)ready_p;
         bases = *(const volatile lds_u32*)base_p;
+        mids = *(const volatile lds_u32*)mid_p;
         if (staged_to(r) <= ch || bd.out) break;
         if (++spins > bd.limit) bd.expire();
         __builtin_amdgcn_s_sleep(1);
@@ -1370,15 +1407,13 @@ __device__ __forceinline__ void walk(const KParams& p, SweepLds& L, int b, int t
       waited.end();
     };
     // The bytes of chunk ch for rows e_b, e_b - 1, ..., e_b - 63 (lane k:
-    // row e_b - k; ent_b and rr_b: e_b's entry and row within its wave),
-    // read from ch's window into one register.  Lanes past row 0 or the
-    // window read whatever is there, never used.
+    // row e_b - k; rows are consecutive bytes), read from ch's window into
+    // one register.  Lanes past row 0 or the window read whatever is there,
+    // never used.
     const uint32_t lane_off = (uint32_t)(-lane);
-    auto fetch = [&](int ch, int ent_b, int rr_b) __attribute__((always_inline)) -> uint32_t {
-      constexpr uint32_t kGap = kEntPerWave - kRowsPerWave;  // from a wave's row 0 to the last row of the wave above
+    auto fetch = [&](int ch, int e_b) __attribute__((always_inline)) -> uint32_t {
       const uint32_t base = (uint32_t)__builtin_amdgcn_readlane((int)bases, ch & (kWave - 1));
-      const uint32_t a = base + (uint32_t)ent_b + lane_off - (lane > rr_b ? kGap : 0u);
-      return *(const lds_u8*)(uintptr_t)a;
+      return *(const lds_u8*)(uintptr_t)(base + (uint32_t)e_b + lane_off);
     };
     // One chunk: its byte from lane bp - e of P (P holds the chunk's bytes
     // from row bp down), then P refilled with chunk cw - 2 from row e, the
@@ -1388,27 +1423,22 @@ __device__ __forceinline__ void walk(const KParams& p, SweepLds& L, int b, int t
       if (publish) lds_put(wpos_addr, walk_pos(cw, e));
       int s = (int)d;
       if (__builtin_expect(d >= kEscape, 0)) {
-        // The path climbed into the row above the wave at position pos: rr + 1
-        // rows, then what the mid entry pos + 1 of the wave above adds.
+        // The path climbed into the row above the wave at position pos: up
+        // to that row (the wave's last row above, e - 63 g + 1 rows), then
+        // what the mid entry pos + 1 of the wave above adds; it goes on in
+        // the wave above (a path climbs at most 32 rows per chunk).
         const uint32_t pos = d - kEscape;
-        s = rr + 1;
+        s = e - kRowsPerWave * g + 1;
         if (pos < kChunk - 1) {
-          const uint32_t base = (uint32_t)__builtin_amdgcn_readlane((int)bases, cw & (kWave - 1));
-          const uint32_t a = base + (uint32_t)(ent - rr - (kEntPerWave - kMidOff) + 1) + pos;
-          s += uni((int)*(const lds_u8*)(uintptr_t)a);
+          const uint32_t mb = (uint32_t)__builtin_amdgcn_readlane((int)mids, cw & (kWave - 1));
+          s += uni((int)*(const lds_u8*)(uintptr_t)(mb + (uint32_t)(kChunk * (g - 1)) + pos + 1));
         }
+        g -= 1;
       }
       rec_d = (uint32_t)mas_writelane((int)d, cw & (kWave - 1), (int)rec_d);
       rec_e = mas_writelane(e, cw & (kWave - 1), rec_e);
       e -= s;
-      rr -= s;
-      ent -= s;
-      if (rr < 0) {
-        // into the wave above: its row 63 + rr
-        rr += kRowsPerWave;
-        ent -= kEntPerWave - kRowsPerWave;
-      }
-      P = fetch(max(cw - 2, 0), ent, rr);  // (chunk 0 again near the end: never used)
+      P = fetch(max(cw - 2, 0), e);  // (chunk 0 again near the end: never used)
       bp = e;
       cw -= 1;
       // The next chunk's v_readlane stays after this prefetch: hoisted above
@@ -1431,7 +1461,7 @@ __device__ __forceinline__ void walk(const KParams& p, SweepLds& L, int b, int t
     // first two registers.
     const int q_top = cw >> 2;
     ensure(max(4 * q_top - 2, 0));
-    uint32_t Pa = fetch(cw, ent, rr), Pb = fetch(max(cw - 1, 0), ent, rr);
+    uint32_t Pa = fetch(cw, e), Pb = fetch(max(cw - 1, 0), e);
     int ba = e, bb = e;
     // Nothing may be outstanding on the LDS/scalar-memory counter when the
     // loops start: a scalar load still in flight (the compiler hoists
@@ -1457,13 +1487,14 @@ __device__ __forceinline__ void walk(const KParams& p, SweepLds& L, int b, int t
       const int need = max(cw - 5, 0);
       if (((cw + 1) & 7) == 0) wstamps.at((cw + 1) >> 3);
       if (have_read && staged_to(ready_v) <= need)
-        bases = bases_n;
+        bases = bases_n, mids = mids_n;
       else
         ensure(need);
       body(Pa, ba, true);
       body(Pb, bb, false);
       ready_v = *(const volatile lds_i32x4*)ready_p;
       bases_n = *(const volatile lds_u32*)base_p;
+      mids_n = *(const volatile lds_u32*)mid_p;
       have_read = true;
       body(Pa, ba, false);
       body(Pb, bb, false);

@@ -45,14 +45,18 @@ constexpr int kMaxRows = 8192;               // largest T (the walker keeps row_
 constexpr int kEntPerWave = 96;
 constexpr int kMidOff = 64;
 // Descent bytes, the walk's own copy of the step masks at a quarter of
-// their size: per chunk, one byte per entry of the same layout,
-//   entry r (row 63g + r): the number of rows the path climbs in the chunk
-//                          while it stays in the wave's rows (the mask's
-//                          popcount), or 64 + p when it climbs into the row
-//                          above the wave at position p (the highest
-//                          position of the mask);
-//   entry kMidOff + q:     the popcount of mid entry q's mask.
+// their size.  Per chunk, EP bytes: first one byte per mid entry of every
+// wave (wave g's mid entry q at kChunk * g + q), then one byte per text row
+// (row i at pd_row0(NW) + i), so that consecutive rows have consecutive
+// bytes whatever waves they belong to:
+//   row i (in wave g):  the number of rows the path climbs in the chunk while
+//                       it stays in the wave's rows (the mask's popcount), or
+//                       64 + p when it climbs into the row above the wave at
+//                       position p (the highest position of the mask);
+//   mid entry q:        the popcount of mid entry q's mask.
+// (EP = 96 NW covers the 32 NW mid bytes and the 63 NW row bytes.)
 constexpr uint32_t kEscape = 64;
+__host__ __device__ constexpr int pd_row0(int NW) { return kChunk * NW; }
 
 // Boundary hand-off between consecutive workgroups of an item: the last wave
 // g of a workgroup publishes Q[63g+62][j] (its last row) for every column j it

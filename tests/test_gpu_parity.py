@@ -201,6 +201,21 @@ def test_long_items(mas):
     assert_parity(mas, value, tx, ty, "long-1024-chunks")
 
 
+def test_banded_walk_windows(mas):
+    """Items taller than the walk's whole-chunk windows allow (t_x above
+    about 4350 rows at these shapes): the loaders stage banded windows, a
+    row band around the walker plus the mid entries of its waves, and the
+    walk crosses many wave boundaries through them.  T = 8192 is the largest
+    height the library accepts."""
+    st = synth.Stream(4242)
+    B, T, S = 2, 6000, 7000
+    value = st.normal_f32(B * T * S).reshape(B, T, S) * np.float32(3.0) - np.float32(1.0)
+    assert_parity(mas, value, np.array([6000, 4700], np.int32), np.array([7000, 6999], np.int32), "banded-t6000-s7000")
+    B, T, S = 1, 8192, 8200
+    value = st.normal_f32(B * T * S).reshape(B, T, S) * np.float32(3.0) - np.float32(1.0)
+    assert_parity(mas, value, np.array([8192], np.int32), np.array([8200], np.int32), "banded-t8192-s8200")
+
+
 def test_mixed_batch_tall_items(mas):
     """A mixed batch with T above the walk's window height (banded windows),
     several workgroups per item (boundary rows handed on by the loaders, one
