@@ -39,7 +39,7 @@ struct KParams {
 // 100 MHz wall-clock stamps.  wg: [grid][2] start and end of each workgroup;
 // chunk: [B][NW][64] slot k: sweep wave g done with chunk 8k+7 (or its last
 // chunk; chunks past 511 are not recorded); walk: [B][64] slot k: walker done
-// with the chunks from 8k up (slot k = its start, for the first block);
+// with the chunks from 32k up (slot k = its start, for the first block);
 // item: [B][8] step masks of every wave published (windows may start),
 // walk start, walk end, row_start published, ticks the walker waited for
 // windows, (unused) x3; tile: [B * ntile][2] start and

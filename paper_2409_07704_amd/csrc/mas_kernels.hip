@@ -274,6 +274,7 @@ struct SweepLds {
   int wpos;                     // walker position (walk_pos), or -1 once the walk is over
   int tile;                     // path writer: the tile taken next
   int pub;                      // path writer: the item of the tile taken (wave 0's poll), or -1
+  uint64_t bpoll[4][kChunk];    // a workgroup's first loader: the boundary words of one poll (four chunks)
   uint32_t fdone[kWavesPerBlock];  // finisher w's step masks have all landed (the call's tag)
   // Row-start requests from the walker to its helper: records of up to 64
   // chunks (two buffers, request n in buffer n % 2), the chunk range they
@@ -963,9 +964,11 @@ __device__ __forceinline__ void load_tiles(const KParams& p, SweepLds& L, const 
   // (the boundary words of the previous workgroup's last wave)
   const uint64_t* const bsrc = p.slots + ((size_t)x.b * p.NB + (x.g > 0 ? x.g / kWavesPerBlock - 1 : 0)) * ((size_t)p.NC * kChunk);
   const uint32_t prod_addr = lds_off(&L.box[w]) + 4u;
+  const __amdgpu_buffer_rsrc_t brs = make_cursor(bsrc, (uint64_t)p.NC * kChunk * 8u).rsrc_s();
+  const uint32_t bpoll_lds = lds_off(&L.bpoll[0][0]);
   int bspins = 0;
-  while ((readied < x.c_end || bnext < bend) && !bd.out) {
-    // Issue while slots are free (the slot of chunk c held chunk c-4).
+  // Issue while slots are free (the slot of chunk c held chunk c-4).
+  auto issue_tiles = [&]() __attribute__((always_inline)) {
     while (issued < x.c_end && issued - readied < kInflight) {
       if (issued > cons + kRing - 1) {
         cons = uni(lds_poll(progress));
@@ -983,6 +986,9 @@ __device__ __forceinline__ void load_tiles(const KParams& p, SweepLds& L, const 
       vr.advance(kChunk * 4);
       ++issued;
     }
+  };
+  while ((readied < x.c_end || bnext < bend) && !bd.out) {
+    issue_tiles();
     if (!held) {
       held = true;
       const int delay = start_delay(p, x.b, lane);
@@ -994,31 +1000,32 @@ __device__ __forceinline__ void load_tiles(const KParams& p, SweepLds& L, const 
     if (BOUND && bnext < bend) {
       if (bnext > cons + kRing - 1) cons = uni(lds_poll(progress));
       if (bnext <= cons + kRing - 1) {
-        // Lane l polls column l % 32 of chunks bnext + l / 32 (load A) and
-        // bnext + 2 + l / 32 (load B), the last chunk again past the end;
-        // the wait covers the tiles in flight.
+        // The words of chunks c0 .. c0 + 3 (1 KiB, lane l: 16 bytes) into
+        // LDS by one load past the caches, then the tiles for the slots that
+        // are free now.  Loads complete in order, so waiting until only
+        // those tiles are outstanding covers the poll and every tile before
+        // it, and keeps the new tiles in flight: a poll does not drain the
+        // loader's pipeline.  Words past the workgroup's region read as 0
+        // (never a call's tag).
         const int c0 = bnext;
-        const uint64_t* const ba = bsrc + (lane & (kChunk - 1));
-        const uint64_t wa = __hip_atomic_load(ba + (size_t)min(c0 + (lane >> 5), bend - 1) * kChunk, __ATOMIC_RELAXED,
-                                              __HIP_MEMORY_SCOPE_AGENT);
-        const uint64_t wb = __hip_atomic_load(ba + (size_t)min(c0 + 2 + (lane >> 5), bend - 1) * kChunk, __ATOMIC_RELAXED,
-                                              __HIP_MEMORY_SCOPE_AGENT);
-        vm_wait<0>();
-        if (readied < issued) {
-          for (; readied < issued; ++readied)
+        dma16_dev(bpoll_lds, brs, c0 * (kChunk * 8) + 16 * lane);
+        const int before = issued;
+        issue_tiles();
+        vm_wait_le(kOps * (issued - before));
+        if (readied < before) {
+          for (; readied < before; ++readied)
             if (readied < x.mask_end) mask_tile(p, ring + (uint32_t)((readied - x.c_begin) & (kRing - 1)) * kSlotStride, x.g, readied, lane);
           lds_put(ready_addr, readied);
         }
-        const uint64_t stale_a = __builtin_amdgcn_ballot_w64((uint32_t)(wa >> 32) != tag);
-        const uint64_t stale_b = __builtin_amdgcn_ballot_w64((uint32_t)(wb >> 32) != tag);
 #pragma unroll
         for (int h = 0; h < 4; ++h) {
           const int c = c0 + h;
-          const uint64_t stale = h < 2 ? stale_a : stale_b;
-          if (bnext != c || c >= bend || c > cons + kRing - 1 || (uint32_t)(stale >> (kChunk * (h & 1))) != 0u) break;
+          const uint64_t wd = L.bpoll[h][lane & (kChunk - 1)];
+          const uint64_t stale = __builtin_amdgcn_ballot_w64((uint32_t)(wd >> 32) != tag);
+          if (bnext != c || c >= bend || c > cons + kRing - 1 || (uint32_t)stale != 0u) break;
           float* const brow = reinterpret_cast<float*>(reinterpret_cast<char*>(&L.u.ring[w][0]) +
                                                        ((c - x.c_begin) & (kRing - 1)) * kSlotStride + kBoundOff);
-          if ((lane >> 5) == (h & 1)) brow[lane & (kChunk - 1)] = __uint_as_float((uint32_t)(h < 2 ? wa : wb));
+          if (lane < kChunk) brow[lane] = __uint_as_float((uint32_t)wd);
           lds_put(prod_addr, c + 1);
           ++bnext;
         }
@@ -1371,7 +1378,10 @@ __device__ __forceinline__ void walk(const KParams& p, SweepLds& L, int b, int t
     lds_put(lds_off(&L.req_posted), posted);
   };
   if (e > 0) {
-    wstamps.at(min((cw >> 3) + 1, kWave - 1));  // (debug build) lane k: chunks >= 8k walked; lane C/8+1: start
+    // (debug build) lane k: chunks >= 32k walked; lane C/32+1: start.  A
+    // stamp holds the walk for a scalar-memory round trip, so the walk takes
+    // one every 32 chunks only.
+    wstamps.at(min((cw >> 5) + 1, kWave - 1));
     using lds_u32 = __attribute__((address_space(3))) uint32_t;
     using lds_u8 = __attribute__((address_space(3))) uint8_t;
     using lds_i32x4 = __attribute__((address_space(3))) i32x4;
@@ -1485,7 +1495,7 @@ __device__ __forceinline__ void walk(const KParams& p, SweepLds& L, int b, int t
     bool have_read = false;
     while (cw >= 0 && e > 0) {
       const int need = max(cw - 5, 0);
-      if (((cw + 1) & 7) == 0) wstamps.at((cw + 1) >> 3);
+      if (((cw + 1) & 31) == 0) wstamps.at((cw + 1) >> 5);
       if (have_read && staged_to(ready_v) <= need)
         bases = bases_n, mids = mids_n;
       else
@@ -1500,7 +1510,7 @@ __device__ __forceinline__ void walk(const KParams& p, SweepLds& L, int b, int t
       body(Pb, bb, false);
       flush_at(cw + 1);
     }
-    wstamps.at(max(cw + 1, 0) >> 3);
+    wstamps.at(max(cw + 1, 0) >> 5);
   }
   // The partial group of records the walk ended in (chunk cw + 1 was walked
   // last; none if that group was handed over already or nothing was

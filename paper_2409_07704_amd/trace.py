@@ -2,7 +2,7 @@
 
 That build (MAS_TRACE) is the same kernel with 100 MHz wall-clock stamps at
 every wave's milestones: each sweep wave after every eighth 32-column chunk,
-the walker after every eighth chunk, the item's walk start/end and row_start
+the walker after every 32nd chunk, the item's walk start/end and row_start
 publication, each path tile's start/end, each workgroup's start/end (layout:
 TraceLayout in csrc/mas_internal.h).  The product library libmas.so carries
 none of it.
@@ -108,7 +108,7 @@ def summary(lay, st, t_x, t_y, with_path: bool = True, top: int = 3):
     wg = st[lay["wg"]:lay["chunk"]].reshape(grid, 2)
     t0 = int(wg[:, 0][wg[:, 0] > 0].min())
     chunk = st[lay["chunk"]:lay["walk"]].reshape(B, NW, 64)  # slot k: chunk 8k+7 (or the wave's last) done
-    walk = st[lay["walk"]:lay["item"]].reshape(B, 64)         # slot k: chunks >= 8k walked
+    walk = st[lay["walk"]:lay["item"]].reshape(B, 64)         # slot k: chunks >= 32k walked
     item = st[lay["item"]:lay["tile"]].reshape(B, 8)
     tile = st[lay["tile"]:lay["win"]].reshape(B * ntile, 2)
     win = st[lay["win"]:lay["total"]].reshape(B, 4, 2, 64)  # loader k, issue/staged, n-th window
@@ -140,8 +140,8 @@ def summary(lay, st, t_x, t_y, with_path: bool = True, top: int = 3):
                 lags += list((cs[g][both] - cs[g - 1][both]) * TICK_US)
         steps = np.array(steps) if steps else np.array([0.0])
         wk = walk[b].astype(np.int64)
-        ks = [kk for kk in range((C - 1) // 8) if wk[kk] > 0 and wk[kk + 1] > 0]
-        wk_chunk = float(np.median([(wk[kk] - wk[kk + 1]) * TICK_US / 8.0 for kk in ks])) if ks else 0.0
+        ks = [kk for kk in range((C - 1) // 32) if wk[kk] > 0 and wk[kk + 1] > 0]
+        wk_chunk = float(np.median([(wk[kk] - wk[kk + 1]) * TICK_US / 32.0 for kk in ks])) if ks else 0.0
         rec = {"b": b, "t_x": tx, "t_y": ty, "waves": g_last + 1, "chunks": C,
                "sweep_end_us": sweep_end,
                "windows_ready_us": float(_rel(item[b, 0], t0)), "walk_start_us": float(_rel(item[b, 1], t0)),
